@@ -1,0 +1,263 @@
+"""SAKI oracle: calibration, codes, sketch scores, top-k and recall in float64.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).  Each function states
+the passage of the paper it follows.  Notation follows the paper: per head,
+Sigma_q is the uncentred second moment of the queries, Sigma_k and mu the
+centred second moment and mean of the keys, C = Sigma_q^{1/2} Sigma_k^{1/2}
+(Eq. 2), C_r = U_r Lambda_r V_r^T its rank-r truncated SVD, and the optimal
+rank-r score map is M_r = Sigma_q^{-1/2} C_r Sigma_k^{-1/2} (Eq. 3,
+Proposition 1).  Keys are stored as codes c = B_k^T (k - mu) and a query
+scores them as (B_q^T q)^T c + q^T mu (Eq. 4, Sec. 6).
+
+Readings taken where the paper is silent (listed with reasons in the design
+notes): moments use the 1/T normaliser; eigenvalues of each Sigma below
+floor_rel * lambda_max are clamped to that floor (never truncated); singular
+vector pairs are sign-canonicalised so that the largest-magnitude entry of v_i
+is positive (lowest index on ties); top-k ranks by score descending, then key
+index ascending.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "second_moments", "clamped_roots", "saki_calibrate", "key_pca_factors",
+    "weight_svd_factors", "score_loss", "codes", "query_sketch", "sketch_scores",
+    "direct_scores", "exact_scores", "candidate_limits", "topk_row", "topk_rows",
+    "recall_hits", "bf16_round", "f32_round", "score_scale", "predicted_reduction",
+    "head_group", "index_scores", "PAD_IDX",
+]
+
+PAD_IDX = -1
+
+
+def head_group(h: int, H_q: int, H_kv: int) -> int:
+    """GQA: query head h reads KV head floor(h / (H_q / H_kv)) (Sec. 3)."""
+    return h // (H_q // H_kv)
+
+
+def second_moments(q_cal: np.ndarray, k_cal: np.ndarray):
+    """Calibration moments of one head (Sec. 6; Appendix A, centring).
+
+    q_cal [T, d], k_cal [T, d].  Returns (Sigma_q, Sigma_k, mu): Sigma_q is the
+    uncentred second moment of the queries, Sigma_k the second moment of the
+    centred keys k - mu, mu the key mean; all with the 1/T normaliser.
+    """
+    q = np.asarray(q_cal, np.float64)
+    k = np.asarray(k_cal, np.float64)
+    T = q.shape[0]
+    sq = q.T @ q / T
+    mu = k.sum(axis=0) / T
+    kc = k - mu
+    sk = kc.T @ kc / T
+    return sq, sk, mu
+
+
+def clamped_roots(S: np.ndarray, floor_rel: float = 1e-6):
+    """Symmetric square root and inverse square root of a PSD moment.
+
+    Appendix A (singular covariances, finite-sample regularisation): the
+    eigenvalues below floor_rel * lambda_max are raised to that floor, so the
+    regularised moment is always invertible.  A moment whose largest
+    eigenvalue is not positive (e.g. constant keys) carries no information;
+    it is replaced by the identity (every eigenvalue counted as clamped).
+    Returns (S^{1/2}, S^{-1/2}, n_clamped).
+    """
+    S = np.asarray(S, np.float64)
+    w, V = np.linalg.eigh(0.5 * (S + S.T))
+    lmax = w.max()
+    if not lmax > 0.0:
+        w = np.ones_like(w)
+        n = w.size
+    else:
+        floor = floor_rel * lmax
+        n = int(np.count_nonzero(w < floor))
+        w = np.maximum(w, floor)
+    half = (V * np.sqrt(w)) @ V.T
+    ihalf = (V / np.sqrt(w)) @ V.T
+    return half, ihalf, n
+
+
+def _canonical_signs(U: np.ndarray, V: np.ndarray):
+    """Flip each pair (u_i, v_i) so the largest-|.| entry of v_i is positive."""
+    U = U.copy()
+    V = V.copy()
+    for i in range(V.shape[1]):
+        j = int(np.argmax(np.abs(V[:, i])))  # first index on ties
+        if V[j, i] < 0:
+            U[:, i] = -U[:, i]
+            V[:, i] = -V[:, i]
+    return U, V
+
+
+def saki_calibrate(q_cal: np.ndarray, k_cal: np.ndarray, r: int,
+                   floor_rel: float = 1e-6) -> dict:
+    """SAKI-opt calibration of one query head (Eq. 2-4, Proposition 1, Sec. 6).
+
+    q_cal [T, d] are this head's calibration queries, k_cal [T, d] its KV
+    group's calibration keys.  Steps, in the paper's order: moments; clamped
+    roots; C = Sigma_q^{1/2} Sigma_k^{1/2}; SVD C = U Lambda V^T;
+    B_q = Sigma_q^{-1/2} U_r Lambda_r^{1/2}, B_k = Sigma_k^{-1/2} V_r Lambda_r^{1/2};
+    M_r = B_q B_k^T; optimum loss = sum of squared tail singular values.
+    """
+    sq, sk, mu = second_moments(q_cal, k_cal)
+    sq_h, sq_ih, nq = clamped_roots(sq, floor_rel)
+    sk_h, sk_ih, nk = clamped_roots(sk, floor_rel)
+    C = sq_h @ sk_h
+    U, sig, Vt = np.linalg.svd(C)
+    U, V = _canonical_signs(U, Vt.T)
+    root = np.sqrt(sig[:r])
+    B_q = sq_ih @ U[:, :r] * root
+    B_k = sk_ih @ V[:, :r] * root
+    return {
+        "Sigma_q": sq, "Sigma_k": sk, "mu": mu,
+        "Sq_half": sq_h, "Sq_ihalf": sq_ih, "Sk_half": sk_h, "Sk_ihalf": sk_ih,
+        "C": C, "U": U, "sigma": sig, "V": V,
+        "B_q": B_q, "B_k": B_k, "M": B_q @ B_k.T,
+        "tail": float(np.sum(sig[r:] ** 2)), "n_clamped": (nq, nk),
+    }
+
+
+def key_pca_factors(Sigma_k: np.ndarray, r: int) -> np.ndarray:
+    """Key-PCA baseline (Sec. 1, Table 1): the top-r eigenvectors of the
+    centred key moment, as the orthonormal basis V [d, r] of the projector
+    P = V V^T.  Used with B_q = B_k = V."""
+    w, V = np.linalg.eigh(0.5 * (Sigma_k + Sigma_k.T))
+    order = np.argsort(-w, kind="stable")
+    return V[:, order[:r]]
+
+
+def weight_svd_factors(W_K: np.ndarray, r: int) -> np.ndarray:
+    """Weight-SVD baseline (Sec. 1, Table 1; reading: data-blind truncation of
+    the key projection): top-r left singular vectors U [d, r] of W_K [d, D],
+    used as B_q = B_k = U (P = U U^T)."""
+    U, _, _ = np.linalg.svd(np.asarray(W_K, np.float64), full_matrices=False)
+    return U[:, :r]
+
+
+def score_loss(P: np.ndarray, Sq_half: np.ndarray, Sk_half: np.ndarray) -> float:
+    """Expected squared score error of a key-side map P in head space (Eq. 2):
+    || Sigma_q^{1/2} (I - P) Sigma_k^{1/2} ||_F^2."""
+    d = P.shape[0]
+    E = Sq_half @ (np.eye(d) - P) @ Sk_half
+    return float(np.sum(E * E))
+
+
+def codes(B_k: np.ndarray, mu: np.ndarray, keys: np.ndarray) -> np.ndarray:
+    """Key codes c_j = B_k^T (k_j - mu) (Eq. 4).  keys [..., N, d] -> [..., N, r]."""
+    kc = np.asarray(keys, np.float64) - np.asarray(mu, np.float64)
+    return kc @ np.asarray(B_k, np.float64)
+
+
+def query_sketch(B_q: np.ndarray, mu: np.ndarray, q: np.ndarray):
+    """Query side of Eq. 4: z = B_q^T q and the exact mean term b = q^T mu."""
+    q = np.asarray(q, np.float64)
+    return q @ np.asarray(B_q, np.float64), q @ np.asarray(mu, np.float64)
+
+
+def sketch_scores(z: np.ndarray, b: np.ndarray, c: np.ndarray) -> np.ndarray:
+    """Approximate scores s_hat_ij = z_i . c_j + b_i (Sec. 6).  [Q, r], [Q], [N, r] -> [Q, N]."""
+    return np.asarray(z, np.float64) @ np.asarray(c, np.float64).T + np.asarray(b)[:, None]
+
+
+def direct_scores(q: np.ndarray, M: np.ndarray, mu: np.ndarray, keys: np.ndarray) -> np.ndarray:
+    """The same scores by the direct route q^T M_r (k - mu) + q^T mu (Sec. 6)."""
+    q = np.asarray(q, np.float64)
+    kc = np.asarray(keys, np.float64) - mu
+    return q @ M @ kc.T + (q @ mu)[:, None]
+
+
+def exact_scores(q: np.ndarray, keys: np.ndarray) -> np.ndarray:
+    """Exact attention logits s_ij = q_i^T k_j (Sec. 3), float64."""
+    return np.asarray(q, np.float64) @ np.asarray(keys, np.float64).T
+
+
+def candidate_limits(Q: int, N: int, q_pos=None) -> np.ndarray:
+    """Number of visible keys per query row: all N, or the causal prefix
+    j <= position (inclusive, 0-based), capped at N."""
+    if q_pos is None:
+        return np.full(Q, N, np.int64)
+    return np.minimum(np.asarray(q_pos, np.int64) + 1, N)
+
+
+def topk_row(s: np.ndarray, limit: int, k: int = 64) -> np.ndarray:
+    """Top-k of one row by (score descending, key index ascending) over keys
+    j < limit, by a full stable sort (Sec. 3 protocol; ties to the lower index).
+    Rows with fewer than k candidates are padded with PAD_IDX."""
+    n = int(limit)
+    j = np.arange(n)
+    order = np.lexsort((j, -np.asarray(s[:n], np.float64)))
+    out = np.full(k, PAD_IDX, np.int64)
+    m = min(k, n)
+    out[:m] = order[:m]
+    return out
+
+
+def topk_rows(S: np.ndarray, limits: np.ndarray, k: int = 64) -> np.ndarray:
+    """topk_row for every row of S [Q, N]."""
+    return np.stack([topk_row(S[i], limits[i], k) for i in range(S.shape[0])])
+
+
+def recall_hits(approx_idx: np.ndarray, exact_idx: np.ndarray) -> np.ndarray:
+    """hits_i = |S_i intersect T_i| per row (Sec. 3: recall of the true top-k),
+    by Python set intersection; padding entries never count."""
+    a = np.asarray(approx_idx)
+    e = np.asarray(exact_idx)
+    out = np.empty(a.shape[:-1], np.int64)
+    for pos in np.ndindex(*a.shape[:-1]):
+        sa = {int(x) for x in a[pos] if x != PAD_IDX}
+        se = {int(x) for x in e[pos] if x != PAD_IDX}
+        out[pos] = len(sa & se)
+    return out
+
+
+def f32_round(x: np.ndarray) -> np.ndarray:
+    """Round to the nearest float32 (ties to even), returned as float64."""
+    return np.asarray(x, np.float64).astype(np.float32).astype(np.float64)
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """Storage of a sketch in bf16: round to float32, then to the nearest bf16
+    (8-bit significand), ties to even; returned as float64.  Non-finite inputs
+    are not supported."""
+    f = np.ascontiguousarray(np.asarray(x, np.float64).astype(np.float32))
+    u = f.view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    u = ((u + 0x7FFF + lsb) & 0xFFFF0000).astype(np.uint32)
+    return u.view(np.float32).astype(np.float64)
+
+
+def score_scale(B_q, B_k, mu, q, keys) -> np.ndarray:
+    """Magnitude scale of computing s_hat from (q, k) through the factors:
+    S_ij = sum_m (|B_q|^T|q_i|)_m (|B_k|^T|k_j - mu|)_m + |q_i|^T |mu|.
+    A forward error analysis of the factored score bounds its rounding error
+    by a small multiple of unit roundoff times S_ij; tolerances are stated
+    relative to it.  [Q, d], [N, d] -> [Q, N]."""
+    aq = np.abs(np.asarray(q, np.float64))
+    ak = np.abs(np.asarray(keys, np.float64) - mu)
+    zq = aq @ np.abs(B_q)
+    ck = ak @ np.abs(B_k)
+    return zq @ ck.T + (aq @ np.abs(mu))[:, None]
+
+
+def predicted_reduction(sigma: np.ndarray, r: int) -> float:
+    """Predicted relative score-MSE reduction of the rank-r map (Remark 2,
+    Appendix C): 1 - sum_{i>r} sigma_i^2 / sum_i sigma_i^2."""
+    s2 = np.asarray(sigma, np.float64) ** 2
+    return float(1.0 - s2[r:].sum() / s2.sum())
+
+
+def index_scores(B_q, B_k, mu, q, keys, sketch: str = "f64"):
+    """Scores of one head through the stored index (Eq. 4, Sec. 6), with the
+    sketch storage emulated: "f64" keeps exact codes; "f32"/"bf16" round the
+    codes c and the query sketch z to that storage type (the mean term b and
+    the sum stay float64).  Returns (s_hat [Q, N], z, b, c) after rounding."""
+    c = codes(B_k, mu, keys)
+    z, b = query_sketch(B_q, mu, q)
+    if sketch == "f32":
+        c, z = f32_round(c), f32_round(z)
+    elif sketch == "bf16":
+        c, z = bf16_round(c), bf16_round(z)
+    elif sketch != "f64":
+        raise ValueError(sketch)
+    return sketch_scores(z, b, c), z, b, c
