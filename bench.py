@@ -1,0 +1,247 @@
+"""Benchmark of the SAKI retrieval-index path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic input
+(the LLaMA-3.1-8B-shaped layer by default: 32 query / 8 KV heads, d = 128,
+N = 4096 cached keys, causal query rows at positions 64..4095):
+
+  1. calibrate   host float64: moments, clamped roots, SVD, factors (512 tokens)
+  2. upload      factors to the GPU (the only host->device copy in the step)
+  3. build       key codes for all 32 query heads
+  4. score_topk  query sketches, sketch scores and top-64 per (query, head)
+  5. recall      exact float64 q.k top-64 and hits against the sketch top-64
+
+Inputs (keys, queries, positions) are resident in HBM before timing starts.
+`value` = keys scored and top-64-selected per second over the whole step.
+Prints ONE JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "keys scored+top-64 selected/sec; % of HBM / MFMA roofline; recall@64"
+PEAK = {"hbm_GBps": 8000.0, "bf16_TFLOPs": 2516.6, "fp32_TFLOPs": 157.3, "fp64_TFLOPs": 78.6}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama31_8b_layer")
+    ap.add_argument("--r", type=int, default=32)
+    ap.add_argument("--sketch", default="bf16", choices=["bf16", "f32"])
+    ap.add_argument("--k", type=int, default=64)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-heads", type=int, default=4,
+                    help="query heads of the CPU-baseline sample (one KV group)")
+    return ap.parse_args()
+
+
+def candidates(spec, N_valid):
+    """Number of (query, key) pairs scored in one step (all heads, sequences)."""
+    if spec.causal:
+        pos = np.arange(spec.q_start, spec.q_start + spec.Q, dtype=np.int64)
+        per_head = int(np.minimum(pos + 1, N_valid).sum())
+    else:
+        per_head = spec.Q * N_valid
+    return per_head * spec.H_q * spec.batch
+
+
+def roofline_terms(spec, r, sketch, k):
+    """Algorithmic work per launch of each GPU stage (bytes moved at least once,
+    flops of the defined arithmetic)."""
+    es = 2 if sketch == "bf16" else 4
+    rows = spec.batch * spec.H_q * spec.Q
+    pairs = candidates(spec, spec.N)
+    heads = spec.batch * spec.H_q
+    return {
+        # codes read once per head, queries read once, top-k (idx+score) written once
+        "score_topk": {"bytes": heads * spec.N * r * es + rows * spec.d * 4 + rows * k * 8,
+                       "flops": 2 * r * pairs,
+                       "peak_flops": PEAK["bf16_TFLOPs"] if sketch == "bf16" else PEAK["fp32_TFLOPs"],
+                       "flop_unit": "bf16" if sketch == "bf16" else "fp32"},
+        # keys read once per KV head, codes written once per query head
+        "build": {"bytes": spec.batch * spec.H_kv * spec.N * spec.d * 4 + heads * spec.N * r * es,
+                  "flops": 2 * spec.d * r * spec.N * heads,
+                  "peak_flops": PEAK["fp32_TFLOPs"], "flop_unit": "fp32"},
+        # keys and queries read once, approx lists read, hits written
+        "recall": {"bytes": spec.batch * spec.H_kv * spec.N * spec.d * 4 + rows * spec.d * 4
+                   + rows * k * 4 + rows * 4,
+                   "flops": 2 * spec.d * pairs,
+                   "peak_flops": PEAK["fp64_TFLOPs"], "flop_unit": "fp64"},
+    }
+
+
+def cpu_baseline(inp, r, sketch, k, n_heads):
+    """The oracle, as it stands, on a bounded sample: query heads 0..n_heads-1
+    (one KV group), all their query rows, full path (calibrate, codes, scores,
+    top-k, exact top-k, recall)."""
+    import oracle as O
+    from threadpoolctl import threadpool_info
+    spec = inp["spec"]
+    G = spec.H_q // spec.H_kv
+    lim = O.candidate_limits(spec.Q, spec.N, inp["q_pos"])
+    t0 = time.perf_counter()
+    n_pairs = 0
+    for h in range(n_heads):
+        oc = O.saki_calibrate(inp["q_cal"][h], inp["k_cal"][h // G], r)
+        q, keys = inp["queries"][0, h], inp["keys"][0, h // G]
+        s_hat, *_ = O.index_scores(oc["B_q"], oc["B_k"], oc["mu"], q, keys,
+                                   "bf16" if sketch == "bf16" else "f32")
+        approx = O.topk_rows(s_hat, lim, k)
+        exact = O.topk_rows(O.exact_scores(q, keys), lim, k)
+        O.recall_hits(approx, exact)
+        n_pairs += int(lim.sum())
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": n_pairs / dt, "unit": "keys/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"query heads 0-{n_heads - 1} (KV group 0) of layer 0, all {spec.Q} query "
+                      f"rows each ({n_pairs} pairs): calibrate+codes+scores+top-{k}+exact "
+                      f"top-{k}+recall in float64 numpy; {dt:.1f} s; host os.cpu_count()="
+                      f"{os.cpu_count()}, BLAS threads={threads}"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1 "
+                                   "(multi-GPU sharding is described in the design notes)"}))
+        sys.exit(2)
+    import torch
+    import workloads as W
+    from paper_2608_03228_amd import saki as S
+
+    spec = W.SPECS[args.workload]
+    if spec.layers != 1 or spec.batch != 1 or spec.steps != 1:
+        raise SystemExit(f"bench runs single-layer, single-step workloads; {args.workload} is not")
+    r, sk, k = args.r, args.sketch, args.k
+    dev = torch.device("cuda:0")
+    inp = W.make_layer(spec)
+    keys = torch.from_numpy(inp["keys"]).to(dev)
+    q = torch.from_numpy(inp["queries"]).to(dev)
+    pos = torch.from_numpy(inp["q_pos"]).to(dev) if inp["q_pos"] is not None else None
+    B, H_kv, N, d = keys.shape
+    H_q = spec.H_q
+    # device buffers allocated once, reused by every step
+    index = torch.empty(S.saki_index_bytes(B, H_q, N, r, sk), dtype=torch.uint8, device=dev)
+    ws = torch.empty(max(1, S.saki_score_topk_workspace_bytes(B, H_q, spec.Q, N, r, k, sk)),
+                     dtype=torch.uint8, device=dev)
+    wsr = torch.empty(max(1, S.saki_recall_workspace_bytes(B, H_q, spec.Q, N, d, k)),
+                      dtype=torch.uint8, device=dev)
+    top_idx = torch.empty((B, H_q, spec.Q, k), dtype=torch.int32, device=dev)
+    top_sc = torch.empty((B, H_q, spec.Q, k), dtype=torch.float32, device=dev)
+    hits = torch.empty((B, H_q, spec.Q), dtype=torch.int32, device=dev)
+    f_dev = {n: torch.empty(s, dtype=torch.float32, device=dev)
+             for n, s in (("B_q", (H_q, d, r)), ("B_k", (H_q, d, r)), ("mu", (H_kv, d)))}
+    host_f = {n: torch.empty(t.shape, dtype=torch.float32).pin_memory() for n, t in f_dev.items()}
+
+    ev = {}
+
+    def step(timed_stages=False):
+        cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], r)
+        for n in f_dev:
+            host_f[n].numpy()[...] = cal[n]
+            f_dev[n].copy_(host_f[n], non_blocking=True)
+        if timed_stages:
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            e[0].record()
+        S.saki_build_index(keys, f_dev["B_k"], f_dev["mu"], r, sk, H_q, index=index)
+        if timed_stages:
+            e[1].record()
+        S.saki_score_topk(index, sk, q, f_dev["B_q"], f_dev["mu"], H_kv, N, N, r, q_pos=pos,
+                          k=k, ws=ws, top_idx=top_idx, top_score=top_sc)
+        if timed_stages:
+            e[2].record()
+        S.saki_recall(keys, q, top_idx, N, q_pos=pos, k=k, ws=wsr, hits=hits,
+                      want_exact=False)
+        if timed_stages:
+            e[3].record()
+            ev.setdefault("list", []).append(e)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / args.steps
+
+    # stage timing with HIP events on the launch stream (separate pass)
+    for _ in range(args.steps):
+        step(timed_stages=True)
+    torch.cuda.synchronize()
+    names = ["build", "score_topk", "recall"]
+    stage_ms = {n: float(np.mean([es[i].elapsed_time(es[i + 1]) for es in ev["list"]]))
+                for i, n in enumerate(names)}
+    t_cal = time.perf_counter()
+    for _ in range(3):
+        S.saki_calibrate(inp["q_cal"], inp["k_cal"], r)
+    stage_ms["calibrate_host"] = (time.perf_counter() - t_cal) / 3 * 1e3
+
+    h = hits.cpu().numpy().astype(np.int64)
+    per_head = h.sum(axis=(0, 2)) / (k * spec.Q)
+    last512 = h[:, :, -512:].sum(axis=(0, 2)) / (k * min(512, spec.Q))
+    pairs = candidates(spec, N)
+
+    terms = roofline_terms(spec, r, sk, k)
+    dom = max(names, key=lambda n: stage_ms[n])
+    t = terms[dom]
+    sec = stage_ms[dom] / 1e3
+    t_hbm = t["bytes"] / (PEAK["hbm_GBps"] * 1e9)
+    t_fl = t["flops"] / (t["peak_flops"] * 1e12)
+    if t_hbm >= t_fl:
+        roof = {"bound": "hbm", "achieved": t["bytes"] / sec / 1e9, "peak": PEAK["hbm_GBps"],
+                "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma" if t["flop_unit"] != "fp64" else "alu",
+                "achieved": t["flops"] / sec / 1e12, "peak": t["peak_flops"], "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = dom
+    roof["work"] = {"bytes": t["bytes"], "flops": t["flops"], "flop_dtype": t["flop_unit"]}
+    others = {}
+    for n in names:
+        tt = terms[n]
+        s_n = stage_ms[n] / 1e3
+        others[n] = {"ms": stage_ms[n], "GB/s": tt["bytes"] / s_n / 1e9,
+                     "TFLOP/s": tt["flops"] / s_n / 1e12,
+                     "frac_hbm": tt["bytes"] / s_n / 1e9 / PEAK["hbm_GBps"],
+                     "frac_flops": tt["flops"] / s_n / 1e12 / tt["peak_flops"]}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(inp, r, sk, k, args.cpu_heads)
+
+    out = {
+        "metric": METRIC, "value": pairs / dt, "unit": "keys/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": dt * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": sk,
+        "data": "synthetic",
+        "config": {"workload": spec.name, "H_q": H_q, "H_kv": spec.H_kv, "d": spec.d,
+                   "latent_D": spec.D, "N": N, "queries_per_head": spec.Q,
+                   "causal": spec.causal, "r": r, "sketch": sk, "k": k, "calib_tokens": spec.T,
+                   "pairs_per_step": pairs},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "stages_ms": stage_ms,
+        "stage_rooflines": others,
+        "recall_at_64": {"median_over_heads": float(np.median(per_head)),
+                         "mean_over_heads": float(np.mean(per_head)),
+                         "last512_median": float(np.median(last512)),
+                         "hits_total": int(h.sum())},
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,90 @@
+// Internal layout and launch planning shared by the host helpers and the HIP
+// launchers of libsaki.  Not part of the public ABI.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+
+namespace saki {
+
+constexpr int kHeadDim = 128;  // d on the GPU path
+constexpr int kMaxK = 64;      // top-k lists hold 64 entries, one per wave lane
+constexpr int kTile = 64;      // keys per index tile
+constexpr int kChunkBytes = 16;
+
+inline bool rank_supported(int r) { return r == 16 || r == 32 || r == 64 || r == 128; }
+inline int elem_bytes(int dtype) { return dtype == 1 ? 2 : 4; }
+inline size_t n_tiles(int N) { return ((size_t)N + kTile - 1) / kTile; }
+inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Index layout, per (sequence b, query head h): tiles of 64 keys; inside a
+// tile, the code of key t is cut into 16-byte pieces and piece p of all 64
+// keys is stored contiguously:
+//   byte offset = ((b*H_q + h)*n_tiles + tile)*64*r*es + p*64*16 + t*16 + e*es
+// so a wave that reads piece p of 64 consecutive keys reads 1 KiB contiguously.
+inline size_t tile_bytes(int r, int dtype) { return (size_t)kTile * r * elem_bytes(dtype); }
+inline size_t index_bytes(int B, int H_q, int N_cap, int r, int dtype) {
+  return (size_t)B * H_q * n_tiles(N_cap) * tile_bytes(r, dtype);
+}
+
+// How saki_score_topk / saki_recall split the work.  Each wave owns `rows`
+// consecutive query rows of one (b, h) and one key chunk; when a row's keys
+// are split over several chunks each chunk writes a partial top-64 to the
+// workspace and a merge pass reduces them.
+struct Plan {
+  int rows = 1;        // query rows per wave
+  int waves = 1;       // waves per workgroup
+  int row_blocks = 0;  // workgroups along the query axis
+  int chunk = kTile;   // keys per chunk (multiple of 64)
+  int n_chunks = 1;
+  size_t z_off = 0, b_off = 0, part_off = 0, ws_bytes = 0;
+};
+
+inline Plan make_plan(int B, int H_q, int Q, int N_valid, int part_entry_bytes) {
+  Plan p;
+  p.rows = Q >= 4 ? 4 : 1;
+  const int wave_rows = (Q + p.rows - 1) / p.rows;
+  p.waves = wave_rows < 4 ? (wave_rows < 1 ? 1 : wave_rows) : 4;
+  p.row_blocks = (Q + p.rows * p.waves - 1) / (p.rows * p.waves);
+  const size_t total_waves = (size_t)B * H_q * wave_rows;
+  const size_t n = N_valid > 0 ? (size_t)N_valid : 1;
+  size_t chunk = round_up(n, kTile);
+  const size_t target = 8192;  // waves wanted in flight over the whole GPU
+  if (total_waves > 0 && total_waves < target) {
+    const size_t want = (target + total_waves - 1) / total_waves;
+    size_t c = round_up((n + want - 1) / want, kTile);
+    if (c < 2048) c = 2048;
+    if (c < chunk) chunk = c;
+  }
+  p.chunk = (int)chunk;
+  p.n_chunks = (int)((n + chunk - 1) / chunk);
+  const size_t rows_total = (size_t)B * H_q * Q;
+  size_t off = 0;
+  if (p.n_chunks > 1) {
+    p.part_off = off;
+    off = round_up(off + rows_total * p.n_chunks * kMaxK * part_entry_bytes, 256);
+  }
+  p.ws_bytes = off;
+  return p;
+}
+
+// Score path: query sketch z [rows, r] and mean term b [rows] (float32) come
+// first in the workspace, then the partial lists (float score + int index).
+inline Plan score_plan(int B, int H_q, int Q, int N_valid, int r) {
+  Plan p = make_plan(B, H_q, Q, N_valid, 8);
+  const size_t rows_total = (size_t)B * H_q * Q;
+  p.z_off = 0;
+  p.b_off = round_up(rows_total * r * sizeof(float), 256);
+  const size_t base = round_up(p.b_off + rows_total * sizeof(float), 256);
+  if (p.n_chunks > 1) p.part_off = base;
+  p.ws_bytes = base + p.ws_bytes;
+  return p;
+}
+
+// Recall path: partial lists hold a double score and an int index (16 bytes
+// with padding).
+inline Plan recall_plan(int B, int H_q, int Q, int N_valid) {
+  return make_plan(B, H_q, Q, N_valid, 16);
+}
+
+}  // namespace saki

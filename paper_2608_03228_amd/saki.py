@@ -1,0 +1,254 @@
+"""Python binding of libsaki (ctypes).  Argument marshalling only.
+
+Each function has the name of the C entry point it calls (include/saki.h)
+and does no arithmetic of its own: host functions take and return numpy
+arrays, GPU functions take torch CUDA tensors (torch supplies device memory
+and the current HIP stream) and enqueue the library's kernels on that
+stream.  If the shared library is missing, every call raises: there is no
+fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsaki.so")
+_lib = None
+
+F32, BF16 = 0, 1
+METHOD_OPT, METHOD_KEY_PCA = 0, 1
+_DTYPES = {"f32": F32, "bf16": BF16}
+_METHODS = {"opt": METHOD_OPT, "key_pca": METHOD_KEY_PCA}
+
+
+class SakiError(RuntimeError):
+    def __init__(self, fn, status):
+        super().__init__(f"{fn} failed with status {status}: {saki_status_string(status)}")
+        self.status = status
+
+
+def lib():
+    """Load libsaki.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(f"{_LIB_PATH} is missing; build it with "
+                           "`python -m paper_2608_03228_amd.build`")
+    L = C.CDLL(_LIB_PATH)
+    vp, ip, dp = C.c_void_p, C.c_int, C.c_double
+    sz = C.c_size_t
+    sig = {
+        "saki_status_string": (C.c_char_p, [ip]),
+        "saki_version": (ip, []),
+        "saki_calibrate": (ip, [vp, vp, ip, ip, ip, ip, ip, ip, dp, vp, vp, vp, vp, vp, ip]),
+        "saki_weight_svd_factors": (ip, [vp, ip, ip, ip, ip, ip, vp, vp]),
+        "saki_sym_eig": (ip, [ip, vp, vp, vp]),
+        "saki_index_bytes": (sz, [ip, ip, ip, ip, ip]),
+        "saki_build_index": (ip, [vp, ip, ip, ip, ip, ip, ip, ip, vp, vp, ip, vp, sz, ip, ip, vp]),
+        "saki_index_export": (ip, [vp, ip, ip, ip, ip, ip, vp, vp]),
+        "saki_score_topk_workspace_bytes": (sz, [ip, ip, ip, ip, ip, ip, ip]),
+        "saki_score_topk": (ip, [vp, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, ip, vp, vp, ip,
+                                 vp, vp, vp, sz, vp]),
+        "saki_recall_workspace_bytes": (sz, [ip, ip, ip, ip, ip, ip]),
+        "saki_recall": (ip, [vp, ip, vp, vp, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, vp, vp,
+                             sz, vp]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def saki_status_string(status: int) -> str:
+    return lib().saki_status_string(int(status)).decode()
+
+
+def saki_version() -> int:
+    return lib().saki_version()
+
+
+def _check(fn, status):
+    if status != 0:
+        raise SakiError(fn, status)
+
+
+def _host(a, dtype):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data_as(C.c_void_p)
+
+
+# ------------------------------------------------------------------ host calls
+
+def saki_calibrate(q_cal, k_cal, r: int, method: str = "opt", floor_rel: float = 1e-6,
+                   n_threads: int = 0):
+    """q_cal [H_q, T, d], k_cal [H_kv, T, d] (float32) -> dict of numpy arrays
+    B_q, B_k [H_q, d, r] float32, mu [H_kv, d] float32, sigma [H_q, d] float64,
+    n_clamped [H_q, 2] int32."""
+    q, qp = _host(q_cal, np.float32)
+    k, kp = _host(k_cal, np.float32)
+    if q.ndim != 3 or k.ndim != 3 or q.shape[1:] != k.shape[1:]:
+        raise ValueError("q_cal [H_q, T, d] and k_cal [H_kv, T, d] must agree in T and d")
+    H_q, T, d = q.shape
+    H_kv = k.shape[0]
+    B_q = np.empty((H_q, d, r), np.float32)
+    B_k = np.empty((H_q, d, r), np.float32)
+    mu = np.empty((H_kv, d), np.float32)
+    sigma = np.empty((H_q, d), np.float64)
+    ncl = np.empty((H_q, 2), np.int32)
+    st = lib().saki_calibrate(qp, kp, H_q, H_kv, T, d, int(r), _METHODS[method],
+                              float(floor_rel), B_q.ctypes.data, B_k.ctypes.data,
+                              mu.ctypes.data, sigma.ctypes.data, ncl.ctypes.data,
+                              int(n_threads))
+    _check("saki_calibrate", st)
+    return {"B_q": B_q, "B_k": B_k, "mu": mu, "sigma": sigma, "n_clamped": ncl}
+
+
+def saki_weight_svd_factors(W_K, H_q: int, r: int):
+    """W_K [H_kv, d, D] (float64) -> (B_q, B_k) [H_q, d, r] float32."""
+    w, wp = _host(W_K, np.float64)
+    H_kv, d, D = w.shape
+    B_q = np.empty((H_q, d, r), np.float32)
+    B_k = np.empty((H_q, d, r), np.float32)
+    _check("saki_weight_svd_factors",
+           lib().saki_weight_svd_factors(wp, int(H_q), H_kv, d, D, int(r), B_q.ctypes.data,
+                                         B_k.ctypes.data))
+    return B_q, B_k
+
+
+def saki_sym_eig(A):
+    """Symmetric A [n, n] (float64) -> (w ascending [n], V [n, n] columns)."""
+    a, ap = _host(A, np.float64)
+    n = a.shape[0]
+    w = np.empty(n, np.float64)
+    V = np.empty((n, n), np.float64)
+    _check("saki_sym_eig", lib().saki_sym_eig(n, ap, w.ctypes.data, V.ctypes.data))
+    return w, V
+
+
+def saki_index_bytes(B: int, H_q: int, N_cap: int, r: int, sketch: str) -> int:
+    return int(lib().saki_index_bytes(B, H_q, N_cap, r, _DTYPES[sketch]))
+
+
+def saki_score_topk_workspace_bytes(B, H_q, Q, N_valid, r, k, sketch) -> int:
+    return int(lib().saki_score_topk_workspace_bytes(B, H_q, Q, N_valid, r, k,
+                                                     _DTYPES[sketch]))
+
+
+def saki_recall_workspace_bytes(B, H_q, Q, N_valid, d, k) -> int:
+    return int(lib().saki_recall_workspace_bytes(B, H_q, Q, N_valid, d, k))
+
+
+# ------------------------------------------------------------------ GPU calls
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dev(t, dtypes, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _key_dtype(keys):
+    torch = _torch()
+    return BF16 if keys.dtype == torch.bfloat16 else F32
+
+
+def saki_build_index(keys, B_k, mu, r: int, sketch: str, H_q: int, index=None,
+                     n_begin: int = 0, n_count=None, stream=None):
+    """keys [B, H_kv, N_cap, d] (float32 or bfloat16), B_k [H_q, d, r], mu
+    [H_kv, d] (float32, CUDA).  Returns the index buffer (uint8 CUDA tensor),
+    allocated if not given."""
+    torch = _torch()
+    kp = _dev(keys, (torch.float32, torch.bfloat16), "keys")
+    B, H_kv, N_cap, d = keys.shape
+    nbytes = saki_index_bytes(B, H_q, N_cap, r, sketch)
+    if index is None:
+        index = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=keys.device)
+    n_count = N_cap - n_begin if n_count is None else n_count
+    st = lib().saki_build_index(
+        kp, _key_dtype(keys), B, int(H_q), H_kv, N_cap, d, int(r),
+        _dev(B_k, (torch.float32,), "B_k"), _dev(mu, (torch.float32,), "mu"),
+        _DTYPES[sketch], _dev(index, (torch.uint8,), "index"), index.numel(),
+        int(n_begin), int(n_count), _stream(stream))
+    _check("saki_build_index", st)
+    return index
+
+
+def saki_index_export(index, sketch: str, B: int, H_q: int, N_cap: int, r: int, stream=None):
+    torch = _torch()
+    out = torch.empty((B, H_q, N_cap, r), dtype=torch.float32, device=index.device)
+    st = lib().saki_index_export(_dev(index, (torch.uint8,), "index"), _DTYPES[sketch], B, H_q,
+                                 N_cap, r, out.data_ptr(), _stream(stream))
+    _check("saki_index_export", st)
+    return out
+
+
+def saki_score_topk(index, sketch: str, q, B_q, mu, H_kv: int, N_cap: int, N_valid: int,
+                    r: int, q_pos=None, k: int = 64, ws=None, top_idx=None, top_score=None,
+                    with_scores: bool = True, stream=None):
+    """q [B, H_q, Q, d] float32 CUDA; q_pos [Q] int32 CUDA or None.  Returns
+    (top_idx [B, H_q, Q, k] int32, top_score float32 or None)."""
+    torch = _torch()
+    qp = _dev(q, (torch.float32,), "q")
+    B, H_q, Q, d = q.shape
+    need = saki_score_topk_workspace_bytes(B, H_q, Q, N_valid, r, k, sketch)
+    if ws is None:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    if top_idx is None:
+        top_idx = torch.empty((B, H_q, Q, k), dtype=torch.int32, device=q.device)
+    if with_scores and top_score is None:
+        top_score = torch.empty((B, H_q, Q, k), dtype=torch.float32, device=q.device)
+    pos = _dev(q_pos, (torch.int32,), "q_pos") if q_pos is not None else None
+    st = lib().saki_score_topk(
+        _dev(index, (torch.uint8,), "index"), _DTYPES[sketch], B, H_q, int(H_kv), int(N_cap),
+        int(N_valid), d, int(r), qp, pos, Q, _dev(B_q, (torch.float32,), "B_q"),
+        _dev(mu, (torch.float32,), "mu"), int(k), _dev(top_idx, (torch.int32,), "top_idx"),
+        _dev(top_score, (torch.float32,), "top_score") if with_scores else None,
+        _dev(ws, (torch.uint8,), "ws"), ws.numel(), _stream(stream))
+    _check("saki_score_topk", st)
+    return top_idx, (top_score if with_scores else None)
+
+
+def saki_recall(keys, q, approx_idx, N_valid: int, q_pos=None, k: int = 64, ws=None,
+                hits=None, exact_idx=None, want_exact: bool = True, stream=None):
+    """keys [B, H_kv, N_cap, d], q [B, H_q, Q, d], approx_idx [B, H_q, Q, k]
+    (CUDA).  Returns (hits [B, H_q, Q] int32, exact_idx [B, H_q, Q, k] or None)."""
+    torch = _torch()
+    kp = _dev(keys, (torch.float32, torch.bfloat16), "keys")
+    qp = _dev(q, (torch.float32,), "q")
+    B, H_kv, N_cap, d = keys.shape
+    _, H_q, Q, _ = q.shape
+    need = saki_recall_workspace_bytes(B, H_q, Q, N_valid, d, k)
+    if ws is None:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    if hits is None:
+        hits = torch.empty((B, H_q, Q), dtype=torch.int32, device=q.device)
+    if want_exact and exact_idx is None:
+        exact_idx = torch.empty((B, H_q, Q, k), dtype=torch.int32, device=q.device)
+    pos = _dev(q_pos, (torch.int32,), "q_pos") if q_pos is not None else None
+    st = lib().saki_recall(
+        kp, _key_dtype(keys), qp, pos, B, H_q, H_kv, N_cap, int(N_valid), Q, d, int(k),
+        _dev(approx_idx, (torch.int32,), "approx_idx"), _dev(hits, (torch.int32,), "hits"),
+        _dev(exact_idx, (torch.int32,), "exact_idx") if want_exact else None,
+        _dev(ws, (torch.uint8,), "ws"), ws.numel(), _stream(stream))
+    _check("saki_recall", st)
+    return hits, (exact_idx if want_exact else None)

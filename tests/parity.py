@@ -1,0 +1,104 @@
+"""Parity rules between the GPU path and the oracle (helpers for the tests).
+
+Per-score tolerance.  A sketch score computed in float32 from (q, k) through
+the factors has a rounding error bounded by a small multiple of unit roundoff
+times S_ij = (|B_q|^T|q_i|) . (|B_k|^T|k_j - mu|) + |q_i|^T|mu|
+(oracle.score_scale); the GPU must agree with the oracle within
+eps_ij = tol * S_ij, tol = 1e-5 for float32 sketches.  bf16 sketches are
+compared (a) with the exact oracle at tol = 2e-2 and (b) with the
+bf16-emulating oracle at tol = 1e-5, where eps_ij also admits a one-ulp bf16
+difference in any code or query-sketch element whose exact value lies within
+the float32 computation error of a bf16 rounding midpoint (the GPU and the
+oracle may round such an element to different neighbours; both are correct).
+
+Top-k sets.  Following Proposition 2, when the oracle's k-th and (k+1)-th
+scores are closer than the sum of their tolerances, several sets are correct:
+every swap between the GPU set G and the oracle set L must be explainable,
+max_{l in L\\G}(s_l - eps_l) <= min_{j in G\\L}(s_j + eps_j).  Rows with a wider
+margin must match exactly.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle as O
+
+TOL_F32 = 1e-5
+TOL_BF16_EXACT = 2e-2
+AMBIG_REL = 1e-5  # bound on the float32 computation error of one element, relative
+                  # to its absolute-value sum
+
+
+def _bf16_ambiguity(exact, abs_sum):
+    """Elements whose bf16 rounding may legitimately differ, and the size of
+    one bf16 ulp at each element."""
+    r = O.bf16_round(exact)
+    mag = np.maximum(np.abs(exact), 1e-300)
+    ulp = np.exp2(np.ceil(np.log2(mag)) - 7.0)
+    dist_mid = np.abs(0.5 * ulp - np.abs(exact - r))
+    amb = dist_mid <= AMBIG_REL * abs_sum + 2.0 ** -24 * mag
+    return amb, ulp
+
+
+def oracle_head(B_q, B_k, mu, q, keys, mode: str):
+    """Oracle scores and per-score tolerances of one head.
+
+    mode: "f32" (exact codes, tol 1e-5), "bf16_exact" (exact codes, tol 2e-2),
+    "bf16_emul" (bf16-rounded codes and z, tol 1e-5 plus ambiguity).
+    Returns (s [Q, N], eps [Q, N])."""
+    q = np.asarray(q, np.float64)
+    keys = np.asarray(keys, np.float64)
+    S = O.score_scale(B_q, B_k, mu, q, keys)
+    if mode in ("f32", "bf16_exact"):
+        s, *_ = O.index_scores(B_q, B_k, mu, q, keys, "f64")
+        return s, (TOL_F32 if mode == "f32" else TOL_BF16_EXACT) * S
+    assert mode == "bf16_emul"
+    s, z, b, c = O.index_scores(B_q, B_k, mu, q, keys, "bf16")
+    c_ex = O.codes(B_k, mu, keys)
+    z_ex, _ = O.query_sketch(B_q, mu, q)
+    amb_c, ulp_c = _bf16_ambiguity(c_ex, np.abs(keys - mu) @ np.abs(B_k))
+    amb_z, ulp_z = _bf16_ambiguity(z_ex, np.abs(q) @ np.abs(B_q))
+    extra = np.abs(z) @ (amb_c * ulp_c).T + (amb_z * ulp_z) @ np.abs(c).T
+    return s, TOL_F32 * S + extra
+
+
+def check_rows(gpu_idx, gpu_score, s, eps, limits, k):
+    """Validate GPU top-k rows against oracle scores.  Raises AssertionError
+    with the first offending row; returns (rows, exempt rows, differing rows)."""
+    n_exempt = n_diff = 0
+    for i in range(s.shape[0]):
+        lim = int(limits[i])
+        m = min(k, lim)
+        gi = np.asarray(gpu_idx[i])
+        assert np.all(gi[m:] == -1), f"row {i}: expected {k - m} pads"
+        G = gi[:m]
+        assert np.all((G >= 0) & (G < lim)), f"row {i}: index out of range {G}"
+        assert len(set(G.tolist())) == m, f"row {i}: duplicate indices"
+        if gpu_score is not None:
+            gs = np.asarray(gpu_score[i], np.float64)
+            assert np.all(np.isneginf(gs[m:])), f"row {i}: pad scores"
+            err = np.abs(gs[:m] - s[i, G])
+            bad = err > eps[i, G]
+            assert not bad.any(), (f"row {i}: score error {err[bad][:4]} > eps "
+                                   f"{eps[i, G][bad][:4]} at idx {G[bad][:4]}")
+            for a in range(m - 1):  # sorted by (score desc, index asc)
+                assert gs[a] > gs[a + 1] or (gs[a] == gs[a + 1] and G[a] < G[a + 1]), \
+                    f"row {i}: order at {a}"
+        full = O.topk_row(s[i], lim, min(k + 1, lim))
+        L = full[:m]
+        exempt = False
+        if lim > k:
+            a, b = full[k - 1], full[k]
+            exempt = (s[i, a] - s[i, b]) <= eps[i, a] + eps[i, b]
+        n_exempt += exempt
+        sG, sL = set(G.tolist()), set(L.tolist())
+        if sG == sL:
+            continue
+        n_diff += 1
+        assert exempt, f"row {i}: sets differ on a non-exempt row"
+        out = np.array(sorted(sL - sG))
+        inn = np.array(sorted(sG - sL))
+        lo_out = np.max(s[i, out] - eps[i, out])
+        hi_in = np.min(s[i, inn] + eps[i, inn])
+        assert lo_out <= hi_in, f"row {i}: unexplainable swap {out} <-> {inn}"
+    return s.shape[0], n_exempt, n_diff

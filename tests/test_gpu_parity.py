@@ -1,0 +1,319 @@
+"""GPU parity: libsaki's HIP path against the float64 oracle on identical
+seeded inputs.  Every GPU call goes through the C ABI (ctypes binding)."""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from tests.parity import check_rows, oracle_head
+
+torch = pytest.importorskip("torch")
+S = pytest.importorskip("paper_2608_03228_amd.saki")
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _t(a, dtype=torch.float32):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV, dtype)
+
+
+def gpu_pipeline(inp, r, sketch, k=64, method="opt", factors=None, keys_bf16=False,
+                 N_valid=None, q_pos=None):
+    """Calibrate on the host library, build the index and score on the GPU.
+    Returns dict with numpy top_idx, top_score and the library's factors."""
+    spec = inp["spec"]
+    if factors is None:
+        cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], r, method=method)
+        B_q, B_k, mu = cal["B_q"], cal["B_k"], cal["mu"]
+    else:
+        B_q, B_k, mu = factors
+    keys = _t(inp["keys"], torch.bfloat16 if keys_bf16 else torch.float32)
+    q = _t(inp["queries"])
+    B, H_kv, N_cap, d = keys.shape
+    N_valid = N_cap if N_valid is None else N_valid
+    pos = inp["q_pos"] if q_pos is None else q_pos
+    pos_t = _t(pos, torch.int32) if pos is not None else None
+    index = S.saki_build_index(keys, _t(B_k), _t(mu), r, sketch, spec.H_q)
+    idx, sc = S.saki_score_topk(index, sketch, q, _t(B_q), _t(mu), H_kv, N_cap, N_valid, r,
+                                q_pos=pos_t, k=k)
+    torch.cuda.synchronize()
+    return {"idx": idx.cpu().numpy(), "score": sc.cpu().numpy(), "index": index,
+            "keys": keys, "q": q, "pos": pos_t, "B_q": B_q, "B_k": B_k, "mu": mu}
+
+
+def oracle_factors(inp, h, r):
+    G = inp["spec"].H_q // inp["spec"].H_kv
+    oc = O.saki_calibrate(inp["q_cal"][h], inp["k_cal"][h // G], r)
+    return oc["B_q"], oc["B_k"], oc["mu"]
+
+
+def check_head(inp, out, b, h, r, mode, rows=None, k=64, N_valid=None, factors=None,
+               keys_override=None):
+    spec = inp["spec"]
+    G = spec.H_q // spec.H_kv
+    Bq, Bk, mu = factors if factors is not None else oracle_factors(inp, h, r)
+    keys = inp["keys"][b, h // G] if keys_override is None else keys_override
+    N = keys.shape[0] if N_valid is None else N_valid
+    rows = np.arange(spec.Q) if rows is None else np.asarray(rows)
+    q = inp["queries"][b, h][rows]
+    s, eps = oracle_head(Bq, Bk, mu, q, keys[:N], mode)
+    pos = inp["q_pos"][rows] if inp["q_pos"] is not None else None
+    lim = O.candidate_limits(len(rows), N, pos)
+    return check_rows(out["idx"][b, h][rows], out["score"][b, h][rows], s, eps, lim, k)
+
+
+def test_single_head_f32_full():
+    """1 head, d=128, r=32, N=1024, 256 fresh queries, no mask, fp32 sketches."""
+    inp = W.make_layer(W.SPECS["single_head_d128"])
+    out = gpu_pipeline(inp, 32, "f32")
+    n, ex, diff = check_head(inp, out, 0, 0, 32, "f32")
+    print(f"rows {n} exempt {ex} differing {diff}")
+    assert n == 256 and diff <= ex
+
+
+def test_codes_match_oracle():
+    """Exported codes vs oracle codes (float32 storage), and bf16 storage is a
+    correct rounding of them."""
+    spec = W.SPECS["llama31_8b_layer"].with_(N=1000, Q=8, q_start=64)
+    inp = W.make_layer(spec)
+    for sketch in ("f32", "bf16"):
+        out = gpu_pipeline(inp, 32, sketch, N_valid=1000)
+        codes = S.saki_index_export(out["index"], sketch, 1, spec.H_q, 1000, 32)
+        codes = codes.cpu().numpy()
+        for h in (0, 17, 31):
+            g = h // 4
+            Bk = out["B_k"][h].astype(np.float64)
+            kc = inp["keys"][0, g].astype(np.float64) - out["mu"][g]
+            exact = kc @ Bk
+            scale = np.abs(kc) @ np.abs(Bk)
+            got = codes[0, h]
+            if sketch == "f32":
+                assert np.max(np.abs(got - exact) / scale) < 1e-5
+            else:
+                assert np.all(O.bf16_round(got) == got)  # representable in bf16
+                ulp = np.exp2(np.ceil(np.log2(np.maximum(np.abs(exact), 1e-30))) - 7)
+                assert np.all(np.abs(got - exact) <= 0.5 * ulp + 1e-5 * scale)
+
+
+@pytest.mark.parametrize("r", [16, 32, 64])
+@pytest.mark.parametrize("sketch", ["f32", "bf16"])
+def test_llama_layer_causal(r, sketch):
+    """One LLaMA-3.1-8B-shaped layer: 32 query / 8 KV heads, N=4096, causal
+    rows at positions 64..4095; all rows on the GPU, sampled rows of three
+    heads against the oracle."""
+    inp = W.make_layer(W.SPECS["llama31_8b_layer"])
+    out = gpu_pipeline(inp, r, sketch)
+    rng = np.random.default_rng(r)
+    rows = np.unique(np.concatenate([[0, 1, 2, 63, 64, 4031], rng.choice(4032, 90, False)]))
+    modes = ["f32"] if sketch == "f32" else ["bf16_emul", "bf16_exact"]
+    for h in (0, 13, 31):
+        for mode in modes:
+            n, ex, diff = check_head(inp, out, 0, h, r, mode, rows=rows)
+            print(f"h{h} {mode}: rows {n} exempt {ex} differing {diff}")
+
+
+def test_ragged_causal_all_rows():
+    """N = 1000 (not a multiple of 64), causal, every row of two heads checked,
+    including rows with fewer than 64 visible keys (padded output)."""
+    spec = W.SPECS["llama31_8b_layer"].with_(N=1000, Q=1000, q_start=0)
+    inp = W.make_layer(spec)
+    out = gpu_pipeline(inp, 32, "f32")
+    for h in (0, 30):
+        check_head(inp, out, 0, h, 32, "f32")
+    assert np.all(out["idx"][0, 0, 0, 1:] == -1) and out["idx"][0, 0, 0, 0] == 0
+    assert np.all(np.isneginf(out["score"][0, 0, 10, 11:]))
+
+
+def test_rank_equals_d_recovers_exact_ranking():
+    """r = d: M_d = I, so sketch scores are exact q.k up to float32 rounding,
+    and recall is 1 on every row whose 64/65 margin exceeds that rounding."""
+    spec = W.SPECS["single_head_d128"].with_(N=2048, Q=128)
+    inp = W.make_layer(spec)
+    out = gpu_pipeline(inp, 128, "f32")
+    q = inp["queries"][0, 0].astype(np.float64)
+    keys = inp["keys"][0, 0].astype(np.float64)
+    s = q @ keys.T
+    eps = 1e-5 * (np.abs(q) @ np.abs(keys).T + np.abs(q) @ np.abs(out["mu"][0])[:, None])
+    # the library's own factors give M = I to float32 precision; compare with exact scores
+    n, ex, diff = check_rows(out["idx"][0, 0], out["score"][0, 0], s, eps,
+                             np.full(128, 2048), 64)
+    hits, _ = S.saki_recall(out["keys"], out["q"], torch.from_numpy(out["idx"]).to(DEV),
+                            2048)
+    h = hits.cpu().numpy()[0, 0]
+    assert np.sum(h < 64) <= ex
+    print(f"r=d recall {h.mean() / 64:.6f}, exempt rows {ex}")
+
+
+def test_decode_split_chunks_and_merge():
+    """Q = 1 over a long context: the key range is split over many chunks and
+    the partial top-64 lists are merged.  Every head checked exactly."""
+    spec = W.SPECS["decode_1m"].with_(N=200_000, H_q=8, H_kv=2)
+    inp = W.make_layer(spec)
+    assert S.saki_score_topk_workspace_bytes(1, 8, 1, 200_000, 32, 64, "bf16") > 8 * 64 * 8
+    for sketch, mode in (("bf16", "bf16_emul"), ("f32", "f32")):
+        out = gpu_pipeline(inp, 32, sketch)
+        for h in range(8):
+            check_head(inp, out, 0, h, 32, mode)
+
+
+@pytest.mark.parametrize("k", [1, 10, 64])
+def test_small_k_is_prefix_of_top64(k):
+    spec = W.SPECS["single_head_d128"].with_(N=777, Q=33)
+    inp = W.make_layer(spec)
+    out = gpu_pipeline(inp, 16, "f32", k=k)
+    check_head(inp, out, 0, 0, 16, "f32", k=k)
+
+
+def test_exact_ties_go_to_lower_index():
+    """Duplicated keys give bit-identical codes and scores: the lower index
+    wins.  Constant keys make every score equal: indices 0..63 in order."""
+    spec = W.SPECS["single_head_d128"].with_(N=512, Q=16)
+    inp = W.make_layer(spec)
+    keys = inp["keys"].copy()
+    keys[0, 0, 256:] = keys[0, 0, :256]  # every key appears twice
+    inp2 = dict(inp, keys=keys)
+    out = gpu_pipeline(inp2, 32, "f32")
+    idx = out["idx"][0, 0]
+    for i in range(16):
+        row = set(idx[i].tolist())
+        for j in row:  # a duplicate's twin with the lower index is also selected
+            if j >= 256:
+                assert (j - 256) in row
+    const = np.tile(inp["keys"][0, 0, :1], (512, 1))[None, None]
+    inp3 = dict(inp, keys=const)
+    out = gpu_pipeline(inp3, 32, "f32")
+    assert np.all(out["idx"][0, 0] == np.arange(64)[None, :])
+
+
+def test_constant_calibration_keys():
+    """Calibration keys all equal: Sigma_k = 0 is replaced by the identity, the
+    cached keys equal the mean, every code is zero and all scores tie."""
+    spec = W.SPECS["single_head_d128"].with_(N=256, Q=8)
+    inp = W.make_layer(spec)
+    row = inp["k_cal"][0, :1]
+    inp2 = dict(inp, k_cal=np.tile(row, (spec.T, 1))[None],
+                keys=np.tile(row, (256, 1))[None, None])
+    out = gpu_pipeline(inp2, 32, "bf16")
+    assert np.all(out["idx"][0, 0] == np.arange(64)[None, :])
+
+
+def test_multi_sequence_gqa_bf16_keys_and_n_valid():
+    """B = 2 sequences, 4 query heads on 2 KV heads, bf16 keys, N_valid < N_cap
+    and a causal mask, exercising every index computation of the launch."""
+    spec = W.SPECS["qwen25_7b_decode"].with_(H_q=4, H_kv=2, N=700, Q=70, batch=2,
+                                             causal=True, q_start=600)
+    inp = W.make_layer(spec)
+    keys_bf = O.bf16_round(inp["keys"]).astype(np.float32)  # the bf16 keys are the input
+    inp_bf = dict(inp, keys=keys_bf)
+    out = gpu_pipeline(inp_bf, 64, "bf16", keys_bf16=True, N_valid=650)
+    for b in range(2):
+        for h in range(4):
+            check_head(inp_bf, out, b, h, 64, "bf16_emul", N_valid=650)
+
+
+def test_incremental_append_equals_full_build():
+    spec = W.SPECS["llama31_8b_layer"].with_(N=300, Q=4, q_start=64, H_q=8, H_kv=2)
+    inp = W.make_layer(spec)
+    cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32)
+    keys = _t(inp["keys"])
+    for sketch in ("f32", "bf16"):
+        full = S.saki_build_index(keys, _t(cal["B_k"]), _t(cal["mu"]), 32, sketch, 8)
+        inc = torch.zeros_like(full)
+        S.saki_build_index(keys, _t(cal["B_k"]), _t(cal["mu"]), 32, sketch, 8, index=inc,
+                           n_begin=0, n_count=290)
+        for n in range(290, 300):
+            S.saki_build_index(keys, _t(cal["B_k"]), _t(cal["mu"]), 32, sketch, 8, index=inc,
+                               n_begin=n, n_count=1)
+        a = S.saki_index_export(full, sketch, 1, 8, 300, 32)
+        c = S.saki_index_export(inc, sketch, 1, 8, 300, 32)
+        assert torch.equal(a, c)
+
+
+def test_empty_and_degenerate_sizes():
+    spec = W.SPECS["single_head_d128"].with_(N=128, Q=5)
+    inp = W.make_layer(spec)
+    out = gpu_pipeline(inp, 32, "f32", N_valid=0)
+    assert np.all(out["idx"] == -1) and np.all(np.isneginf(out["score"]))
+    out = gpu_pipeline(inp, 32, "f32", N_valid=1)
+    assert np.all(out["idx"][0, 0, :, 0] == 0) and np.all(out["idx"][0, 0, :, 1:] == -1)
+    hits, ex = S.saki_recall(out["keys"], out["q"], torch.from_numpy(out["idx"]).to(DEV), 1)
+    assert np.all(hits.cpu().numpy() == 1)
+
+
+def test_recall_kernel_matches_oracle():
+    """saki_recall on approximate sets that come from the oracle (not from the
+    GPU): exact top-64 and hit counts identical to the oracle's."""
+    spec = W.SPECS["llama31_8b_layer"].with_(N=1500, Q=1500 - 64, H_q=4, H_kv=1)
+    inp = W.make_layer(spec)
+    rng = np.random.default_rng(0)
+    approx = np.empty((1, 4, spec.Q, 64), np.int32)
+    exact = np.empty_like(approx)
+    lim = O.candidate_limits(spec.Q, 1500, inp["q_pos"])
+    for h in range(4):
+        s_ex = O.exact_scores(inp["queries"][0, h], inp["keys"][0, 0])
+        exact[0, h] = O.topk_rows(s_ex, lim)
+        Bq, Bk, mu = oracle_factors(inp, h, 16)
+        s_hat, *_ = O.index_scores(Bq, Bk, mu, inp["queries"][0, h], inp["keys"][0, 0])
+        approx[0, h] = O.topk_rows(s_hat, lim)
+    approx[0, 3, :100] = rng.integers(-1, 1500, (100, 64))  # arbitrary sets, with pads
+    want = O.recall_hits(approx, exact)
+    hits, ex = S.saki_recall(_t(inp["keys"]), _t(inp["queries"]), _t(approx, torch.int32),
+                             1500, q_pos=_t(inp["q_pos"], torch.int32))
+    np.testing.assert_array_equal(ex.cpu().numpy(), exact)
+    np.testing.assert_array_equal(hits.cpu().numpy(), want)
+
+
+def test_recall_split_chunks_matches_oracle():
+    spec = W.SPECS["decode_1m"].with_(N=150_000, H_q=4, H_kv=1, Q=3)
+    inp = W.make_layer(spec)
+    exact = np.stack([O.topk_rows(O.exact_scores(inp["queries"][0, h], inp["keys"][0, 0]),
+                                  O.candidate_limits(3, 150_000)) for h in range(4)])[None]
+    approx = np.roll(exact, 7, axis=-2).astype(np.int32)  # other rows' sets
+    approx[..., :5] = exact[..., :5]
+    hits, ex = S.saki_recall(_t(inp["keys"]), _t(inp["queries"]), _t(approx, torch.int32),
+                             150_000)
+    np.testing.assert_array_equal(ex.cpu().numpy(), exact)
+    np.testing.assert_array_equal(hits.cpu().numpy(), O.recall_hits(approx, exact))
+
+
+def test_single_head_recall_table_saki_pca_wsvd():
+    """The single-head workload's recall@64 for SAKI, key PCA and weight SVD,
+    GPU vs oracle: identical hits on every row where the two top-64 sets agree."""
+    inp = W.make_layer(W.SPECS["single_head_d128"])
+    q, keys = inp["queries"][0, 0], inp["keys"][0, 0]
+    lim = O.candidate_limits(256, 1024)
+    ex_o = O.topk_rows(O.exact_scores(q, keys), lim)
+    oc = O.saki_calibrate(inp["q_cal"][0], inp["k_cal"][0], 32)
+    V = O.key_pca_factors(oc["Sigma_k"], 32)
+    U = O.weight_svd_factors(inp["W_K"][0], 32)
+    cal_pca = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32, method="key_pca")
+    wq, wk = S.saki_weight_svd_factors(inp["W_K"], 1, 32)
+    lib_f = {"saki": None, "pca": (cal_pca["B_q"], cal_pca["B_k"], cal_pca["mu"]),
+             "wsvd": (wq, wk, cal_pca["mu"])}
+    orc_f = {"saki": (oc["B_q"], oc["B_k"], oc["mu"]), "pca": (V, V, oc["mu"]),
+             "wsvd": (U, U, oc["mu"])}
+    table = {}
+    for name in ("saki", "pca", "wsvd"):
+        out = gpu_pipeline(inp, 32, "f32", factors=lib_f[name])
+        hits, ex = S.saki_recall(out["keys"], out["q"], torch.from_numpy(out["idx"]).to(DEV),
+                                 1024)
+        np.testing.assert_array_equal(ex.cpu().numpy()[0, 0], ex_o)
+        Bq, Bk, mu = orc_f[name]
+        s_hat, *_ = O.index_scores(Bq, Bk, mu, q, keys)
+        ap_o = O.topk_rows(s_hat, lim)
+        h_o = O.recall_hits(ap_o, ex_o)
+        h_g = hits.cpu().numpy()[0, 0]
+        same = np.array([set(a) == set(b) for a, b in zip(out["idx"][0, 0], ap_o)])
+        np.testing.assert_array_equal(h_g[same], h_o[same])
+        table[name] = (h_g.mean() / 64, h_o.mean() / 64, int((~same).sum()))
+    print("recall@64 (gpu, oracle, rows with differing sets):", table)
+    assert table["saki"][1] > table["pca"][1] > table["wsvd"][1]
+
+
+def test_determinism():
+    inp = W.make_layer(W.SPECS["llama31_8b_layer"].with_(N=2048, Q=2048 - 64))
+    a = gpu_pipeline(inp, 32, "bf16")
+    b = gpu_pipeline(inp, 32, "bf16")
+    np.testing.assert_array_equal(a["idx"], b["idx"])
+    np.testing.assert_array_equal(a["score"], b["score"])

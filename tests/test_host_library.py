@@ -1,0 +1,179 @@
+"""CPU tests of libsaki: exported symbols, the host float64 calibration
+against the oracle, size helpers and argument validation (no GPU calls)."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+
+S = pytest.importorskip("paper_2608_03228_amd.saki")
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "saki.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return S.lib()
+
+
+def test_exports_every_declared_symbol(lib):
+    text = open(HEADER).read()
+    names = sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(saki_\w+)\(", text, re.M)))
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), n
+    assert S.saki_version() == 1
+    assert "workspace" in S.saki_status_string(-3)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 17, 128])
+def test_sym_eig_matches_lapack(n):
+    rng = np.random.default_rng(n)
+    A = rng.standard_normal((n, n))
+    A = A + A.T
+    w, V = S.saki_sym_eig(A)
+    w2 = np.linalg.eigvalsh(A)
+    scale = np.abs(w2).max()
+    assert np.max(np.abs(w - w2)) <= 1e-13 * n * scale
+    assert np.max(np.abs(A @ V - V * w)) <= 1e-13 * n * scale
+    np.testing.assert_allclose(V.T @ V, np.eye(n), atol=1e-13 * n)
+
+
+def test_sym_eig_degenerate_and_graded():
+    # repeated eigenvalues, exact zeros, and a wide dynamic range
+    Q, _ = np.linalg.qr(np.random.default_rng(0).standard_normal((40, 40)))
+    w0 = np.concatenate([np.full(10, 2.0), np.zeros(10), np.geomspace(1e-12, 1e3, 20)])
+    A = (Q * w0) @ Q.T
+    w, V = S.saki_sym_eig(A)
+    np.testing.assert_allclose(w, np.sort(w0), atol=1e-12 * 1e3)
+    assert np.max(np.abs(A @ V - V * w)) <= 1e-11 * 1e3
+    w, V = S.saki_sym_eig(np.diag([3.0, 1.0, 2.0]))
+    np.testing.assert_array_equal(w, [1.0, 2.0, 3.0])
+
+
+def _m(B_q, B_k):
+    return B_q.astype(np.float64) @ B_k.astype(np.float64).T
+
+
+@pytest.mark.parametrize("spec_name,r", [("single_head_d128", 32), ("llama31_8b_layer", 16),
+                                         ("llama31_8b_layer", 64), ("qwen25_7b_decode", 32)])
+def test_calibration_matches_oracle(spec_name, r):
+    """Host calibration vs the oracle.  The library returns float32 factors, so
+    the rank-r map agrees to float32 rounding (~1e-7 relative); singular
+    values are float64 throughout (SVD via the eigenvalues of C^T C)."""
+    spec = W.SPECS[spec_name].with_(N=64, Q=1, q_start=0, batch=1)
+    inp = W.make_layer(spec)
+    cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], r)
+    G = spec.H_q // spec.H_kv
+    for h in sorted({0, spec.H_q // 2, spec.H_q - 1}):
+        oc = O.saki_calibrate(inp["q_cal"][h], inp["k_cal"][h // G], r)
+        M = _m(cal["B_q"][h], cal["B_k"][h])
+        assert np.linalg.norm(M - oc["M"]) <= 2e-6 * np.linalg.norm(oc["M"])
+        sig = oc["sigma"]
+        assert np.max(np.abs(cal["sigma"][h] ** 2 - sig ** 2)) <= 1e-12 * sig[0] ** 2 * spec.d
+        assert tuple(cal["n_clamped"][h]) == oc["n_clamped"]
+        np.testing.assert_allclose(cal["mu"][h // G], oc["mu"], rtol=0,
+                                   atol=1e-6 * np.abs(oc["mu"]).max())
+        for name in ("B_q", "B_k"):  # columns agree, signs canonicalised alike
+            a, b = cal[name][h].astype(np.float64), oc[name]
+            assert np.max(np.abs(a - b) / np.abs(b).max(axis=0)) < 1e-5
+
+
+def test_calibration_clamps_like_oracle():
+    """T < d: both moments are singular and the floor binds."""
+    rng = np.random.default_rng(9)
+    q = rng.standard_normal((2, 40, 128)).astype(np.float32)
+    k = (rng.standard_normal((1, 40, 128)) + 0.25).astype(np.float32)
+    cal = S.saki_calibrate(q, k, 128)
+    for h in range(2):
+        oc = O.saki_calibrate(q[h], k[0], 128)
+        assert tuple(cal["n_clamped"][h]) == oc["n_clamped"]
+        assert oc["n_clamped"][0] >= 88
+        np.testing.assert_allclose(_m(cal["B_q"][h], cal["B_k"][h]), np.eye(128), atol=2e-4)
+
+
+def test_key_pca_and_weight_svd_factors_match_oracle():
+    spec = W.SPECS["llama31_8b_layer"].with_(N=64, Q=1, q_start=0)
+    inp = W.make_layer(spec)
+    cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32, method="key_pca")
+    Bq, Bk = S.saki_weight_svd_factors(inp["W_K"], spec.H_q, 32)
+    for h in (0, 13, 31):
+        g = h // 4
+        _, sk, _ = O.second_moments(inp["q_cal"][h], inp["k_cal"][g])
+        V = O.key_pca_factors(sk, 32)
+        np.testing.assert_allclose(_m(cal["B_q"][h], cal["B_k"][h]), V @ V.T, atol=2e-6)
+        U = O.weight_svd_factors(inp["W_K"][g], 32)
+        np.testing.assert_allclose(_m(Bq[h], Bk[h]), U @ U.T, atol=2e-6)
+
+
+def test_constant_keys_identity_fallback():
+    q = np.random.default_rng(1).standard_normal((1, 64, 16)).astype(np.float32)
+    k = np.tile(np.arange(16, dtype=np.float32), (1, 64, 1))
+    cal = S.saki_calibrate(q, k, 4)
+    assert cal["n_clamped"][0, 1] == 16
+    np.testing.assert_array_equal(cal["mu"][0], np.arange(16, dtype=np.float32))
+
+
+def test_size_helpers():
+    assert S.saki_index_bytes(1, 32, 4096, 32, "bf16") == 32 * 4096 * 32 * 2
+    assert S.saki_index_bytes(2, 4, 65, 16, "f32") == 2 * 4 * 128 * 16 * 4  # tiles of 64 keys
+    assert S.saki_index_bytes(1, 1, 64, 48, "f32") == 0  # unsupported rank
+    assert S.saki_score_topk_workspace_bytes(1, 32, 4032, 4096, 32, 64, "bf16") > 0
+    assert S.saki_score_topk_workspace_bytes(1, 32, 4032, 4096, 32, 65, "bf16") == 0
+    # decode rows are split over many key chunks -> room for partial lists
+    assert S.saki_score_topk_workspace_bytes(1, 32, 1, 1 << 20, 32, 64, "bf16") > 32 * 64 * 8
+    assert S.saki_recall_workspace_bytes(1, 32, 1, 1 << 20, 128, 64) > 0
+    assert S.saki_recall_workspace_bytes(1, 32, 1, 1 << 20, 64, 64) == 0
+
+
+def test_argument_validation_without_launch(lib):
+    """Invalid arguments are rejected before anything touches the GPU."""
+    P = C.c_void_p(1)  # never dereferenced: validation fails first
+    ERR_ARG, ERR_UNSUP, ERR_WS = -1, -2, -3
+    # build_index: d != 128, bad rank, null pointers, range past N_cap, small buffer
+    assert lib.saki_build_index(P, 0, 1, 1, 1, 64, 64, 32, P, P, 0, P, 1 << 20, 0, 64, None) == ERR_UNSUP
+    assert lib.saki_build_index(P, 0, 1, 1, 1, 64, 128, 48, P, P, 0, P, 1 << 20, 0, 64, None) == ERR_UNSUP
+    assert lib.saki_build_index(None, 0, 1, 1, 1, 64, 128, 32, P, P, 0, P, 1 << 20, 0, 64, None) == ERR_ARG
+    assert lib.saki_build_index(P, 0, 1, 1, 1, 64, 128, 32, P, P, 0, P, 1 << 20, 10, 60, None) == ERR_ARG
+    assert lib.saki_build_index(P, 0, 1, 1, 1, 64, 128, 32, P, P, 0, P, 100, 0, 64, None) == ERR_WS
+    assert lib.saki_build_index(P, 0, 1, 3, 2, 64, 128, 32, P, P, 0, P, 1 << 20, 0, 64, None) == ERR_ARG
+    assert lib.saki_build_index(P, 7, 1, 1, 1, 64, 128, 32, P, P, 0, P, 1 << 20, 0, 64, None) == ERR_UNSUP
+    # score_topk: k out of range, N_valid > N_cap, small workspace, null output
+    args = [P, 0, 1, 1, 1, 256, 256, 128, 32, P, None, 4, P, P]
+    assert lib.saki_score_topk(*args, 65, P, None, P, 1 << 30, None) == ERR_UNSUP
+    assert lib.saki_score_topk(*args, 0, P, None, P, 1 << 30, None) == ERR_UNSUP
+    assert lib.saki_score_topk(*args, 64, None, None, P, 1 << 30, None) == ERR_ARG
+    assert lib.saki_score_topk(*args, 64, P, None, P, 1, None) == ERR_WS
+    bad = [P, 0, 1, 1, 1, 256, 300, 128, 32, P, None, 4, P, P]
+    assert lib.saki_score_topk(*bad, 64, P, None, P, 1 << 30, None) == ERR_ARG
+    # Q == 0 is a no-op that succeeds
+    zero = [P, 0, 1, 1, 1, 256, 256, 128, 32, P, None, 0, P, P]
+    assert lib.saki_score_topk(*zero, 64, P, None, P, 0, None) == 0
+    # recall: null hits, bad key dtype
+    assert lib.saki_recall(P, 0, P, None, 1, 1, 1, 256, 256, 4, 128, 64, P, None, None, P,
+                           1 << 30, None) == ERR_ARG
+    assert lib.saki_recall(P, 3, P, None, 1, 1, 1, 256, 256, 4, 128, 64, P, P, None, P,
+                           1 << 30, None) == ERR_UNSUP
+    # calibration: H_q not a multiple of H_kv, r > d, null output
+    f = np.zeros((2, 8, 4), np.float32)
+    out = np.zeros(64, np.float32)
+    fp = f.ctypes.data
+    assert lib.saki_calibrate(fp, fp, 3, 2, 8, 4, 2, 0, 1e-6, out.ctypes.data, out.ctypes.data,
+                              out.ctypes.data, None, None, 1) == ERR_ARG
+    assert lib.saki_calibrate(fp, fp, 2, 2, 8, 4, 5, 0, 1e-6, out.ctypes.data, out.ctypes.data,
+                              out.ctypes.data, None, None, 1) == ERR_ARG
+    assert lib.saki_calibrate(fp, fp, 2, 2, 8, 4, 2, 0, 1e-6, None, out.ctypes.data,
+                              out.ctypes.data, None, None, 1) == ERR_ARG
+    assert lib.saki_calibrate(fp, fp, 2, 2, 8, 4, 2, 9, 1e-6, out.ctypes.data, out.ctypes.data,
+                              out.ctypes.data, None, None, 1) == ERR_UNSUP
+
+
+def test_nonfinite_calibration_input_is_reported():
+    q = np.ones((1, 16, 8), np.float32)
+    q[0, 3, 2] = np.nan
+    with pytest.raises(S.SakiError) as e:
+        S.saki_calibrate(q, np.ones((1, 16, 8), np.float32), 2)
+    assert e.value.status == -6
