@@ -142,15 +142,25 @@ def main():
     hits = torch.empty((B, H_q, spec.Q), dtype=torch.int32, device=dev)
     f_dev = {n: torch.empty(s, dtype=torch.float32, device=dev)
              for n, s in (("B_q", (H_q, d, r)), ("B_k", (H_q, d, r)), ("mu", (H_kv, d)))}
-    host_f = {n: torch.empty(t.shape, dtype=torch.float32).pin_memory() for n, t in f_dev.items()}
-
+    # two pinned staging slots: the host calibrates batch i+1 while the GPU
+    # still works on batch i; a slot is rewritten only after its copy finished
+    slots = [{n: torch.empty(t.shape, dtype=torch.float32).pin_memory() for n, t in f_dev.items()}
+             for _ in range(2)]
+    slot_done = [None, None]
     ev = {}
+    n_step = [0]
 
     def step(timed_stages=False):
         cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], r)
+        sl = n_step[0] % 2
+        n_step[0] += 1
+        if slot_done[sl] is not None:
+            slot_done[sl].synchronize()
         for n in f_dev:
-            host_f[n].numpy()[...] = cal[n]
-            f_dev[n].copy_(host_f[n], non_blocking=True)
+            slots[sl][n].numpy()[...] = cal[n]
+            f_dev[n].copy_(slots[sl][n], non_blocking=True)
+        slot_done[sl] = torch.cuda.Event()
+        slot_done[sl].record()
         if timed_stages:
             e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
             e[0].record()

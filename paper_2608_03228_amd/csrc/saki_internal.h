@@ -32,6 +32,7 @@ inline size_t index_bytes(int B, int H_q, int N_cap, int r, int dtype) {
 // are split over several chunks each chunk writes a partial top-64 to the
 // workspace and a merge pass reduces them.
 struct Plan {
+  bool mfma = false;   // 16-row MFMA kernels (Q >= 16) or the streaming kernels
   int rows = 1;        // query rows per wave
   int waves = 1;       // waves per workgroup
   int row_blocks = 0;  // workgroups along the query axis
@@ -42,14 +43,17 @@ struct Plan {
 
 inline Plan make_plan(int B, int H_q, int Q, int N_valid, int part_entry_bytes) {
   Plan p;
-  p.rows = Q >= 4 ? 4 : 1;
+  p.mfma = Q >= 16;
+  p.rows = p.mfma ? 16 : (Q >= 4 ? 4 : 1);
   const int wave_rows = (Q + p.rows - 1) / p.rows;
-  p.waves = wave_rows < 4 ? (wave_rows < 1 ? 1 : wave_rows) : 4;
+  const int max_waves = p.mfma ? 2 : 4;  // workgroup size of the kernels
+  p.waves = wave_rows < max_waves ? (wave_rows < 1 ? 1 : wave_rows) : max_waves;
   p.row_blocks = (Q + p.rows * p.waves - 1) / (p.rows * p.waves);
   const size_t total_waves = (size_t)B * H_q * wave_rows;
   const size_t n = N_valid > 0 ? (size_t)N_valid : 1;
   size_t chunk = round_up(n, kTile);
-  const size_t target = 8192;  // waves wanted in flight over the whole GPU
+  // waves wanted over the whole GPU before the key axis is split too
+  const size_t target = p.mfma ? 2048 : 8192;
   if (total_waves > 0 && total_waves < target) {
     const size_t want = (target + total_waves - 1) / total_waves;
     size_t c = round_up((n + want - 1) / want, kTile);

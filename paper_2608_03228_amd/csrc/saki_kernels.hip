@@ -3,18 +3,16 @@
 // Kernels (one launch each, all on the caller's stream):
 //   build_index_kernel   key codes c = B_k^T (k - mu) for every query head (Eq. 4)
 //   query_sketch_kernel  z = B_q^T q and b = q^T mu per query row (Sec. 6)
-//   score_topk_kernel    s = z . c + b over a row's visible keys, running top-64
-//   exact_topk_kernel    exact float64 q . k, running top-64, recall hits (Sec. 3)
+//   score_mfma_kernel    s = z . c + b on MFMA for blocks of 16 query rows,
+//                        running top-64 per row
+//   score_stream_kernel  the same for few query rows per head (decode): one
+//                        key per lane, float32 dot products, key range split
+//                        into chunks across waves
+//   exact_mfma_kernel    exact float64 q . k (f64 MFMA), top-64, recall hits
+//   exact_stream_kernel  the same with float64 FMAs for few query rows
 //   merge_kernel         reduces per-chunk partial top-64 lists of one row
 //   export_kernel        debug read-back of the codes
-//
-// Top-k selection.  A row's running top-64 lives in one wave, one entry per
-// lane, sorted by (score desc, index asc).  New candidates are compared with
-// the current 64th entry; the few that beat it are appended to a per-row LDS
-// buffer, and when 64 have gathered the wave sorts them with a bitonic network
-// and merges them into the list (max(A_i, B_{63-i}) followed by a bitonic
-// merge).  Each wave visits its keys in increasing index order, so a
-// candidate that only ties the threshold's score can never outrank it.
+// Top-k selection is in saki_topk.h.
 
 #include <hip/hip_runtime.h>
 
@@ -24,154 +22,17 @@
 
 #include "saki.h"
 #include "saki_internal.h"
+#include "saki_topk.h"
 
 namespace {
 
 using saki::kMaxK;
 using saki::kTile;
+using namespace saki_dev;
 
-constexpr int kWave = 64;
-constexpr int kMaxWaves = 4;
-constexpr int kBuf = 128;  // candidate buffer slots per row
-constexpr int kPadIdx = INT_MAX;
-
-// ---------------------------------------------------------------- helpers
-
-__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (kWave - 1)); }
-
-__device__ __forceinline__ int prefix_count(uint64_t mask) {
-  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                        __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-}
-
-// Orders LDS accesses of one wave: writes by some lanes become visible to
-// reads by other lanes issued after this point.
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-__device__ __forceinline__ float bcast(float v, int l) {
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
-}
-__device__ __forceinline__ int bcast(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
-__device__ __forceinline__ double bcast(double v, int l) {
-  const uint64_t u = (uint64_t)__double_as_longlong(v);
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
-  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
-}
-
-template <class S>
-__device__ __forceinline__ S neg_inf() { return -INFINITY; }
-
-// Strict ranking order: a before b.
-template <class S>
-__device__ __forceinline__ bool better(S as, int aj, S bs, int bj) {
-  return as > bs || (as == bs && aj < bj);
-}
-
-// Bitonic sort of one entry per lane into descending rank order.
-template <class S>
-__device__ __forceinline__ void wave_sort(S& s, int& j) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int k = 2; k <= kWave; k <<= 1) {
-#pragma unroll
-    for (int m = k >> 1; m > 0; m >>= 1) {
-      const S os = __shfl_xor(s, m, kWave);
-      const int oj = __shfl_xor(j, m, kWave);
-      const bool desc = (lane & k) == 0;
-      const bool low = (lane & m) == 0;
-      const bool mine = better(s, j, os, oj);
-      const bool keep = (low == desc) ? mine : !mine;
-      if (!keep) { s = os; j = oj; }
-    }
-  }
-}
-
-// list <- top 64 of (list U b), both sorted descending.
-template <class S>
-__device__ __forceinline__ void wave_merge(S& ls, int& lj, S bs, int bj) {
-  const int lane = lane_id();
-  const S rs = __shfl(bs, kWave - 1 - lane, kWave);
-  const int rj = __shfl(bj, kWave - 1 - lane, kWave);
-  if (better(rs, rj, ls, lj)) { ls = rs; lj = rj; }
-#pragma unroll
-  for (int m = kWave / 2; m > 0; m >>= 1) {
-    const S os = __shfl_xor(ls, m, kWave);
-    const int oj = __shfl_xor(lj, m, kWave);
-    const bool low = (lane & m) == 0;
-    const bool mine = better(ls, lj, os, oj);
-    const bool keep = low ? mine : !mine;
-    if (!keep) { ls = os; lj = oj; }
-  }
-}
-
-// Running top-64 of R rows owned by one wave.
-template <class S, int R>
-struct WaveTopK {
-  S ls[R];
-  int lj[R];
-  S ts[R];    // current 64th score (wave-uniform)
-  int tj[R];  // and its index
-  int cnt[R]; // buffered candidates (wave-uniform)
-  S* bs;      // LDS [R][kBuf]
-  int* bj;
-
-  __device__ void init(S* sbuf, int* jbuf) {
-    bs = sbuf;
-    bj = jbuf;
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      ls[r] = neg_inf<S>();
-      lj[r] = kPadIdx;
-      ts[r] = neg_inf<S>();
-      tj[r] = kPadIdx;
-      cnt[r] = 0;
-    }
-  }
-
-  __device__ void flush(int r) {
-    const int lane = lane_id();
-    wave_lds_sync();
-    S s = bs[r * kBuf + lane];
-    int j = bj[r * kBuf + lane];
-    if (lane >= cnt[r]) { s = neg_inf<S>(); j = kPadIdx; }
-    wave_sort(s, j);
-    wave_merge(ls[r], lj[r], s, j);
-    ts[r] = bcast(ls[r], kWave - 1);
-    tj[r] = bcast(lj[r], kWave - 1);
-    const int rem = cnt[r] - kWave;
-    if (rem > 0 && lane < rem) {
-      const S s2 = bs[r * kBuf + kWave + lane];
-      const int j2 = bj[r * kBuf + kWave + lane];
-      bs[r * kBuf + lane] = s2;
-      bj[r * kBuf + lane] = j2;
-    }
-    cnt[r] = rem > 0 ? rem : 0;
-    wave_lds_sync();
-  }
-
-  // One candidate per lane for row r.
-  __device__ __forceinline__ void offer(int r, S s, int j) {
-    const bool take = better(s, j, ts[r], tj[r]);
-    const uint64_t mask = __ballot(take);
-    if (mask == 0) return;
-    const int pos = cnt[r] + prefix_count(mask);
-    if (take) {
-      bs[r * kBuf + pos] = s;
-      bj[r * kBuf + pos] = j;
-    }
-    cnt[r] += __popcll(mask);
-    if (cnt[r] >= kWave) flush(r);
-  }
-
-  __device__ void finish(int r) {
-    if (cnt[r] > 0) flush(r);
-  }
-};
+constexpr int kStreamWaves = 4;  // waves per workgroup, streaming kernels
+constexpr int kMfmaWaves = 2;    // waves per workgroup, MFMA kernels
+constexpr int kMR = 16;          // query rows per wave on the MFMA kernels
 
 // fp32 -> bf16 bits, round to nearest even (finite inputs).
 __device__ __forceinline__ uint32_t bf16_bits(float x) {
@@ -207,6 +68,58 @@ __device__ __forceinline__ void unpack_piece(uint4 v, float* out) {
     out[2] = __uint_as_float(v.z);
     out[3] = __uint_as_float(v.w);
   }
+}
+
+__device__ __forceinline__ int row_limit(int i, int Q, int N_valid, const int* q_pos) {
+  if (i >= Q) return 0;
+  if (!q_pos) return N_valid;
+  const long long lim = (long long)q_pos[i] + 1;
+  return lim < 0 ? 0 : (lim > N_valid ? N_valid : (int)lim);
+}
+
+// MI355X deals consecutive work-groups round-robin over its 8 XCDs, each with
+// its own L2.  The MFMA kernels run on a 1-D grid of 8 * per_xcd work-groups
+// and renumber them so that XCD x gets the contiguous logical range
+// [x * per_xcd, (x + 1) * per_xcd): the row blocks of one head (which read the
+// same codes / keys) then share one L2.  Returns -1 for padding work-groups.
+constexpr int kXcds = 8;
+__device__ __forceinline__ long long xcd_logical_block(long long total) {
+  const long long hw = blockIdx.x;
+  const long long per_xcd = (total + kXcds - 1) / kXcds;
+  const long long logical = (hw % kXcds) * per_xcd + hw / kXcds;
+  return logical < total ? logical : -1;
+}
+
+__device__ __forceinline__ int wave_max_i(int v) {
+#pragma unroll
+  for (int m = kWave / 2; m > 0; m >>= 1) v = max(v, __shfl_xor(v, m, kWave));
+  return v;
+}
+__device__ __forceinline__ int wave_min_i(int v) {
+#pragma unroll
+  for (int m = kWave / 2; m > 0; m >>= 1) v = min(v, __shfl_xor(v, m, kWave));
+  return v;
+}
+
+// Final list entry of a row -> output index / score.
+template <class KO>
+__device__ __forceinline__ int out_index(typename KO::K e) {
+  const int j = KO::index(e);
+  return j == kPadIdx ? -1 : j;
+}
+
+// Hits of an exact list (one entry per lane, the first k lanes count) against
+// approx_idx row `row` (length k; entries < 0 never match).
+__device__ __forceinline__ int row_hits(int ej, const int* __restrict__ approx, size_t row, int k) {
+  const int lane = lane_id();
+  const int aj = lane < k ? approx[row * k + lane] : -1;
+  bool found = false;
+  for (int m = 0; m < k; ++m) {
+    const int v = __shfl(aj, m, kWave);
+    found |= (v >= 0 && v == ej);
+  }
+  const bool counts = lane < k && ej >= 0 && found;
+  return __popcll(__ballot(counts));
 }
 
 // ---------------------------------------------------------------- build index
@@ -331,29 +244,25 @@ __global__ __launch_bounds__(256) void query_sketch_kernel(
   }
 }
 
-__device__ __forceinline__ int row_limit(int i, int Q, int N_valid, const int* q_pos) {
-  if (i >= Q) return 0;
-  if (!q_pos) return N_valid;
-  const long long lim = (long long)q_pos[i] + 1;
-  return lim < 0 ? 0 : (lim > N_valid ? N_valid : (int)lim);
-}
+// ---------------------------------------------------------------- sketch scoring, streaming
 
-// ---------------------------------------------------------------- sketch scoring
-
-// grid (row_blocks * n_chunks, B*H_q), block 64*waves.  Each wave owns R rows.
+// grid (row_blocks * n_chunks, B*H_q), block 64*waves.  Each wave owns R rows
+// and one key chunk; lane t scores key t of each 64-key tile (VALU, float32).
 template <int RK, bool SBF, int R>
-__global__ __launch_bounds__(256) void score_topk_kernel(
+__global__ __launch_bounds__(256) void score_stream_kernel(
     const uint8_t* __restrict__ index, int n_tiles, int N_valid, int Q,
     const int* __restrict__ q_pos, const float* __restrict__ z,
     const float* __restrict__ bvec, int row_blocks, int chunk, int n_chunks, int k,
     int* __restrict__ top_idx, float* __restrict__ top_score,
-    float* __restrict__ part_s, int* __restrict__ part_j) {
+    uint64_t* __restrict__ part) {
   constexpr int ES = SBF ? 2 : 4;
   constexpr int CPP = saki::kChunkBytes / ES;
   constexpr int NP = RK / CPP;
-  __shared__ float zs[kMaxWaves][R][RK];
-  __shared__ float sbuf[kMaxWaves][R][kBuf];
-  __shared__ int jbuf[kMaxWaves][R][kBuf];
+  constexpr size_t TB = (size_t)kTile * RK * ES;
+  using KO = KeysF32;
+  __shared__ float zs[kStreamWaves][R][RK];
+  __shared__ uint64_t lmem[kStreamWaves][R][kList];
+  __shared__ uint64_t bmem[kStreamWaves][R][kList];
   const int wave = threadIdx.x / kWave, lane = lane_id();
   const int waves = blockDim.x / kWave;
   const int rb = blockIdx.x % row_blocks, ch = blockIdx.x / row_blocks;
@@ -374,16 +283,15 @@ __global__ __launch_bounds__(256) void score_topk_kernel(
     const int r = i / RK;
     zs[wave][r][i % RK] = (row0 + r < Q) ? z[(bh * Q + row0 + r) * RK + (i % RK)] : 0.f;
   }
-  wave_lds_sync();
+  RowLists<KO, R> top;
+  top.init(&lmem[wave][0][0], &bmem[wave][0][0]);
 
-  WaveTopK<float, R> top;
-  top.init(&sbuf[wave][0][0], &jbuf[wave][0][0]);
   const int kbeg = ch * chunk;
   const int kend = min(kbeg + chunk, kmax);
-  const uint8_t* hbase = index + bh * n_tiles * ((size_t)kTile * RK * (SBF ? 2 : 4));
+  const uint8_t* hbase = index + bh * n_tiles * TB;
   for (int t0 = kbeg; t0 < kend; t0 += kTile) {
     const int j = t0 + lane;
-    const uint8_t* tb = hbase + (size_t)(t0 / kTile) * ((size_t)kTile * RK * (SBF ? 2 : 4));
+    const uint8_t* tb = hbase + (size_t)(t0 / kTile) * TB;
     float c[RK];
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
@@ -395,63 +303,439 @@ __global__ __launch_bounds__(256) void score_topk_kernel(
       float acc = 0.f;
 #pragma unroll
       for (int m = 0; m < RK; ++m) acc = fmaf(zs[wave][r][m], c[m], acc);
-      const bool ok = j < lim[r];
-      top.offer(r, ok ? acc + bb[r] : -INFINITY, ok ? j : kPadIdx);
+      top.offer(r, j < lim[r] ? acc + bb[r] : -INFINITY, j);
     }
   }
-#pragma unroll
   for (int r = 0; r < R; ++r) {
     top.finish(r);
     const int i = row0 + r;
     if (i >= Q) continue;
+    const uint64_t e = top.entry(r);
     if (n_chunks == 1) {
       if (lane < k) {
         const size_t o = (bh * Q + i) * k + lane;
-        top_idx[o] = top.lj[r] == kPadIdx ? -1 : top.lj[r];
-        if (top_score) top_score[o] = top.ls[r];
+        top_idx[o] = out_index<KO>(e);
+        if (top_score) top_score[o] = KO::score(e);
       }
     } else {
-      const size_t o = ((bh * Q + i) * n_chunks + ch) * kMaxK + lane;
-      part_s[o] = top.ls[r];
-      part_j[o] = top.lj[r];
+      part[((bh * Q + i) * n_chunks + ch) * kMaxK + lane] = e;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- sketch scoring, MFMA
+
+// Query blocks of 16 rows per wave, the column count of the 16x16 MFMA tiles.
+// A = 16 keys of the current tile (rows), B = the wave's 16 queries (columns),
+// so each lane holds scores of one query (lane % 16) against 16 keys of every
+// 64-key tile.
+//
+// Selection runs in three cheap passes over the keys instead of one pass with
+// many sort/merge flushes (scores are recomputed by MFMA in every pass, which
+// costs far less than sorting):
+//   1. moments: per row, mean and variance of its scores in this key chunk;
+//   2. histogram: 64 bins around the predicted 64th score
+//      mean + sd * Phi^-1(1 - 64/n) (bins from 2 sd below to 1 sd above it;
+//      scores below the range are not counted, bin 63 takes everything above);
+//      the highest bin b* whose count from the top reaches 64 gives a gate
+//      that at least 64 and at most 128 candidates pass;
+//   3. collect: the gated candidates go to a per-row LDS buffer, which is
+//      sorted once at the end (bitonic, 64 or 128 entries).
+// The gate only decides which keys are sorted, never their order, so the
+// result is the exact top-64 whenever the gate admits >= 64 keys, which the
+// histogram counts guarantee.  Rows with at most 128 candidates skip the
+// histogram and collect everything.  When the prediction misses (fewer than
+// 64 counted scores in range, more than 128 gated, or zero variance) the wave
+// redoes its rows with the online selection of saki_topk.h.
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
+  bf16x8_t r;
+  __builtin_memcpy(&r, &v, sizeof(r));
+  return r;
+}
+__device__ __forceinline__ i16x4_t as_i16x4(uint2 v) {
+  i16x4_t r;
+  __builtin_memcpy(&r, &v, sizeof(r));
+  return r;
+}
+// Pack 8 floats that already hold bf16 values into a bf16x8 operand.
+__device__ __forceinline__ uint4 pack_bf16x8(const float* f) {
+  uint4 u;
+  u.x = (__float_as_uint(f[0]) >> 16) | (__float_as_uint(f[1]) & 0xffff0000u);
+  u.y = (__float_as_uint(f[2]) >> 16) | (__float_as_uint(f[3]) & 0xffff0000u);
+  u.z = (__float_as_uint(f[4]) >> 16) | (__float_as_uint(f[5]) & 0xffff0000u);
+  u.w = (__float_as_uint(f[6]) >> 16) | (__float_as_uint(f[7]) & 0xffff0000u);
+  return u;
+}
+__device__ __forceinline__ float xor_shfl_f32(float v, int m) {
+  return __uint_as_float(xor_shfl_u32(__float_as_uint(v), m));
+}
+// Sum over the four lanes that share lane % 16.
+__device__ __forceinline__ float sum_lane_groups(float v) {
+  v += xor_shfl_f32(v, 16);
+  return v + xor_shfl_f32(v, 32);
+}
+
+// Upper-tail standard normal quantile: z with P(X > z) = tail, tail in (0, 0.5]
+// (Abramowitz & Stegun 26.2.23, absolute error below 4.5e-4).  Only used to
+// predict where a row's 64th score lies.
+__device__ __forceinline__ float normal_upper_quantile(float tail) {
+  const float t = sqrtf(-2.f * __logf(tail));
+  return t - (2.515517f + t * (0.802853f + t * 0.010328f)) /
+                 (1.f + t * (1.432788f + t * (0.189269f + t * 0.001308f)));
+}
+
+constexpr int kBins = 64;
+constexpr int kCollect = 128;
+enum RowMode : int { kModeAll = 0, kModeHist = 1, kModeFallback = 2 };
+
+// Scores of one 64-key tile for the wave's 16 queries: acc[sub][v] is query
+// (lane % 16) against key t0 + 16*sub + 4*(lane/16) + v (without the mean term).
+template <int RK, bool SBF>
+struct MfmaScorer {
+  static constexpr int NKB = (SBF && RK >= 32) ? RK / 32 : 1;
+  static constexpr int NKF = SBF ? 1 : RK / 4;
+  static constexpr size_t TB = (size_t)kTile * RK * (SBF ? 2 : 4);
+  bf16x8_t zb[NKB];
+  i16x4_t zb4;
+  float zf[NKF];
+
+  // zs: this lane's query sketch row (RK floats, bf16 values when SBF)
+  __device__ void load_operand(const float* zs, int g) {
+    if constexpr (SBF) {
+      if constexpr (RK == 16) {
+        uint2 u;
+        u.x = (__float_as_uint(zs[4 * g + 0]) >> 16) | (__float_as_uint(zs[4 * g + 1]) & 0xffff0000u);
+        u.y = (__float_as_uint(zs[4 * g + 2]) >> 16) | (__float_as_uint(zs[4 * g + 3]) & 0xffff0000u);
+        zb4 = as_i16x4(u);
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < NKB; ++kk) zb[kk] = as_bf16x8(pack_bf16x8(zs + 32 * kk + 8 * g));
+      }
+    } else {
+#pragma unroll
+      for (int m = 0; m < RK / 16; ++m)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) zf[4 * m + e] = zs[4 * (g + 4 * m) + e];
+    }
+  }
+
+  __device__ __forceinline__ void tile(const uint8_t* tb, int qi, int g, f32x4_t acc[4]) const {
+#pragma unroll
+    for (int sub = 0; sub < 4; ++sub) {
+      const int key = 16 * sub + qi;
+      f32x4_t a = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (SBF) {
+        if constexpr (RK == 16) {
+          const uint2 raw = *reinterpret_cast<const uint2*>(tb + (size_t)(g / 2) * kTile * 16 +
+                                                           (size_t)key * 16 + (g % 2) * 8);
+          a = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_i16x4(raw), zb4, a, 0, 0, 0);
+        } else {
+#pragma unroll
+          for (int kk = 0; kk < NKB; ++kk) {
+            const uint4 raw = *reinterpret_cast<const uint4*>(
+                tb + (size_t)(4 * kk + g) * kTile * 16 + (size_t)key * 16);
+            a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(raw), zb[kk], a, 0, 0, 0);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int m = 0; m < RK / 16; ++m) {
+          const uint4 raw = *reinterpret_cast<const uint4*>(
+              tb + (size_t)(g + 4 * m) * kTile * 16 + (size_t)key * 16);
+          a = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(raw.x), zf[4 * m + 0], a, 0, 0, 0);
+          a = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(raw.y), zf[4 * m + 1], a, 0, 0, 0);
+          a = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(raw.z), zf[4 * m + 2], a, 0, 0, 0);
+          a = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(raw.w), zf[4 * m + 3], a, 0, 0, 0);
+        }
+      }
+      acc[sub] = a;
+    }
+  }
+};
+
+// grid (row_blocks * n_chunks, B*H_q), block 64*waves.  Computes the query
+// sketch itself (z = B_q^T q on the f32 MFMA, rounded to bf16 for bf16
+// sketches; b = q^T mu), then scores and selects as described above.
+template <int RK, bool SBF>
+__global__ __launch_bounds__(128) void score_mfma_kernel(
+    const uint8_t* __restrict__ index, int n_tiles, int N_valid, int Q,
+    const int* __restrict__ q_pos, const float* __restrict__ q,
+    const float* __restrict__ Bq, const float* __restrict__ mu, int H_q, int H_kv, int n_bh,
+    int row_blocks, int chunk, int n_chunks, int k, int* __restrict__ top_idx,
+    float* __restrict__ top_score, uint64_t* __restrict__ part) {
+  constexpr int D = saki::kHeadDim;
+  using KO = KeysF32;
+  using Scorer = MfmaScorer<RK, SBF>;
+  // per wave: 16 KB of candidate space (also the z staging area, and the
+  // list + buffer of the online fallback) and 4 KB of histogram (also the
+  // fallback's score staging)
+  __shared__ uint64_t cand_mem[kMfmaWaves][kMR * kCollect];
+  __shared__ int hist_mem[kMfmaWaves][kMR * kBins];
+  __shared__ int ccount[kMfmaWaves][kMR];
+  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int waves = blockDim.x / kWave;
+  const long long lb = xcd_logical_block((long long)row_blocks * n_chunks * n_bh);
+  if (lb < 0) return;
+  const int rb = (int)(lb % row_blocks), ch = (int)((lb / row_blocks) % n_chunks);
+  const size_t bh = (size_t)(lb / ((long long)row_blocks * n_chunks));
+  const int h = (int)(bh % H_q);
+  const int gkv = h / (H_q / H_kv);
+  const int row0 = (rb * waves + wave) * kMR;
+  if (row0 >= Q) return;
+  const int qi = lane % 16, g = lane / 16;
+  const int my_row = row0 + qi;
+  const bool row_ok = my_row < Q;
+  const int my_lim = row_limit(my_row, Q, N_valid, q_pos);
+  const int kmax = wave_max_i(my_lim);
+  const int kmin = wave_min_i(row_ok ? my_lim : INT_MAX);
+  const int kbeg = ch * chunk;
+  const int kend = min(kbeg + chunk, kmax);
+  uint64_t* cand = cand_mem[wave];
+  int* hist = hist_mem[wave];
+
+  // ---- query sketch: D[m][qi] = sum_c B_q[c][m] q[qi][c], lane group g feeds c = 4s + g
+  float my_b;
+  Scorer sc;
+  {
+    const float* qr = q + (bh * Q + (row_ok ? my_row : row0)) * D;
+    const float* bq = Bq + (size_t)h * D * RK;
+    const float* mr = mu + (size_t)gkv * D;
+    f32x4_t za[RK / 16];
+#pragma unroll
+    for (int mb = 0; mb < RK / 16; ++mb) za[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float bp = 0.f;
+    for (int s = 0; s < D / 4; ++s) {
+      const int c = 4 * s + g;
+      const float qv = row_ok ? qr[c] : 0.f;
+      bp = fmaf(qv, mr[c], bp);
+#pragma unroll
+      for (int mb = 0; mb < RK / 16; ++mb)
+        za[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(bq[c * RK + 16 * mb + qi], qv, za[mb], 0, 0, 0);
+    }
+    my_b = sum_lane_groups(bp);
+    float* zs = reinterpret_cast<float*>(cand);  // [16][RK]
+#pragma unroll
+    for (int mb = 0; mb < RK / 16; ++mb)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const float zv = za[mb][v];
+        zs[qi * RK + 16 * mb + 4 * g + v] = SBF ? bf16_round(zv) : zv;
+      }
+    wave_lds_sync();
+    sc.load_operand(zs + qi * RK, g);
+    wave_lds_sync();
+  }
+  const uint8_t* hbase = index + bh * n_tiles * Scorer::TB;
+
+  // ---- pass 1: moments of this lane's row over the chunk
+  float sum = 0.f, sumsq = 0.f;
+  for (int t0 = kbeg; t0 < kend; t0 += kTile) {
+    f32x4_t acc[4];
+    sc.tile(hbase + (size_t)(t0 / kTile) * Scorer::TB, qi, g, acc);
+    const bool need_mask = t0 + kTile > kmin;
+#pragma unroll
+    for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        float x = acc[sub][v];
+        if (need_mask && t0 + 16 * sub + 4 * g + v >= my_lim) x = 0.f;
+        sum += x;
+        sumsq = fmaf(x, x, sumsq);
+      }
+  }
+  sum = sum_lane_groups(sum);
+  sumsq = sum_lane_groups(sumsq);
+  const int n_row = row_ok ? max(0, min(my_lim, kend) - kbeg) : 0;
+  int mode = kModeAll;
+  float inv_w = 0.f, off = 0.f;
+  if (n_row > kCollect) {
+    const float mean = sum / (float)n_row;
+    const float var = fmaxf(sumsq / (float)n_row - mean * mean, 0.f);
+    const float sd = sqrtf(var);
+    if (sd > 0.f && isfinite(sd) && isfinite(mean)) {
+      const float t_hat = my_b + mean + sd * normal_upper_quantile((float)kList / (float)n_row);
+      const float lo = t_hat - 2.f * sd;
+      inv_w = (float)(kBins - 2) / (3.f * sd);
+      off = 1.f - lo * inv_w;  // bin(s) = fmaf(s, inv_w, off): below 1 = out of range
+      mode = kModeHist;
+    } else {
+      mode = kModeFallback;
+    }
+  }
+
+  // ---- pass 2: histogram of the rows in histogram mode
+  const bool any_hist = __ballot(mode == kModeHist) != 0;
+  float gate = -INFINITY;  // bin value (>= 1) a score must reach to be collected
+  if (any_hist) {
+    for (int i = lane; i < kMR * kBins; i += kWave) hist[i] = 0;
+    wave_lds_sync();
+    for (int t0 = kbeg; t0 < kend; t0 += kTile) {
+      f32x4_t acc[4];
+      sc.tile(hbase + (size_t)(t0 / kTile) * Scorer::TB, qi, g, acc);
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float x = fmaf(acc[sub][v] + my_b, inv_w, off);
+          if (mode == kModeHist && x >= 1.f && t0 + 16 * sub + 4 * g + v < my_lim)
+            atomicAdd(&hist[qi * kBins + min((int)x, kBins - 1)], 1);
+        }
+    }
+    wave_lds_sync();
+    // per row: the highest bin whose count from the top reaches 64
+    for (int r = 0; r < kMR; ++r) {
+      if (__builtin_amdgcn_readlane(mode, r) != kModeHist) continue;
+      int x = hist[r * kBins + (kBins - 1 - lane)];  // lane i: bin 63 - i
+      if (lane == kBins - 1) x = 0;                  // bin 0 is never counted
+#pragma unroll
+      for (int d = 1; d < kWave; d <<= 1) {
+        const int t = __shfl_up(x, d, kWave);
+        if (lane >= d) x += t;
+      }
+      const uint64_t reach = __ballot(x >= kList);
+      int new_mode = kModeHist;
+      float bstar = 0.f;
+      if (reach == 0) {
+        new_mode = kModeFallback;
+      } else {
+        const int l = __builtin_ctzll(reach);
+        if (__builtin_amdgcn_readlane(x, l) > kCollect) new_mode = kModeFallback;
+        bstar = (float)(kBins - 1 - l);
+      }
+      if (qi == r) {
+        mode = new_mode;
+        gate = bstar;
+      }
+    }
+  }
+
+  if (__ballot(mode == kModeFallback) == 0) {
+    // ---- pass 3: collect the gated candidates
+    if (lane < kMR) ccount[wave][lane] = 0;
+    wave_lds_sync();
+    for (int t0 = kbeg; t0 < kend; t0 += kTile) {
+      f32x4_t acc[4];
+      sc.tile(hbase + (size_t)(t0 / kTile) * Scorer::TB, qi, g, acc);
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int key = t0 + 16 * sub + 4 * g + v;
+          const float sv = acc[sub][v] + my_b;
+          const bool take = key < my_lim && (mode == kModeAll || fmaf(sv, inv_w, off) >= gate);
+          if (take) {
+            const int pos = atomicAdd(&ccount[wave][qi], 1);
+            if (pos < kCollect) cand[qi * kCollect + pos] = KO::make(sv, key);
+          }
+        }
+    }
+    wave_lds_sync();
+    for (int r = 0; r < kMR; ++r) {
+      const int i = row0 + r;
+      if (i >= Q) break;
+      const int c = min(ccount[wave][r], kCollect);
+      uint64_t a = lane < c ? cand[r * kCollect + lane] : KO::pad();
+      wave_sort<KO>(a);
+      if (c > kList) {
+        uint64_t b2 = lane + kList < c ? cand[r * kCollect + kList + lane] : KO::pad();
+        wave_sort<KO>(b2);
+        wave_merge<KO>(a, b2);
+      }
+      if (n_chunks == 1) {
+        if (lane < k) {
+          const size_t o = (bh * Q + i) * k + lane;
+          top_idx[o] = out_index<KO>(a);
+          if (top_score) top_score[o] = KO::score(a);
+        }
+      } else {
+        part[((bh * Q + i) * n_chunks + ch) * kMaxK + lane] = a;
+      }
+    }
+    return;
+  }
+
+  // ---- fallback: online selection over the chunk (rare)
+  float* stage = reinterpret_cast<float*>(hist);  // [16][64], key column swizzled
+  RowLists<KO, kMR> top;
+  top.init(cand, cand + kMR * kList);
+  for (int t0 = kbeg; t0 < kend; t0 += kTile) {
+    f32x4_t acc[4];
+    sc.tile(hbase + (size_t)(t0 / kTile) * Scorer::TB, qi, g, acc);
+#pragma unroll
+    for (int sub = 0; sub < 4; ++sub) {
+      const f32x4_t sv = acc[sub] + my_b;
+      *reinterpret_cast<f32x4_t*>(&stage[qi * kTile + ((16 * sub + 4 * g) ^ (qi << 2))]) = sv;
+    }
+    wave_lds_sync();
+    const bool need_mask = t0 + kTile > kmin;
+    for (int r = 0; r < kMR; ++r) {
+      float sv = stage[r * kTile + (lane ^ (r << 2))];
+      const int j = t0 + lane;
+      if (need_mask && j >= __builtin_amdgcn_readlane(my_lim, r)) sv = -INFINITY;
+      top.offer(r, sv, j);
+    }
+    wave_lds_sync();
+  }
+  for (int r = 0; r < kMR; ++r) {
+    top.finish(r);
+    const int i = row0 + r;
+    if (i >= Q) continue;
+    const uint64_t e = top.entry(r);
+    if (n_chunks == 1) {
+      if (lane < k) {
+        const size_t o = (bh * Q + i) * k + lane;
+        top_idx[o] = out_index<KO>(e);
+        if (top_score) top_score[o] = KO::score(e);
+      }
+    } else {
+      part[((bh * Q + i) * n_chunks + ch) * kMaxK + lane] = e;
     }
   }
 }
 
 // ---------------------------------------------------------------- exact scores + recall
 
-// Hits of the exact list (one entry per lane, the first k lanes count)
-// against approx_idx row `row` (length k).
-__device__ __forceinline__ int row_hits(int ej, const int* __restrict__ approx, size_t row, int k) {
+// Writes the exact top-k of a finished row, or its partial list.
+template <class KO>
+__device__ __forceinline__ void exact_row_out(typename KO::K e, size_t row, int ch, int n_chunks,
+                                              int k, const int* approx, int* hits,
+                                              int* exact_idx, typename KO::K* part) {
   const int lane = lane_id();
-  const int aj = lane < k ? approx[row * k + lane] : -1;
-  bool found = false;
-  for (int m = 0; m < k; ++m) {
-    const int v = __shfl(aj, m, kWave);
-    found |= (v >= 0 && v == ej);
+  if (n_chunks == 1) {
+    const int ej = out_index<KO>(e);
+    if (exact_idx && lane < k) exact_idx[row * k + lane] = ej;
+    const int hsum = row_hits(ej, approx, row, k);
+    if (lane == 0) hits[row] = hsum;
+  } else {
+    part[(row * n_chunks + ch) * kMaxK + lane] = e;
   }
-  const bool counts = lane < k && ej != kPadIdx && found;
-  return __popcll(__ballot(counts));
 }
 
-// grid (row_blocks * n_chunks, B*H_q), block 64*waves.  Exact float64 scores.
+// grid (row_blocks * n_chunks, B*H_q), block 64*waves.  Exact float64 scores
+// with float64 FMAs, one key per lane, R rows per wave.
 template <bool KBF, int R>
-__global__ __launch_bounds__(256) void exact_topk_kernel(
+__global__ __launch_bounds__(256) void exact_stream_kernel(
     const void* __restrict__ keys, const float* __restrict__ q,
     const int* __restrict__ q_pos, int H_q, int H_kv, int N_cap, int N_valid, int Q,
     int row_blocks, int chunk, int n_chunks, int k, const int* __restrict__ approx,
-    int* __restrict__ hits, int* __restrict__ exact_idx, double* __restrict__ part_s,
-    int* __restrict__ part_j) {
+    int* __restrict__ hits, int* __restrict__ exact_idx, KeyF64* __restrict__ part) {
   constexpr int D = saki::kHeadDim;
-  __shared__ float qsh[kMaxWaves][R][D];
-  __shared__ double sbuf[kMaxWaves][R][kBuf];
-  __shared__ int jbuf[kMaxWaves][R][kBuf];
+  using KO = KeysF64;
+  __shared__ double qsh[kStreamWaves][R][D];
+  __shared__ KeyF64 lmem[kStreamWaves][R][kList];
+  __shared__ KeyF64 bmem[kStreamWaves][R][kList];
   const int wave = threadIdx.x / kWave, lane = lane_id();
   const int waves = blockDim.x / kWave;
   const int rb = blockIdx.x % row_blocks, ch = blockIdx.x / row_blocks;
   const size_t bh = blockIdx.y;
   const int b = (int)(bh / H_q), h = (int)(bh % H_q);
-  const int g = h / (H_q / H_kv);
+  const int gkv = h / (H_q / H_kv);
   const int row0 = (rb * waves + wave) * R;
   if (row0 >= Q) return;
   int lim[R];
@@ -463,12 +747,11 @@ __global__ __launch_bounds__(256) void exact_topk_kernel(
   }
   for (int i = lane; i < R * D; i += kWave) {
     const int r = i / D;
-    qsh[wave][r][i % D] = (row0 + r < Q) ? q[(bh * Q + row0 + r) * D + (i % D)] : 0.f;
+    qsh[wave][r][i % D] = (row0 + r < Q) ? (double)q[(bh * Q + row0 + r) * D + (i % D)] : 0.0;
   }
-  wave_lds_sync();
-  WaveTopK<double, R> top;
-  top.init(&sbuf[wave][0][0], &jbuf[wave][0][0]);
-  const size_t kbase = ((size_t)b * H_kv + g) * N_cap;
+  RowLists<KO, R> top;
+  top.init(&lmem[wave][0][0], &bmem[wave][0][0]);
+  const size_t kbase = ((size_t)b * H_kv + gkv) * N_cap;
   const int kbeg = ch * chunk;
   const int kend = min(kbeg + chunk, kmax);
   for (int t0 = kbeg; t0 < kend; t0 += kTile) {
@@ -477,72 +760,153 @@ __global__ __launch_bounds__(256) void exact_topk_kernel(
     double acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = 0.0;
+#pragma unroll 2
     for (int c0 = 0; c0 < D; c0 += 8) {
-      float kv[8];
+      double kv[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) kv[e] = inb ? load_key_elem<KBF>(keys, (kbase + j) * D + c0 + e) : 0.f;
+      for (int e = 0; e < 8; ++e) kv[e] = inb ? (double)load_key_elem<KBF>(keys, (kbase + j) * D + c0 + e) : 0.0;
 #pragma unroll
       for (int r = 0; r < R; ++r)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[r] = fma((double)qsh[wave][r][c0 + e], (double)kv[e], acc[r]);
+        for (int e = 0; e < 8; ++e) acc[r] = fma(qsh[wave][r][c0 + e], kv[e], acc[r]);
     }
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const bool ok = j < lim[r];
-      top.offer(r, ok ? acc[r] : -(double)INFINITY, ok ? j : kPadIdx);
-    }
+    for (int r = 0; r < R; ++r) top.offer(r, j < lim[r] ? acc[r] : -(double)INFINITY, j);
   }
-#pragma unroll
   for (int r = 0; r < R; ++r) {
     top.finish(r);
     const int i = row0 + r;
     if (i >= Q) continue;
-    const size_t row = bh * Q + i;
-    if (n_chunks == 1) {
-      if (exact_idx && lane < k) exact_idx[row * k + lane] = top.lj[r] == kPadIdx ? -1 : top.lj[r];
-      const int hsum = row_hits(top.lj[r], approx, row, k);
-      if (lane == 0) hits[row] = hsum;
-    } else {
-      const size_t o = (row * n_chunks + ch) * kMaxK + lane;
-      part_s[o] = top.ls[r];
-      part_j[o] = top.lj[r];
+    exact_row_out<KO>(top.entry(r), bh * Q + i, ch, n_chunks, k, approx, hits, exact_idx, part);
+  }
+}
+
+// Exact float64 scores on the f64 MFMA (16x16x4).  Lane group g feeds dims
+// 32g .. 32g+31 of its key and query, one per k-step.  The f64 MFMA returns
+// D[g + 4v][lane % 16] in register v.  grid and block as for score_mfma_kernel.
+template <bool KBF>
+__global__ __launch_bounds__(128) void exact_mfma_kernel(
+    const void* __restrict__ keys, const float* __restrict__ q,
+    const int* __restrict__ q_pos, int H_q, int H_kv, int N_cap, int N_valid, int Q,
+    int row_blocks, int chunk, int n_chunks, int k, const int* __restrict__ approx,
+    int* __restrict__ hits, int* __restrict__ exact_idx, KeyF64* __restrict__ part, int n_bh) {
+  constexpr int D = saki::kHeadDim;
+  using KO = KeysF64;
+  // staged scores [row][key], key column swizzled by the row index
+  __shared__ double stage[kMfmaWaves][kMR][kTile];
+  __shared__ KeyF64 lmem[kMfmaWaves][kMR][kList];
+  __shared__ KeyF64 bmem[kMfmaWaves][kMR][kList];
+  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int waves = blockDim.x / kWave;
+  const long long lb = xcd_logical_block((long long)row_blocks * n_chunks * n_bh);
+  if (lb < 0) return;
+  const int rb = (int)(lb % row_blocks), ch = (int)((lb / row_blocks) % n_chunks);
+  const size_t bh = (size_t)(lb / ((long long)row_blocks * n_chunks));
+  const int b = (int)(bh / H_q), h = (int)(bh % H_q);
+  const int gkv = h / (H_q / H_kv);
+  const int row0 = (rb * waves + wave) * kMR;
+  if (row0 >= Q) return;
+  const int qi = lane % 16, g = lane / 16;
+  const int my_row = row0 + qi;
+  const bool row_ok = my_row < Q;
+  const int my_lim = row_limit(my_row, Q, N_valid, q_pos);
+  const int kmax = wave_max_i(my_lim);
+  const int kmin = wave_min_i(row_ok ? my_lim : INT_MAX);
+  double qreg[32];
+  {
+    const float* qr = q + (bh * Q + (row_ok ? my_row : row0)) * D + 32 * g;
+#pragma unroll
+    for (int s4 = 0; s4 < 8; ++s4) {
+      const float4 v = *reinterpret_cast<const float4*>(qr + 4 * s4);
+      qreg[4 * s4 + 0] = row_ok ? (double)v.x : 0.0;
+      qreg[4 * s4 + 1] = row_ok ? (double)v.y : 0.0;
+      qreg[4 * s4 + 2] = row_ok ? (double)v.z : 0.0;
+      qreg[4 * s4 + 3] = row_ok ? (double)v.w : 0.0;
     }
+  }
+  RowLists<KO, kMR> top;
+  top.init(&lmem[wave][0][0], &bmem[wave][0][0]);
+  const size_t kbase = ((size_t)b * H_kv + gkv) * N_cap;
+  const int kbeg = ch * chunk;
+  const int kend = min(kbeg + chunk, kmax);
+  for (int t0 = kbeg; t0 < kend; t0 += kTile) {
+#pragma unroll
+    for (int sub = 0; sub < 4; ++sub) {
+      const int j = t0 + 16 * sub + qi;
+      const bool inb = j < N_valid;
+      float kf[32];
+      if constexpr (KBF) {
+        const uint16_t* kr = reinterpret_cast<const uint16_t*>(keys) + (kbase + (inb ? j : 0)) * D + 32 * g;
+#pragma unroll
+        for (int s8 = 0; s8 < 4; ++s8) {
+          const uint4 v = *reinterpret_cast<const uint4*>(kr + 8 * s8);
+          unpack_piece<true>(v, kf + 8 * s8);
+        }
+      } else {
+        const float* kr = reinterpret_cast<const float*>(keys) + (kbase + (inb ? j : 0)) * D + 32 * g;
+#pragma unroll
+        for (int s4 = 0; s4 < 8; ++s4) {
+          const float4 v = *reinterpret_cast<const float4*>(kr + 4 * s4);
+          kf[4 * s4 + 0] = v.x;
+          kf[4 * s4 + 1] = v.y;
+          kf[4 * s4 + 2] = v.z;
+          kf[4 * s4 + 3] = v.w;
+        }
+      }
+      f64x4_t acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+      for (int s = 0; s < 32; ++s)
+        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(inb ? (double)kf[s] : 0.0, qreg[s], acc, 0, 0, 0);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) stage[wave][qi][(16 * sub + g + 4 * v) ^ qi] = acc[v];
+    }
+    wave_lds_sync();
+    const bool need_mask = t0 + kTile > kmin;
+    for (int r = 0; r < kMR; ++r) {
+      double sv = stage[wave][r][lane ^ r];
+      const int j = t0 + lane;
+      if (need_mask && j >= __builtin_amdgcn_readlane(my_lim, r)) sv = -(double)INFINITY;
+      top.offer(r, sv, j);
+    }
+    wave_lds_sync();
+  }
+  for (int r = 0; r < kMR; ++r) {
+    top.finish(r);
+    const int i = row0 + r;
+    if (i >= Q) continue;
+    exact_row_out<KO>(top.entry(r), bh * Q + i, ch, n_chunks, k, approx, hits, exact_idx, part);
   }
 }
 
 // ---------------------------------------------------------------- merge of partials
 
-// grid (ceil(rows/4)), block 256: one wave per row merges n_chunks sorted lists.
-template <class S, bool RECALL>
+// grid (ceil(rows/4)), block 256: one wave per row merges n_chunks sorted
+// partial lists.  RECALL: the row is an exact list -> exact_idx and hits.
+template <class KO, bool RECALL>
 __global__ __launch_bounds__(256) void merge_kernel(
-    const S* __restrict__ part_s, const int* __restrict__ part_j, size_t rows,
-    int n_chunks, int k, int* __restrict__ out_idx, float* __restrict__ out_score,
+    const typename KO::K* __restrict__ part, size_t rows, int n_chunks, int k,
+    int* __restrict__ out_idx, float* __restrict__ out_score,
     const int* __restrict__ approx, int* __restrict__ hits) {
+  using K = typename KO::K;
   const int lane = lane_id();
   const size_t row = (size_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
   if (row >= rows) return;
-  S ls = neg_inf<S>();
-  int lj = kPadIdx;
+  K a = KO::pad();
   for (int c = 0; c < n_chunks; ++c) {
-    const size_t o = (row * n_chunks + c) * kMaxK + lane;
-    const S s = part_s[o];
-    const int j = part_j[o];
+    const K b = part[(row * n_chunks + c) * kMaxK + lane];
     // the partial is sorted: skip it when its best cannot enter the list
-    const S s0 = bcast(s, 0);
-    const int j0 = bcast(j, 0);
-    const S t = bcast(ls, kWave - 1);
-    const int tjx = bcast(lj, kWave - 1);
-    if (!better(s0, j0, t, tjx)) continue;
-    wave_merge(ls, lj, s, j);
+    if (!KO::gt(KO::readlane(b, 0), KO::readlane(a, kWave - 1))) continue;
+    wave_merge<KO>(a, b);
   }
+  const int j = out_index<KO>(a);
   if constexpr (RECALL) {
-    if (out_idx && lane < k) out_idx[row * k + lane] = lj == kPadIdx ? -1 : lj;
-    const int hsum = row_hits(lj, approx, row, k);
+    if (out_idx && lane < k) out_idx[row * k + lane] = j;
+    const int hsum = row_hits(j, approx, row, k);
     if (lane == 0) hits[row] = hsum;
   } else {
     if (lane < k) {
-      out_idx[row * k + lane] = lj == kPadIdx ? -1 : lj;
-      if (out_score) out_score[row * k + lane] = (float)ls;
+      out_idx[row * k + lane] = j;
+      if (out_score) out_score[row * k + lane] = (float)KO::score(a);
     }
   }
 }
@@ -550,6 +914,12 @@ __global__ __launch_bounds__(256) void merge_kernel(
 // ---------------------------------------------------------------- dispatch helpers
 
 bool launch_ok() { return hipGetLastError() == hipSuccess; }
+
+// 1-D grid for xcd_logical_block: 8 * ceil(total / 8) work-groups.
+dim3 xcd_grid(const saki::Plan& p, int n_bh) {
+  const long long total = (long long)p.row_blocks * p.n_chunks * n_bh;
+  return dim3((unsigned)(((total + kXcds - 1) / kXcds) * kXcds));
+}
 
 template <int RK, bool KBF, bool SBF>
 void launch_build(const void* keys, const float* Bk, const float* mu, int B, int H_q,
@@ -570,29 +940,30 @@ void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int N_cap, int
                   const saki::Plan& p, hipStream_t s) {
   float* z = reinterpret_cast<float*>(ws + p.z_off);
   float* bv = reinterpret_cast<float*>(ws + p.b_off);
-  hipLaunchKernelGGL((query_sketch_kernel<RK, SBF>), dim3((Q + 15) / 16, B * H_q),
-                     dim3(256), 0, s, q, Bq, mu, H_q, H_kv, Q, z, bv);
-  float* ps = nullptr;
-  int* pj = nullptr;
   const size_t rows = (size_t)B * H_q * Q;
-  if (p.n_chunks > 1) {
-    ps = reinterpret_cast<float*>(ws + p.part_off);
-    pj = reinterpret_cast<int*>(ws + p.part_off + rows * p.n_chunks * kMaxK * sizeof(float));
-  }
+  uint64_t* part = p.n_chunks > 1 ? reinterpret_cast<uint64_t*>(ws + p.part_off) : nullptr;
   dim3 grid((unsigned)(p.row_blocks * p.n_chunks), B * H_q);
+  dim3 block(kWave * p.waves);
   const int nt = (int)saki::n_tiles(N_cap);
-  if (p.rows == 4)
-    hipLaunchKernelGGL((score_topk_kernel<RK, SBF, 4>), grid, dim3(kWave * p.waves), 0, s,
-                       index, nt, N_valid, Q, q_pos, z, bv, p.row_blocks, p.chunk,
-                       p.n_chunks, k, top_idx, top_score, ps, pj);
+  if (!p.mfma)
+    hipLaunchKernelGGL((query_sketch_kernel<RK, SBF>), dim3((Q + 15) / 16, B * H_q),
+                       dim3(256), 0, s, q, Bq, mu, H_q, H_kv, Q, z, bv);
+  if (p.mfma)
+    hipLaunchKernelGGL((score_mfma_kernel<RK, SBF>), xcd_grid(p, B * H_q), block, 0, s, index,
+                       nt, N_valid, Q, q_pos, q, Bq, mu, H_q, H_kv, B * H_q, p.row_blocks,
+                       p.chunk, p.n_chunks, k, top_idx, top_score, part);
+  else if (p.rows == 4)
+    hipLaunchKernelGGL((score_stream_kernel<RK, SBF, 4>), grid, block, 0, s, index, nt, N_valid,
+                       Q, q_pos, z, bv, p.row_blocks, p.chunk, p.n_chunks, k, top_idx,
+                       top_score, part);
   else
-    hipLaunchKernelGGL((score_topk_kernel<RK, SBF, 1>), grid, dim3(kWave * p.waves), 0, s,
-                       index, nt, N_valid, Q, q_pos, z, bv, p.row_blocks, p.chunk,
-                       p.n_chunks, k, top_idx, top_score, ps, pj);
+    hipLaunchKernelGGL((score_stream_kernel<RK, SBF, 1>), grid, block, 0, s, index, nt, N_valid,
+                       Q, q_pos, z, bv, p.row_blocks, p.chunk, p.n_chunks, k, top_idx,
+                       top_score, part);
   if (p.n_chunks > 1)
-    hipLaunchKernelGGL((merge_kernel<float, false>), dim3((unsigned)((rows + 3) / 4)),
-                       dim3(256), 0, s, ps, pj, rows, p.n_chunks, k, top_idx, top_score,
-                       nullptr, nullptr);
+    hipLaunchKernelGGL((merge_kernel<KeysF32, false>), dim3((unsigned)((rows + 3) / 4)),
+                       dim3(256), 0, s, part, rows, p.n_chunks, k, top_idx, top_score, nullptr,
+                       nullptr);
 }
 
 template <bool KBF>
@@ -600,26 +971,26 @@ void launch_recall(const void* keys, const float* q, const int* q_pos, int B, in
                    int H_kv, int N_cap, int N_valid, int Q, int k, const int* approx,
                    int* hits, int* exact_idx, uint8_t* ws, const saki::Plan& p,
                    hipStream_t s) {
-  double* ps = nullptr;
-  int* pj = nullptr;
   const size_t rows = (size_t)B * H_q * Q;
-  if (p.n_chunks > 1) {
-    ps = reinterpret_cast<double*>(ws + p.part_off);
-    pj = reinterpret_cast<int*>(ws + p.part_off + rows * p.n_chunks * kMaxK * sizeof(double));
-  }
+  KeyF64* part = p.n_chunks > 1 ? reinterpret_cast<KeyF64*>(ws + p.part_off) : nullptr;
   dim3 grid((unsigned)(p.row_blocks * p.n_chunks), B * H_q);
-  if (p.rows == 4)
-    hipLaunchKernelGGL((exact_topk_kernel<KBF, 4>), grid, dim3(kWave * p.waves), 0, s, keys,
-                       q, q_pos, H_q, H_kv, N_cap, N_valid, Q, p.row_blocks, p.chunk,
-                       p.n_chunks, k, approx, hits, exact_idx, ps, pj);
+  dim3 block(kWave * p.waves);
+  if (p.mfma)
+    hipLaunchKernelGGL((exact_mfma_kernel<KBF>), xcd_grid(p, B * H_q), block, 0, s, keys, q,
+                       q_pos, H_q, H_kv, N_cap, N_valid, Q, p.row_blocks, p.chunk, p.n_chunks, k,
+                       approx, hits, exact_idx, part, B * H_q);
+  else if (p.rows == 4)
+    hipLaunchKernelGGL((exact_stream_kernel<KBF, 4>), grid, block, 0, s, keys, q, q_pos, H_q,
+                       H_kv, N_cap, N_valid, Q, p.row_blocks, p.chunk, p.n_chunks, k, approx,
+                       hits, exact_idx, part);
   else
-    hipLaunchKernelGGL((exact_topk_kernel<KBF, 1>), grid, dim3(kWave * p.waves), 0, s, keys,
-                       q, q_pos, H_q, H_kv, N_cap, N_valid, Q, p.row_blocks, p.chunk,
-                       p.n_chunks, k, approx, hits, exact_idx, ps, pj);
+    hipLaunchKernelGGL((exact_stream_kernel<KBF, 1>), grid, block, 0, s, keys, q, q_pos, H_q,
+                       H_kv, N_cap, N_valid, Q, p.row_blocks, p.chunk, p.n_chunks, k, approx,
+                       hits, exact_idx, part);
   if (p.n_chunks > 1)
-    hipLaunchKernelGGL((merge_kernel<double, true>), dim3((unsigned)((rows + 3) / 4)),
-                       dim3(256), 0, s, ps, pj, rows, p.n_chunks, k, exact_idx, nullptr,
-                       approx, hits);
+    hipLaunchKernelGGL((merge_kernel<KeysF64, true>), dim3((unsigned)((rows + 3) / 4)),
+                       dim3(256), 0, s, part, rows, p.n_chunks, k, exact_idx, nullptr, approx,
+                       hits);
 }
 
 bool dtype_ok(int t) { return t == SAKI_F32 || t == SAKI_BF16; }
