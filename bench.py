@@ -135,7 +135,7 @@ def main():
     index = torch.empty(S.saki_index_bytes(B, H_q, N, r, sk), dtype=torch.uint8, device=dev)
     ws = torch.empty(max(1, S.saki_score_topk_workspace_bytes(B, H_q, spec.Q, N, r, k, sk)),
                      dtype=torch.uint8, device=dev)
-    wsr = torch.empty(max(1, S.saki_recall_workspace_bytes(B, H_q, spec.Q, N, d, k)),
+    wsr = torch.empty(max(1, S.saki_recall_workspace_bytes(B, H_q, H_kv, spec.Q, N, d, k)),
                       dtype=torch.uint8, device=dev)
     top_idx = torch.empty((B, H_q, spec.Q, k), dtype=torch.int32, device=dev)
     top_sc = torch.empty((B, H_q, spec.Q, k), dtype=torch.float32, device=dev)

@@ -175,7 +175,7 @@ int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_k
                     size_t ws_bytes, void* stream);
 
 /* Workspace for saki_recall with these sizes (bytes; 0 on bad arguments). */
-size_t saki_recall_workspace_bytes(int B, int H_q, int Q, int N_valid, int d, int k);
+size_t saki_recall_workspace_bytes(int B, int H_q, int H_kv, int Q, int N_valid, int d, int k);
 
 /*
  * saki_recall (GPU) -- evaluation of Sec. 3: exact scores q_i . k_j in float64

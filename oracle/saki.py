@@ -12,9 +12,9 @@ scores them as (B_q^T q)^T c + q^T mu (Eq. 4, Sec. 6).
 Readings taken where the paper is silent (listed with reasons in the design
 notes): moments use the 1/T normaliser; eigenvalues of each Sigma below
 floor_rel * lambda_max are clamped to that floor (never truncated); singular
-vector pairs are sign-canonicalised so that the largest-magnitude entry of v_i
-is positive (lowest index on ties); top-k ranks by score descending, then key
-index ascending.
+vector pairs are sign-canonicalised so that the largest-magnitude entry of each
+column of B_k is positive (lowest index on ties); top-k ranks by score
+descending, then key index ascending.
 """
 from __future__ import annotations
 
@@ -78,13 +78,18 @@ def clamped_roots(S: np.ndarray, floor_rel: float = 1e-6):
     return half, ihalf, n
 
 
-def _canonical_signs(U: np.ndarray, V: np.ndarray):
-    """Flip each pair (u_i, v_i) so the largest-|.| entry of v_i is positive."""
+def _canonical_signs(U: np.ndarray, V: np.ndarray, Sk_ihalf: np.ndarray):
+    """Flip each singular pair (u_i, v_i) so that the largest-|.| entry of the
+    key factor column Sigma_k^{-1/2} v_i is positive (first index on ties).
+    M_r does not depend on these signs; tying them to B_k rather than to v_i
+    makes the stored codes independent of which square root of the moments a
+    calibration uses (Eq. 3 is invariant to that choice)."""
     U = U.copy()
     V = V.copy()
+    W = Sk_ihalf @ V
     for i in range(V.shape[1]):
-        j = int(np.argmax(np.abs(V[:, i])))  # first index on ties
-        if V[j, i] < 0:
+        j = int(np.argmax(np.abs(W[:, i])))  # first index on ties
+        if W[j, i] < 0:
             U[:, i] = -U[:, i]
             V[:, i] = -V[:, i]
     return U, V
@@ -105,7 +110,7 @@ def saki_calibrate(q_cal: np.ndarray, k_cal: np.ndarray, r: int,
     sk_h, sk_ih, nk = clamped_roots(sk, floor_rel)
     C = sq_h @ sk_h
     U, sig, Vt = np.linalg.svd(C)
-    U, V = _canonical_signs(U, Vt.T)
+    U, V = _canonical_signs(U, Vt.T, sk_ih)
     root = np.sqrt(sig[:r])
     B_q = sq_ih @ U[:, :r] * root
     B_k = sk_ih @ V[:, :r] * root

@@ -5,8 +5,21 @@
 // symmetric eigensolver (Householder tridiagonalisation followed by the
 // implicit QL iteration with Wilkinson-type shifts, as in Golub & Van Loan,
 // "Matrix Computations", Sec. 8.3) so that the library depends on no LAPACK.
-// The SVD of C is taken from the eigendecomposition of C^T C: V are its
-// eigenvectors, sigma_i^2 its eigenvalues, and U_r = C V_r diag(sigma_r)^-1.
+//
+// Two mathematically identical routes compute the factors:
+//  * Cholesky route, used when the eigenvalue floor provably does not bind on
+//    either moment (Cholesky of Sigma - floor_rel * ||Sigma||_F * I succeeds;
+//    ||Sigma||_F >= lambda_max, so every eigenvalue is above the floor).  With
+//    Sigma_k = L L^T, C' = L_q^T L has the singular values of C, and
+//    M = C'^T C' = L^T Sigma_q L has eigenvectors V' = O V for the orthogonal
+//    O relating L to Sigma_k^{1/2}.  Then B_q = L V'_r diag(sigma_r)^-1/2 and
+//    B_k = L^{-T} V'_r diag(sigma_r)^1/2 are exactly Eq. 4's factors (the
+//    square root chosen does not matter) at one eigendecomposition per head.
+//  * Symmetric route otherwise: clamped eigendecompositions of both moments,
+//    C = Sigma_q^{1/2} Sigma_k^{1/2}, V and sigma^2 from the eigenvalues of
+//    C^T C, U_r = C V_r diag(sigma_r)^-1.
+// Either way each singular pair is signed so that the largest-magnitude
+// entry of its B_k column is positive (lowest index on ties).
 
 #include "saki.h"
 #include "saki_internal.h"
@@ -34,6 +47,81 @@ void matmul(int n, const double* A, const double* B, double* C) {
       const double* bk = B + (size_t)k * n;
       for (int j = 0; j < n; ++j) ci[j] += a * bk[j];
     }
+  }
+}
+
+// S = (1/T) sum_t (x_t - mu)(x_t - mu)^T for the T rows of X (float, T x d);
+// mu may be null (uncentred).  Four tokens per sweep over the triangle.
+void moment(int T, int d, const float* X, const double* mu, double* S) {
+  std::fill(S, S + (size_t)d * d, 0.0);
+  std::vector<double> x((size_t)4 * d);
+  for (int t0 = 0; t0 < T; t0 += 4) {
+    const int nb = std::min(4, T - t0);
+    for (int b = 0; b < 4; ++b)
+      for (int i = 0; i < d; ++i)
+        x[(size_t)b * d + i] = b < nb ? (double)X[(size_t)(t0 + b) * d + i] - (mu ? mu[i] : 0.0) : 0.0;
+    const double *x0 = x.data(), *x1 = x0 + d, *x2 = x1 + d, *x3 = x2 + d;
+    for (int i = 0; i < d; ++i) {
+      double* row = S + (size_t)i * d;
+      const double a0 = x0[i], a1 = x1[i], a2 = x2[i], a3 = x3[i];
+      for (int j = 0; j <= i; ++j) row[j] += a0 * x0[j] + a1 * x1[j] + a2 * x2[j] + a3 * x3[j];
+    }
+  }
+  for (int i = 0; i < d; ++i)
+    for (int j = 0; j <= i; ++j) {
+      const double v = S[(size_t)i * d + j] / (double)T;
+      S[(size_t)i * d + j] = v;
+      S[(size_t)j * d + i] = v;
+    }
+}
+
+// Lower Cholesky factor of S - shift * I (row-major, upper part zero).
+// Returns false unless every pivot is positive.
+bool cholesky(int n, const double* S, double shift, double* L) {
+  std::fill(L, L + (size_t)n * n, 0.0);
+  for (int j = 0; j < n; ++j) {
+    const double* lj = L + (size_t)j * n;
+    double dsum = S[(size_t)j * n + j] - shift;
+    for (int k = 0; k < j; ++k) dsum -= lj[k] * lj[k];
+    if (!(dsum > 0.0) || !std::isfinite(dsum)) return false;
+    const double piv = std::sqrt(dsum);
+    L[(size_t)j * n + j] = piv;
+    for (int i = j + 1; i < n; ++i) {
+      const double* li = L + (size_t)i * n;
+      double acc = S[(size_t)i * n + j];
+      for (int k = 0; k < j; ++k) acc -= li[k] * lj[k];
+      L[(size_t)i * n + j] = acc / piv;
+    }
+  }
+  return true;
+}
+
+double frobenius(int n, const double* S) {
+  double acc = 0.0;
+  for (size_t i = 0; i < (size_t)n * n; ++i) acc += S[i] * S[i];
+  return std::sqrt(acc);
+}
+
+// True when no eigenvalue of the PSD moment lies below floor_rel * lambda_max
+// (sufficient test); L then holds the Cholesky factor of S itself.
+bool unclamped_cholesky(int n, const double* S, double floor_rel, double* L) {
+  const double f = frobenius(n, S);
+  if (!(f > 0.0) || !std::isfinite(f)) return false;
+  if (!cholesky(n, S, floor_rel * f, L)) return false;
+  return cholesky(n, S, 0.0, L);
+}
+
+// Flip column m of both factors (d x r, row-major, float output) when the
+// largest-magnitude entry of the B_k column is negative.
+void store_pair(int d, int r, int m, const double* bq, const double* bk, float* Bq, float* Bk) {
+  int jmax = 0;
+  double amax = std::fabs(bk[0]);
+  for (int j = 1; j < d; ++j)
+    if (std::fabs(bk[j]) > amax) { amax = std::fabs(bk[j]); jmax = j; }
+  const double sgn = bk[jmax] < 0 ? -1.0 : 1.0;
+  for (int i = 0; i < d; ++i) {
+    Bq[(size_t)i * r + m] = (float)(sgn * bq[i]);
+    Bk[(size_t)i * r + m] = (float)(sgn * bk[i]);
   }
 }
 
@@ -255,10 +343,12 @@ void parallel_for(int count, int n_threads, F fn) {
 }
 
 struct KvState {
-  Mat half, ihalf;         // Sigma_k^{1/2}, Sigma_k^{-1/2}
+  Mat half, ihalf;         // Sigma_k^{1/2}, Sigma_k^{-1/2} (symmetric route)
+  Mat L;                   // Cholesky factor of Sigma_k (Cholesky route)
   std::vector<double> mu;  // key mean
   Mat sk;                  // Sigma_k
   int n_clamped = 0;
+  bool chol = false;       // the floor provably does not bind on Sigma_k
   bool ok = false;
 };
 
@@ -306,7 +396,8 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
   const int G = H_q / H_kv;
   const size_t dd = (size_t)d * d;
   try {
-    // ---- per KV head: key mean, centred key moment and its clamped roots
+    // ---- per KV head: key mean, centred key moment, and either its Cholesky
+    //      factor or its clamped symmetric roots
     std::vector<KvState> kv(H_kv);
     parallel_for(H_kv, n_threads, [&](int g) {
       KvState& st = kv[g];
@@ -315,27 +406,19 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
       for (int t = 0; t < T; ++t)
         for (int i = 0; i < d; ++i) st.mu[i] += (double)k[(size_t)t * d + i];
       for (int i = 0; i < d; ++i) st.mu[i] /= (double)T;
-      st.sk.assign(dd, 0.0);
-      std::vector<double> kc(d);
-      for (int t = 0; t < T; ++t) {
-        for (int i = 0; i < d; ++i) kc[i] = (double)k[(size_t)t * d + i] - st.mu[i];
-        for (int i = 0; i < d; ++i) {
-          double* row = st.sk.data() + (size_t)i * d;
-          const double ki = kc[i];
-          for (int j = 0; j <= i; ++j) row[j] += ki * kc[j];
-        }
-      }
-      for (int i = 0; i < d; ++i)
-        for (int j = 0; j <= i; ++j) {
-          const double v = st.sk[(size_t)i * d + j] / (double)T;
-          st.sk[(size_t)i * d + j] = v;
-          st.sk[(size_t)j * d + i] = v;
-        }
+      st.sk.resize(dd);
+      moment(T, d, k, st.mu.data(), st.sk.data());
       if (method == SAKI_METHOD_OPT) {
-        st.half.resize(dd);
-        st.ihalf.resize(dd);
-        st.ok = clamped_roots(d, st.sk.data(), floor_rel, st.half.data(),
-                              st.ihalf.data(), &st.n_clamped);
+        st.L.resize(dd);
+        st.chol = unclamped_cholesky(d, st.sk.data(), floor_rel, st.L.data());
+        if (st.chol) {
+          st.ok = true;
+        } else {
+          st.half.resize(dd);
+          st.ihalf.resize(dd);
+          st.ok = clamped_roots(d, st.sk.data(), floor_rel, st.half.data(), st.ihalf.data(),
+                                &st.n_clamped);
+        }
       } else {
         st.ok = true;
       }
@@ -362,66 +445,111 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
         if (n_clamped) { n_clamped[2 * h] = 0; n_clamped[2 * h + 1] = 0; }
         return;
       }
-      // Sigma_q (uncentred) and its clamped roots
+      // Sigma_q (uncentred)
       const float* q = q_cal + (size_t)h * T * d;
-      Mat sq(dd, 0.0);
-      std::vector<double> qt(d);
-      for (int t = 0; t < T; ++t) {
-        for (int i = 0; i < d; ++i) qt[i] = (double)q[(size_t)t * d + i];
-        for (int i = 0; i < d; ++i) {
-          double* row = sq.data() + (size_t)i * d;
-          const double qi = qt[i];
-          for (int j = 0; j <= i; ++j) row[j] += qi * qt[j];
+      Mat sq(dd);
+      moment(T, d, q, nullptr, sq.data());
+      std::vector<double> sig(d), bqc(d), bkc(d);
+      Mat scratch(dd);
+      if (st.chol && unclamped_cholesky(d, sq.data(), floor_rel, scratch.data())) {
+        // ---- Cholesky route: M = L^T Sigma_q L, B_q = L v / sqrt(s), B_k = L^-T v sqrt(s)
+        const double* L = st.L.data();
+        Mat W(dd, 0.0), M(dd, 0.0);
+        for (int i = 0; i < d; ++i) {  // W = Sigma_q L  (L lower: column j uses rows k >= j)
+          const double* si = sq.data() + (size_t)i * d;
+          double* wi = W.data() + (size_t)i * d;
+          for (int k = 0; k < d; ++k) {
+            const double a = si[k];
+            const double* lk = L + (size_t)k * d;
+            for (int j = 0; j <= k; ++j) wi[j] += a * lk[j];
+          }
         }
+        for (int k = 0; k < d; ++k) {  // M = L^T W: row i gathers rows k >= i of W
+          const double* lk = L + (size_t)k * d;
+          const double* wk = W.data() + (size_t)k * d;
+          for (int i = 0; i <= k; ++i) {
+            const double a = lk[i];
+            double* mi = M.data() + (size_t)i * d;
+            for (int j = 0; j < d; ++j) mi[j] += a * wk[j];
+          }
+        }
+        std::vector<double> w(d), vt(dd);
+        if (!sym_eig_rows(d, M.data(), w.data(), vt.data())) { failed = 1; return; }
+        for (int m = 0; m < d; ++m) sig[m] = std::sqrt(std::max(w[d - 1 - m], 0.0));
+        for (int m = 0; m < r; ++m) {
+          const double* v = vt.data() + (size_t)(d - 1 - m) * d;
+          const double sm = sig[m], rs = std::sqrt(sm);
+          for (int i = 0; i < d; ++i) {  // L v
+            const double* li = L + (size_t)i * d;
+            double acc = 0.0;
+            for (int j = 0; j <= i; ++j) acc += li[j] * v[j];
+            bqc[i] = sm > 0.0 ? acc / rs : 0.0;
+          }
+          for (int i = d - 1; i >= 0; --i) {  // L^T x = v (back substitution)
+            double acc = v[i];
+            for (int k = i + 1; k < d; ++k) acc -= L[(size_t)k * d + i] * bkc[k];
+            bkc[i] = acc / L[(size_t)i * d + i];
+          }
+          for (int i = 0; i < d; ++i) bkc[i] *= rs;
+          store_pair(d, r, m, bqc.data(), bkc.data(), bq, bk);
+        }
+        if (sigma)
+          for (int m = 0; m < d; ++m) sigma[(size_t)h * d + m] = sig[m];
+        if (n_clamped) { n_clamped[2 * h] = 0; n_clamped[2 * h + 1] = 0; }
+        return;
       }
-      for (int i = 0; i < d; ++i)
-        for (int j = 0; j <= i; ++j) {
-          const double v = sq[(size_t)i * d + j] / (double)T;
-          sq[(size_t)i * d + j] = v;
-          sq[(size_t)j * d + i] = v;
-        }
+      // ---- symmetric route: clamped roots of both moments
       Mat qh(dd), qih(dd);
       int nq = 0;
       if (!clamped_roots(d, sq.data(), floor_rel, qh.data(), qih.data(), &nq)) { failed = 1; return; }
+      Mat kh_local, kih_local;
+      const double* khalf = st.half.data();
+      const double* kihalf = st.ihalf.data();
+      int nk = st.n_clamped;
+      if (st.chol) {  // Sigma_k took the Cholesky route: its roots are needed here only
+        kh_local.resize(dd);
+        kih_local.resize(dd);
+        if (!clamped_roots(d, st.sk.data(), floor_rel, kh_local.data(), kih_local.data(), &nk)) {
+          failed = 1;
+          return;
+        }
+        khalf = kh_local.data();
+        kihalf = kih_local.data();
+      }
       // C = Sigma_q^{1/2} Sigma_k^{1/2};  C^T C -> V, sigma^2
       Mat C(dd), Ct(dd), CtC(dd);
-      matmul(d, qh.data(), st.half.data(), C.data());
+      matmul(d, qh.data(), khalf, C.data());
       for (int i = 0; i < d; ++i)
         for (int j = 0; j < d; ++j) Ct[(size_t)j * d + i] = C[(size_t)i * d + j];
       matmul(d, Ct.data(), C.data(), CtC.data());
       std::vector<double> w(d), vt(dd);
       if (!sym_eig_rows(d, CtC.data(), w.data(), vt.data())) { failed = 1; return; }
-      std::vector<double> sig(d);
       for (int m = 0; m < d; ++m) sig[m] = std::sqrt(std::max(w[d - 1 - m], 0.0));
       if (sigma)
         for (int m = 0; m < d; ++m) sigma[(size_t)h * d + m] = sig[m];
-      if (n_clamped) { n_clamped[2 * h] = nq; n_clamped[2 * h + 1] = st.n_clamped; }
+      if (n_clamped) { n_clamped[2 * h] = nq; n_clamped[2 * h + 1] = nk; }
       // top-r pairs: v_m (row of vt), u_m = C v_m / sigma_m
-      std::vector<double> v(d), u(d), colq(d), colk(d);
+      std::vector<double> u(d);
       for (int m = 0; m < r; ++m) {
-        std::memcpy(v.data(), vt.data() + (size_t)(d - 1 - m) * d, sizeof(double) * d);
-        const double s = sig[m];
-        if (s > 0.0) {
-          for (int i = 0; i < d; ++i) {
-            double acc = 0.0;
-            const double* ci = C.data() + (size_t)i * d;
-            for (int j = 0; j < d; ++j) acc += ci[j] * v[j];
-            u[i] = acc / s;
-          }
-        } else {
-          std::fill(u.begin(), u.end(), 0.0);
+        const double* v = vt.data() + (size_t)(d - 1 - m) * d;
+        const double sm = sig[m];
+        for (int i = 0; i < d; ++i) {
+          double acc = 0.0;
+          const double* ci = C.data() + (size_t)i * d;
+          for (int j = 0; j < d; ++j) acc += ci[j] * v[j];
+          u[i] = sm > 0.0 ? acc / sm : 0.0;
         }
-        canonical_sign(d, v.data(), u.data());
-        const double rs = std::sqrt(s);
+        const double rs = std::sqrt(sm);
         // B_q[:, m] = Sigma_q^{-1/2} u sqrt(s);  B_k[:, m] = Sigma_k^{-1/2} v sqrt(s)
         for (int i = 0; i < d; ++i) {
           const double* ai = qih.data() + (size_t)i * d;
-          const double* bi = st.ihalf.data() + (size_t)i * d;
+          const double* bi = kihalf + (size_t)i * d;
           double aq = 0.0, ak = 0.0;
           for (int j = 0; j < d; ++j) { aq += ai[j] * u[j]; ak += bi[j] * v[j]; }
-          bq[(size_t)i * r + m] = (float)(aq * rs);
-          bk[(size_t)i * r + m] = (float)(ak * rs);
+          bqc[i] = aq * rs;
+          bkc[i] = ak * rs;
         }
+        store_pair(d, r, m, bqc.data(), bkc.data(), bq, bk);
       }
     });
     if (failed) return SAKI_ERR_NUMERIC;
@@ -479,11 +607,11 @@ size_t saki_score_topk_workspace_bytes(int B, int H_q, int Q, int N_valid, int r
   return saki::score_plan(B, H_q, Q, N_valid, r).ws_bytes;
 }
 
-size_t saki_recall_workspace_bytes(int B, int H_q, int Q, int N_valid, int d, int k) {
-  if (B <= 0 || H_q <= 0 || Q < 0 || N_valid < 0 || d != saki::kHeadDim || k < 1 ||
-      k > saki::kMaxK)
+size_t saki_recall_workspace_bytes(int B, int H_q, int H_kv, int Q, int N_valid, int d, int k) {
+  if (B <= 0 || H_q <= 0 || H_kv <= 0 || H_q % H_kv != 0 || Q < 0 || N_valid < 0 ||
+      d != saki::kHeadDim || k < 1 || k > saki::kMaxK)
     return 0;
-  return saki::recall_plan(B, H_q, Q, N_valid).ws_bytes;
+  return saki::recall_plan(B, H_q, H_kv, Q, N_valid).ws_bytes;
 }
 
 }  // extern "C"

@@ -19,6 +19,7 @@
 #include <climits>
 #include <cmath>
 #include <cstdint>
+#include <type_traits>
 
 #include "saki.h"
 #include "saki_internal.h"
@@ -392,6 +393,8 @@ __device__ __forceinline__ float normal_upper_quantile(float tail) {
 
 constexpr int kBins = 64;
 constexpr int kCollect = 128;
+constexpr int kCandRow = kCollect + 1;  // padded row strides (LDS bank spread)
+constexpr int kHistRow = kBins + 1;
 enum RowMode : int { kModeAll = 0, kModeHist = 1, kModeFallback = 2 };
 
 // Scores of one 64-key tile for the wave's 16 queries: acc[sub][v] is query
@@ -475,8 +478,8 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
   // per wave: 16 KB of candidate space (also the z staging area, and the
   // list + buffer of the online fallback) and 4 KB of histogram (also the
   // fallback's score staging)
-  __shared__ uint64_t cand_mem[kMfmaWaves][kMR * kCollect];
-  __shared__ int hist_mem[kMfmaWaves][kMR * kBins];
+  __shared__ uint64_t cand_mem[kMfmaWaves][kMR * kCandRow];
+  __shared__ int hist_mem[kMfmaWaves][kMR * kHistRow];
   __shared__ int ccount[kMfmaWaves][kMR];
   const int wave = threadIdx.x / kWave, lane = lane_id();
   const int waves = blockDim.x / kWave;
@@ -573,7 +576,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
   const bool any_hist = __ballot(mode == kModeHist) != 0;
   float gate = -INFINITY;  // bin value (>= 1) a score must reach to be collected
   if (any_hist) {
-    for (int i = lane; i < kMR * kBins; i += kWave) hist[i] = 0;
+    for (int i = lane; i < kMR * kHistRow; i += kWave) hist[i] = 0;
     wave_lds_sync();
     for (int t0 = kbeg; t0 < kend; t0 += kTile) {
       f32x4_t acc[4];
@@ -584,14 +587,14 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
         for (int v = 0; v < 4; ++v) {
           const float x = fmaf(acc[sub][v] + my_b, inv_w, off);
           if (mode == kModeHist && x >= 1.f && t0 + 16 * sub + 4 * g + v < my_lim)
-            atomicAdd(&hist[qi * kBins + min((int)x, kBins - 1)], 1);
+            atomicAdd(&hist[qi * kHistRow + min((int)x, kBins - 1)], 1);
         }
     }
     wave_lds_sync();
     // per row: the highest bin whose count from the top reaches 64
     for (int r = 0; r < kMR; ++r) {
       if (__builtin_amdgcn_readlane(mode, r) != kModeHist) continue;
-      int x = hist[r * kBins + (kBins - 1 - lane)];  // lane i: bin 63 - i
+      int x = hist[r * kHistRow + (kBins - 1 - lane)];  // lane i: bin 63 - i
       if (lane == kBins - 1) x = 0;                  // bin 0 is never counted
 #pragma unroll
       for (int d = 1; d < kWave; d <<= 1) {
@@ -631,7 +634,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
           const bool take = key < my_lim && (mode == kModeAll || fmaf(sv, inv_w, off) >= gate);
           if (take) {
             const int pos = atomicAdd(&ccount[wave][qi], 1);
-            if (pos < kCollect) cand[qi * kCollect + pos] = KO::make(sv, key);
+            if (pos < kCollect) cand[qi * kCandRow + pos] = KO::make(sv, key);
           }
         }
     }
@@ -640,10 +643,10 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
       const int i = row0 + r;
       if (i >= Q) break;
       const int c = min(ccount[wave][r], kCollect);
-      uint64_t a = lane < c ? cand[r * kCollect + lane] : KO::pad();
+      uint64_t a = lane < c ? cand[r * kCandRow + lane] : KO::pad();
       wave_sort<KO>(a);
       if (c > kList) {
-        uint64_t b2 = lane + kList < c ? cand[r * kCollect + kList + lane] : KO::pad();
+        uint64_t b2 = lane + kList < c ? cand[r * kCandRow + kList + lane] : KO::pad();
         wave_sort<KO>(b2);
         wave_merge<KO>(a, b2);
       }
@@ -789,7 +792,8 @@ __global__ __launch_bounds__(128) void exact_mfma_kernel(
     const void* __restrict__ keys, const float* __restrict__ q,
     const int* __restrict__ q_pos, int H_q, int H_kv, int N_cap, int N_valid, int Q,
     int row_blocks, int chunk, int n_chunks, int k, const int* __restrict__ approx,
-    int* __restrict__ hits, int* __restrict__ exact_idx, KeyF64* __restrict__ part, int n_bh) {
+    int* __restrict__ hits, int* __restrict__ exact_idx, KeyF64* __restrict__ part, int n_bh,
+    const int* __restrict__ redo) {
   constexpr int D = saki::kHeadDim;
   using KO = KeysF64;
   // staged scores [row][key], key column swizzled by the row index
@@ -806,6 +810,8 @@ __global__ __launch_bounds__(128) void exact_mfma_kernel(
   const int gkv = h / (H_q / H_kv);
   const int row0 = (rb * waves + wave) * kMR;
   if (row0 >= Q) return;
+  // as the fallback of exact_bf16_kernel: only the waves it flagged
+  if (redo && redo[lb * kMfmaWaves + wave] == 0) return;
   const int qi = lane % 16, g = lane / 16;
   const int my_row = row0 + qi;
   const bool row_ok = my_row < Q;
@@ -875,6 +881,301 @@ __global__ __launch_bounds__(128) void exact_mfma_kernel(
     const int i = row0 + r;
     if (i >= Q) continue;
     exact_row_out<KO>(top.entry(r), bh * Q + i, ch, n_chunks, k, approx, hits, exact_idx, part);
+  }
+}
+
+// ---------------------------------------------------------------- exact scores, bound-and-rescore
+
+// Keys rounded to bf16 in the MFMA tile layout of the codes (16 pieces of 8
+// dims per key), and an upper bound of every key's Euclidean norm.
+// grid (n_tiles(N_valid), B*H_kv), block 256.
+template <bool KBF>
+__global__ __launch_bounds__(256) void keys_hi_kernel(const void* __restrict__ keys, int N_cap,
+                                                      int N_valid, int n_tiles,
+                                                      uint8_t* __restrict__ khi,
+                                                      uint8_t* __restrict__ klo,
+                                                      float* __restrict__ knorm) {
+  constexpr int D = saki::kHeadDim;
+  constexpr int NP = D / 8;
+  __shared__ float part[4][kTile];
+  const int tile = blockIdx.x;
+  const size_t bg = blockIdx.y;
+  const int t = threadIdx.x % kTile, pg = threadIdx.x / kTile;
+  const int n = tile * kTile + t;
+  const bool ok = n < N_valid;
+  const size_t toff = (bg * n_tiles + tile) * (size_t)kTile * D * 2;
+  float ss = 0.f;
+  for (int p = pg; p < NP; p += 4) {
+    float f[8], hi[8], lo[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      f[e] = ok ? load_key_elem<KBF>(keys, (bg * N_cap + n) * D + 8 * p + e) : 0.f;
+      ss = fmaf(f[e], f[e], ss);
+      hi[e] = bf16_round(f[e]);
+      lo[e] = bf16_round(f[e] - hi[e]);  // exact difference, then rounded
+    }
+    const size_t o = toff + (size_t)p * kTile * 16 + (size_t)t * 16;
+    *reinterpret_cast<uint4*>(khi + o) = pack_bf16x8(hi);
+    *reinterpret_cast<uint4*>(klo + o) = pack_bf16x8(lo);
+  }
+  part[pg][t] = ss;
+  __syncthreads();
+  if (pg == 0 && ok)
+    knorm[bg * N_valid + n] = sqrtf(part[0][t] + part[1][t] + part[2][t] + part[3][t]) * (1.f + 1e-5f);
+}
+
+// Exact top-64 and recall hits by bound-and-rescore.  With x = x_h + x_l + x_r
+// (x_h = bf16(x), x_l = bf16(x - x_h)), the three bf16 MFMA products
+// a3 = q_h.k_h + q_h.k_l + q_l.k_h miss q.k by the dropped terms (at most about
+// 3 * 2^-16 sum|q_i k_i|) plus float32 accumulation (at most 384 * 2^-24 of the
+// same sum), so |a3 - q.k| <= E = kExactEps3 * ||q|| ||k|| with 40% margin.
+// The three passes of score_mfma_kernel run on these intervals: moments of the
+// single product q_h.k_h (only a prediction), a histogram of the lower bounds
+// a3 - E, and a gate on the upper bounds a3 + E at the bin where the
+// lower-bound count reaches 64: every key whose exact score can reach the 64th
+// exact score passes it.  Gated keys are rescored in float64 (float32 inputs,
+// so every product is exact) and sorted.  A wave whose rows miss the
+// prediction or gate more than 128 keys is flagged and redone by
+// exact_mfma_kernel.  grid/block as score_mfma_kernel.
+constexpr float kExactEps3 = 1e-4f;
+
+template <bool KBF>
+__global__ __launch_bounds__(128) void exact_bf16_kernel(
+    const void* __restrict__ keys, const uint8_t* __restrict__ khi,
+    const uint8_t* __restrict__ klo, const float* __restrict__ knorm, const float* __restrict__ q,
+    const int* __restrict__ q_pos, int H_q, int H_kv, int N_cap, int N_valid, int Q,
+    int n_tiles_hi, int n_bh, int row_blocks, int chunk, int n_chunks, int k,
+    const int* __restrict__ approx, int* __restrict__ hits, int* __restrict__ exact_idx,
+    KeyF64* __restrict__ part, int* __restrict__ redo) {
+  constexpr int D = saki::kHeadDim;
+  constexpr size_t TB = (size_t)kTile * D * 2;
+  using KO = KeysF64;
+  __shared__ int cand_mem[kMfmaWaves][kMR * kCandRow];
+  __shared__ int hist_mem[kMfmaWaves][kMR * kHistRow];
+  __shared__ float qrow_mem[kMfmaWaves][kMR * D];
+  __shared__ int ccount[kMfmaWaves][kMR];
+  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int waves = blockDim.x / kWave;
+  const long long lb = xcd_logical_block((long long)row_blocks * n_chunks * n_bh);
+  if (lb < 0) return;
+  const int rb = (int)(lb % row_blocks), ch = (int)((lb / row_blocks) % n_chunks);
+  const size_t bh = (size_t)(lb / ((long long)row_blocks * n_chunks));
+  const int b = (int)(bh / H_q), h = (int)(bh % H_q);
+  const int gkv = h / (H_q / H_kv);
+  const size_t bg = (size_t)b * H_kv + gkv;
+  const int row0 = (rb * waves + wave) * kMR;
+  if (row0 >= Q) return;
+  const int qi = lane % 16, g = lane / 16;
+  const int my_row = row0 + qi;
+  const bool row_ok = my_row < Q;
+  const int my_lim = row_limit(my_row, Q, N_valid, q_pos);
+  const int kmax = wave_max_i(my_lim);
+  const int kmin = wave_min_i(row_ok ? my_lim : INT_MAX);
+  const int kbeg = ch * chunk;
+  const int kend = min(kbeg + chunk, kmax);
+  int* cand = cand_mem[wave];
+  int* hist = hist_mem[wave];
+  float* qrows = qrow_mem[wave];
+  const size_t hoff = bg * n_tiles_hi * TB;
+  const float* kn = knorm + bg * N_valid;
+
+  // query: bf16 hi/lo operands (dims 32kk + 8g .. +7), float32 copy in LDS,
+  // norm bound
+  bf16x8_t qh[4], ql[4];
+  float qn;
+  {
+    const float* qr = q + (bh * Q + (row_ok ? my_row : row0)) * D;
+    float ss = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      float fh[8], fl[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float f = row_ok ? qr[32 * kk + 8 * g + e] : 0.f;
+        ss = fmaf(f, f, ss);
+        qrows[qi * D + 32 * kk + 8 * g + e] = f;
+        fh[e] = bf16_round(f);
+        fl[e] = bf16_round(f - fh[e]);
+      }
+      qh[kk] = as_bf16x8(pack_bf16x8(fh));
+      ql[kk] = as_bf16x8(pack_bf16x8(fl));
+    }
+    qn = sqrtf(sum_lane_groups(ss)) * (1.f + 1e-5f);
+  }
+  const float eq = kExactEps3 * qn;
+  wave_lds_sync();
+
+  // THREE: a3 (three products) and its error radius; otherwise q_h.k_h only.
+  auto tile = [&](int t0, f32x4_t acc[4], float e[4][4], auto three) {
+    const size_t to = hoff + (size_t)(t0 / kTile) * TB;
+#pragma unroll
+    for (int sub = 0; sub < 4; ++sub) {
+      const int key = 16 * sub + qi;
+      f32x4_t a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const size_t o = to + (size_t)(4 * kk + g) * kTile * 16 + (size_t)key * 16;
+        const bf16x8_t kh = as_bf16x8(*reinterpret_cast<const uint4*>(khi + o));
+        a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, qh[kk], a, 0, 0, 0);
+        if constexpr (decltype(three)::value) {
+          const bf16x8_t kl = as_bf16x8(*reinterpret_cast<const uint4*>(klo + o));
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kl, qh[kk], a, 0, 0, 0);
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, ql[kk], a, 0, 0, 0);
+        }
+      }
+      acc[sub] = a;
+      if constexpr (decltype(three)::value) {
+        // radii of keys t0 + 16 sub + 4g .. +3 (keys past N_valid are masked)
+        const int kb = t0 + 16 * sub + 4 * g;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) e[sub][v] = (kb + v < N_valid) ? eq * kn[kb + v] : 0.f;
+      }
+    }
+  };
+  using One = std::integral_constant<bool, false>;
+  using Three = std::integral_constant<bool, true>;
+
+  // ---- pass 1: moments of the approximate scores
+  float sum = 0.f, sumsq = 0.f;
+  for (int t0 = kbeg; t0 < kend; t0 += kTile) {
+    f32x4_t acc[4];
+    float e[4][4];
+    tile(t0, acc, e, One{});
+    const bool need_mask = t0 + kTile > kmin;
+#pragma unroll
+    for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        float x = acc[sub][v];
+        if (need_mask && t0 + 16 * sub + 4 * g + v >= my_lim) x = 0.f;
+        sum += x;
+        sumsq = fmaf(x, x, sumsq);
+      }
+  }
+  sum = sum_lane_groups(sum);
+  sumsq = sum_lane_groups(sumsq);
+  const int n_row = row_ok ? max(0, min(my_lim, kend) - kbeg) : 0;
+  int mode = kModeAll;
+  float inv_w = 0.f, off = 0.f;
+  if (n_row > kCollect) {
+    const float mean = sum / (float)n_row;
+    const float sd = sqrtf(fmaxf(sumsq / (float)n_row - mean * mean, 0.f));
+    if (sd > 0.f && isfinite(sd) && isfinite(mean)) {
+      const float t_hat = mean + sd * normal_upper_quantile((float)kList / (float)n_row);
+      const float lo = t_hat - 2.f * sd;
+      inv_w = (float)(kBins - 2) / (3.f * sd);
+      off = 1.f - lo * inv_w;
+      mode = kModeHist;
+    } else {
+      mode = kModeFallback;
+    }
+  }
+
+  // ---- pass 2: histogram of the lower bounds
+  float gate = -INFINITY;
+  if (__ballot(mode == kModeHist) != 0) {
+    for (int i = lane; i < kMR * kHistRow; i += kWave) hist[i] = 0;
+    wave_lds_sync();
+    for (int t0 = kbeg; t0 < kend; t0 += kTile) {
+      f32x4_t acc[4];
+      float e[4][4];
+      tile(t0, acc, e, Three{});
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float x = fmaf(acc[sub][v] - e[sub][v], inv_w, off);
+          if (mode == kModeHist && x >= 1.f && t0 + 16 * sub + 4 * g + v < my_lim)
+            atomicAdd(&hist[qi * kHistRow + min((int)x, kBins - 1)], 1);
+        }
+    }
+    wave_lds_sync();
+    for (int r = 0; r < kMR; ++r) {
+      if (__builtin_amdgcn_readlane(mode, r) != kModeHist) continue;
+      int x = hist[r * kHistRow + (kBins - 1 - lane)];
+      if (lane == kBins - 1) x = 0;
+#pragma unroll
+      for (int d = 1; d < kWave; d <<= 1) {
+        const int t = __shfl_up(x, d, kWave);
+        if (lane >= d) x += t;
+      }
+      const uint64_t reach = __ballot(x >= kList);
+      const int new_mode = reach == 0 ? (int)kModeFallback : (int)kModeHist;
+      const float bstar = reach == 0 ? 0.f : (float)(kBins - 1 - __builtin_ctzll(reach));
+      if (qi == r) {
+        mode = new_mode;
+        gate = bstar;
+      }
+    }
+  }
+
+  // ---- pass 3: collect the keys whose upper bound reaches the gate
+  bool fallback = __ballot(mode == kModeFallback) != 0;
+  if (!fallback) {
+    if (lane < kMR) ccount[wave][lane] = 0;
+    wave_lds_sync();
+    for (int t0 = kbeg; t0 < kend; t0 += kTile) {
+      f32x4_t acc[4];
+      float e[4][4];
+      tile(t0, acc, e, Three{});
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int key = t0 + 16 * sub + 4 * g + v;
+          const bool take = key < my_lim &&
+                            (mode == kModeAll || fmaf(acc[sub][v] + e[sub][v], inv_w, off) >= gate);
+          if (take) {
+            const int pos = atomicAdd(&ccount[wave][qi], 1);
+            if (pos < kCollect) cand[qi * kCandRow + pos] = key;
+          }
+        }
+    }
+    wave_lds_sync();
+    fallback = __ballot(lane < kMR && ccount[wave][lane < kMR ? lane : 0] > kCollect) != 0;
+  }
+  if (lane == 0) redo[lb * kMfmaWaves + wave] = fallback ? 1 : 0;
+  if (fallback) return;
+
+  // ---- rescoring in float64 and the exact top-64 of each row
+  const size_t kbase = bg * N_cap;
+  for (int r = 0; r < kMR; ++r) {
+    const int i = row0 + r;
+    if (i >= Q) break;
+    const int c = ccount[wave][r];
+    KeyF64 best = KO::pad();
+    for (int base = 0; base < c; base += kWave) {
+      KeyF64 x = KO::pad();
+      if (base + lane < c) {
+        const int j = cand[r * kCandRow + base + lane];
+        double acc = 0.0;
+        if constexpr (KBF) {
+          const uint16_t* kr = reinterpret_cast<const uint16_t*>(keys) + (kbase + j) * D;
+#pragma unroll 4
+          for (int d8 = 0; d8 < D; d8 += 8) {
+            float f[8];
+            unpack_piece<true>(*reinterpret_cast<const uint4*>(kr + d8), f);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc = fma((double)qrows[r * D + d8 + e], (double)f[e], acc);
+          }
+        } else {
+          const float* kr = reinterpret_cast<const float*>(keys) + (kbase + j) * D;
+#pragma unroll 4
+          for (int d4 = 0; d4 < D; d4 += 4) {
+            const float4 f = *reinterpret_cast<const float4*>(kr + d4);
+            acc = fma((double)qrows[r * D + d4 + 0], (double)f.x, acc);
+            acc = fma((double)qrows[r * D + d4 + 1], (double)f.y, acc);
+            acc = fma((double)qrows[r * D + d4 + 2], (double)f.z, acc);
+            acc = fma((double)qrows[r * D + d4 + 3], (double)f.w, acc);
+          }
+        }
+        x = KO::make(acc, j);
+      }
+      wave_sort<KO>(x);
+      if (base == 0) best = x;
+      else wave_merge<KO>(best, x);
+    }
+    exact_row_out<KO>(best, bh * Q + i, ch, n_chunks, k, approx, hits, exact_idx, part);
   }
 }
 
@@ -975,18 +1276,30 @@ void launch_recall(const void* keys, const float* q, const int* q_pos, int B, in
   KeyF64* part = p.n_chunks > 1 ? reinterpret_cast<KeyF64*>(ws + p.part_off) : nullptr;
   dim3 grid((unsigned)(p.row_blocks * p.n_chunks), B * H_q);
   dim3 block(kWave * p.waves);
-  if (p.mfma)
+  if (p.mfma) {
+    const int nt_hi = (int)saki::n_tiles(N_valid);
+    uint8_t* khi = ws + p.z_off;
+    uint8_t* klo = khi + (size_t)B * H_kv * nt_hi * kTile * saki::kHeadDim * 2;
+    float* knorm = reinterpret_cast<float*>(ws + p.b_off);
+    int* redo = reinterpret_cast<int*>(ws + p.flag_off);
+    if (nt_hi > 0)
+      hipLaunchKernelGGL((keys_hi_kernel<KBF>), dim3(nt_hi, B * H_kv), dim3(256), 0, s, keys, N_cap,
+                         N_valid, nt_hi, khi, klo, knorm);
+    hipLaunchKernelGGL((exact_bf16_kernel<KBF>), xcd_grid(p, B * H_q), block, 0, s, keys, khi,
+                       klo, knorm, q, q_pos, H_q, H_kv, N_cap, N_valid, Q, nt_hi, B * H_q,
+                       p.row_blocks, p.chunk, p.n_chunks, k, approx, hits, exact_idx, part, redo);
     hipLaunchKernelGGL((exact_mfma_kernel<KBF>), xcd_grid(p, B * H_q), block, 0, s, keys, q,
                        q_pos, H_q, H_kv, N_cap, N_valid, Q, p.row_blocks, p.chunk, p.n_chunks, k,
-                       approx, hits, exact_idx, part, B * H_q);
-  else if (p.rows == 4)
+                       approx, hits, exact_idx, part, B * H_q, (const int*)redo);
+  } else if (p.rows == 4) {
     hipLaunchKernelGGL((exact_stream_kernel<KBF, 4>), grid, block, 0, s, keys, q, q_pos, H_q,
                        H_kv, N_cap, N_valid, Q, p.row_blocks, p.chunk, p.n_chunks, k, approx,
                        hits, exact_idx, part);
-  else
+  } else {
     hipLaunchKernelGGL((exact_stream_kernel<KBF, 1>), grid, block, 0, s, keys, q, q_pos, H_q,
                        H_kv, N_cap, N_valid, Q, p.row_blocks, p.chunk, p.n_chunks, k, approx,
                        hits, exact_idx, part);
+  }
   if (p.n_chunks > 1)
     hipLaunchKernelGGL((merge_kernel<KeysF64, true>), dim3((unsigned)((rows + 3) / 4)),
                        dim3(256), 0, s, part, rows, p.n_chunks, k, exact_idx, nullptr, approx,
@@ -1123,7 +1436,7 @@ int saki_recall(const void* keys, int key_dtype, const float* q, const int* q_po
   if (!dtype_ok(key_dtype) || k < 1 || k > kMaxK) return SAKI_ERR_UNSUPPORTED;
   if (Q == 0) return SAKI_OK;
   if (!keys || !q || !approx_idx || !hits) return SAKI_ERR_ARG;
-  const saki::Plan p = saki::recall_plan(B, H_q, Q, N_valid);
+  const saki::Plan p = saki::recall_plan(B, H_q, H_kv, Q, N_valid);
   if (ws_bytes < p.ws_bytes) return SAKI_ERR_WORKSPACE;
   if (p.ws_bytes > 0 && !ws) return SAKI_ERR_ARG;
   if ((size_t)p.row_blocks * p.n_chunks > 0x7fffffffu) return SAKI_ERR_UNSUPPORTED;

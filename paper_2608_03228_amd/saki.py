@@ -52,7 +52,7 @@ def lib():
         "saki_score_topk_workspace_bytes": (sz, [ip, ip, ip, ip, ip, ip, ip]),
         "saki_score_topk": (ip, [vp, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, ip, vp, vp, ip,
                                  vp, vp, vp, sz, vp]),
-        "saki_recall_workspace_bytes": (sz, [ip, ip, ip, ip, ip, ip]),
+        "saki_recall_workspace_bytes": (sz, [ip, ip, ip, ip, ip, ip, ip]),
         "saki_recall": (ip, [vp, ip, vp, vp, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, vp, vp,
                              sz, vp]),
     }
@@ -139,8 +139,8 @@ def saki_score_topk_workspace_bytes(B, H_q, Q, N_valid, r, k, sketch) -> int:
                                                      _DTYPES[sketch]))
 
 
-def saki_recall_workspace_bytes(B, H_q, Q, N_valid, d, k) -> int:
-    return int(lib().saki_recall_workspace_bytes(B, H_q, Q, N_valid, d, k))
+def saki_recall_workspace_bytes(B, H_q, H_kv, Q, N_valid, d, k) -> int:
+    return int(lib().saki_recall_workspace_bytes(B, H_q, H_kv, Q, N_valid, d, k))
 
 
 # ------------------------------------------------------------------ GPU calls
@@ -237,7 +237,7 @@ def saki_recall(keys, q, approx_idx, N_valid: int, q_pos=None, k: int = 64, ws=N
     qp = _dev(q, (torch.float32,), "q")
     B, H_kv, N_cap, d = keys.shape
     _, H_q, Q, _ = q.shape
-    need = saki_recall_workspace_bytes(B, H_q, Q, N_valid, d, k)
+    need = saki_recall_workspace_bytes(B, H_q, H_kv, Q, N_valid, d, k)
     if ws is None:
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
     if hits is None:

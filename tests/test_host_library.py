@@ -125,8 +125,8 @@ def test_size_helpers():
     assert S.saki_score_topk_workspace_bytes(1, 32, 4032, 4096, 32, 65, "bf16") == 0
     # decode rows are split over many key chunks -> room for partial lists
     assert S.saki_score_topk_workspace_bytes(1, 32, 1, 1 << 20, 32, 64, "bf16") > 32 * 64 * 8
-    assert S.saki_recall_workspace_bytes(1, 32, 1, 1 << 20, 128, 64) > 0
-    assert S.saki_recall_workspace_bytes(1, 32, 1, 1 << 20, 64, 64) == 0
+    assert S.saki_recall_workspace_bytes(1, 32, 8, 1, 1 << 20, 128, 64) > 0
+    assert S.saki_recall_workspace_bytes(1, 32, 8, 1, 1 << 20, 64, 64) == 0
 
 
 def test_argument_validation_without_launch(lib):
