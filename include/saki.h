@@ -77,12 +77,17 @@ int saki_version(void);
  * eigenvalues below floor_rel * lambda_max are clamped to that floor (a moment
  * with lambda_max <= 0 is replaced by the identity).  C = Sigma_q^{1/2}
  * Sigma_k^{1/2} with symmetric roots; C = U diag(sigma) V^T with sigma
- * descending and each (u_i, v_i) signed so that the largest-magnitude entry of
- * v_i is positive (the lowest index on ties).  Outputs
+ * descending.  Outputs
  *     B_q = Sigma_q^{-1/2} U_r diag(sigma_r)^{1/2},
- *     B_k = Sigma_k^{-1/2} V_r diag(sigma_r)^{1/2}.
+ *     B_k = Sigma_k^{-1/2} V_r diag(sigma_r)^{1/2},
+ * each pair (u_i, v_i) signed so that the largest-magnitude entry of column i
+ * of B_k is positive (the lowest index on ties).  The factors do not depend
+ * on which square root of the moments is used: when both moments are safely
+ * above the floor the library takes the Cholesky route (M = L_k^T Sigma_q L_k
+ * with Sigma_k = L_k L_k^T, whose eigenvectors give the same B_q, B_k).
  * With SAKI_METHOD_KEY_PCA instead B_q = B_k = the top-r eigenvectors of
- * Sigma_k (signed the same way), sigma = eigenvalues of Sigma_k, descending.
+ * Sigma_k (each column's largest-magnitude entry positive), sigma = eigenvalues
+ * of Sigma_k, descending.
  *
  *   q_cal      host float [H_q, T, d]   calibration queries (pre-RoPE)
  *   k_cal      host float [H_kv, T, d]  calibration keys of the same tokens
