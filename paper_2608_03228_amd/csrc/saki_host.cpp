@@ -24,6 +24,8 @@
 #include "saki.h"
 #include "saki_internal.h"
 
+#include <immintrin.h>
+
 #include <algorithm>
 #include <atomic>
 #include <cmath>
@@ -37,34 +39,136 @@ namespace {
 
 using Mat = std::vector<double>;  // row-major square matrix
 
-// C = A * B for n x n row-major matrices (i-k-j order, contiguous inner loop).
-void matmul(int n, const double* A, const double* B, double* C) {
-  std::fill(C, C + (size_t)n * n, 0.0);
-  for (int i = 0; i < n; ++i) {
-    double* ci = C + (size_t)i * n;
-    for (int k = 0; k < n; ++k) {
-      const double a = A[(size_t)i * n + k];
-      const double* bk = B + (size_t)k * n;
-      for (int j = 0; j < n; ++j) ci[j] += a * bk[j];
+// ---------------------------------------------------------------- AVX2 kernels
+// The library is built for x86-64-v3 hosts (AVX2 + FMA); these helpers keep
+// the O(T d^2) and O(d^3) steps of the calibration in 256-bit registers.
+
+inline double hsum(__m256d v) {
+  const __m128d lo = _mm256_castpd256_pd128(v), hi = _mm256_extractf128_pd(v, 1);
+  const __m128d s = _mm_add_pd(lo, hi);
+  return _mm_cvtsd_f64(_mm_add_sd(s, _mm_unpackhi_pd(s, s)));
+}
+
+// sum_i a[i] * b[i]
+double dot(const double* a, const double* b, int n) {
+  __m256d s0 = _mm256_setzero_pd(), s1 = _mm256_setzero_pd();
+  int i = 0;
+  for (; i + 8 <= n; i += 8) {
+    s0 = _mm256_fmadd_pd(_mm256_loadu_pd(a + i), _mm256_loadu_pd(b + i), s0);
+    s1 = _mm256_fmadd_pd(_mm256_loadu_pd(a + i + 4), _mm256_loadu_pd(b + i + 4), s1);
+  }
+  double acc = hsum(_mm256_add_pd(s0, s1));
+  for (; i < n; ++i) acc += a[i] * b[i];
+  return acc;
+}
+
+// y[i] += alpha * x[i]
+void axpy(double alpha, const double* x, double* y, int n) {
+  const __m256d a = _mm256_set1_pd(alpha);
+  int i = 0;
+  for (; i + 4 <= n; i += 4)
+    _mm256_storeu_pd(y + i, _mm256_fmadd_pd(a, _mm256_loadu_pd(x + i), _mm256_loadu_pd(y + i)));
+  for (; i < n; ++i) y[i] += alpha * x[i];
+}
+
+// y[i] += a * x[i] + b * z[i]
+void axpy2(double a, const double* x, double b, const double* z, double* y, int n) {
+  const __m256d va = _mm256_set1_pd(a), vb = _mm256_set1_pd(b);
+  int i = 0;
+  for (; i + 4 <= n; i += 4) {
+    __m256d t = _mm256_fmadd_pd(va, _mm256_loadu_pd(x + i), _mm256_loadu_pd(y + i));
+    _mm256_storeu_pd(y + i, _mm256_fmadd_pd(vb, _mm256_loadu_pd(z + i), t));
+  }
+  for (; i < n; ++i) y[i] += a * x[i] + b * z[i];
+}
+
+// sqrt(a^2 + b^2); the plain formula where it cannot over- or underflow.
+inline double hypot2(double a, double b) {
+  const double m = std::max(std::fabs(a), std::fabs(b));
+  if (m > 1e-150 && m < 1e150) return std::sqrt(a * a + b * b);
+  return std::hypot(a, b);
+}
+
+// C[i][j] += sum_{k in [kb(i0,j0), ke(i0,j0))} A(i, k) * B[k][j] for one 4 x 8
+// block (i0.., j0..) of row-major n x n matrices; A(i, k) = A[i*sai + k*sak]
+// so that a transposed operand needs no copy.
+inline void block4x8(int n, const double* A, long sai, long sak, const double* B, double* C,
+                     int i0, int j0, int kb, int ke) {
+  __m256d c[4][2];
+  for (int a = 0; a < 4; ++a) c[a][0] = c[a][1] = _mm256_setzero_pd();
+  for (int k = kb; k < ke; ++k) {
+    const __m256d b0 = _mm256_loadu_pd(B + (size_t)k * n + j0);
+    const __m256d b1 = _mm256_loadu_pd(B + (size_t)k * n + j0 + 4);
+    for (int a = 0; a < 4; ++a) {
+      const __m256d x = _mm256_broadcast_sd(A + (i0 + a) * sai + k * sak);
+      c[a][0] = _mm256_fmadd_pd(x, b0, c[a][0]);
+      c[a][1] = _mm256_fmadd_pd(x, b1, c[a][1]);
     }
+  }
+  for (int a = 0; a < 4; ++a) {
+    double* ci = C + (size_t)(i0 + a) * n + j0;
+    _mm256_storeu_pd(ci, _mm256_add_pd(_mm256_loadu_pd(ci), c[a][0]));
+    _mm256_storeu_pd(ci + 4, _mm256_add_pd(_mm256_loadu_pd(ci + 4), c[a][1]));
   }
 }
 
+// C = A * B for n x n row-major matrices (i-k-j order, contiguous inner loop).
+void matmul(int n, const double* A, const double* B, double* C) {
+  std::fill(C, C + (size_t)n * n, 0.0);
+  if (n % 8 == 0) {
+    for (int i0 = 0; i0 < n; i0 += 4)
+      for (int j0 = 0; j0 < n; j0 += 8) block4x8(n, A, n, 1, B, C, i0, j0, 0, n);
+    return;
+  }
+  for (int i = 0; i < n; ++i) {
+    double* ci = C + (size_t)i * n;
+    for (int k = 0; k < n; ++k) axpy(A[(size_t)i * n + k], B + (size_t)k * n, ci, n);
+  }
+}
+
+// M = L^T S L for lower-triangular L and symmetric S (n x n row-major).
+// W = S L skips the zero upper part of L (column block j0 needs k >= j0);
+// M = L^T W needs k >= i for row i, and only blocks on or below the diagonal
+// are formed before mirroring.
+void congruence_lower(int n, const double* S, const double* L, double* M) {
+  std::vector<double> W((size_t)n * n, 0.0);
+  std::fill(M, M + (size_t)n * n, 0.0);
+  if (n % 8 == 0) {
+    for (int i0 = 0; i0 < n; i0 += 4)
+      for (int j0 = 0; j0 < n; j0 += 8) block4x8(n, S, n, 1, L, W.data(), i0, j0, j0, n);
+    for (int i0 = 0; i0 < n; i0 += 4)
+      for (int j0 = 0; j0 < i0 + 4; j0 += 8) block4x8(n, L, 1, n, W.data(), M, i0, j0, i0, n);
+  } else {
+    for (int i = 0; i < n; ++i)
+      for (int k = 0; k < n; ++k) axpy(S[(size_t)i * n + k], L + (size_t)k * n, W.data() + (size_t)i * n, k + 1);
+    for (int k = 0; k < n; ++k)
+      for (int i = 0; i <= k; ++i) axpy(L[(size_t)k * n + i], W.data() + (size_t)k * n, M + (size_t)i * n, n);
+  }
+  for (int i = 0; i < n; ++i)
+    for (int j = 0; j < i; ++j) M[(size_t)j * n + i] = M[(size_t)i * n + j];
+}
+
 // S = (1/T) sum_t (x_t - mu)(x_t - mu)^T for the T rows of X (float, T x d);
-// mu may be null (uncentred).  Four tokens per sweep over the triangle.
+// mu may be null (uncentred).  Tokens are converted to float64 in blocks and
+// the lower triangle is accumulated in 4 x 8 register blocks.
 void moment(int T, int d, const float* X, const double* mu, double* S) {
   std::fill(S, S + (size_t)d * d, 0.0);
-  std::vector<double> x((size_t)4 * d);
-  for (int t0 = 0; t0 < T; t0 += 4) {
-    const int nb = std::min(4, T - t0);
-    for (int b = 0; b < 4; ++b)
+  constexpr int TB = 128;
+  std::vector<double> x((size_t)TB * d);
+  for (int t0 = 0; t0 < T; t0 += TB) {
+    const int nb = std::min(TB, T - t0);
+    for (int b = 0; b < nb; ++b)
       for (int i = 0; i < d; ++i)
-        x[(size_t)b * d + i] = b < nb ? (double)X[(size_t)(t0 + b) * d + i] - (mu ? mu[i] : 0.0) : 0.0;
-    const double *x0 = x.data(), *x1 = x0 + d, *x2 = x1 + d, *x3 = x2 + d;
-    for (int i = 0; i < d; ++i) {
-      double* row = S + (size_t)i * d;
-      const double a0 = x0[i], a1 = x1[i], a2 = x2[i], a3 = x3[i];
-      for (int j = 0; j <= i; ++j) row[j] += a0 * x0[j] + a1 * x1[j] + a2 * x2[j] + a3 * x3[j];
+        x[(size_t)b * d + i] = (double)X[(size_t)(t0 + b) * d + i] - (mu ? mu[i] : 0.0);
+    if (d % 8 == 0) {
+      // the transposed token block: A(i, t) = x[t][i]
+      for (int i0 = 0; i0 < d; i0 += 4)
+        for (int j0 = 0; j0 < i0 + 4; j0 += 8) block4x8(d, x.data(), 1, d, x.data(), S, i0, j0, 0, nb);
+    } else {
+      for (int b = 0; b < nb; ++b) {
+        const double* xb = x.data() + (size_t)b * d;
+        for (int i = 0; i < d; ++i) axpy(xb[i], xb, S + (size_t)i * d, i + 1);
+      }
     }
   }
   for (int i = 0; i < d; ++i)
@@ -81,16 +185,13 @@ bool cholesky(int n, const double* S, double shift, double* L) {
   std::fill(L, L + (size_t)n * n, 0.0);
   for (int j = 0; j < n; ++j) {
     const double* lj = L + (size_t)j * n;
-    double dsum = S[(size_t)j * n + j] - shift;
-    for (int k = 0; k < j; ++k) dsum -= lj[k] * lj[k];
+    const double dsum = S[(size_t)j * n + j] - shift - dot(lj, lj, j);
     if (!(dsum > 0.0) || !std::isfinite(dsum)) return false;
     const double piv = std::sqrt(dsum);
     L[(size_t)j * n + j] = piv;
     for (int i = j + 1; i < n; ++i) {
       const double* li = L + (size_t)i * n;
-      double acc = S[(size_t)i * n + j];
-      for (int k = 0; k < j; ++k) acc -= li[k] * lj[k];
-      L[(size_t)i * n + j] = acc / piv;
+      L[(size_t)i * n + j] = (S[(size_t)i * n + j] - dot(li, lj, j)) / piv;
     }
   }
   return true;
@@ -103,12 +204,14 @@ double frobenius(int n, const double* S) {
 }
 
 // True when no eigenvalue of the PSD moment lies below floor_rel * lambda_max
-// (sufficient test); L then holds the Cholesky factor of S itself.
-bool unclamped_cholesky(int n, const double* S, double floor_rel, double* L) {
+// (sufficient test: S - floor_rel ||S||_F I is positive definite and
+// ||S||_F >= lambda_max).  With want_factor, L then holds the Cholesky factor
+// of S itself; otherwise L is scratch.
+bool unclamped_cholesky(int n, const double* S, double floor_rel, double* L, bool want_factor) {
   const double f = frobenius(n, S);
   if (!(f > 0.0) || !std::isfinite(f)) return false;
   if (!cholesky(n, S, floor_rel * f, L)) return false;
-  return cholesky(n, S, 0.0, L);
+  return !want_factor || cholesky(n, S, 0.0, L);
 }
 
 // Flip column m of both factors (d x r, row-major, float output) when the
@@ -125,68 +228,89 @@ void store_pair(int d, int r, int m, const double* bq, const double* bk, float* 
   }
 }
 
-// Reduce symmetric `a` (n x n, overwritten) to tridiagonal form T = Q^T A Q.
-// On return diag/off hold T's diagonal and sub-diagonal (off[n-1] = 0) and
-// `q` (n x n row-major) holds Q.
-void tridiagonalize(int n, double* a, double* diag, double* off, double* q) {
-  std::fill(q, q + (size_t)n * n, 0.0);
-  for (int i = 0; i < n; ++i) q[(size_t)i * n + i] = 1.0;
-  std::vector<double> v(n), p(n), w(n);
+// Householder reduction of symmetric `a` (n x n, lower triangle read and
+// overwritten; the upper triangle is ignored) to tridiagonal
+// form T = Q^T A Q, Q = H_0 H_1 ... H_{n-3} with H_k = I - beta_k v_k v_k^T
+// acting on indices k+1 .. n-1 (Golub & Van Loan, Sec. 8.3.1).  diag/off
+// receive T's diagonal and sub-diagonal (off[n-1] = 0); row k of `hv` holds
+// v_k in its entries k+1 .. n-1 and beta[k] its factor (0 when H_k = I).
+void householder_tridiag(int n, double* a, double* diag, double* off, double* hv, double* beta) {
+  std::fill(hv, hv + (size_t)n * n, 0.0);
+  std::fill(beta, beta + n, 0.0);
+  std::vector<double> p(n), w(n);
   for (int k = 0; k + 2 < n; ++k) {
     const int m = n - k - 1;  // length of the column part below the diagonal
-    double sumsq = 0.0;
-    for (int i = 0; i < m; ++i) {
-      const double x = a[(size_t)(k + 1 + i) * n + k];
-      v[i] = x;
-      sumsq += x * x;
-    }
+    double* v = hv + (size_t)k * n + (k + 1);
+    for (int i = 0; i < m; ++i) v[i] = a[(size_t)(k + 1 + i) * n + k];
+    const double sumsq = dot(v, v, m);
     const double x0 = v[0];
     double alpha = std::sqrt(sumsq);
-    if (alpha == 0.0) continue;              // column already reduced
-    if (x0 > 0) alpha = -alpha;              // reflect away from x0's sign
+    if (alpha == 0.0) { std::fill(v, v + m, 0.0); continue; }  // column already reduced
+    if (x0 > 0) alpha = -alpha;                                // reflect away from x0's sign
     v[0] = x0 - alpha;
     const double vv = sumsq - x0 * x0 + v[0] * v[0];
-    if (vv == 0.0) continue;
-    const double beta = 2.0 / vv;
+    if (vv == 0.0) { std::fill(v, v + m, 0.0); continue; }
+    const double bk = 2.0 / vv;
+    beta[k] = bk;
     // p = beta * A22 v,  K = beta/2 * v.p,  w = p - K v
+    // Only the lower triangle of A22 is kept up to date: row i holds
+    // entries j <= i, and A22 v gathers row i (j < i) and column i (j > i).
+    std::fill(p.begin(), p.begin() + m, 0.0);
     for (int i = 0; i < m; ++i) {
       const double* ai = a + (size_t)(k + 1 + i) * n + (k + 1);
-      double s = 0.0;
-      for (int j = 0; j < m; ++j) s += ai[j] * v[j];
-      p[i] = beta * s;
+      p[i] += dot(ai, v, i) + ai[i] * v[i];
+      axpy(v[i], ai, p.data(), i);
     }
-    double vp = 0.0;
-    for (int i = 0; i < m; ++i) vp += v[i] * p[i];
-    const double K = 0.5 * beta * vp;
+    for (int i = 0; i < m; ++i) p[i] *= bk;
+    const double K = 0.5 * bk * dot(v, p.data(), m);
     for (int i = 0; i < m; ++i) w[i] = p[i] - K * v[i];
-    // A22 -= v w^T + w v^T
-    for (int i = 0; i < m; ++i) {
-      double* ai = a + (size_t)(k + 1 + i) * n + (k + 1);
-      const double vi = v[i], wi = w[i];
-      for (int j = 0; j < m; ++j) ai[j] -= vi * w[j] + wi * v[j];
-    }
-    // column/row k now has a single sub-diagonal entry alpha
-    for (int i = 0; i < m; ++i) {
-      a[(size_t)(k + 1 + i) * n + k] = (i == 0) ? alpha : 0.0;
-      a[(size_t)k * n + (k + 1 + i)] = (i == 0) ? alpha : 0.0;
-    }
-    // Q <- Q (I - beta v v^T) on columns k+1 .. n-1
-    for (int r = 0; r < n; ++r) {
-      double* qr = q + (size_t)r * n + (k + 1);
-      double s = 0.0;
-      for (int j = 0; j < m; ++j) s += qr[j] * v[j];
-      s *= beta;
-      for (int j = 0; j < m; ++j) qr[j] -= s * v[j];
-    }
+    // A22 -= v w^T + w v^T (lower triangle)
+    for (int i = 0; i < m; ++i)
+      axpy2(-v[i], w.data(), -w[i], v, a + (size_t)(k + 1 + i) * n + (k + 1), i + 1);
+    // column k now has a single sub-diagonal entry alpha
+    for (int i = 0; i < m; ++i) a[(size_t)(k + 1 + i) * n + k] = (i == 0) ? alpha : 0.0;
   }
   for (int i = 0; i < n; ++i) diag[i] = a[(size_t)i * n + i];
   for (int i = 0; i + 1 < n; ++i) off[i] = a[(size_t)(i + 1) * n + i];
   off[n - 1] = 0.0;
 }
 
-// Implicit QL on the tridiagonal (diag, off).  zt holds the transpose of the
-// accumulated orthogonal matrix (row i = current column i), so that the
-// rotations update two contiguous rows.  Returns false without convergence.
+// X <- Q X for the Q of householder_tridiag; X is n x c row-major (c
+// vectors side by side), so each reflector is two passes of row axpys.
+void apply_q(int n, const double* hv, const double* beta, double* X, int c) {
+  std::vector<double> t(c);
+  for (int k = n - 3; k >= 0; --k) {
+    if (beta[k] == 0.0) continue;
+    const double* v = hv + (size_t)k * n + (k + 1);
+    const int m = n - k - 1;
+    double* xk = X + (size_t)(k + 1) * c;
+    std::fill(t.begin(), t.end(), 0.0);
+    for (int i = 0; i < m; ++i) axpy(v[i], xk + (size_t)i * c, t.data(), c);  // t = v^T X
+    for (int i = 0; i < m; ++i) axpy(-beta[k] * v[i], t.data(), xk + (size_t)i * c, c);
+  }
+}
+
+// zt <- Q^T = H_{n-3} ... H_0 (row-major n x n), the starting point of the QL
+// eigenvector accumulation.
+void form_qt(int n, const double* hv, const double* beta, double* zt) {
+  std::fill(zt, zt + (size_t)n * n, 0.0);
+  for (int i = 0; i < n; ++i) zt[(size_t)i * n + i] = 1.0;
+  std::vector<double> w(n);
+  for (int k = 0; k + 2 < n; ++k) {
+    if (beta[k] == 0.0) continue;
+    const double* v = hv + (size_t)k * n + (k + 1);
+    const int m = n - k - 1;
+    // rows k+1.. of zt: row_i -= beta v_i (sum_l v_l row_l)
+    std::fill(w.begin(), w.end(), 0.0);
+    for (int l = 0; l < m; ++l) axpy(v[l], zt + (size_t)(k + 1 + l) * n, w.data(), n);
+    for (int i = 0; i < m; ++i) axpy(-beta[k] * v[i], w.data(), zt + (size_t)(k + 1 + i) * n, n);
+  }
+}
+
+// Implicit QL on the tridiagonal (diag, off).  zt, when not null, holds the
+// transpose of the accumulated orthogonal matrix (row i = current column i),
+// so that the rotations update two contiguous rows; without it only the
+// eigenvalues are computed.  Returns false without convergence.
 bool tridiag_ql(int n, double* diag, double* off, double* zt) {
   const double eps = std::numeric_limits<double>::epsilon();
   // Deflation test: relative to the neighbouring diagonal entries, or
@@ -208,14 +332,14 @@ bool tridiag_ql(int n, double* diag, double* off, double* zt) {
       if (++iter > 80) return false;
       // shift from the leading 2x2 block of the unreduced part
       double g = (diag[l + 1] - diag[l]) / (2.0 * off[l]);
-      double rad = std::hypot(g, 1.0);
+      double rad = hypot2(g, 1.0);
       g = diag[m] - diag[l] + off[l] / (g + std::copysign(rad, g));
       double s = 1.0, c = 1.0, p = 0.0;
       bool split = false;
       for (int i = m - 1; i >= l; --i) {
         const double f = s * off[i];
         const double b = c * off[i];
-        rad = std::hypot(f, g);
+        rad = hypot2(f, g);
         off[i + 1] = rad;
         if (rad == 0.0) {  // an off-diagonal underflowed: deflate and restart
           diag[i + 1] -= p;
@@ -230,12 +354,14 @@ bool tridiag_ql(int n, double* diag, double* off, double* zt) {
         p = s * rad;
         diag[i + 1] = g + p;
         g = c * rad - b;
-        double* zi = zt + (size_t)i * n;
-        double* zj = zt + (size_t)(i + 1) * n;
-        for (int k = 0; k < n; ++k) {
-          const double zik = zi[k], zjk = zj[k];
-          zj[k] = s * zik + c * zjk;
-          zi[k] = c * zik - s * zjk;
+        if (zt) {
+          double* zi = zt + (size_t)i * n;
+          double* zj = zt + (size_t)(i + 1) * n;
+          for (int k = 0; k < n; ++k) {
+            const double zik = zi[k], zjk = zj[k];
+            zj[k] = s * zik + c * zjk;
+            zi[k] = c * zik - s * zjk;
+          }
         }
       }
       if (split) continue;
@@ -259,10 +385,9 @@ bool sym_eig_rows(int n, const double* A, double* w, double* vt) {
       const double s = 0.5 * (a[(size_t)i * n + j] + a[(size_t)j * n + i]);
       a[(size_t)i * n + j] = a[(size_t)j * n + i] = s;
     }
-  std::vector<double> diag(n), off(n);
-  tridiagonalize(n, a.data(), diag.data(), off.data(), q.data());
-  for (int i = 0; i < n; ++i)
-    for (int j = 0; j < n; ++j) zt[(size_t)j * n + i] = q[(size_t)i * n + j];
+  std::vector<double> diag(n), off(n), beta(n);
+  householder_tridiag(n, a.data(), diag.data(), off.data(), q.data(), beta.data());
+  form_qt(n, q.data(), beta.data(), zt.data());
   if (!tridiag_ql(n, diag.data(), off.data(), zt.data())) return false;
   std::vector<int> order(n);
   for (int i = 0; i < n; ++i) order[i] = i;
@@ -272,6 +397,141 @@ bool sym_eig_rows(int n, const double* A, double* w, double* vt) {
     w[i] = diag[order[i]];
     std::memcpy(vt + (size_t)i * n, zt.data() + (size_t)order[i] * n, sizeof(double) * n);
   }
+  return true;
+}
+
+// LU factorisation with partial pivoting of T - lambda I for the symmetric
+// tridiagonal T (diag, off); pivots smaller than `tiny` are replaced by
+// +-tiny, as inverse iteration requires, and stored as reciprocals.
+struct ShiftedTridiagLU {
+  std::vector<double> rdg, du, du2, dl;
+  std::vector<unsigned char> swap;
+  explicit ShiftedTridiagLU(int n) : rdg(n), du(n), du2(n), dl(n), swap(n) {}
+
+  void factor(int n, const double* diag, const double* off, double lambda, double tiny) {
+    double* dg = rdg.data();
+    for (int i = 0; i < n; ++i) dg[i] = diag[i] - lambda;
+    for (int i = 0; i + 1 < n; ++i) { du[i] = off[i]; dl[i] = off[i]; }
+    for (int i = 0; i + 1 < n; ++i) {
+      du2[i] = 0.0;
+      if (std::fabs(dg[i]) >= std::fabs(dl[i])) {
+        swap[i] = 0;
+        const double piv = dg[i] != 0.0 ? dg[i] : tiny;
+        const double f = dl[i] / piv;
+        dl[i] = f;
+        dg[i + 1] -= f * du[i];
+      } else {  // rows i and i+1 change places
+        swap[i] = 1;
+        const double f = dg[i] / dl[i];
+        dg[i] = dl[i];
+        dl[i] = f;
+        const double t = du[i];
+        du[i] = dg[i + 1];
+        dg[i + 1] = t - f * dg[i + 1];
+        if (i + 2 < n) {
+          du2[i] = du[i + 1];
+          du[i + 1] = -f * du[i + 1];
+        }
+      }
+    }
+    for (int i = 0; i < n; ++i) {
+      if (std::fabs(dg[i]) < tiny) dg[i] = dg[i] < 0.0 ? -tiny : tiny;
+      dg[i] = 1.0 / dg[i];
+    }
+  }
+
+  // b <- (T - lambda I)^{-1} b
+  void solve(int n, double* b) const {
+    for (int i = 0; i + 1 < n; ++i) {  // L y = P b
+      if (swap[i]) {
+        const double t = b[i] - dl[i] * b[i + 1];
+        b[i] = b[i + 1];
+        b[i + 1] = t;
+      } else {
+        b[i + 1] -= dl[i] * b[i];
+      }
+    }
+    b[n - 1] *= rdg[n - 1];  // U x = y
+    if (n > 1) b[n - 2] = (b[n - 2] - du[n - 2] * b[n - 1]) * rdg[n - 2];
+    for (int i = n - 3; i >= 0; --i) b[i] = (b[i] - du[i] * b[i + 1] - du2[i] * b[i + 2]) * rdg[i];
+  }
+};
+
+// The r largest eigenpairs of symmetric A (n x n row-major, read from its
+// lower triangle): w receives all n
+// eigenvalues in descending order, row m of `vecs` (r x n) the unit
+// eigenvector of w[m].  Householder tridiagonalisation, eigenvalues by QL
+// without vectors, then inverse iteration on the tridiagonal for the r
+// vectors (Golub & Van Loan, Sec. 8.2.2 and 8.4), re-orthogonalised within
+// clusters of close eigenvalues, and back-transformation by the reflectors.
+// Cost 2n^3 + O(n^2 r) flops instead of the roughly 9n^3 of the full solver.
+bool sym_eig_top(int n, const double* A, int r, double* w, double* vecs) {
+  for (size_t i = 0; i < (size_t)n * n; ++i)
+    if (!std::isfinite(A[i])) return false;
+  Mat a(A, A + (size_t)n * n), hv((size_t)n * n);  // the lower triangle defines A
+  std::vector<double> diag(n), off(n), beta(n);
+  householder_tridiag(n, a.data(), diag.data(), off.data(), hv.data(), beta.data());
+  std::vector<double> ev(diag), eo(off);
+  if (!tridiag_ql(n, ev.data(), eo.data(), nullptr)) return false;
+  std::sort(ev.begin(), ev.end(), [](double x, double y) { return x > y; });
+  std::copy(ev.begin(), ev.end(), w);
+
+  const double eps = std::numeric_limits<double>::epsilon();
+  double tnorm = 0.0;  // 1-norm of T
+  for (int i = 0; i < n; ++i)
+    tnorm = std::max(tnorm, std::fabs(diag[i]) + std::fabs(off[i]) + (i ? std::fabs(off[i - 1]) : 0.0));
+  if (tnorm == 0.0) tnorm = 1.0;
+  const double cluster_gap = 1e-3 * tnorm;  // re-orthogonalise closer eigenvalues
+  const double tiny = eps * tnorm;
+  const double converged = std::sqrt(0.1 / n);
+  std::vector<double> x(n);
+  ShiftedTridiagLU lu(n);
+  int cluster_begin = 0;
+  double shift_prev = 0.0;
+  uint64_t seed = 0x9E3779B97F4A7C15ull;
+  for (int m = 0; m < r; ++m) {
+    double lambda = ev[m];
+    if (m > 0) {
+      if (shift_prev - lambda > cluster_gap) cluster_begin = m;
+      // equal eigenvalues get distinct shifts so the iterations separate them
+      const double sep = 10.0 * eps * std::max(std::fabs(shift_prev), tnorm * eps);
+      if (lambda > shift_prev - sep) lambda = shift_prev - sep;
+    }
+    shift_prev = lambda;
+    for (int i = 0; i < n; ++i) {  // fixed pseudo-random start in [-1, 1)
+      seed = seed * 6364136223846793005ull + 1442695040888963407ull;
+      x[i] = (double)(seed >> 11) * (2.0 / 9007199254740992.0) - 1.0;
+    }
+    lu.factor(n, diag.data(), off.data(), lambda, tiny);
+    int extra = 0;
+    bool done = false;
+    for (int it = 0; it < 6 && !done; ++it) {
+      double l1 = 0.0;
+      for (int i = 0; i < n; ++i) l1 += std::fabs(x[i]);
+      // start small: a converged solve then grows by about 1 / (eps n)
+      const double scale = n * tnorm * eps / l1;
+      for (int i = 0; i < n; ++i) x[i] *= scale;
+      lu.solve(n, x.data());
+      for (int p = cluster_begin; p < m; ++p) {  // against earlier vectors of the cluster
+        const double* vp = vecs + (size_t)p * n;  // still in the tridiagonal basis
+        axpy(-dot(vp, x.data(), n), vp, x.data(), n);
+      }
+      double amax = 0.0;
+      for (int i = 0; i < n; ++i) amax = std::max(amax, std::fabs(x[i]));
+      if (!std::isfinite(amax) || amax == 0.0) return false;
+      if (amax >= converged && ++extra >= 2) done = true;
+    }
+    const double nrm = std::sqrt(dot(x.data(), x.data(), n));
+    double* vm = vecs + (size_t)m * n;
+    for (int i = 0; i < n; ++i) vm[i] = x[i] / nrm;
+  }
+  // back to the basis of A, all r vectors at once (n x r, then transposed)
+  std::vector<double> X((size_t)n * r);
+  for (int m = 0; m < r; ++m)
+    for (int i = 0; i < n; ++i) X[(size_t)i * r + m] = vecs[(size_t)m * n + i];
+  apply_q(n, hv.data(), beta.data(), X.data(), r);
+  for (int m = 0; m < r; ++m)
+    for (int i = 0; i < n; ++i) vecs[(size_t)m * n + i] = X[(size_t)i * r + m];
   return true;
 }
 
@@ -410,7 +670,7 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
       moment(T, d, k, st.mu.data(), st.sk.data());
       if (method == SAKI_METHOD_OPT) {
         st.L.resize(dd);
-        st.chol = unclamped_cholesky(d, st.sk.data(), floor_rel, st.L.data());
+        st.chol = unclamped_cholesky(d, st.sk.data(), floor_rel, st.L.data(), true);
         if (st.chol) {
           st.ok = true;
         } else {
@@ -451,46 +711,32 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
       moment(T, d, q, nullptr, sq.data());
       std::vector<double> sig(d), bqc(d), bkc(d);
       Mat scratch(dd);
-      if (st.chol && unclamped_cholesky(d, sq.data(), floor_rel, scratch.data())) {
+      if (st.chol && unclamped_cholesky(d, sq.data(), floor_rel, scratch.data(), false)) {
         // ---- Cholesky route: M = L^T Sigma_q L, B_q = L v / sqrt(s), B_k = L^-T v sqrt(s)
         const double* L = st.L.data();
-        Mat W(dd, 0.0), M(dd, 0.0);
-        for (int i = 0; i < d; ++i) {  // W = Sigma_q L  (L lower: column j uses rows k >= j)
-          const double* si = sq.data() + (size_t)i * d;
-          double* wi = W.data() + (size_t)i * d;
-          for (int k = 0; k < d; ++k) {
-            const double a = si[k];
-            const double* lk = L + (size_t)k * d;
-            for (int j = 0; j <= k; ++j) wi[j] += a * lk[j];
-          }
+        Mat M(dd);
+        congruence_lower(d, sq.data(), L, M.data());
+        std::vector<double> w(d), vt((size_t)r * d);
+        if (!sym_eig_top(d, M.data(), r, w.data(), vt.data())) { failed = 1; return; }
+        for (int m = 0; m < d; ++m) sig[m] = std::sqrt(std::max(w[m], 0.0));
+        // all r columns at once (d x r, row-major): P = L V', X = L^-T V'
+        Mat V((size_t)d * r), P((size_t)d * r, 0.0), X((size_t)d * r);
+        for (int m = 0; m < r; ++m)
+          for (int i = 0; i < d; ++i) V[(size_t)i * r + m] = vt[(size_t)m * d + i];
+        for (int i = 0; i < d; ++i)
+          for (int j = 0; j <= i; ++j) axpy(L[(size_t)i * d + j], V.data() + (size_t)j * r, P.data() + (size_t)i * r, r);
+        for (int i = d - 1; i >= 0; --i) {  // L^T X = V by back substitution, row i of L at a time
+          double* xi = X.data() + (size_t)i * r;
+          const double rl = 1.0 / L[(size_t)i * d + i];
+          for (int m = 0; m < r; ++m) xi[m] = V[(size_t)i * r + m] * rl;
+          for (int j = 0; j < i; ++j) axpy(-L[(size_t)i * d + j], xi, V.data() + (size_t)j * r, r);
         }
-        for (int k = 0; k < d; ++k) {  // M = L^T W: row i gathers rows k >= i of W
-          const double* lk = L + (size_t)k * d;
-          const double* wk = W.data() + (size_t)k * d;
-          for (int i = 0; i <= k; ++i) {
-            const double a = lk[i];
-            double* mi = M.data() + (size_t)i * d;
-            for (int j = 0; j < d; ++j) mi[j] += a * wk[j];
-          }
-        }
-        std::vector<double> w(d), vt(dd);
-        if (!sym_eig_rows(d, M.data(), w.data(), vt.data())) { failed = 1; return; }
-        for (int m = 0; m < d; ++m) sig[m] = std::sqrt(std::max(w[d - 1 - m], 0.0));
         for (int m = 0; m < r; ++m) {
-          const double* v = vt.data() + (size_t)(d - 1 - m) * d;
           const double sm = sig[m], rs = std::sqrt(sm);
-          for (int i = 0; i < d; ++i) {  // L v
-            const double* li = L + (size_t)i * d;
-            double acc = 0.0;
-            for (int j = 0; j <= i; ++j) acc += li[j] * v[j];
-            bqc[i] = sm > 0.0 ? acc / rs : 0.0;
+          for (int i = 0; i < d; ++i) {
+            bqc[i] = sm > 0.0 ? P[(size_t)i * r + m] / rs : 0.0;
+            bkc[i] = X[(size_t)i * r + m] * rs;
           }
-          for (int i = d - 1; i >= 0; --i) {  // L^T x = v (back substitution)
-            double acc = v[i];
-            for (int k = i + 1; k < d; ++k) acc -= L[(size_t)k * d + i] * bkc[k];
-            bkc[i] = acc / L[(size_t)i * d + i];
-          }
-          for (int i = 0; i < d; ++i) bkc[i] *= rs;
           store_pair(d, r, m, bqc.data(), bkc.data(), bq, bk);
         }
         if (sigma)
@@ -522,16 +768,16 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
       for (int i = 0; i < d; ++i)
         for (int j = 0; j < d; ++j) Ct[(size_t)j * d + i] = C[(size_t)i * d + j];
       matmul(d, Ct.data(), C.data(), CtC.data());
-      std::vector<double> w(d), vt(dd);
-      if (!sym_eig_rows(d, CtC.data(), w.data(), vt.data())) { failed = 1; return; }
-      for (int m = 0; m < d; ++m) sig[m] = std::sqrt(std::max(w[d - 1 - m], 0.0));
+      std::vector<double> w(d), vt((size_t)r * d);
+      if (!sym_eig_top(d, CtC.data(), r, w.data(), vt.data())) { failed = 1; return; }
+      for (int m = 0; m < d; ++m) sig[m] = std::sqrt(std::max(w[m], 0.0));
       if (sigma)
         for (int m = 0; m < d; ++m) sigma[(size_t)h * d + m] = sig[m];
       if (n_clamped) { n_clamped[2 * h] = nq; n_clamped[2 * h + 1] = nk; }
       // top-r pairs: v_m (row of vt), u_m = C v_m / sigma_m
       std::vector<double> u(d);
       for (int m = 0; m < r; ++m) {
-        const double* v = vt.data() + (size_t)(d - 1 - m) * d;
+        const double* v = vt.data() + (size_t)m * d;
         const double sm = sig[m];
         for (int i = 0; i < d; ++i) {
           double acc = 0.0;

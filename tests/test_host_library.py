@@ -109,6 +109,31 @@ def test_key_pca_and_weight_svd_factors_match_oracle():
         np.testing.assert_allclose(_m(Bq[h], Bk[h]), U @ U.T, atol=2e-6)
 
 
+def test_calibration_with_repeated_singular_values():
+    """Sigma_q = I and Sigma_k with repeated eigenvalues: the top-r eigenspace
+    is unique when the cut falls between distinct values, so M_r (the
+    oblique projector onto it) must match even though the individual
+    columns are not unique.  Exercises the re-orthogonalisation of close
+    eigenvalues in the host eigensolver."""
+    rng = np.random.default_rng(3)
+    T, d, r = 256, 16, 5
+    ones = np.ones((T, 1)) / np.sqrt(T)
+    Z = rng.standard_normal((T, 2 * d))
+    Z -= ones @ (ones.T @ Z)                        # zero-mean columns
+    U, _ = np.linalg.qr(Z)
+    Uq, Uk = U[:, :d], U[:, d:]                     # orthonormal, mutually orthogonal
+    q = np.sqrt(T) * Uq                             # Sigma_q = I
+    s2 = np.array([5, 5, 5, 3, 3, 2, 1, 1, 1, 0.5, 0.5, 0.25, 0.2, 0.2, 0.1, 0.05])
+    V, _ = np.linalg.qr(rng.standard_normal((d, d)))
+    k = np.sqrt(T) * (Uk * np.sqrt(s2)) @ V.T + 0.3  # centred moment V diag(s2) V^T
+    cal = S.saki_calibrate(q[None].astype(np.float32), k[None].astype(np.float32), r)
+    oc = O.saki_calibrate(q.astype(np.float32), k.astype(np.float32), r)
+    M = _m(cal["B_q"][0], cal["B_k"][0])
+    assert np.linalg.norm(M - oc["M"]) <= 1e-5 * np.linalg.norm(oc["M"])
+    assert np.linalg.norm(M @ M - M) <= 1e-5 * np.linalg.norm(M)
+    np.testing.assert_allclose(cal["sigma"][0] ** 2, oc["sigma"] ** 2, rtol=0, atol=1e-6 * 5)
+
+
 def test_constant_keys_identity_fallback():
     q = np.random.default_rng(1).standard_normal((1, 64, 16)).astype(np.float32)
     k = np.tile(np.arange(16, dtype=np.float32), (1, 64, 1))
