@@ -39,6 +39,7 @@ struct Plan {
   int chunk = kTile;   // keys per chunk (multiple of 64)
   int n_chunks = 1;
   size_t z_off = 0, b_off = 0, part_off = 0, flag_off = 0, ws_bytes = 0;
+  size_t flag_count = 0;  // flags per tier (recall path)
 };
 
 inline Plan make_plan(int B, int H_q, int Q, int N_valid, int part_entry_bytes) {
@@ -87,17 +88,19 @@ inline Plan score_plan(int B, int H_q, int Q, int N_valid, int r) {
 
 // Recall path: partial lists hold a double score and an int index (16 bytes
 // with padding).  The MFMA path also keeps the keys split into bf16 hi and lo
-// parts in tile layout (z_off), the key norm bounds (b_off) and one redo flag per wave
-// (flag_off).
+// parts in tile layout (z_off), the key norm bounds in rows of n_tiles * 64
+// (b_off) and two arrays of one flag per wave (flag_off) through which each
+// tier hands the waves it could not finish to the next.
 inline Plan recall_plan(int B, int H_q, int H_kv, int Q, int N_valid) {
   Plan p = make_plan(B, H_q, Q, N_valid, 16);
   if (!p.mfma) return p;
   const size_t nt = n_tiles(N_valid);
   p.z_off = round_up(p.ws_bytes, 256);
   p.b_off = round_up(p.z_off + 2 * (size_t)B * H_kv * nt * kTile * kHeadDim * 2, 256);
-  p.flag_off = round_up(p.b_off + (size_t)B * H_kv * (size_t)N_valid * sizeof(float), 256);
+  p.flag_off = round_up(p.b_off + (size_t)B * H_kv * nt * kTile * sizeof(float), 256);
   const size_t blocks = (size_t)p.row_blocks * p.n_chunks * B * H_q;
-  p.ws_bytes = round_up(p.flag_off + (blocks + 8) * 2 * sizeof(int), 256);
+  p.flag_count = (blocks + 8) * 2;
+  p.ws_bytes = round_up(p.flag_off + 2 * p.flag_count * sizeof(int), 256);
   return p;
 }
 

@@ -887,7 +887,8 @@ __global__ __launch_bounds__(128) void exact_mfma_kernel(
 // ---------------------------------------------------------------- exact scores, bound-and-rescore
 
 // Keys rounded to bf16 in the MFMA tile layout of the codes (16 pieces of 8
-// dims per key), and an upper bound of every key's Euclidean norm.
+// dims per key), and an upper bound of every key's Euclidean norm (rows of
+// n_tiles * 64 per (b, g), so that aligned groups of four can be loaded).
 // grid (n_tiles(N_valid), B*H_kv), block 256.
 template <bool KBF>
 __global__ __launch_bounds__(256) void keys_hi_kernel(const void* __restrict__ keys, int N_cap,
@@ -920,8 +921,9 @@ __global__ __launch_bounds__(256) void keys_hi_kernel(const void* __restrict__ k
   }
   part[pg][t] = ss;
   __syncthreads();
-  if (pg == 0 && ok)
-    knorm[bg * N_valid + n] = sqrtf(part[0][t] + part[1][t] + part[2][t] + part[3][t]) * (1.f + 1e-5f);
+  if (pg == 0)  // one row of n_tiles * 64 bounds per (b, g); 0 past N_valid
+    knorm[bg * n_tiles * kTile + n] =
+        ok ? sqrtf(part[0][t] + part[1][t] + part[2][t] + part[3][t]) * (1.f + 1e-5f) : 0.f;
 }
 
 // Exact top-64 and recall hits by bound-and-rescore.  With x = x_h + x_l + x_r
@@ -946,7 +948,7 @@ __global__ __launch_bounds__(128) void exact_bf16_kernel(
     const int* __restrict__ q_pos, int H_q, int H_kv, int N_cap, int N_valid, int Q,
     int n_tiles_hi, int n_bh, int row_blocks, int chunk, int n_chunks, int k,
     const int* __restrict__ approx, int* __restrict__ hits, int* __restrict__ exact_idx,
-    KeyF64* __restrict__ part, int* __restrict__ redo) {
+    KeyF64* __restrict__ part, const int* __restrict__ only, int* __restrict__ redo) {
   constexpr int D = saki::kHeadDim;
   constexpr size_t TB = (size_t)kTile * D * 2;
   using KO = KeysF64;
@@ -965,6 +967,11 @@ __global__ __launch_bounds__(128) void exact_bf16_kernel(
   const size_t bg = (size_t)b * H_kv + gkv;
   const int row0 = (rb * waves + wave) * kMR;
   if (row0 >= Q) return;
+  // as the second tier after exact_gate_kernel: only the waves it flagged
+  if (only && only[lb * kMfmaWaves + wave] == 0) {
+    if (lane == 0) redo[lb * kMfmaWaves + wave] = 0;
+    return;
+  }
   const int qi = lane % 16, g = lane / 16;
   const int my_row = row0 + qi;
   const bool row_ok = my_row < Q;
@@ -977,7 +984,7 @@ __global__ __launch_bounds__(128) void exact_bf16_kernel(
   int* hist = hist_mem[wave];
   float* qrows = qrow_mem[wave];
   const size_t hoff = bg * n_tiles_hi * TB;
-  const float* kn = knorm + bg * N_valid;
+  const float* kn = knorm + bg * n_tiles_hi * kTile;
 
   // query: bf16 hi/lo operands (dims 32kk + 8g .. +7), float32 copy in LDS,
   // norm bound
@@ -1179,6 +1186,448 @@ __global__ __launch_bounds__(128) void exact_bf16_kernel(
   }
 }
 
+// ---------------------------------------------------------------- exact scores, gated by the candidate list
+
+// The k-th best exact score among any k distinct visible keys is a lower
+// bound of the row's exact k-th score, so the candidate list S_i itself gives
+// every row a gate tau_i before the scan.  The gate is taken from float32 dot
+// products, whose error is at most gamma_128 sum|q_e k_e| <= 7.7e-6 ||q|| ||k||.
+constexpr float kTauEps = 1e-5f;
+
+// Order-preserving 32-bit key of a float score whose low 7 bits carry a slot
+// number (0..127); 0 is never produced for a finite score and marks a pad.
+__device__ __forceinline__ uint32_t slot_key(float s, int slot) {
+  return (ord_f32(s) & ~127u) | (uint32_t)slot;
+}
+
+__device__ __forceinline__ float wave_min_f32(float v) {
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) v = fminf(v, xor_shfl_f32(v, m));
+  return v;
+}
+__device__ __forceinline__ float wave_max_f32(float v) {
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) v = fmaxf(v, xor_shfl_f32(v, m));
+  return v;
+}
+
+// Float32 q.k of one key per lane (four partial sums); q in LDS.
+template <bool KBF>
+__device__ __forceinline__ float lane_dot_f32(const void* keys, size_t key_row, const float* qs) {
+  constexpr int D = saki::kHeadDim;
+  float s[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int d8 = 0; d8 < D; d8 += 8) {
+    float f[8];
+    if constexpr (KBF) {
+      unpack_piece<true>(*reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(keys) +
+                                                         key_row * D + d8), f);
+    } else {
+      const float4* kr = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(keys) +
+                                                         key_row * D + d8);
+      const float4 a = kr[0], b = kr[1];
+      f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
+      f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e & 3] = fmaf(qs[d8 + e], f[e], s[e & 3]);
+  }
+  return (s[0] + s[1]) + (s[2] + s[3]);
+}
+
+// Float64 q.k of one key per lane (float32 inputs: every product is exact).
+template <bool KBF>
+__device__ __forceinline__ double lane_dot_f64(const void* keys, size_t key_row, const float* qs) {
+  constexpr int D = saki::kHeadDim;
+  double acc = 0.0;
+#pragma unroll 4
+  for (int d8 = 0; d8 < D; d8 += 8) {
+    float f[8];
+    if constexpr (KBF) {
+      unpack_piece<true>(*reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(keys) +
+                                                         key_row * D + d8), f);
+    } else {
+      const float4* kr = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(keys) +
+                                                         key_row * D + d8);
+      const float4 a = kr[0], b = kr[1];
+      f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
+      f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc = fma((double)qs[d8 + e], (double)f[e], acc);
+  }
+  return acc;
+}
+
+// Whether j is in a row's candidate list, kept sorted descending in LDS
+// (64 entries; unused slots hold values >= 2^31, which no index equals).
+__device__ __forceinline__ bool in_sorted_desc(const uint32_t* a, int j) {
+  if (j < 0) return false;
+  const uint32_t x = (uint32_t)j;
+  int lo = 0;
+#pragma unroll
+  for (int st = 32; st > 0; st >>= 1)
+    if (a[lo + st - 1] > x) lo += st;
+  return lo < kWave && a[lo] == x;
+}
+
+// Float64 q.k of one key per lane, q read from global memory.
+template <bool KBF>
+__device__ __forceinline__ double lane_dot_f64_g(const void* keys, size_t key_row,
+                                                 const float* __restrict__ qr) {
+  constexpr int D = saki::kHeadDim;
+  double acc = 0.0;
+#pragma unroll 2
+  for (int d8 = 0; d8 < D; d8 += 8) {
+    float f[8];
+    if constexpr (KBF) {
+      unpack_piece<true>(*reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(keys) +
+                                                         key_row * D + d8), f);
+    } else {
+      const float4* kr = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(keys) +
+                                                         key_row * D + d8);
+      const float4 a = kr[0], b = kr[1];
+      f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
+      f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+    }
+    const float4 qa = *reinterpret_cast<const float4*>(qr + d8);
+    const float4 qb = *reinterpret_cast<const float4*>(qr + d8 + 4);
+    const float qv[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc = fma((double)qv[e], (double)f[e], acc);
+  }
+  return acc;
+}
+
+constexpr int kGateCollect = 256;           // keys collected per row
+constexpr int kGateRow = kGateCollect + 1;  // padded LDS row stride
+constexpr int kBatch = 256;                 // keys rescored per wave and batch
+constexpr int kGateWaves = 4;               // waves per 16-row work-group
+
+// Exact top-k and recall hits in one scan.  A row's candidate list S (k
+// distinct visible keys) gives the gate tau = min over S of a float32 lower
+// bound of q.k; the scan collects C = {j : a3_j + E_j >= tau} with the bf16x3
+// upper bound, so C contains the exact top-k T and, since every key of S
+// passes, S as well.  Only the keys of C outside S (normally a handful) are
+// rescored in float64.  Then, with |S| = k,
+//   hits = |T intersect S| = k - |T intersect (C \ S)|,
+// and a key o of C \ S is in T iff fewer than k keys of C beat it: the keys
+// of S are compared through their float32 intervals (an undecided pair is
+// settled in float64) and the others exactly.  With exact_idx or split keys
+// the exact order is needed: S's keys in the chunk are rescored as well and
+// merged with the others.  A row whose list is invalid (an entry outside
+// [0, lim) or a duplicate) takes tau = -inf and treats all of C as others.
+//
+// A work-group of four waves owns 16 rows: the waves take four rows each for
+// the gate and the final count, and every fourth key tile of the scan (all
+// 16 rows, shared collection lists), so that the latency of the per-row work
+// is spread over four times as many waves.  A work-group that collects more
+// than 256 keys for a row is flagged for exact_bf16_kernel.  grid: 1-D xcd
+// grid of ceil(Q / 16) * n_chunks * B * H_q work-groups; the flags use the
+// numbering of the two-wave tiers.
+template <bool KBF>
+__global__ __launch_bounds__(kGateWaves * kWave) void exact_gate_kernel(
+    const void* __restrict__ keys, const uint8_t* __restrict__ khi,
+    const uint8_t* __restrict__ klo, const float* __restrict__ knorm, const float* __restrict__ q,
+    const int* __restrict__ q_pos, int H_q, int H_kv, int N_cap, int N_valid, int Q,
+    int n_tiles_hi, int n_bh, int row_blocks2, int chunk, int n_chunks, int k,
+    const int* __restrict__ approx, int* __restrict__ hits, int* __restrict__ exact_idx,
+    KeyF64* __restrict__ part, int* __restrict__ redo) {
+  constexpr int D = saki::kHeadDim;
+  constexpr size_t TB = (size_t)kTile * D * 2;
+  using KD = KeysF64;
+  __shared__ int cj[kMR * kGateRow];     // collected keys
+  __shared__ uint32_t sl[kMR * kWave];   // candidate lists, sorted descending
+  __shared__ float ss[kMR * kWave];      // float32 score of list entry a
+  __shared__ float tau_s[kMR];           // gates
+  __shared__ int bad_s[kMR];             // invalid lists
+  __shared__ int ccount[kMR];
+  __shared__ int wg_fallback;
+  __shared__ int bj_m[kGateWaves][kBatch];  // per wave: others' key, exact score, row, S-count
+  __shared__ double bsc_m[kGateWaves][kBatch];
+  __shared__ unsigned char brow_m[kGateWaves][kBatch];
+  __shared__ int bcnt_m[kGateWaves][kBatch];
+  __shared__ int boff_m[kGateWaves][kMR / kGateWaves + 1];
+  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int row_blocks = (Q + kMR - 1) / kMR;
+  const long long lb = xcd_logical_block((long long)row_blocks * n_chunks * n_bh);
+  if (lb < 0) return;  // uniform over the work-group
+  const int rb = (int)(lb % row_blocks), ch = (int)((lb / row_blocks) % n_chunks);
+  const size_t bh = (size_t)(lb / ((long long)row_blocks * n_chunks));
+  const int b = (int)(bh / H_q), h = (int)(bh % H_q);
+  const int gkv = h / (H_q / H_kv);
+  const size_t bg = (size_t)b * H_kv + gkv;
+  const int row0 = rb * kMR;  // < Q
+  const long long flag =
+      (((long long)bh * n_chunks + ch) * row_blocks2 + rb / 2) * kMfmaWaves + (rb % 2);
+  const int qi = lane % 16, g = lane / 16;
+  const int my_row = row0 + qi;
+  const bool row_ok = my_row < Q;
+  const int my_lim = row_limit(my_row, Q, N_valid, q_pos);
+  const int kmax = wave_max_i(my_lim);
+  const int kbeg = ch * chunk;
+  const int kend = min(kbeg + chunk, kmax);
+  const int n_rows = min(kMR, Q - row0);
+  const bool ordered = exact_idx != nullptr || n_chunks > 1;
+  const size_t hoff = bg * n_tiles_hi * TB;
+  const float* kn = knorm + bg * n_tiles_hi * kTile;
+  const size_t kbase = bg * N_cap;
+  int* bj = bj_m[wave];
+  double* bsc = bsc_m[wave];
+  unsigned char* brow = brow_m[wave];
+  int* bcnt = bcnt_m[wave];
+  int* boff = boff_m[wave];
+
+  // query: bf16 hi/lo operands (dims 32kk + 8g .. +7) and norm bound
+  bf16x8_t qh[4], ql[4];
+  float qn;
+  {
+    const float* qr = q + (bh * Q + (row_ok ? my_row : row0)) * D;
+    float sq = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      float fh[8], fl[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float f = row_ok ? qr[32 * kk + 8 * g + e] : 0.f;
+        sq = fmaf(f, f, sq);
+        fh[e] = bf16_round(f);
+        fl[e] = bf16_round(f - fh[e]);
+      }
+      qh[kk] = as_bf16x8(pack_bf16x8(fh));
+      ql[kk] = as_bf16x8(pack_bf16x8(fl));
+    }
+    qn = sqrtf(sum_lane_groups(sq)) * (1.f + 1e-5f);
+  }
+  const float eq = kExactEps3 * qn;
+  if (threadIdx.x < kMR) {
+    ccount[threadIdx.x] = 0;
+    tau_s[threadIdx.x] = -INFINITY;
+    bad_s[threadIdx.x] = 1;
+  }
+  if (threadIdx.x == 0) wg_fallback = 0;
+  __syncthreads();
+
+  // ---- gate of rows wave, wave + 4, ... from their candidate lists
+  for (int r = wave; r < n_rows; r += kGateWaves) {
+    const size_t row = bh * Q + row0 + r;
+    const int lim_r = __builtin_amdgcn_readlane(my_lim, r);
+    const int aj = lane < k ? approx[row * k + lane] : -1;
+    bool bad = lane < k && (aj < 0 || aj >= lim_r);
+    uint32_t key = lane < k ? (uint32_t)aj : (0x80000000u | (uint32_t)lane);
+    wave_sort<KeysU32>(key);
+    const uint32_t nxt = (uint32_t)__shfl_down((int)key, 1, kWave);
+    bad |= lane < kWave - 1 && key == nxt;
+    sl[r * kWave + lane] = key;
+    if (__ballot(bad) != 0) continue;  // tau stays -inf: collect every key
+    // float32 scores, 8 lanes per entry (dims 16p .. 16p+15), 8 entries per
+    // step; each sum is at most 12 roundings deep: error <= gamma_12 ||q|| ||k||
+    const int p = lane & 7, slot = lane >> 3;
+    const float* qr = q + row * D + 16 * p;
+    float qv[16];
+#pragma unroll
+    for (int e4 = 0; e4 < 4; ++e4) {
+      const float4 v = *reinterpret_cast<const float4*>(qr + 4 * e4);
+      qv[4 * e4] = v.x; qv[4 * e4 + 1] = v.y; qv[4 * e4 + 2] = v.z; qv[4 * e4 + 3] = v.w;
+    }
+    const float qn_r = readlane_s(qn, r);
+    float lo = INFINITY;
+#pragma unroll 2
+    for (int a0 = 0; a0 < k; a0 += 8) {
+      const int a = a0 + slot;
+      const int j = __shfl(aj, a < k ? a : 0, kWave);
+      float s0 = 0.f, s1 = 0.f;
+      if (a < k) {
+        float f[16];
+        if constexpr (KBF) {
+          const uint16_t* kr = reinterpret_cast<const uint16_t*>(keys) + (kbase + j) * D + 16 * p;
+          unpack_piece<true>(*reinterpret_cast<const uint4*>(kr), f);
+          unpack_piece<true>(*reinterpret_cast<const uint4*>(kr + 8), f + 8);
+        } else {
+          const float4* kr = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(keys) +
+                                                             (kbase + j) * D + 16 * p);
+#pragma unroll
+          for (int e4 = 0; e4 < 4; ++e4) {
+            const float4 v = kr[e4];
+            f[4 * e4] = v.x; f[4 * e4 + 1] = v.y; f[4 * e4 + 2] = v.z; f[4 * e4 + 3] = v.w;
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 16; e += 2) {
+          s0 = fmaf(qv[e], f[e], s0);
+          s1 = fmaf(qv[e + 1], f[e + 1], s1);
+        }
+      }
+      float sc = s0 + s1;
+      sc += xor_shfl_f32(sc, 1);
+      sc += xor_shfl_f32(sc, 2);
+      sc += xor_shfl_f32(sc, 4);
+      if (a < k) {
+        if (p == 0) ss[r * kWave + a] = sc;
+        lo = fminf(lo, sc - kTauEps * qn_r * kn[j]);
+      }
+    }
+    lo = wave_min_f32(lo);
+    if (lane == 0) {
+      tau_s[r] = lo;
+      bad_s[r] = 0;
+    }
+  }
+  __syncthreads();
+
+  // ---- scan (every fourth tile): collect the keys whose upper bound reaches the gate
+  {
+    const float my_tau = tau_s[qi];
+    for (int t0 = kbeg + wave * kTile; t0 < kend; t0 += kGateWaves * kTile) {
+      const size_t to = hoff + (size_t)(t0 / kTile) * TB;
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub) {
+        const int key = 16 * sub + qi;
+        f32x4_t a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const size_t o = to + (size_t)(4 * kk + g) * kTile * 16 + (size_t)key * 16;
+          const bf16x8_t kh = as_bf16x8(*reinterpret_cast<const uint4*>(khi + o));
+          const bf16x8_t kl = as_bf16x8(*reinterpret_cast<const uint4*>(klo + o));
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, qh[kk], a, 0, 0, 0);
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kl, qh[kk], a, 0, 0, 0);
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, ql[kk], a, 0, 0, 0);
+        }
+        const int kb = t0 + 16 * sub + 4 * g;
+        const float4 nv = *reinterpret_cast<const float4*>(kn + kb);  // kb < n_tiles_hi * 64
+        const float nvs[4] = {nv.x, nv.y, nv.z, nv.w};
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int j = kb + v;
+          if (j < my_lim && fmaf(eq, nvs[v], a[v]) >= my_tau) {
+            const int pos = atomicAdd(&ccount[qi], 1);
+            if (pos < kGateCollect) cj[qi * kGateRow + pos] = j;
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+  bool fallback = __ballot(lane < kMR && ccount[lane % kMR] > kGateCollect) != 0;
+
+  // ---- rows wave, wave + 4, ...: the others C \ S, rescored in batches of whole rows
+  int r_done = 0;  // of this wave's rows
+  const int my_rows = n_rows > wave ? (n_rows - wave + kGateWaves - 1) / kGateWaves : 0;
+  while (!fallback && r_done < my_rows) {
+    int nb = 0, r_end = r_done;
+    for (; r_end < my_rows; ++r_end) {
+      const int r = wave + kGateWaves * r_end;
+      const int c = ccount[r];
+      const bool rbad = bad_s[r] != 0;
+      // others of this row: all of C for an invalid list, else C minus S
+      int n_oth = 0, n_in_s = 0;
+      for (int base = 0; base < c; base += kWave) {
+        const int e = base + lane;
+        const int j = e < c ? cj[r * kGateRow + e] : -1;
+        const bool is_s = e < c && !rbad && in_sorted_desc(sl + r * kWave, j);
+        n_in_s += __popcll(__ballot(is_s));
+        n_oth += __popcll(__ballot(e < c && !is_s));
+      }
+      // every key of a valid list passes the gate (a failed check means a bound
+      // did not hold: hand the rows over rather than trust the result)
+      if (!rbad && n_chunks == 1 && n_in_s != k) {
+        fallback = true;
+        break;
+      }
+      if (nb + n_oth > kBatch) break;  // this row starts the next batch
+      if (lane == 0) boff[r_end - r_done] = nb;
+      for (int base = 0; base < c; base += kWave) {
+        const int e = base + lane;
+        const int j = e < c ? cj[r * kGateRow + e] : -1;
+        const bool other = e < c && (rbad || !in_sorted_desc(sl + r * kWave, j));
+        const uint64_t m = __ballot(other);
+        if (other) {
+          bj[nb + prefix_count(m)] = j;
+          brow[nb + prefix_count(m)] = (unsigned char)r;
+        }
+        nb += __popcll(m);
+      }
+      if (lane == 0) boff[r_end - r_done + 1] = nb;
+    }
+    if (fallback) break;
+    wave_lds_sync();
+
+    // exact scores of the batch, one key per lane
+    for (int base = 0; base < nb; base += kWave) {
+      const int e = base + lane;
+      if (e < nb) {
+        const size_t row = bh * Q + row0 + brow[e];
+        bsc[e] = lane_dot_f64_g<KBF>(keys, kbase + bj[e], q + row * D);
+      }
+    }
+    wave_lds_sync();
+
+    // per row: the exact top-k decided by counting
+    for (int rr = r_done; rr < r_end; ++rr) {
+      const int r = wave + kGateWaves * rr;
+      const size_t row = bh * Q + row0 + r;
+      const float* qr = q + row * D;
+      const bool rbad = bad_s[r] != 0;
+      const int o0 = boff[rr - r_done], o1 = boff[rr - r_done + 1];
+      const int aj = lane < k ? approx[row * k + lane] : -1;
+      if (ordered) {
+        KeyF64 xs = KD::pad();
+        if (!rbad && lane < k && aj >= kbeg && aj < kend)
+          xs = KD::make(lane_dot_f64_g<KBF>(keys, kbase + aj, qr), aj);
+        wave_sort<KD>(xs);
+        for (int base = o0; base < o1; base += kWave) {
+          KeyF64 xo = base + lane < o1 ? KD::make(bsc[base + lane], bj[base + lane]) : KD::pad();
+          wave_sort<KD>(xo);
+          wave_merge<KD>(xs, xo);
+        }
+        exact_row_out<KD>(xs, row, ch, n_chunks, k, approx, hits, exact_idx, part);
+        continue;
+      }
+      // how many keys of S beat each other o (S's float32 intervals)
+      if (!rbad) {
+        const float sa = lane < k ? ss[r * kWave + lane] : 0.f;
+        const float ea = lane < k ? kTauEps * readlane_s(qn, r) * kn[aj] : 0.f;
+        const double lo_a = (double)sa - (double)ea, hi_a = (double)sa + (double)ea;
+        for (int o = o0; o < o1; ++o) {
+          const double so = bsc[o];
+          const int jo = bj[o];
+          bool beat = lane < k && lo_a > so;
+          const bool amb = lane < k && !beat && hi_a >= so;
+          if (__ballot(amb) != 0 && amb) {
+            const double sx = lane_dot_f64_g<KBF>(keys, kbase + aj, qr);
+            beat = sx > so || (sx == so && aj < jo);
+          }
+          const int cs = __popcll(__ballot(beat));
+          if (lane == 0) bcnt[o] = cs;
+        }
+      }
+      wave_lds_sync();
+      int in_t = 0, in_ts = 0;
+      for (int base = o0; base < o1; base += kWave) {
+        const int e = base + lane;
+        const bool live = e < o1;
+        const double so = live ? bsc[e] : 0.0;
+        const int jo = live ? bj[e] : 0;
+        int cnt = (live && !rbad) ? bcnt[e] : 0;
+        for (int o2 = o0; o2 < o1; ++o2) {
+          const double s2 = bsc[o2];
+          const int j2 = bj[o2];
+          cnt += (s2 > so || (s2 == so && j2 < jo)) ? 1 : 0;
+        }
+        const bool in = live && cnt < k;
+        in_t += __popcll(__ballot(in));
+        in_ts += __popcll(__ballot(in && rbad && in_sorted_desc(sl + r * kWave, jo)));
+      }
+      if (lane == 0) hits[row] = rbad ? in_ts : k - in_t;
+    }
+    wave_lds_sync();
+    r_done = r_end;
+  }
+  if (fallback && lane == 0) atomicOr(&wg_fallback, 1);
+  __syncthreads();
+  if (threadIdx.x == 0) redo[flag] = wg_fallback;
+}
+
 // ---------------------------------------------------------------- merge of partials
 
 // grid (ceil(rows/4)), block 256: one wave per row merges n_chunks sorted
@@ -1281,16 +1730,26 @@ void launch_recall(const void* keys, const float* q, const int* q_pos, int B, in
     uint8_t* khi = ws + p.z_off;
     uint8_t* klo = khi + (size_t)B * H_kv * nt_hi * kTile * saki::kHeadDim * 2;
     float* knorm = reinterpret_cast<float*>(ws + p.b_off);
-    int* redo = reinterpret_cast<int*>(ws + p.flag_off);
+    // three tiers, each running only the waves the previous one flagged
+    int* flag1 = reinterpret_cast<int*>(ws + p.flag_off);
+    int* flag2 = flag1 + p.flag_count;
     if (nt_hi > 0)
       hipLaunchKernelGGL((keys_hi_kernel<KBF>), dim3(nt_hi, B * H_kv), dim3(256), 0, s, keys, N_cap,
                          N_valid, nt_hi, khi, klo, knorm);
+    {
+      const long long total = (long long)((Q + kMR - 1) / kMR) * p.n_chunks * B * H_q;
+      hipLaunchKernelGGL((exact_gate_kernel<KBF>), dim3((unsigned)(((total + kXcds - 1) / kXcds) * kXcds)),
+                         dim3(kGateWaves * kWave), 0, s, keys, khi, klo, knorm, q, q_pos, H_q, H_kv, N_cap,
+                         N_valid, Q, nt_hi, B * H_q, p.row_blocks, p.chunk, p.n_chunks, k, approx,
+                         hits, exact_idx, part, flag1);
+    }
     hipLaunchKernelGGL((exact_bf16_kernel<KBF>), xcd_grid(p, B * H_q), block, 0, s, keys, khi,
                        klo, knorm, q, q_pos, H_q, H_kv, N_cap, N_valid, Q, nt_hi, B * H_q,
-                       p.row_blocks, p.chunk, p.n_chunks, k, approx, hits, exact_idx, part, redo);
+                       p.row_blocks, p.chunk, p.n_chunks, k, approx, hits, exact_idx, part,
+                       (const int*)flag1, flag2);
     hipLaunchKernelGGL((exact_mfma_kernel<KBF>), xcd_grid(p, B * H_q), block, 0, s, keys, q,
                        q_pos, H_q, H_kv, N_cap, N_valid, Q, p.row_blocks, p.chunk, p.n_chunks, k,
-                       approx, hits, exact_idx, part, B * H_q, (const int*)redo);
+                       approx, hits, exact_idx, part, B * H_q, (const int*)flag2);
   } else if (p.rows == 4) {
     hipLaunchKernelGGL((exact_stream_kernel<KBF, 4>), grid, block, 0, s, keys, q, q_pos, H_q,
                        H_kv, N_cap, N_valid, Q, p.row_blocks, p.chunk, p.n_chunks, k, approx,

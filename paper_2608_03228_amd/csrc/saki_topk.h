@@ -132,6 +132,15 @@ struct KeysF32 {
   __device__ static int index(K a) { return (int)~(uint32_t)a; }
 };
 
+// Plain 32-bit unsigned keys (the caller packs whatever order it needs).
+struct KeysU32 {
+  using K = uint32_t;
+  __device__ static bool gt(K a, K b) { return a > b; }
+  __device__ static K sel(bool c, K a, K b) { return c ? a : b; }
+  __device__ static K shfl_xor(K a, int m) { return xor_shfl_u32(a, m); }
+  __device__ static K reverse(K a) { return rev_shfl_u32(a); }
+};
+
 // Key operations for double scores: (ordered bits, ~index).
 struct KeyF64 {
   uint64_t s;

@@ -241,9 +241,13 @@ def test_empty_and_degenerate_sizes():
     assert np.all(hits.cpu().numpy() == 1)
 
 
-def test_recall_kernel_matches_oracle():
+@pytest.mark.parametrize("want_exact", [True, False])
+def test_recall_kernel_matches_oracle(want_exact):
     """saki_recall on approximate sets that come from the oracle (not from the
-    GPU): exact top-64 and hit counts identical to the oracle's."""
+    GPU): exact top-64 and hit counts identical to the oracle's.  Without
+    exact_idx the kernel decides most of the set from bf16 bounds and rescores
+    only the keys near the 64th place; rows with arbitrary sets (pads,
+    duplicates, out-of-range entries) take the ungated path."""
     spec = W.SPECS["llama31_8b_layer"].with_(N=1500, Q=1500 - 64, H_q=4, H_kv=1)
     inp = W.make_layer(spec)
     rng = np.random.default_rng(0)
@@ -259,9 +263,38 @@ def test_recall_kernel_matches_oracle():
     approx[0, 3, :100] = rng.integers(-1, 1500, (100, 64))  # arbitrary sets, with pads
     want = O.recall_hits(approx, exact)
     hits, ex = S.saki_recall(_t(inp["keys"]), _t(inp["queries"]), _t(approx, torch.int32),
-                             1500, q_pos=_t(inp["q_pos"], torch.int32))
-    np.testing.assert_array_equal(ex.cpu().numpy(), exact)
+                             1500, q_pos=_t(inp["q_pos"], torch.int32), want_exact=want_exact)
+    if want_exact:
+        np.testing.assert_array_equal(ex.cpu().numpy(), exact)
+    else:
+        assert ex is None
     np.testing.assert_array_equal(hits.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("quality", ["weak", "shuffled"])
+def test_recall_hits_with_poor_candidate_lists(quality):
+    """Hits-only recall when the candidate lists are far from the exact top-64
+    (a rank-16 key-PCA index, or other rows' lists): the gate is low, many
+    keys pass it, and waves hand over to the histogram tier."""
+    spec = W.SPECS["llama31_8b_layer"].with_(N=1200, Q=1200 - 64, H_q=4, H_kv=1)
+    inp = W.make_layer(spec)
+    lim = O.candidate_limits(spec.Q, 1200, inp["q_pos"])
+    approx = np.empty((1, 4, spec.Q, 64), np.int32)
+    exact = np.empty_like(approx)
+    for h in range(4):
+        exact[0, h] = O.topk_rows(O.exact_scores(inp["queries"][0, h], inp["keys"][0, 0]), lim)
+        if quality == "weak":
+            _, sk, _ = O.second_moments(inp["q_cal"][h], inp["k_cal"][0])
+            V = O.key_pca_factors(sk, 16)
+            mu = inp["k_cal"][0].astype(np.float64).mean(0)
+            s_hat, *_ = O.index_scores(V, V, mu, inp["queries"][0, h], inp["keys"][0, 0])
+            approx[0, h] = O.topk_rows(s_hat, lim)
+        else:
+            approx[0, h] = exact[0, h][::-1]       # row i gets row Q-1-i's list ...
+            approx[0, h] = np.where(approx[0, h] < lim[:, None], approx[0, h], -1)  # ... if visible
+    hits, ex = S.saki_recall(_t(inp["keys"]), _t(inp["queries"]), _t(approx, torch.int32),
+                             1200, q_pos=_t(inp["q_pos"], torch.int32), want_exact=False)
+    np.testing.assert_array_equal(hits.cpu().numpy(), O.recall_hits(approx, exact))
 
 
 def test_recall_split_chunks_matches_oracle():
