@@ -110,6 +110,133 @@ def cpu_baseline(inp, r, sketch, k, n_heads):
                       f"{os.cpu_count()}, BLAS threads={threads}"}
 
 
+def decode_queries(spec, step):
+    """The fresh query tokens of one decode step, [B, H_q, Q, d] float32."""
+    import workloads as W
+    wq, _ = W.weights(spec)
+    out = np.empty((spec.batch, spec.H_q, spec.Q, spec.d), np.float32)
+    for b in range(spec.batch):
+        out[b] = W._project(W.tokens(spec, "queries", spec.Q, seq=b, step=step), wq)
+    return out
+
+
+def run_decode(args, spec):
+    """Long-context decode: the index of N cached keys is built once; a step
+    appends the newest key's codes (one position per query head) and scores
+    every head's fresh query against all N codes with a top-64 per row.  The
+    exact recall of every step is evaluated after the timed loop."""
+    import torch
+    import workloads as W
+    import oracle as O
+    from paper_2608_03228_amd import saki as S
+    r, sk, k = args.r, args.sketch, args.k
+    dev = torch.device("cuda:0")
+    t_gen = time.perf_counter()
+    inp = W.make_layer(spec)
+    t_gen = time.perf_counter() - t_gen
+    keys = torch.from_numpy(inp["keys"]).to(dev)
+    B, H_kv, N, d = keys.shape
+    H_q, Q = spec.H_q, spec.Q
+    n_q = args.warmup + args.steps
+    qs = torch.from_numpy(np.stack([decode_queries(spec, s) for s in range(n_q)])).to(dev)
+    cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], r)
+    Bq, Bk, mu = (torch.from_numpy(cal[n]).to(dev) for n in ("B_q", "B_k", "mu"))
+    index = torch.empty(S.saki_index_bytes(B, H_q, N, r, sk), dtype=torch.uint8, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    S.saki_build_index(keys, Bk, mu, r, sk, H_q, index=index)
+    e1.record()
+    torch.cuda.synchronize()
+    build_full_ms = e0.elapsed_time(e1)
+    ws = torch.empty(max(1, S.saki_score_topk_workspace_bytes(B, H_q, Q, N, r, k, sk)),
+                     dtype=torch.uint8, device=dev)
+    top_idx = torch.empty((n_q, B, H_q, Q, k), dtype=torch.int32, device=dev)
+    top_sc = torch.empty((n_q, B, H_q, Q, k), dtype=torch.float32, device=dev)
+    ev = []
+
+    def step(s, timed=False):
+        if timed:
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e[0].record()
+        S.saki_build_index(keys, Bk, mu, r, sk, H_q, index=index, n_begin=N - 1, n_count=1)
+        if timed:
+            e[1].record()
+        S.saki_score_topk(index, sk, qs[s], Bq, mu, H_kv, N, N, r, k=k, ws=ws,
+                          top_idx=top_idx[s], top_score=top_sc[s])
+        if timed:
+            e[2].record()
+            ev.append(e)
+
+    for s in range(args.warmup):
+        step(s)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.warmup, n_q):
+        step(s)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / args.steps
+    for s in range(args.warmup, n_q):
+        step(s, timed=True)
+    torch.cuda.synchronize()
+    append_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    score_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+
+    # exact recall of every step (evaluation, outside the timed loop)
+    wsr = torch.empty(max(1, S.saki_recall_workspace_bytes(B, H_q, H_kv, Q, N, d, k)),
+                      dtype=torch.uint8, device=dev)
+    hits = torch.empty((n_q, B, H_q, Q), dtype=torch.int32, device=dev)
+    e0.record()
+    for s in range(n_q):
+        S.saki_recall(keys, qs[s], top_idx[s], N, k=k, ws=wsr, hits=hits[s], want_exact=False)
+    e1.record()
+    torch.cuda.synchronize()
+    recall_ms = e0.elapsed_time(e1) / n_q
+    h = hits.cpu().numpy().astype(np.int64)
+    per_head = h.sum(axis=(0, 1, 3)) / (k * Q * n_q)
+
+    es = 2 if sk == "bf16" else 4
+    code_bytes = B * H_q * N * r * es
+    scan_bytes = code_bytes + B * H_q * Q * d * 4 + B * H_q * Q * k * 8
+    roof = {"bound": "hbm", "achieved": scan_bytes / (score_ms / 1e3) / 1e9,
+            "peak": PEAK["hbm_GBps"], "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = "score_topk"
+    roof["work"] = {"bytes": scan_bytes, "code_bytes": code_bytes}
+
+    cpu = None
+    if not args.no_cpu_baseline:  # the oracle on one head of one step
+        t = time.perf_counter()
+        oc = O.saki_calibrate(inp["q_cal"][0], inp["k_cal"][0], r)
+        q0 = decode_queries(spec, args.warmup)[0, 0]
+        s_hat, *_ = O.index_scores(oc["B_q"], oc["B_k"], oc["mu"], q0, inp["keys"][0, 0],
+                                   "bf16" if sk == "bf16" else "f32")
+        O.topk_rows(s_hat, O.candidate_limits(Q, N), k)
+        dtc = time.perf_counter() - t
+        cpu = {"value": Q * N / dtc, "unit": "keys/s", "cores": os.cpu_count(), "kind": "oracle",
+               "sample": f"query head 0 of one step ({Q * N} keys): calibrate+codes+scores+"
+                         f"top-{k} in float64 numpy; {dtc:.1f} s"}
+
+    out = {
+        "metric": METRIC, "value": B * H_q * Q * N / dt, "unit": "keys/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": dt * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": sk,
+        "data": "synthetic",
+        "config": {"workload": spec.name, "H_q": H_q, "H_kv": H_kv, "d": d, "latent_D": spec.D,
+                   "N": N, "queries_per_head": Q, "batch": B, "r": r, "sketch": sk, "k": k,
+                   "step": "append one key + score + top-64 (index built once)"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "stages_ms": {"append": append_ms, "score_topk": score_ms,
+                      "build_full_once": build_full_ms, "recall_eval": recall_ms,
+                      "input_generation_s": t_gen * 1e3},
+        "recall_at_64": {"median_over_heads": float(np.median(per_head)),
+                         "mean_over_heads": float(np.mean(per_head)),
+                         "hits_total": int(h.sum())},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -121,6 +248,8 @@ def main():
     from paper_2608_03228_amd import saki as S
 
     spec = W.SPECS[args.workload]
+    if spec.steps > 1 and not spec.causal:
+        return run_decode(args, spec)
     if spec.layers != 1 or spec.batch != 1 or spec.steps != 1:
         raise SystemExit(f"bench runs single-layer, single-step workloads; {args.workload} is not")
     r, sk, k = args.r, args.sketch, args.k

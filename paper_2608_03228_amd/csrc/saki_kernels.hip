@@ -245,6 +245,13 @@ __global__ __launch_bounds__(256) void query_sketch_kernel(
   }
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ bf16x2_t as_bf16x2(uint32_t v) {
+  bf16x2_t r;
+  __builtin_memcpy(&r, &v, sizeof(r));
+  return r;
+}
+
 // ---------------------------------------------------------------- sketch scoring, streaming
 
 // grid (row_blocks * n_chunks, B*H_q), block 64*waves.  Each wave owns R rows
@@ -290,21 +297,68 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   const int kbeg = ch * chunk;
   const int kend = min(kbeg + chunk, kmax);
   const uint8_t* hbase = index + bh * n_tiles * TB;
-  for (int t0 = kbeg; t0 < kend; t0 += kTile) {
-    const int j = t0 + lane;
-    const uint8_t* tb = hbase + (size_t)(t0 / kTile) * TB;
-    float c[RK];
+  // the next tile's pieces are loaded before this tile is scored (sketches of
+  // up to 128 bytes per key; wider ones are loaded as they are used)
+  constexpr int PF = NP <= 8 ? NP : 1;
+  uint4 nxt[PF];
+  auto load_tile = [&](int t0, uint4* v) {
+    const uint8_t* tb = hbase + (size_t)(t0 / kTile) * TB + (size_t)lane * 16;
 #pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      const uint4 v = *reinterpret_cast<const uint4*>(tb + (size_t)p * kTile * 16 + (size_t)lane * 16);
-      unpack_piece<SBF>(v, c + p * CPP);
+    for (int p = 0; p < PF; ++p) v[p] = *reinterpret_cast<const uint4*>(tb + (size_t)p * kTile * 16);
+  };
+  if (kbeg < kend) load_tile(kbeg, nxt);
+  if constexpr (SBF) {
+    // bf16 codes: each 32-bit word holds elements (2e, 2e + 1), scored with
+    // the packed bf16 dot product against the query sketch's pairs
+    uint32_t zp[R][RK / 2];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int m = 0; m < RK / 2; ++m)
+        zp[r][m] = (__float_as_uint(zs[wave][r][2 * m]) >> 16) |
+                   (__float_as_uint(zs[wave][r][2 * m + 1]) & 0xffff0000u);
+    for (int t0 = kbeg; t0 < kend; t0 += kTile) {
+      const int j = t0 + lane;
+      const uint8_t* tb = hbase + (size_t)(t0 / kTile) * TB;
+      uint32_t w[RK / 2];
+#pragma unroll
+      for (int p = 0; p < PF; ++p) {
+        w[4 * p] = nxt[p].x; w[4 * p + 1] = nxt[p].y; w[4 * p + 2] = nxt[p].z; w[4 * p + 3] = nxt[p].w;
+      }
+#pragma unroll
+      for (int p = PF; p < NP; ++p) {
+        const uint4 v = *reinterpret_cast<const uint4*>(tb + (size_t)p * kTile * 16 + (size_t)lane * 16);
+        w[4 * p] = v.x; w[4 * p + 1] = v.y; w[4 * p + 2] = v.z; w[4 * p + 3] = v.w;
+      }
+      if (t0 + kTile < kend) load_tile(t0 + kTile, nxt);
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        float acc = 0.f;
+#pragma unroll
+        for (int m = 0; m < RK / 2; ++m) acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(w[m]), as_bf16x2(zp[r][m]), acc, false);
+        top.offer(r, j < lim[r] ? acc + bb[r] : -INFINITY, j);
+      }
     }
+  } else {
+    for (int t0 = kbeg; t0 < kend; t0 += kTile) {
+      const int j = t0 + lane;
+      const uint8_t* tb = hbase + (size_t)(t0 / kTile) * TB;
+      float c[RK];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      float acc = 0.f;
+      for (int p = 0; p < PF; ++p) unpack_piece<SBF>(nxt[p], c + p * CPP);
 #pragma unroll
-      for (int m = 0; m < RK; ++m) acc = fmaf(zs[wave][r][m], c[m], acc);
-      top.offer(r, j < lim[r] ? acc + bb[r] : -INFINITY, j);
+      for (int p = PF; p < NP; ++p) {
+        const uint4 v = *reinterpret_cast<const uint4*>(tb + (size_t)p * kTile * 16 + (size_t)lane * 16);
+        unpack_piece<SBF>(v, c + p * CPP);
+      }
+      if (t0 + kTile < kend) load_tile(t0 + kTile, nxt);
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        float acc = 0.f;
+#pragma unroll
+        for (int m = 0; m < RK; ++m) acc = fmaf(zs[wave][r][m], c[m], acc);
+        top.offer(r, j < lim[r] ? acc + bb[r] : -INFINITY, j);
+      }
     }
   }
   for (int r = 0; r < R; ++r) {
@@ -1630,23 +1684,42 @@ __global__ __launch_bounds__(kGateWaves * kWave) void exact_gate_kernel(
 
 // ---------------------------------------------------------------- merge of partials
 
-// grid (ceil(rows/4)), block 256: one wave per row merges n_chunks sorted
-// partial lists.  RECALL: the row is an exact list -> exact_idx and hits.
+// grid (rows), block 64 * waves (waves <= kMergeWaves): the waves of a row's
+// work-group merge interleaved subsets of its sorted partial lists, then wave
+// 0 merges their lists.  RECALL: the row is an exact list -> exact_idx and hits.
+constexpr int kMergeWaves = 8;
+
 template <class KO, bool RECALL>
-__global__ __launch_bounds__(256) void merge_kernel(
+__global__ __launch_bounds__(kMergeWaves * kWave) void merge_kernel(
     const typename KO::K* __restrict__ part, size_t rows, int n_chunks, int k,
     int* __restrict__ out_idx, float* __restrict__ out_score,
     const int* __restrict__ approx, int* __restrict__ hits) {
   using K = typename KO::K;
-  const int lane = lane_id();
-  const size_t row = (size_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+  __shared__ K lists[kMergeWaves][kWave];
+  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int waves = blockDim.x / kWave;
+  const size_t row = blockIdx.x;
   if (row >= rows) return;
+  // wave w merges partials w, w + waves, ..., four loads in flight at a time
   K a = KO::pad();
-  for (int c = 0; c < n_chunks; ++c) {
-    const K b = part[(row * n_chunks + c) * kMaxK + lane];
-    // the partial is sorted: skip it when its best cannot enter the list
-    if (!KO::gt(KO::readlane(b, 0), KO::readlane(a, kWave - 1))) continue;
-    wave_merge<KO>(a, b);
+  for (int c0 = wave; c0 < n_chunks; c0 += 4 * waves) {
+    K b[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = c0 + u * waves;
+      b[u] = c < n_chunks ? part[(row * n_chunks + c) * kMaxK + lane] : KO::pad();
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      // a partial is sorted: skip it when its best cannot enter the list
+      if (KO::gt(KO::readlane(b[u], 0), KO::readlane(a, kWave - 1))) wave_merge<KO>(a, b[u]);
+  }
+  lists[wave][lane] = a;
+  __syncthreads();
+  if (wave != 0) return;
+  for (int w = 1; w < waves; ++w) {
+    const K b = lists[w][lane];
+    if (KO::gt(KO::readlane(b, 0), KO::readlane(a, kWave - 1))) wave_merge<KO>(a, b);
   }
   const int j = out_index<KO>(a);
   if constexpr (RECALL) {
@@ -1711,9 +1784,9 @@ void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int N_cap, int
                        Q, q_pos, z, bv, p.row_blocks, p.chunk, p.n_chunks, k, top_idx,
                        top_score, part);
   if (p.n_chunks > 1)
-    hipLaunchKernelGGL((merge_kernel<KeysF32, false>), dim3((unsigned)((rows + 3) / 4)),
-                       dim3(256), 0, s, part, rows, p.n_chunks, k, top_idx, top_score, nullptr,
-                       nullptr);
+    hipLaunchKernelGGL((merge_kernel<KeysF32, false>), dim3((unsigned)rows),
+                       dim3(kWave * min(kMergeWaves, p.n_chunks)), 0, s, part, rows, p.n_chunks,
+                       k, top_idx, top_score, nullptr, nullptr);
 }
 
 template <bool KBF>
@@ -1760,9 +1833,9 @@ void launch_recall(const void* keys, const float* q, const int* q_pos, int B, in
                        hits, exact_idx, part);
   }
   if (p.n_chunks > 1)
-    hipLaunchKernelGGL((merge_kernel<KeysF64, true>), dim3((unsigned)((rows + 3) / 4)),
-                       dim3(256), 0, s, part, rows, p.n_chunks, k, exact_idx, nullptr, approx,
-                       hits);
+    hipLaunchKernelGGL((merge_kernel<KeysF64, true>), dim3((unsigned)rows),
+                       dim3(kWave * min(kMergeWaves, p.n_chunks)), 0, s, part, rows, p.n_chunks,
+                       k, exact_idx, nullptr, approx, hits);
 }
 
 bool dtype_ok(int t) { return t == SAKI_F32 || t == SAKI_BF16; }
