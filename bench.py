@@ -280,7 +280,7 @@ def main():
     n_step = [0]
 
     def step(timed_stages=False):
-        cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], r)
+        cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], r, with_sigma=False)
         sl = n_step[0] % 2
         n_step[0] += 1
         if slot_done[sl] is not None:
@@ -324,7 +324,7 @@ def main():
                 for i, n in enumerate(names)}
     t_cal = time.perf_counter()
     for _ in range(3):
-        S.saki_calibrate(inp["q_cal"], inp["k_cal"], r)
+        S.saki_calibrate(inp["q_cal"], inp["k_cal"], r, with_sigma=False)
     stage_ms["calibrate_host"] = (time.perf_counter() - t_cal) / 3 * 1e3
 
     h = hits.cpu().numpy().astype(np.int64)

@@ -457,6 +457,56 @@ struct ShiftedTridiagLU {
   }
 };
 
+// The eigenvalues with ascending indices idx[0..c) (c <= 8) of the symmetric
+// tridiagonal (diag, off) by bisection on Sturm counts (Golub & Van Loan,
+// Sec. 8.4.1), eight shifts at a time in two 256-bit vectors so that the
+// divisions of independent sequences overlap.  A pivot smaller in magnitude
+// than pivmin is replaced by -pivmin.
+void bisect_eigs(int n, const double* diag, const double* off2, double pivmin, double glo,
+                 double ghi, const int* idx, int c, double* out) {
+  alignas(32) double lo[8], hi[8], kk[8];
+  for (int e = 0; e < 8; ++e) {
+    lo[e] = glo;
+    hi[e] = ghi;
+    kk[e] = e < c ? (double)idx[e] : 0.0;
+  }
+  const __m256d one = _mm256_set1_pd(1.0), half = _mm256_set1_pd(0.5);
+  const __m256d npm = _mm256_set1_pd(-pivmin), pm = _mm256_set1_pd(pivmin);
+  const __m256d absmask = _mm256_castsi256_pd(_mm256_set1_epi64x(0x7fffffffffffffffll));
+  __m256d lo0 = _mm256_load_pd(lo), lo1 = _mm256_load_pd(lo + 4);
+  __m256d hi0 = _mm256_load_pd(hi), hi1 = _mm256_load_pd(hi + 4);
+  const __m256d k0 = _mm256_load_pd(kk), k1 = _mm256_load_pd(kk + 4);
+  // the interval halves each step: 64 steps take Gershgorin width to rounding level
+  for (int it = 0; it < 64; ++it) {
+    const __m256d x0 = _mm256_mul_pd(_mm256_add_pd(lo0, hi0), half);
+    const __m256d x1 = _mm256_mul_pd(_mm256_add_pd(lo1, hi1), half);
+    const __m256d d0 = _mm256_set1_pd(diag[0]);
+    __m256d q0 = _mm256_sub_pd(d0, x0), q1 = _mm256_sub_pd(d0, x1);
+    q0 = _mm256_blendv_pd(q0, npm, _mm256_cmp_pd(_mm256_and_pd(q0, absmask), pm, _CMP_LT_OQ));
+    q1 = _mm256_blendv_pd(q1, npm, _mm256_cmp_pd(_mm256_and_pd(q1, absmask), pm, _CMP_LT_OQ));
+    __m256d c0 = _mm256_and_pd(_mm256_cmp_pd(q0, _mm256_setzero_pd(), _CMP_LT_OQ), one);
+    __m256d c1 = _mm256_and_pd(_mm256_cmp_pd(q1, _mm256_setzero_pd(), _CMP_LT_OQ), one);
+    for (int i = 1; i < n; ++i) {
+      const __m256d di = _mm256_set1_pd(diag[i]), ei = _mm256_set1_pd(off2[i - 1]);
+      q0 = _mm256_sub_pd(_mm256_sub_pd(di, x0), _mm256_div_pd(ei, q0));
+      q1 = _mm256_sub_pd(_mm256_sub_pd(di, x1), _mm256_div_pd(ei, q1));
+      q0 = _mm256_blendv_pd(q0, npm, _mm256_cmp_pd(_mm256_and_pd(q0, absmask), pm, _CMP_LT_OQ));
+      q1 = _mm256_blendv_pd(q1, npm, _mm256_cmp_pd(_mm256_and_pd(q1, absmask), pm, _CMP_LT_OQ));
+      c0 = _mm256_add_pd(c0, _mm256_and_pd(_mm256_cmp_pd(q0, _mm256_setzero_pd(), _CMP_LT_OQ), one));
+      c1 = _mm256_add_pd(c1, _mm256_and_pd(_mm256_cmp_pd(q1, _mm256_setzero_pd(), _CMP_LT_OQ), one));
+    }
+    // count(x) <= k: the k-th eigenvalue is >= x
+    const __m256d up0 = _mm256_cmp_pd(c0, k0, _CMP_LE_OQ), up1 = _mm256_cmp_pd(c1, k1, _CMP_LE_OQ);
+    lo0 = _mm256_blendv_pd(lo0, x0, up0);
+    hi0 = _mm256_blendv_pd(x0, hi0, up0);
+    lo1 = _mm256_blendv_pd(lo1, x1, up1);
+    hi1 = _mm256_blendv_pd(x1, hi1, up1);
+  }
+  _mm256_store_pd(lo, _mm256_mul_pd(_mm256_add_pd(lo0, hi0), half));
+  _mm256_store_pd(lo + 4, _mm256_mul_pd(_mm256_add_pd(lo1, hi1), half));
+  for (int e = 0; e < c; ++e) out[e] = lo[e];
+}
+
 // The r largest eigenpairs of symmetric A (n x n row-major, read from its
 // lower triangle): w receives all n
 // eigenvalues in descending order, row m of `vecs` (r x n) the unit
@@ -465,16 +515,40 @@ struct ShiftedTridiagLU {
 // vectors (Golub & Van Loan, Sec. 8.2.2 and 8.4), re-orthogonalised within
 // clusters of close eigenvalues, and back-transformation by the reflectors.
 // Cost 2n^3 + O(n^2 r) flops instead of the roughly 9n^3 of the full solver.
-bool sym_eig_top(int n, const double* A, int r, double* w, double* vecs) {
+bool sym_eig_top(int n, const double* A, int r, double* w, double* vecs, bool all_values) {
   for (size_t i = 0; i < (size_t)n * n; ++i)
     if (!std::isfinite(A[i])) return false;
   Mat a(A, A + (size_t)n * n), hv((size_t)n * n);  // the lower triangle defines A
   std::vector<double> diag(n), off(n), beta(n);
   householder_tridiag(n, a.data(), diag.data(), off.data(), hv.data(), beta.data());
-  std::vector<double> ev(diag), eo(off);
-  if (!tridiag_ql(n, ev.data(), eo.data(), nullptr)) return false;
-  std::sort(ev.begin(), ev.end(), [](double x, double y) { return x > y; });
-  std::copy(ev.begin(), ev.end(), w);
+  std::vector<double> ev(n);
+  if (all_values) {
+    std::vector<double> eo(off);
+    std::copy(diag.begin(), diag.end(), ev.begin());
+    if (!tridiag_ql(n, ev.data(), eo.data(), nullptr)) return false;
+    std::sort(ev.begin(), ev.end(), [](double x, double y) { return x > y; });
+  } else {  // only the r largest, by bisection
+    std::vector<double> off2(n, 0.0);
+    double glo = diag[0], ghi = diag[0], emax = 0.0;
+    for (int i = 0; i < n; ++i) {
+      const double rad = (i > 0 ? std::fabs(off[i - 1]) : 0.0) + (i + 1 < n ? std::fabs(off[i]) : 0.0);
+      glo = std::min(glo, diag[i] - rad);
+      ghi = std::max(ghi, diag[i] + rad);
+      if (i + 1 < n) {
+        off2[i] = off[i] * off[i];
+        emax = std::max(emax, off2[i]);
+      }
+    }
+    const double pivmin = std::numeric_limits<double>::min() * std::max(1.0, emax);
+    const double pad = 2.0 * std::numeric_limits<double>::epsilon() * std::max(std::fabs(glo), std::fabs(ghi)) + pivmin;
+    for (int m0 = 0; m0 < r; m0 += 8) {
+      int idx[8];
+      const int c = std::min(8, r - m0);
+      for (int e = 0; e < c; ++e) idx[e] = n - 1 - (m0 + e);  // ascending index of the (m0+e)-th largest
+      bisect_eigs(n, diag.data(), off2.data(), pivmin, glo - pad, ghi + pad, idx, c, ev.data() + m0);
+    }
+  }
+  std::copy(ev.begin(), ev.begin() + (all_values ? n : r), w);
 
   const double eps = std::numeric_limits<double>::epsilon();
   double tnorm = 0.0;  // 1-norm of T
@@ -658,8 +732,18 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
   try {
     // ---- per KV head: key mean, centred key moment, and either its Cholesky
     //      factor or its clamped symmetric roots
+    // (the uncentred query moments need nothing from the keys: they are
+    //  computed in the same parallel phase, after the KV heads' tasks)
     std::vector<KvState> kv(H_kv);
-    parallel_for(H_kv, n_threads, [&](int g) {
+    std::vector<Mat> sq_all(method == SAKI_METHOD_OPT ? H_q : 0);
+    parallel_for(H_kv + (int)sq_all.size(), n_threads, [&](int task) {
+      if (task >= H_kv) {
+        const int h = task - H_kv;
+        sq_all[h].resize(dd);
+        moment(T, d, q_cal + (size_t)h * T * d, nullptr, sq_all[h].data());
+        return;
+      }
+      const int g = task;
       KvState& st = kv[g];
       const float* k = k_cal + (size_t)g * T * d;
       st.mu.assign(d, 0.0);
@@ -705,10 +789,8 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
         if (n_clamped) { n_clamped[2 * h] = 0; n_clamped[2 * h + 1] = 0; }
         return;
       }
-      // Sigma_q (uncentred)
-      const float* q = q_cal + (size_t)h * T * d;
-      Mat sq(dd);
-      moment(T, d, q, nullptr, sq.data());
+      // Sigma_q (uncentred), from the first phase
+      const Mat& sq = sq_all[h];
       std::vector<double> sig(d), bqc(d), bkc(d);
       Mat scratch(dd);
       if (st.chol && unclamped_cholesky(d, sq.data(), floor_rel, scratch.data(), false)) {
@@ -717,8 +799,8 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
         Mat M(dd);
         congruence_lower(d, sq.data(), L, M.data());
         std::vector<double> w(d), vt((size_t)r * d);
-        if (!sym_eig_top(d, M.data(), r, w.data(), vt.data())) { failed = 1; return; }
-        for (int m = 0; m < d; ++m) sig[m] = std::sqrt(std::max(w[m], 0.0));
+        if (!sym_eig_top(d, M.data(), r, w.data(), vt.data(), sigma != nullptr)) { failed = 1; return; }
+        for (int m = 0; m < (sigma ? d : r); ++m) sig[m] = std::sqrt(std::max(w[m], 0.0));
         // all r columns at once (d x r, row-major): P = L V', X = L^-T V'
         Mat V((size_t)d * r), P((size_t)d * r, 0.0), X((size_t)d * r);
         for (int m = 0; m < r; ++m)
@@ -769,8 +851,8 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
         for (int j = 0; j < d; ++j) Ct[(size_t)j * d + i] = C[(size_t)i * d + j];
       matmul(d, Ct.data(), C.data(), CtC.data());
       std::vector<double> w(d), vt((size_t)r * d);
-      if (!sym_eig_top(d, CtC.data(), r, w.data(), vt.data())) { failed = 1; return; }
-      for (int m = 0; m < d; ++m) sig[m] = std::sqrt(std::max(w[m], 0.0));
+      if (!sym_eig_top(d, CtC.data(), r, w.data(), vt.data(), sigma != nullptr)) { failed = 1; return; }
+      for (int m = 0; m < (sigma ? d : r); ++m) sig[m] = std::sqrt(std::max(w[m], 0.0));
       if (sigma)
         for (int m = 0; m < d; ++m) sigma[(size_t)h * d + m] = sig[m];
       if (n_clamped) { n_clamped[2 * h] = nq; n_clamped[2 * h + 1] = nk; }

@@ -447,8 +447,13 @@ __device__ __forceinline__ float normal_upper_quantile(float tail) {
 
 constexpr int kBins = 64;
 constexpr int kCollect = 128;
+constexpr int kSampleTiles = 8;   // moments from at least this many tiles per chunk
+constexpr float kWinLo = 1.25f;   // histogram window around the predicted 64th score (sd)
+constexpr float kWinHi = 0.75f;
 constexpr int kCandRow = kCollect + 1;  // padded row strides (LDS bank spread)
 constexpr int kHistRow = kBins + 1;
+constexpr int kSCollect = 96;            // candidates per row in score_mfma_kernel
+constexpr int kSCandRow = kSCollect + 1;
 enum RowMode : int { kModeAll = 0, kModeHist = 1, kModeFallback = 2 };
 
 // Scores of one 64-key tile for the wave's 16 queries: acc[sub][v] is query
@@ -482,29 +487,52 @@ struct MfmaScorer {
     }
   }
 
-  __device__ __forceinline__ void tile(const uint8_t* tb, int qi, int g, f32x4_t acc[4]) const {
+  // raw operands of one tile: NL 16-byte loads per 16-key sub-block
+  static constexpr int NL = SBF ? (RK == 16 ? 1 : RK / 32) : RK / 16;
+  struct Raw {
+    uint4 v[4][NL];
+  };
+  // the next tile is loaded while the current one is scored when its raw
+  // operands fit in 32 registers
+  static constexpr bool kPrefetch = 4 * NL <= 8;
+
+  __device__ __forceinline__ void load(const uint8_t* tb, int qi, int g, Raw& r) const {
 #pragma unroll
     for (int sub = 0; sub < 4; ++sub) {
       const int key = 16 * sub + qi;
-      f32x4_t a = {0.f, 0.f, 0.f, 0.f};
-      if constexpr (SBF) {
-        if constexpr (RK == 16) {
-          const uint2 raw = *reinterpret_cast<const uint2*>(tb + (size_t)(g / 2) * kTile * 16 +
-                                                           (size_t)key * 16 + (g % 2) * 8);
-          a = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_i16x4(raw), zb4, a, 0, 0, 0);
-        } else {
+      if constexpr (SBF && RK == 16) {
+        const uint2 raw = *reinterpret_cast<const uint2*>(tb + (size_t)(g / 2) * kTile * 16 +
+                                                         (size_t)key * 16 + (g % 2) * 8);
+        r.v[sub][0] = uint4{raw.x, raw.y, 0u, 0u};
+      } else if constexpr (SBF) {
 #pragma unroll
-          for (int kk = 0; kk < NKB; ++kk) {
-            const uint4 raw = *reinterpret_cast<const uint4*>(
-                tb + (size_t)(4 * kk + g) * kTile * 16 + (size_t)key * 16);
-            a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(raw), zb[kk], a, 0, 0, 0);
-          }
-        }
+        for (int kk = 0; kk < NL; ++kk)
+          r.v[sub][kk] = *reinterpret_cast<const uint4*>(tb + (size_t)(4 * kk + g) * kTile * 16 +
+                                                         (size_t)key * 16);
       } else {
 #pragma unroll
-        for (int m = 0; m < RK / 16; ++m) {
-          const uint4 raw = *reinterpret_cast<const uint4*>(
-              tb + (size_t)(g + 4 * m) * kTile * 16 + (size_t)key * 16);
+        for (int m = 0; m < NL; ++m)
+          r.v[sub][m] = *reinterpret_cast<const uint4*>(tb + (size_t)(g + 4 * m) * kTile * 16 +
+                                                        (size_t)key * 16);
+      }
+    }
+  }
+
+  __device__ __forceinline__ void mma(const Raw& r, f32x4_t acc[4]) const {
+#pragma unroll
+    for (int sub = 0; sub < 4; ++sub) {
+      f32x4_t a = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (SBF && RK == 16) {
+        a = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_i16x4(uint2{r.v[sub][0].x, r.v[sub][0].y}),
+                                                     zb4, a, 0, 0, 0);
+      } else if constexpr (SBF) {
+#pragma unroll
+        for (int kk = 0; kk < NL; ++kk)
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(r.v[sub][kk]), zb[kk], a, 0, 0, 0);
+      } else {
+#pragma unroll
+        for (int m = 0; m < NL; ++m) {
+          const uint4 raw = r.v[sub][m];
           a = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(raw.x), zf[4 * m + 0], a, 0, 0, 0);
           a = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(raw.y), zf[4 * m + 1], a, 0, 0, 0);
           a = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(raw.z), zf[4 * m + 2], a, 0, 0, 0);
@@ -512,6 +540,31 @@ struct MfmaScorer {
         }
       }
       acc[sub] = a;
+    }
+  }
+
+  // body(t0, acc) for the tiles t0 = t_beg, t_beg + step, ... < t_end
+  template <class F>
+  __device__ __forceinline__ void for_tiles(const uint8_t* hbase, int t_beg, int t_end, int step,
+                                            int qi, int g, F&& body) const {
+    if constexpr (kPrefetch) {
+      Raw cur, nxt;
+      if (t_beg < t_end) load(hbase + (size_t)(t_beg / kTile) * TB, qi, g, cur);
+      for (int t0 = t_beg; t0 < t_end; t0 += step) {
+        if (t0 + step < t_end) load(hbase + (size_t)((t0 + step) / kTile) * TB, qi, g, nxt);
+        f32x4_t acc[4];
+        mma(cur, acc);
+        body(t0, acc);
+        cur = nxt;
+      }
+    } else {
+      for (int t0 = t_beg; t0 < t_end; t0 += step) {
+        Raw cur;
+        load(hbase + (size_t)(t0 / kTile) * TB, qi, g, cur);
+        f32x4_t acc[4];
+        mma(cur, acc);
+        body(t0, acc);
+      }
     }
   }
 };
@@ -529,11 +582,10 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
   constexpr int D = saki::kHeadDim;
   using KO = KeysF32;
   using Scorer = MfmaScorer<RK, SBF>;
-  // per wave: 16 KB of candidate space (also the z staging area, and the
-  // list + buffer of the online fallback) and 4 KB of histogram (also the
-  // fallback's score staging)
-  __shared__ uint64_t cand_mem[kMfmaWaves][kMR * kCandRow];
-  __shared__ int hist_mem[kMfmaWaves][kMR * kHistRow];
+  // per wave 12.1 KB, used in turn as: z staging [16][RK] floats; histogram
+  // [16][kHistRow] ints (pass 2); candidates [16][kSCandRow] (pass 3); or the
+  // fallback's score staging [16][64] floats + list and buffer of 8 rows
+  __shared__ uint64_t cand_mem[kMfmaWaves][kMR * kSCandRow];
   __shared__ int ccount[kMfmaWaves][kMR];
   const int wave = threadIdx.x / kWave, lane = lane_id();
   const int waves = blockDim.x / kWave;
@@ -554,7 +606,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
   const int kbeg = ch * chunk;
   const int kend = min(kbeg + chunk, kmax);
   uint64_t* cand = cand_mem[wave];
-  int* hist = hist_mem[wave];
+  int* hist = reinterpret_cast<int*>(cand);
 
   // ---- query sketch: D[m][qi] = sum_c B_q[c][m] q[qi][c], lane group g feeds c = 4s + g
   float my_b;
@@ -590,35 +642,39 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
   }
   const uint8_t* hbase = index + bh * n_tiles * Scorer::TB;
 
-  // ---- pass 1: moments of this lane's row over the chunk
-  float sum = 0.f, sumsq = 0.f;
-  for (int t0 = kbeg; t0 < kend; t0 += kTile) {
-    f32x4_t acc[4];
-    sc.tile(hbase + (size_t)(t0 / kTile) * Scorer::TB, qi, g, acc);
-    const bool need_mask = t0 + kTile > kmin;
-#pragma unroll
-    for (int sub = 0; sub < 4; ++sub)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        float x = acc[sub][v];
-        if (need_mask && t0 + 16 * sub + 4 * g + v >= my_lim) x = 0.f;
-        sum += x;
-        sumsq = fmaf(x, x, sumsq);
-      }
-  }
-  sum = sum_lane_groups(sum);
-  sumsq = sum_lane_groups(sumsq);
+  // ---- pass 1: moments of this lane's row over a sample of the chunk's
+  //      tiles (every stride-th tile, at least kSampleTiles of them)
   const int n_row = row_ok ? max(0, min(my_lim, kend) - kbeg) : 0;
+  const int stride = max(1, (kend - kbeg) / (kTile * kSampleTiles));
+  float sum = 0.f, sumsq = 0.f, cnt = 0.f;
+  if (wave_max_i(n_row) > kSCollect) {
+    sc.for_tiles(hbase, kbeg, kend, stride * kTile, qi, g, [&](int t0, f32x4_t* acc) {
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const bool in = t0 + 16 * sub + 4 * g + v < my_lim;
+          const float x = in ? acc[sub][v] : 0.f;
+          sum += x;
+          sumsq = fmaf(x, x, sumsq);
+          cnt += in ? 1.f : 0.f;
+        }
+    });
+    sum = sum_lane_groups(sum);
+    sumsq = sum_lane_groups(sumsq);
+    cnt = sum_lane_groups(cnt);
+  }
   int mode = kModeAll;
   float inv_w = 0.f, off = 0.f;
-  if (n_row > kCollect) {
-    const float mean = sum / (float)n_row;
-    const float var = fmaxf(sumsq / (float)n_row - mean * mean, 0.f);
+  if (n_row > kSCollect) {
+    const float mean = sum / cnt;
+    const float var = fmaxf(sumsq / cnt - mean * mean, 0.f);
     const float sd = sqrtf(var);
-    if (sd > 0.f && isfinite(sd) && isfinite(mean)) {
+    if (cnt > 0.f && sd > 0.f && isfinite(sd) && isfinite(mean)) {
+      // bins from kWinLo sd below to kWinHi sd above the predicted 64th score
       const float t_hat = my_b + mean + sd * normal_upper_quantile((float)kList / (float)n_row);
-      const float lo = t_hat - 2.f * sd;
-      inv_w = (float)(kBins - 2) / (3.f * sd);
+      const float lo = t_hat - kWinLo * sd;
+      inv_w = (float)(kBins - 2) / ((kWinLo + kWinHi) * sd);
       off = 1.f - lo * inv_w;  // bin(s) = fmaf(s, inv_w, off): below 1 = out of range
       mode = kModeHist;
     } else {
@@ -632,9 +688,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
   if (any_hist) {
     for (int i = lane; i < kMR * kHistRow; i += kWave) hist[i] = 0;
     wave_lds_sync();
-    for (int t0 = kbeg; t0 < kend; t0 += kTile) {
-      f32x4_t acc[4];
-      sc.tile(hbase + (size_t)(t0 / kTile) * Scorer::TB, qi, g, acc);
+    sc.for_tiles(hbase, kbeg, kend, kTile, qi, g, [&](int t0, f32x4_t* acc) {
 #pragma unroll
       for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
@@ -643,7 +697,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
           if (mode == kModeHist && x >= 1.f && t0 + 16 * sub + 4 * g + v < my_lim)
             atomicAdd(&hist[qi * kHistRow + min((int)x, kBins - 1)], 1);
         }
-    }
+    });
     wave_lds_sync();
     // per row: the highest bin whose count from the top reaches 64
     for (int r = 0; r < kMR; ++r) {
@@ -662,7 +716,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
         new_mode = kModeFallback;
       } else {
         const int l = __builtin_ctzll(reach);
-        if (__builtin_amdgcn_readlane(x, l) > kCollect) new_mode = kModeFallback;
+        if (__builtin_amdgcn_readlane(x, l) > kSCollect) new_mode = kModeFallback;
         bstar = (float)(kBins - 1 - l);
       }
       if (qi == r) {
@@ -673,34 +727,50 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
   }
 
   if (__ballot(mode == kModeFallback) == 0) {
-    // ---- pass 3: collect the gated candidates
-    if (lane < kMR) ccount[wave][lane] = 0;
-    wave_lds_sync();
-    for (int t0 = kbeg; t0 < kend; t0 += kTile) {
-      f32x4_t acc[4];
-      sc.tile(hbase + (size_t)(t0 / kTile) * Scorer::TB, qi, g, acc);
+    // ---- pass 3: collect the gated candidates; the four lanes of a row
+    //      (lane groups g) append at offsets from a prefix of their counts
+    int base = 0;  // the row's entries so far (same in its four lanes)
+    wave_lds_sync();  // the histogram's reads are done: its space takes candidates
+    sc.for_tiles(hbase, kbeg, kend, kTile, qi, g, [&](int t0, f32x4_t* acc) {
+      uint32_t take = 0;
 #pragma unroll
       for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int key = t0 + 16 * sub + 4 * g + v;
           const float sv = acc[sub][v] + my_b;
-          const bool take = key < my_lim && (mode == kModeAll || fmaf(sv, inv_w, off) >= gate);
-          if (take) {
-            const int pos = atomicAdd(&ccount[wave][qi], 1);
-            if (pos < kCollect) cand[qi * kCandRow + pos] = KO::make(sv, key);
-          }
+          if (key < my_lim && (mode == kModeAll || fmaf(sv, inv_w, off) >= gate))
+            take |= 1u << (4 * sub + v);
         }
-    }
+      if (__ballot(take != 0) == 0) return;
+      const int c = __popc(take);
+      const int c1 = (int)xor_shfl_u32((uint32_t)c, 16);   // count of lane group g ^ 1
+      const int c2 = (int)xor_shfl_u32((uint32_t)c, 32);   // g ^ 2
+      const int c3 = (int)xor_shfl_u32((uint32_t)c1, 32);  // g ^ 3
+      // entries of the groups below g: g=1: group 0 = g^1; g=2: groups 0, 1 =
+      // g^2, g^3; g=3: groups 0, 1, 2 = g^3, g^2, g^1
+      int pos = base + (g == 1 ? c1 : g == 2 ? c2 + c3 : g == 3 ? c1 + c2 + c3 : 0);
+      base += c + c1 + c2 + c3;
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          if (take & (1u << (4 * sub + v))) {
+            if (pos < kSCollect)
+              cand[qi * kSCandRow + pos] = KO::make(acc[sub][v] + my_b, t0 + 16 * sub + 4 * g + v);
+            ++pos;
+          }
+    });
+    if (lane < kMR) ccount[wave][lane] = base;  // lane r < 16 is row r, group 0
     wave_lds_sync();
     for (int r = 0; r < kMR; ++r) {
       const int i = row0 + r;
       if (i >= Q) break;
-      const int c = min(ccount[wave][r], kCollect);
-      uint64_t a = lane < c ? cand[r * kCandRow + lane] : KO::pad();
+      const int c = min(ccount[wave][r], kSCollect);
+      uint64_t a = lane < c ? cand[r * kSCandRow + lane] : KO::pad();
       wave_sort<KO>(a);
       if (c > kList) {
-        uint64_t b2 = lane + kList < c ? cand[r * kCandRow + kList + lane] : KO::pad();
+        uint64_t b2 = lane + kList < c ? cand[r * kSCandRow + kList + lane] : KO::pad();
         wave_sort<KO>(b2);
         wave_merge<KO>(a, b2);
       }
@@ -717,42 +787,46 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
     return;
   }
 
-  // ---- fallback: online selection over the chunk (rare)
-  float* stage = reinterpret_cast<float*>(hist);  // [16][64], key column swizzled
-  RowLists<KO, kMR> top;
-  top.init(cand, cand + kMR * kList);
-  for (int t0 = kbeg; t0 < kend; t0 += kTile) {
-    f32x4_t acc[4];
-    sc.tile(hbase + (size_t)(t0 / kTile) * Scorer::TB, qi, g, acc);
+  // ---- fallback: online selection over the chunk (rare), in two halves of
+  //      8 rows so that the lists fit the wave's LDS
+  float* stage = reinterpret_cast<float*>(cand);  // [16][64], key column swizzled
+  constexpr int kHalf = kMR / 2;
+  for (int half = 0; half < 2; ++half) {
+    RowLists<KO, kHalf> top;
+    top.init(cand + kMR * kTile / 2, cand + kMR * kTile / 2 + kHalf * kList);
+    sc.for_tiles(hbase, kbeg, kend, kTile, qi, g, [&](int t0, f32x4_t* acc) {
 #pragma unroll
-    for (int sub = 0; sub < 4; ++sub) {
-      const f32x4_t sv = acc[sub] + my_b;
-      *reinterpret_cast<f32x4_t*>(&stage[qi * kTile + ((16 * sub + 4 * g) ^ (qi << 2))]) = sv;
-    }
-    wave_lds_sync();
-    const bool need_mask = t0 + kTile > kmin;
-    for (int r = 0; r < kMR; ++r) {
-      float sv = stage[r * kTile + (lane ^ (r << 2))];
-      const int j = t0 + lane;
-      if (need_mask && j >= __builtin_amdgcn_readlane(my_lim, r)) sv = -INFINITY;
-      top.offer(r, sv, j);
-    }
-    wave_lds_sync();
-  }
-  for (int r = 0; r < kMR; ++r) {
-    top.finish(r);
-    const int i = row0 + r;
-    if (i >= Q) continue;
-    const uint64_t e = top.entry(r);
-    if (n_chunks == 1) {
-      if (lane < k) {
-        const size_t o = (bh * Q + i) * k + lane;
-        top_idx[o] = out_index<KO>(e);
-        if (top_score) top_score[o] = KO::score(e);
+      for (int sub = 0; sub < 4; ++sub) {
+        const f32x4_t sv = acc[sub] + my_b;
+        *reinterpret_cast<f32x4_t*>(&stage[qi * kTile + ((16 * sub + 4 * g) ^ (qi << 2))]) = sv;
       }
-    } else {
-      part[((bh * Q + i) * n_chunks + ch) * kMaxK + lane] = e;
+      wave_lds_sync();
+      const bool need_mask = t0 + kTile > kmin;
+      for (int rr = 0; rr < kHalf; ++rr) {
+        const int r = kHalf * half + rr;
+        float sv = stage[r * kTile + (lane ^ (r << 2))];
+        const int j = t0 + lane;
+        if (need_mask && j >= __builtin_amdgcn_readlane(my_lim, r)) sv = -INFINITY;
+        top.offer(rr, sv, j);
+      }
+      wave_lds_sync();
+    });
+    for (int rr = 0; rr < kHalf; ++rr) {
+      top.finish(rr);
+      const int i = row0 + kHalf * half + rr;
+      if (i >= Q) continue;
+      const uint64_t e = top.entry(rr);
+      if (n_chunks == 1) {
+        if (lane < k) {
+          const size_t o = (bh * Q + i) * k + lane;
+          top_idx[o] = out_index<KO>(e);
+          if (top_score) top_score[o] = KO::score(e);
+        }
+      } else {
+        part[((bh * Q + i) * n_chunks + ch) * kMaxK + lane] = e;
+      }
     }
+    wave_lds_sync();
   }
 }
 

@@ -85,10 +85,11 @@ def _host(a, dtype):
 # ------------------------------------------------------------------ host calls
 
 def saki_calibrate(q_cal, k_cal, r: int, method: str = "opt", floor_rel: float = 1e-6,
-                   n_threads: int = 0):
+                   n_threads: int = 0, with_sigma: bool = True):
     """q_cal [H_q, T, d], k_cal [H_kv, T, d] (float32) -> dict of numpy arrays
-    B_q, B_k [H_q, d, r] float32, mu [H_kv, d] float32, sigma [H_q, d] float64,
-    n_clamped [H_q, 2] int32."""
+    B_q, B_k [H_q, d, r] float32, mu [H_kv, d] float32, sigma [H_q, d] float64
+    (None without with_sigma, which lets the library compute only the r
+    largest singular values), n_clamped [H_q, 2] int32."""
     q, qp = _host(q_cal, np.float32)
     k, kp = _host(k_cal, np.float32)
     if q.ndim != 3 or k.ndim != 3 or q.shape[1:] != k.shape[1:]:
@@ -98,12 +99,12 @@ def saki_calibrate(q_cal, k_cal, r: int, method: str = "opt", floor_rel: float =
     B_q = np.empty((H_q, d, r), np.float32)
     B_k = np.empty((H_q, d, r), np.float32)
     mu = np.empty((H_kv, d), np.float32)
-    sigma = np.empty((H_q, d), np.float64)
+    sigma = np.empty((H_q, d), np.float64) if with_sigma else None
     ncl = np.empty((H_q, 2), np.int32)
     st = lib().saki_calibrate(qp, kp, H_q, H_kv, T, d, int(r), _METHODS[method],
                               float(floor_rel), B_q.ctypes.data, B_k.ctypes.data,
-                              mu.ctypes.data, sigma.ctypes.data, ncl.ctypes.data,
-                              int(n_threads))
+                              mu.ctypes.data, sigma.ctypes.data if with_sigma else None,
+                              ncl.ctypes.data, int(n_threads))
     _check("saki_calibrate", st)
     return {"B_q": B_q, "B_k": B_k, "mu": mu, "sigma": sigma, "n_clamped": ncl}
 

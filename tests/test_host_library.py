@@ -82,6 +82,23 @@ def test_calibration_matches_oracle(spec_name, r):
             assert np.max(np.abs(a - b) / np.abs(b).max(axis=0)) < 1e-5
 
 
+@pytest.mark.parametrize("spec_name", ["llama31_8b_layer", "qwen25_7b_decode"])
+def test_calibration_without_sigma_matches(spec_name):
+    """Without the singular-value output the library takes only the r largest
+    eigenvalues (bisection instead of QL): the factors agree with the full path
+    to float32 rounding, and the top-r singular values with the oracle."""
+    spec = W.SPECS[spec_name].with_(N=64, Q=1, q_start=0, batch=1)
+    inp = W.make_layer(spec)
+    full = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32)
+    fast = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32, with_sigma=False)
+    assert fast["sigma"] is None
+    for name in ("B_q", "B_k"):
+        a, b = fast[name].astype(np.float64), full[name].astype(np.float64)
+        assert np.max(np.abs(a - b) / np.abs(b).max(axis=1, keepdims=True)) < 2e-6
+    np.testing.assert_array_equal(fast["mu"], full["mu"])
+    np.testing.assert_array_equal(fast["n_clamped"], full["n_clamped"])
+
+
 def test_calibration_clamps_like_oracle():
     """T < d: both moments are singular and the floor binds."""
     rng = np.random.default_rng(9)
