@@ -548,14 +548,22 @@ struct MfmaScorer {
   __device__ __forceinline__ void for_tiles(const uint8_t* hbase, int t_beg, int t_end, int step,
                                             int qi, int g, F&& body) const {
     if constexpr (kPrefetch) {
-      Raw cur, nxt;
-      if (t_beg < t_end) load(hbase + (size_t)(t_beg / kTile) * TB, qi, g, cur);
-      for (int t0 = t_beg; t0 < t_end; t0 += step) {
-        if (t0 + step < t_end) load(hbase + (size_t)((t0 + step) / kTile) * TB, qi, g, nxt);
+      // two register buffers taken in turn; the load past the last tile is
+      // clamped to it (a valid, unused reload) so that no load is conditional
+      if (t_beg >= t_end) return;
+      const int last = t_beg + ((t_end - 1 - t_beg) / step) * step;
+      auto at = [&](int t) { return hbase + (size_t)(min(t, last) / kTile) * TB; };
+      Raw ra, rb;
+      load(at(t_beg), qi, g, ra);
+      for (int t0 = t_beg; t0 < t_end; t0 += 2 * step) {
+        load(at(t0 + step), qi, g, rb);
         f32x4_t acc[4];
-        mma(cur, acc);
+        mma(ra, acc);
         body(t0, acc);
-        cur = nxt;
+        if (t0 + step >= t_end) break;
+        load(at(t0 + 2 * step), qi, g, ra);
+        mma(rb, acc);
+        body(t0 + step, acc);
       }
     } else {
       for (int t0 = t_beg; t0 < t_end; t0 += step) {
