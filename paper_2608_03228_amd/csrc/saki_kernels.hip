@@ -451,7 +451,7 @@ constexpr int kSampleTiles = 8;   // moments from at least this many tiles per c
 constexpr float kWinLo = 1.25f;   // histogram window around the predicted 64th score (sd)
 constexpr float kWinHi = 0.75f;
 constexpr int kCandRow = kCollect + 1;  // padded row strides (LDS bank spread)
-constexpr int kHistRow = kBins + 1;
+constexpr int kHistRow = kBins + 5;  // 64 bins, 4 private overflow slots, 1 pad
 constexpr int kSCollect = 96;            // candidates per row in score_mfma_kernel
 constexpr int kSCandRow = kSCollect + 1;
 enum RowMode : int { kModeAll = 0, kModeHist = 1, kModeFallback = 2 };
@@ -696,14 +696,23 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
   if (any_hist) {
     for (int i = lane; i < kMR * kHistRow; i += kWave) hist[i] = 0;
     wave_lds_sync();
+    // every score adds to a bin; scores below the window, masked keys and rows
+    // not in histogram mode go to the lane's own slot (kBins + g), which no
+    // other lane touches and which is never read
+    const float x_hi = (float)(kBins - 1);
+    const int trash = kBins + g;
+    const bool hmode = mode == kModeHist;
     sc.for_tiles(hbase, kbeg, kend, kTile, qi, g, [&](int t0, f32x4_t* acc) {
+      const bool need_mask = t0 + kTile > kmin;
 #pragma unroll
       for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const float x = fmaf(acc[sub][v] + my_b, inv_w, off);
-          if (mode == kModeHist && x >= 1.f && t0 + 16 * sub + 4 * g + v < my_lim)
-            atomicAdd(&hist[qi * kHistRow + min((int)x, kBins - 1)], 1);
+          int bin = (int)fminf(x, x_hi);
+          bin = (hmode && x >= 1.f) ? bin : trash;
+          if (need_mask && t0 + 16 * sub + 4 * g + v >= my_lim) bin = trash;
+          atomicAdd(&hist[qi * kHistRow + bin], 1);
         }
     });
     wave_lds_sync();
@@ -740,16 +749,21 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
     int base = 0;  // the row's entries so far (same in its four lanes)
     wave_lds_sync();  // the histogram's reads are done: its space takes candidates
     sc.for_tiles(hbase, kbeg, kend, kTile, qi, g, [&](int t0, f32x4_t* acc) {
+      // the same bin test as the histogram (rows that collect everything have
+      // inv_w = off = 0 and gate = -inf)
       uint32_t take = 0;
 #pragma unroll
       for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int key = t0 + 16 * sub + 4 * g + v;
-          const float sv = acc[sub][v] + my_b;
-          if (key < my_lim && (mode == kModeAll || fmaf(sv, inv_w, off) >= gate))
-            take |= 1u << (4 * sub + v);
-        }
+        for (int v = 0; v < 4; ++v)
+          take |= (fmaf(acc[sub][v] + my_b, inv_w, off) >= gate) ? (1u << (4 * sub + v)) : 0u;
+      if (t0 + kTile > kmin) {  // a tile crossing some row's causal limit
+#pragma unroll
+        for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (t0 + 16 * sub + 4 * g + v >= my_lim) take &= ~(1u << (4 * sub + v));
+      }
       if (__ballot(take != 0) == 0) return;
       const int c = __popc(take);
       const int c1 = (int)xor_shfl_u32((uint32_t)c, 16);   // count of lane group g ^ 1
