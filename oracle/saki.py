@@ -21,7 +21,8 @@ from __future__ import annotations
 import numpy as np
 
 __all__ = [
-    "second_moments", "clamped_roots", "saki_calibrate", "key_pca_factors",
+    "second_moments", "clamped_roots", "saki_calibrate", "saki_calibrate_shared",
+    "key_pca_factors",
     "weight_svd_factors", "score_loss", "codes", "query_sketch", "sketch_scores",
     "direct_scores", "exact_scores", "candidate_limits", "topk_row", "topk_rows",
     "recall_hits", "bf16_round", "f32_round", "score_scale", "predicted_reduction",
@@ -106,6 +107,28 @@ def saki_calibrate(q_cal: np.ndarray, k_cal: np.ndarray, r: int,
     M_r = B_q B_k^T; optimum loss = sum of squared tail singular values.
     """
     sq, sk, mu = second_moments(q_cal, k_cal)
+    return _calibrate_from_moments(sq, sk, mu, r, floor_rel)
+
+
+def saki_calibrate_shared(q_cals: np.ndarray, k_cal: np.ndarray, r: int,
+                          floor_rel: float = 1e-6) -> dict:
+    """One rank-r map shared by the G query heads of a KV group.
+
+    Extension beyond the paper, which optimises each head on its own: the
+    group's summed objective sum_h L_h(P) of Eq. 2 is linear in Sigma_q, so it
+    equals G * L(P) for the pooled moment Sigma_q = (1/G) sum_h Sigma_q^(h), and
+    Proposition 1 applied to the pooled moment gives the optimal shared map.
+    q_cals [G, T, d], k_cal [T, d].
+    """
+    q_cals = np.asarray(q_cals, np.float64)
+    G = q_cals.shape[0]
+    sk, mu = second_moments(q_cals[0], k_cal)[1:]
+    sq = sum(second_moments(q_cals[h], k_cal)[0] for h in range(G)) / G
+    return _calibrate_from_moments(sq, sk, mu, r, floor_rel)
+
+
+def _calibrate_from_moments(sq, sk, mu, r, floor_rel):
+    """The steps of saki_calibrate after the moments."""
     sq_h, sq_ih, nq = clamped_roots(sq, floor_rel)
     sk_h, sk_ih, nk = clamped_roots(sk, floor_rel)
     C = sq_h @ sk_h

@@ -274,3 +274,54 @@ def test_predicted_reduction_matches_heldout_measurement():
     measured = 1.0 - np.mean((s - s_hat) ** 2) / np.mean(base ** 2)
     predicted = O.predicted_reduction(cal["sigma"], 32)
     assert abs(measured - predicted) < 0.01, (measured, predicted)
+
+
+def _rows(S):
+    """2d rows whose (1/T) sum x x^T is exactly S (zero mean)."""
+    d = S.shape[0]
+    L = np.linalg.cholesky(S)
+    return np.concatenate([np.sqrt(d) * L.T, -np.sqrt(d) * L.T])
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_shared_group_map_minimises_the_group_loss(seed):
+    """The GQA-shared map (pooled query moment) against the summed per-head
+    objective of Eq. 2: it equals G times the pooled tail energy (linearity of
+    the loss in Sigma_q), and no other rank-r map -- each head's own optimum,
+    key PCA, random maps -- does better on the group."""
+    rng = np.random.default_rng(seed)
+    G, d, r = 3, 12, 3
+    Sqs = [_spd(rng, d, 50.0) for _ in range(G)]
+    Sk = _spd(rng, d, 50.0)
+    k = _rows(Sk)
+    q = np.stack([_rows(S) for S in Sqs])
+    sh = O.saki_calibrate_shared(q, k, r)
+    halves = [O.clamped_roots(S)[0] for S in Sqs]
+    sk_half = O.clamped_roots(Sk)[0]
+
+    def group_loss(P):
+        return sum(O.score_loss(P, hq, sk_half) for hq in halves)
+
+    Lg = group_loss(sh["M"])
+    assert abs(Lg - G * sh["tail"]) <= 1e-10 * G * float(np.sum(sh["sigma"] ** 2))
+    for h in range(G):
+        own = O.saki_calibrate(q[h], k, r)
+        assert Lg <= group_loss(own["M"]) + 1e-12
+    V = O.key_pca_factors(Sk, r)
+    assert Lg <= group_loss(V @ V.T) + 1e-12
+    for _ in range(300):
+        P = rng.standard_normal((d, r)) @ rng.standard_normal((r, d))
+        assert Lg <= group_loss(P) + 1e-12
+
+
+def test_shared_map_special_cases():
+    """One head per group, or identical heads: the shared map is the
+    per-head map."""
+    rng = np.random.default_rng(5)
+    d, r = 10, 4
+    Sq, Sk = _spd(rng, d, 20.0), _spd(rng, d, 20.0)
+    q, k = _rows(Sq), _rows(Sk)
+    own = O.saki_calibrate(q, k, r)
+    np.testing.assert_allclose(O.saki_calibrate_shared(q[None], k, r)["M"], own["M"], atol=1e-12)
+    np.testing.assert_allclose(O.saki_calibrate_shared(np.stack([q, q, q]), k, r)["M"], own["M"],
+                               atol=1e-12)
