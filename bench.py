@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--r", type=int, default=32)
     ap.add_argument("--sketch", default="bf16", choices=["bf16", "f32"])
     ap.add_argument("--k", type=int, default=64)
+    ap.add_argument("--shared", action="store_true",
+                    help="GQA-shared index: one code set per KV head (pooled query moment)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=4,
                     help="query heads of the CPU-baseline sample (one KV group)")
@@ -139,16 +141,21 @@ def run_decode(args, spec):
     H_q, Q = spec.H_q, spec.Q
     n_q = args.warmup + args.steps
     qs = torch.from_numpy(np.stack([decode_queries(spec, s) for s in range(n_q)])).to(dev)
-    cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], r)
+    G = H_q // H_kv
+    IH = H_kv if args.shared else H_q  # code sets per sequence
+    cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], r,
+                           method="shared" if args.shared else "opt")
     Bq, Bk, mu = (torch.from_numpy(cal[n]).to(dev) for n in ("B_q", "B_k", "mu"))
-    index = torch.empty(S.saki_index_bytes(B, H_q, N, r, sk), dtype=torch.uint8, device=dev)
+    if args.shared:
+        Bk = Bk[::G].contiguous()
+    index = torch.empty(S.saki_index_bytes(B, IH, N, r, sk), dtype=torch.uint8, device=dev)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    S.saki_build_index(keys, Bk, mu, r, sk, H_q, index=index)
+    S.saki_build_index(keys, Bk, mu, r, sk, IH, index=index)
     e1.record()
     torch.cuda.synchronize()
     build_full_ms = e0.elapsed_time(e1)
-    ws = torch.empty(max(1, S.saki_score_topk_workspace_bytes(B, H_q, Q, N, r, k, sk)),
+    ws = torch.empty(max(1, S.saki_score_topk_workspace_bytes(B, H_q, Q, N, r, k, sk, IH)),
                      dtype=torch.uint8, device=dev)
     top_idx = torch.empty((n_q, B, H_q, Q, k), dtype=torch.int32, device=dev)
     top_sc = torch.empty((n_q, B, H_q, Q, k), dtype=torch.float32, device=dev)
@@ -158,11 +165,11 @@ def run_decode(args, spec):
         if timed:
             e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
             e[0].record()
-        S.saki_build_index(keys, Bk, mu, r, sk, H_q, index=index, n_begin=N - 1, n_count=1)
+        S.saki_build_index(keys, Bk, mu, r, sk, IH, index=index, n_begin=N - 1, n_count=1)
         if timed:
             e[1].record()
         S.saki_score_topk(index, sk, qs[s], Bq, mu, H_kv, N, N, r, k=k, ws=ws,
-                          top_idx=top_idx[s], top_score=top_sc[s])
+                          top_idx=top_idx[s], top_score=top_sc[s], index_heads=IH)
         if timed:
             e[2].record()
             ev.append(e)
@@ -195,7 +202,7 @@ def run_decode(args, spec):
     per_head = h.sum(axis=(0, 1, 3)) / (k * Q * n_q)
 
     es = 2 if sk == "bf16" else 4
-    code_bytes = B * H_q * N * r * es
+    code_bytes = B * IH * N * r * es
     scan_bytes = code_bytes + B * H_q * Q * d * 4 + B * H_q * Q * k * 8
     roof = {"bound": "hbm", "achieved": scan_bytes / (score_ms / 1e3) / 1e9,
             "peak": PEAK["hbm_GBps"], "unit": "GB/s"}
@@ -224,6 +231,7 @@ def run_decode(args, spec):
         "data": "synthetic",
         "config": {"workload": spec.name, "H_q": H_q, "H_kv": H_kv, "d": d, "latent_D": spec.D,
                    "N": N, "queries_per_head": Q, "batch": B, "r": r, "sketch": sk, "k": k,
+                   "index": "gqa_shared" if args.shared else "per_query_head",
                    "step": "append one key + score + top-64 (index built once)"},
         "roofline": roof,
         "cpu_baseline": cpu,

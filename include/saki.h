@@ -59,14 +59,15 @@ enum { SAKI_F32 = 0, SAKI_BF16 = 1 };
 
 /* Rank-r map used by saki_calibrate. */
 enum {
-  SAKI_METHOD_OPT = 0,    /* the paper's optimum M_r (Eq. 3-4) */
-  SAKI_METHOD_KEY_PCA = 1 /* baseline: P = V V^T, top-r eigenvectors of Sigma_k */
+  SAKI_METHOD_OPT = 0,     /* the paper's optimum M_r (Eq. 3-4), one map per query head */
+  SAKI_METHOD_KEY_PCA = 1, /* baseline: P = V V^T, top-r eigenvectors of Sigma_k */
+  SAKI_METHOD_SHARED = 2   /* one map per KV group: M_r of the pooled query moment */
 };
 
 /* Human-readable description of a status code (static storage). */
 const char* saki_status_string(int status);
 
-/* ABI version of this header: 1. */
+/* ABI version of this header: 2. */
 int saki_version(void);
 
 /*
@@ -85,6 +86,13 @@ int saki_version(void);
  * on which square root of the moments is used: when both moments are safely
  * above the floor the library takes the Cholesky route (M = L_k^T Sigma_q L_k
  * with Sigma_k = L_k L_k^T, whose eigenvectors give the same B_q, B_k).
+ * With SAKI_METHOD_SHARED the query heads of a KV group share one map (an
+ * extension for GQA indexes; the paper calibrates each head alone): the
+ * group's summed objective of Eq. 2 is linear in Sigma_q, so the optimum is
+ * Eq. 3-4 with the pooled moment (1/G) sum_h Sigma_q^(h).  Every head of the
+ * group receives the same B_q, B_k, sigma and n_clamped; an index built with
+ * one code set per KV head (saki_build_index with H_q = H_kv and the group's
+ * B_k) then serves all of them (index_heads = H_kv in saki_score_topk).
  * With SAKI_METHOD_KEY_PCA instead B_q = B_k = the top-r eigenvectors of
  * Sigma_k (each column's largest-magnitude entry positive), sigma = eigenvalues
  * of Sigma_k, descending.
@@ -155,8 +163,8 @@ int saki_index_export(const void* index, int sketch_dtype, int B, int H_q,
                       int N_cap, int r, float* out, void* stream);
 
 /* Workspace for saki_score_topk with these sizes (bytes; 0 on bad arguments). */
-size_t saki_score_topk_workspace_bytes(int B, int H_q, int Q, int N_valid, int r,
-                                       int k, int sketch_dtype);
+size_t saki_score_topk_workspace_bytes(int B, int H_q, int index_heads, int Q, int N_valid,
+                                       int r, int k, int sketch_dtype);
 
 /*
  * saki_score_topk (GPU) -- Sec. 6: z_i = B_q^T q_i and b_i = q_i^T mu (float32;
@@ -165,7 +173,13 @@ size_t saki_score_topk_workspace_bytes(int B, int H_q, int Q, int N_valid, int r
  * Query row i sees keys j < N_valid, and with q_pos also only j <= q_pos[i]
  * (causal, inclusive).
  *
- *   index      device, built by saki_build_index with the same B, H_q, N_cap, r, dtype
+ *   index_heads  code sets per sequence in the index: H_q (one per query
+ *              head, the paper's index) or H_kv (a GQA-shared index, built by
+ *              saki_build_index with H_q = H_kv from SAKI_METHOD_SHARED
+ *              factors); query head h reads code set h / (H_q / index_heads).
+ *              With a shared index, decode-style calls (Q < 16) score all
+ *              query heads of a group in one pass over its codes.
+ *   index      device, built by saki_build_index with B, index_heads, N_cap, r, dtype
  *   q          device float [B, H_q, Q, d]
  *   q_pos      device int [Q] (shared by all sequences and heads), or NULL = no mask
  *   B_q        device float [H_q, d, r];  mu  device float [H_kv, d]
@@ -174,7 +188,7 @@ size_t saki_score_topk_workspace_bytes(int B, int H_q, int Q, int N_valid, int r
  *   ws         device workspace of ws_bytes >= saki_score_topk_workspace_bytes(...)
  */
 int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_kv,
-                    int N_cap, int N_valid, int d, int r, const float* q,
+                    int index_heads, int N_cap, int N_valid, int d, int r, const float* q,
                     const int* q_pos, int Q, const float* B_q, const float* mu,
                     int k, int* top_idx, float* top_score, void* ws,
                     size_t ws_bytes, void* stream);

@@ -703,7 +703,7 @@ const char* saki_status_string(int status) {
   }
 }
 
-int saki_version(void) { return 1; }
+int saki_version(void) { return 2; }
 
 int saki_sym_eig(int n, const double* A, double* w, double* V) {
   if (n <= 0 || n > 4096 || !A || !w || !V) return SAKI_ERR_ARG;
@@ -726,7 +726,8 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
   if (H_q <= 0 || H_kv <= 0 || H_q % H_kv != 0 || T <= 0 || d <= 0 || d > 4096 ||
       r <= 0 || r > d || !(floor_rel >= 0.0))
     return SAKI_ERR_ARG;
-  if (method != SAKI_METHOD_OPT && method != SAKI_METHOD_KEY_PCA) return SAKI_ERR_UNSUPPORTED;
+  if (method != SAKI_METHOD_OPT && method != SAKI_METHOD_KEY_PCA && method != SAKI_METHOD_SHARED)
+    return SAKI_ERR_UNSUPPORTED;
   const int G = H_q / H_kv;
   const size_t dd = (size_t)d * d;
   try {
@@ -735,7 +736,8 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
     // (the uncentred query moments need nothing from the keys: they are
     //  computed in the same parallel phase, after the KV heads' tasks)
     std::vector<KvState> kv(H_kv);
-    std::vector<Mat> sq_all(method == SAKI_METHOD_OPT ? H_q : 0);
+    const bool opt = method == SAKI_METHOD_OPT || method == SAKI_METHOD_SHARED;
+    std::vector<Mat> sq_all(opt ? H_q : 0);
     parallel_for(H_kv + (int)sq_all.size(), n_threads, [&](int task) {
       if (task >= H_kv) {
         const int h = task - H_kv;
@@ -752,7 +754,7 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
       for (int i = 0; i < d; ++i) st.mu[i] /= (double)T;
       st.sk.resize(dd);
       moment(T, d, k, st.mu.data(), st.sk.data());
-      if (method == SAKI_METHOD_OPT) {
+      if (opt) {
         st.L.resize(dd);
         st.chol = unclamped_cholesky(d, st.sk.data(), floor_rel, st.L.data(), true);
         if (st.chol) {
@@ -771,8 +773,23 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
     for (int g = 0; g < H_kv; ++g)
       if (!kv[g].ok) return SAKI_ERR_NUMERIC;
 
+    // one shared map per KV group: the group's pooled query moment
+    // (1/G) sum_h Sigma_q^(h) goes through the per-head steps once, for the
+    // group's first head, and the factors are copied to the others
+    const bool shared = method == SAKI_METHOD_SHARED;
+    if (shared) {
+      parallel_for(H_kv, n_threads, [&](int g) {
+        Mat& pool = sq_all[(size_t)g * G];
+        for (int hh = 1; hh < G; ++hh) {
+          const Mat& o = sq_all[(size_t)g * G + hh];
+          for (size_t i = 0; i < dd; ++i) pool[i] += o[i];
+        }
+        for (size_t i = 0; i < dd; ++i) pool[i] /= (double)G;
+      });
+    }
     std::atomic<int> failed(0);
-    parallel_for(H_q, n_threads, [&](int h) {
+    parallel_for(shared ? H_kv : H_q, n_threads, [&](int task) {
+      const int h = shared ? task * G : task;
       const KvState& st = kv[h / G];
       float* bq = B_q + (size_t)h * d * r;
       float* bk = B_k + (size_t)h * d * r;
@@ -880,6 +897,19 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
         store_pair(d, r, m, bqc.data(), bkc.data(), bq, bk);
       }
     });
+    if (shared && !failed) {  // the group's other heads get its factors
+      for (int g = 0; g < H_kv; ++g)
+        for (int hh = 1; hh < G; ++hh) {
+          const size_t h0 = (size_t)g * G, h1 = h0 + hh;
+          std::copy(B_q + h0 * d * r, B_q + (h0 + 1) * d * r, B_q + h1 * d * r);
+          std::copy(B_k + h0 * d * r, B_k + (h0 + 1) * d * r, B_k + h1 * d * r);
+          if (sigma) std::copy(sigma + h0 * d, sigma + (h0 + 1) * d, sigma + h1 * d);
+          if (n_clamped) {
+            n_clamped[2 * h1] = n_clamped[2 * h0];
+            n_clamped[2 * h1 + 1] = n_clamped[2 * h0 + 1];
+          }
+        }
+    }
     if (failed) return SAKI_ERR_NUMERIC;
   } catch (const std::bad_alloc&) {
     return SAKI_ERR_NOMEM;
@@ -927,12 +957,13 @@ size_t saki_index_bytes(int B, int H_q, int N_cap, int r, int sketch_dtype) {
   return saki::index_bytes(B, H_q, N_cap, r, sketch_dtype);
 }
 
-size_t saki_score_topk_workspace_bytes(int B, int H_q, int Q, int N_valid, int r,
-                                       int k, int sketch_dtype) {
-  if (B <= 0 || H_q <= 0 || Q < 0 || N_valid < 0 || !saki::rank_supported(r) ||
-      k < 1 || k > saki::kMaxK || (sketch_dtype != SAKI_F32 && sketch_dtype != SAKI_BF16))
+size_t saki_score_topk_workspace_bytes(int B, int H_q, int index_heads, int Q, int N_valid,
+                                       int r, int k, int sketch_dtype) {
+  if (B <= 0 || H_q <= 0 || index_heads <= 0 || H_q % index_heads != 0 || Q < 0 ||
+      N_valid < 0 || !saki::rank_supported(r) || k < 1 || k > saki::kMaxK ||
+      (sketch_dtype != SAKI_F32 && sketch_dtype != SAKI_BF16))
     return 0;
-  return saki::score_plan(B, H_q, Q, N_valid, r).ws_bytes;
+  return saki::score_plan(B, H_q, index_heads, Q, N_valid, r).ws_bytes;
 }
 
 size_t saki_recall_workspace_bytes(int B, int H_q, int H_kv, int Q, int N_valid, int d, int k) {

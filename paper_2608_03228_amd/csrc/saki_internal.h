@@ -42,11 +42,13 @@ struct Plan {
   size_t flag_count = 0;  // flags per tier (recall path)
 };
 
-inline Plan make_plan(int B, int H_q, int Q, int N_valid, int part_entry_bytes) {
+// `heads` groups of `Q` rows each (the rows of one group read the same codes).
+inline Plan make_plan(int B, int heads, int Q, int N_valid, int part_entry_bytes, bool mfma) {
   Plan p;
-  p.mfma = Q >= 16;
+  p.mfma = mfma;
   p.rows = p.mfma ? 16 : (Q >= 4 ? 4 : 1);
   const int wave_rows = (Q + p.rows - 1) / p.rows;
+  const int H_q = heads;
   const int max_waves = p.mfma ? 2 : 4;  // workgroup size of the kernels
   p.waves = wave_rows < max_waves ? (wave_rows < 1 ? 1 : wave_rows) : max_waves;
   p.row_blocks = (Q + p.rows * p.waves - 1) / (p.rows * p.waves);
@@ -75,8 +77,13 @@ inline Plan make_plan(int B, int H_q, int Q, int N_valid, int part_entry_bytes) 
 
 // Score path: query sketch z [rows, r] and mean term b [rows] (float32) come
 // first in the workspace, then the partial lists (float score + int index).
-inline Plan score_plan(int B, int H_q, int Q, int N_valid, int r) {
-  Plan p = make_plan(B, H_q, Q, N_valid, 8);
+// The MFMA kernel takes 16 queries of one head per wave; the streaming kernel
+// takes the rows of one code set: the H_q / index_heads heads sharing it,
+// times Q.
+inline Plan score_plan(int B, int H_q, int index_heads, int Q, int N_valid, int r) {
+  const bool mfma = Q >= 16;
+  Plan p = mfma ? make_plan(B, H_q, Q, N_valid, 8, true)
+                : make_plan(B, index_heads, (H_q / index_heads) * Q, N_valid, 8, false);
   const size_t rows_total = (size_t)B * H_q * Q;
   p.z_off = 0;
   p.b_off = round_up(rows_total * r * sizeof(float), 256);
@@ -92,7 +99,7 @@ inline Plan score_plan(int B, int H_q, int Q, int N_valid, int r) {
 // (b_off) and two arrays of one flag per wave (flag_off) through which each
 // tier hands the waves it could not finish to the next.
 inline Plan recall_plan(int B, int H_q, int H_kv, int Q, int N_valid) {
-  Plan p = make_plan(B, H_q, Q, N_valid, 16);
+  Plan p = make_plan(B, H_q, Q, N_valid, 16, Q >= 16);
   if (!p.mfma) return p;
   const size_t nt = n_tiles(N_valid);
   p.z_off = round_up(p.ws_bytes, 256);

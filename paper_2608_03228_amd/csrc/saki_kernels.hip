@@ -16,6 +16,10 @@
 
 #include <hip/hip_runtime.h>
 
+#include <map>
+#include <mutex>
+#include <tuple>
+
 #include <climits>
 #include <cmath>
 #include <cstdint>
@@ -254,14 +258,17 @@ __device__ __forceinline__ bf16x2_t as_bf16x2(uint32_t v) {
 
 // ---------------------------------------------------------------- sketch scoring, streaming
 
-// grid (row_blocks * n_chunks, B*H_q), block 64*waves.  Each wave owns R rows
-// and one key chunk; lane t scores key t of each 64-key tile (VALU, float32).
+// grid (row_blocks * n_chunks, B * index_heads), block 64*waves.  The rows of
+// a code set are its gq = H_q / index_heads query heads times the Q queries,
+// numbered rho = i * gq + (h % gq) so that one wave's R rows are the heads
+// sharing the codes (for a GQA-shared index) before further queries.  Each
+// wave owns R rows and one key chunk; lane t scores key t of each 64-key tile.
 template <int RK, bool SBF, int R>
 __global__ __launch_bounds__(256) void score_stream_kernel(
     const uint8_t* __restrict__ index, int n_tiles, int N_valid, int Q,
     const int* __restrict__ q_pos, const float* __restrict__ z,
-    const float* __restrict__ bvec, int row_blocks, int chunk, int n_chunks, int k,
-    int* __restrict__ top_idx, float* __restrict__ top_score,
+    const float* __restrict__ bvec, int H_q, int gq, int row_blocks, int chunk, int n_chunks,
+    int k, int* __restrict__ top_idx, float* __restrict__ top_score,
     uint64_t* __restrict__ part) {
   constexpr int ES = SBF ? 2 : 4;
   constexpr int CPP = saki::kChunkBytes / ES;
@@ -274,29 +281,39 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   const int wave = threadIdx.x / kWave, lane = lane_id();
   const int waves = blockDim.x / kWave;
   const int rb = blockIdx.x % row_blocks, ch = blockIdx.x / row_blocks;
-  const size_t bh = blockIdx.y;
+  const size_t bi = blockIdx.y;  // b * index_heads + code set
+  const int index_heads = H_q / gq;
+  const size_t b = bi / index_heads;
+  const int ih = (int)(bi % index_heads);
+  const int n_rho = gq * Q;
   const int row0 = (rb * waves + wave) * R;
-  if (row0 >= Q) return;
+  if (row0 >= n_rho) return;
 
   int lim[R];
   float bb[R];
+  size_t flat[R];  // (b * H_q + h) * Q + i of each row
   int kmax = 0;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    lim[r] = row_limit(row0 + r, Q, N_valid, q_pos);
+    const int rho = row0 + r;
+    const bool ok = rho < n_rho;
+    const int i = ok ? rho / gq : 0;
+    const int h = ih * gq + (ok ? rho % gq : 0);
+    flat[r] = (b * H_q + h) * Q + i;
+    lim[r] = ok ? row_limit(i, Q, N_valid, q_pos) : 0;
     kmax = lim[r] > kmax ? lim[r] : kmax;
-    bb[r] = (row0 + r < Q) ? bvec[bh * Q + row0 + r] : 0.f;
+    bb[r] = ok ? bvec[flat[r]] : 0.f;
   }
   for (int i = lane; i < R * RK; i += kWave) {
     const int r = i / RK;
-    zs[wave][r][i % RK] = (row0 + r < Q) ? z[(bh * Q + row0 + r) * RK + (i % RK)] : 0.f;
+    zs[wave][r][i % RK] = (row0 + r < n_rho) ? z[flat[r] * RK + (i % RK)] : 0.f;
   }
   RowLists<KO, R> top;
   top.init(&lmem[wave][0][0], &bmem[wave][0][0]);
 
   const int kbeg = ch * chunk;
   const int kend = min(kbeg + chunk, kmax);
-  const uint8_t* hbase = index + bh * n_tiles * TB;
+  const uint8_t* hbase = index + bi * n_tiles * TB;
   // the next tile's pieces are loaded before this tile is scored (sketches of
   // up to 128 bytes per key; wider ones are loaded as they are used)
   constexpr int PF = NP <= 8 ? NP : 1;
@@ -310,13 +327,18 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   if constexpr (SBF) {
     // bf16 codes: each 32-bit word holds elements (2e, 2e + 1), scored with
     // the packed bf16 dot product against the query sketch's pairs
+    // the pairs are the same in every lane: when they fit, scalar registers
+    // hold them and the vector registers are left to the key tiles
+    constexpr bool kScalarZ = R * RK / 2 <= 64;
     uint32_t zp[R][RK / 2];
 #pragma unroll
     for (int r = 0; r < R; ++r)
 #pragma unroll
-      for (int m = 0; m < RK / 2; ++m)
-        zp[r][m] = (__float_as_uint(zs[wave][r][2 * m]) >> 16) |
-                   (__float_as_uint(zs[wave][r][2 * m + 1]) & 0xffff0000u);
+      for (int m = 0; m < RK / 2; ++m) {
+        const uint32_t v = (__float_as_uint(zs[wave][r][2 * m]) >> 16) |
+                           (__float_as_uint(zs[wave][r][2 * m + 1]) & 0xffff0000u);
+        zp[r][m] = kScalarZ ? (uint32_t)__builtin_amdgcn_readfirstlane((int)v) : v;
+      }
     for (int t0 = kbeg; t0 < kend; t0 += kTile) {
       const int j = t0 + lane;
       const uint8_t* tb = hbase + (size_t)(t0 / kTile) * TB;
@@ -363,17 +385,16 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   }
   for (int r = 0; r < R; ++r) {
     top.finish(r);
-    const int i = row0 + r;
-    if (i >= Q) continue;
+    if (row0 + r >= n_rho) continue;
     const uint64_t e = top.entry(r);
     if (n_chunks == 1) {
       if (lane < k) {
-        const size_t o = (bh * Q + i) * k + lane;
+        const size_t o = flat[r] * k + lane;
         top_idx[o] = out_index<KO>(e);
         if (top_score) top_score[o] = KO::score(e);
       }
     } else {
-      part[((bh * Q + i) * n_chunks + ch) * kMaxK + lane] = e;
+      part[(flat[r] * n_chunks + ch) * kMaxK + lane] = e;
     }
   }
 }
@@ -584,8 +605,8 @@ template <int RK, bool SBF>
 __global__ __launch_bounds__(128) void score_mfma_kernel(
     const uint8_t* __restrict__ index, int n_tiles, int N_valid, int Q,
     const int* __restrict__ q_pos, const float* __restrict__ q,
-    const float* __restrict__ Bq, const float* __restrict__ mu, int H_q, int H_kv, int n_bh,
-    int row_blocks, int chunk, int n_chunks, int k, int* __restrict__ top_idx,
+    const float* __restrict__ Bq, const float* __restrict__ mu, int H_q, int H_kv, int gq,
+    int n_bh, int row_blocks, int chunk, int n_chunks, int k, int* __restrict__ top_idx,
     float* __restrict__ top_score, uint64_t* __restrict__ part) {
   constexpr int D = saki::kHeadDim;
   using KO = KeysF32;
@@ -648,7 +669,9 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
     sc.load_operand(zs + qi * RK, g);
     wave_lds_sync();
   }
-  const uint8_t* hbase = index + bh * n_tiles * Scorer::TB;
+  // the head's code set: one per query head (gq = 1) or per group of gq heads
+  const size_t code_set = (bh / H_q) * (H_q / gq) + h / gq;
+  const uint8_t* hbase = index + code_set * n_tiles * Scorer::TB;
 
   // ---- pass 1: moments of this lane's row over a sample of the chunk's
   //      tiles (every stride-th tile, at least kSampleTiles of them)
@@ -1852,16 +1875,66 @@ void launch_build(const void* keys, const float* Bk, const float* mu, int B, int
                      n_end, t0);
 }
 
+// Work-groups of `kernel` (block `threads`) resident on the whole current
+// device at once, or 0 if the runtime cannot tell.  Cached per (kernel,
+// block size, device).
+template <class K>
+int resident_groups(K kernel, int threads) {
+  static std::mutex mu;
+  static std::map<std::tuple<const void*, int, int>, int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  const auto key = std::make_tuple(reinterpret_cast<const void*>(kernel), threads, dev);
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    const auto it = cache.find(key);
+    if (it != cache.end()) return it->second;
+  }
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  cache[key] = cus * per_cu;
+  return cus * per_cu;
+}
+
+// A split-N streaming launch that fills the GPU exactly once: the plan's
+// chunking (which sized the workspace) is coarsened so that the work-groups
+// number at most what the device holds at one time, the chunk count staying
+// within the plan's.
+template <class K>
+saki::Plan one_round(saki::Plan p, K kernel, int groups_per_chunk, int N_valid) {
+  if (p.n_chunks <= 1) return p;
+  const int slots = resident_groups(kernel, kWave * p.waves);
+  if (slots <= 0) return p;
+  const int want = max(1, slots / max(1, groups_per_chunk));
+  const size_t n = N_valid > 0 ? (size_t)N_valid : 1;
+  size_t chunk = saki::round_up((n + want - 1) / want, kTile);
+  const int n_chunks = (int)((n + chunk - 1) / chunk);
+  if (n_chunks >= p.n_chunks) return p;
+  p.chunk = (int)chunk;
+  p.n_chunks = n_chunks;
+  return p;
+}
+
 template <int RK, bool SBF>
-void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int N_cap, int N_valid,
-                  const float* q, const int* q_pos, int Q, const float* Bq, const float* mu,
-                  int k, int* top_idx, float* top_score, uint8_t* ws,
-                  const saki::Plan& p, hipStream_t s) {
+void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int index_heads, int N_cap,
+                  int N_valid, const float* q, const int* q_pos, int Q, const float* Bq,
+                  const float* mu, int k, int* top_idx, float* top_score, uint8_t* ws,
+                  const saki::Plan& p0, hipStream_t s) {
+  const int gq = H_q / index_heads;
+  saki::Plan p = p0;
+  if (!p.mfma)
+    p = p.rows == 4 ? one_round(p0, score_stream_kernel<RK, SBF, 4>, p0.row_blocks * B * index_heads, N_valid)
+                    : one_round(p0, score_stream_kernel<RK, SBF, 1>, p0.row_blocks * B * index_heads, N_valid);
   float* z = reinterpret_cast<float*>(ws + p.z_off);
   float* bv = reinterpret_cast<float*>(ws + p.b_off);
   const size_t rows = (size_t)B * H_q * Q;
   uint64_t* part = p.n_chunks > 1 ? reinterpret_cast<uint64_t*>(ws + p.part_off) : nullptr;
-  dim3 grid((unsigned)(p.row_blocks * p.n_chunks), B * H_q);
+  dim3 grid((unsigned)(p.row_blocks * p.n_chunks), B * index_heads);
   dim3 block(kWave * p.waves);
   const int nt = (int)saki::n_tiles(N_cap);
   if (!p.mfma)
@@ -1869,15 +1942,15 @@ void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int N_cap, int
                        dim3(256), 0, s, q, Bq, mu, H_q, H_kv, Q, z, bv);
   if (p.mfma)
     hipLaunchKernelGGL((score_mfma_kernel<RK, SBF>), xcd_grid(p, B * H_q), block, 0, s, index,
-                       nt, N_valid, Q, q_pos, q, Bq, mu, H_q, H_kv, B * H_q, p.row_blocks,
+                       nt, N_valid, Q, q_pos, q, Bq, mu, H_q, H_kv, gq, B * H_q, p.row_blocks,
                        p.chunk, p.n_chunks, k, top_idx, top_score, part);
   else if (p.rows == 4)
     hipLaunchKernelGGL((score_stream_kernel<RK, SBF, 4>), grid, block, 0, s, index, nt, N_valid,
-                       Q, q_pos, z, bv, p.row_blocks, p.chunk, p.n_chunks, k, top_idx,
+                       Q, q_pos, z, bv, H_q, gq, p.row_blocks, p.chunk, p.n_chunks, k, top_idx,
                        top_score, part);
   else
     hipLaunchKernelGGL((score_stream_kernel<RK, SBF, 1>), grid, block, 0, s, index, nt, N_valid,
-                       Q, q_pos, z, bv, p.row_blocks, p.chunk, p.n_chunks, k, top_idx,
+                       Q, q_pos, z, bv, H_q, gq, p.row_blocks, p.chunk, p.n_chunks, k, top_idx,
                        top_score, part);
   if (p.n_chunks > 1)
     hipLaunchKernelGGL((merge_kernel<KeysF32, false>), dim3((unsigned)rows),
@@ -2018,18 +2091,20 @@ int saki_index_export(const void* index, int sketch_dtype, int B, int H_q, int N
   return launch_ok() ? SAKI_OK : SAKI_ERR_HIP;
 }
 
-int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_kv, int N_cap,
-                    int N_valid, int d, int r, const float* q, const int* q_pos, int Q,
-                    const float* B_q, const float* mu, int k, int* top_idx, float* top_score,
-                    void* ws, size_t ws_bytes, void* stream) {
+int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_kv,
+                    int index_heads, int N_cap, int N_valid, int d, int r, const float* q,
+                    const int* q_pos, int Q, const float* B_q, const float* mu, int k,
+                    int* top_idx, float* top_score, void* ws, size_t ws_bytes, void* stream) {
   int st = check_common(B, H_q, H_kv, N_cap, N_valid, d);
   if (st != SAKI_OK) return st;
   if (Q < 0) return SAKI_ERR_ARG;
+  // a code set serves whole query heads and lies within one KV group
+  if (index_heads <= 0 || H_q % index_heads != 0 || index_heads % H_kv != 0) return SAKI_ERR_ARG;
   if (!dtype_ok(sketch_dtype) || !saki::rank_supported(r) || k < 1 || k > kMaxK)
     return SAKI_ERR_UNSUPPORTED;
   if (Q == 0) return SAKI_OK;
   if (!index || !q || !B_q || !mu || !top_idx || !ws) return SAKI_ERR_ARG;
-  const saki::Plan p = saki::score_plan(B, H_q, Q, N_valid, r);
+  const saki::Plan p = saki::score_plan(B, H_q, index_heads, Q, N_valid, r);
   if (ws_bytes < p.ws_bytes) return SAKI_ERR_WORKSPACE;
   if ((size_t)p.row_blocks * p.n_chunks > 0x7fffffffu) return SAKI_ERR_UNSUPPORTED;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -2038,11 +2113,11 @@ int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_k
 #define SAKI_SCORE(RK)                                                                        \
   do {                                                                                        \
     if (sketch_dtype == SAKI_BF16)                                                            \
-      launch_score<RK, true>(ix, B, H_q, H_kv, N_cap, N_valid, q, q_pos, Q, B_q, mu, k,       \
-                             top_idx, top_score, w, p, s);                                    \
+      launch_score<RK, true>(ix, B, H_q, H_kv, index_heads, N_cap, N_valid, q, q_pos, Q, B_q, \
+                             mu, k, top_idx, top_score, w, p, s);                             \
     else                                                                                      \
-      launch_score<RK, false>(ix, B, H_q, H_kv, N_cap, N_valid, q, q_pos, Q, B_q, mu, k,      \
-                              top_idx, top_score, w, p, s);                                   \
+      launch_score<RK, false>(ix, B, H_q, H_kv, index_heads, N_cap, N_valid, q, q_pos, Q, B_q,\
+                              mu, k, top_idx, top_score, w, p, s);                            \
   } while (0)
   switch (r) {
     case 16: SAKI_SCORE(16); break;

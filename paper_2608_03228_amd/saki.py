@@ -18,9 +18,9 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsaki.so
 _lib = None
 
 F32, BF16 = 0, 1
-METHOD_OPT, METHOD_KEY_PCA = 0, 1
+METHOD_OPT, METHOD_KEY_PCA, METHOD_SHARED = 0, 1, 2
 _DTYPES = {"f32": F32, "bf16": BF16}
-_METHODS = {"opt": METHOD_OPT, "key_pca": METHOD_KEY_PCA}
+_METHODS = {"opt": METHOD_OPT, "key_pca": METHOD_KEY_PCA, "shared": METHOD_SHARED}
 
 
 class SakiError(RuntimeError):
@@ -49,8 +49,8 @@ def lib():
         "saki_index_bytes": (sz, [ip, ip, ip, ip, ip]),
         "saki_build_index": (ip, [vp, ip, ip, ip, ip, ip, ip, ip, vp, vp, ip, vp, sz, ip, ip, vp]),
         "saki_index_export": (ip, [vp, ip, ip, ip, ip, ip, vp, vp]),
-        "saki_score_topk_workspace_bytes": (sz, [ip, ip, ip, ip, ip, ip, ip]),
-        "saki_score_topk": (ip, [vp, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, ip, vp, vp, ip,
+        "saki_score_topk_workspace_bytes": (sz, [ip, ip, ip, ip, ip, ip, ip, ip]),
+        "saki_score_topk": (ip, [vp, ip, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, ip, vp, vp, ip,
                                  vp, vp, vp, sz, vp]),
         "saki_recall_workspace_bytes": (sz, [ip, ip, ip, ip, ip, ip, ip]),
         "saki_recall": (ip, [vp, ip, vp, vp, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, vp, vp,
@@ -135,8 +135,9 @@ def saki_index_bytes(B: int, H_q: int, N_cap: int, r: int, sketch: str) -> int:
     return int(lib().saki_index_bytes(B, H_q, N_cap, r, _DTYPES[sketch]))
 
 
-def saki_score_topk_workspace_bytes(B, H_q, Q, N_valid, r, k, sketch) -> int:
-    return int(lib().saki_score_topk_workspace_bytes(B, H_q, Q, N_valid, r, k,
+def saki_score_topk_workspace_bytes(B, H_q, Q, N_valid, r, k, sketch, index_heads=None) -> int:
+    ih = H_q if index_heads is None else int(index_heads)
+    return int(lib().saki_score_topk_workspace_bytes(B, H_q, ih, Q, N_valid, r, k,
                                                      _DTYPES[sketch]))
 
 
@@ -205,13 +206,16 @@ def saki_index_export(index, sketch: str, B: int, H_q: int, N_cap: int, r: int, 
 
 def saki_score_topk(index, sketch: str, q, B_q, mu, H_kv: int, N_cap: int, N_valid: int,
                     r: int, q_pos=None, k: int = 64, ws=None, top_idx=None, top_score=None,
-                    with_scores: bool = True, stream=None):
-    """q [B, H_q, Q, d] float32 CUDA; q_pos [Q] int32 CUDA or None.  Returns
-    (top_idx [B, H_q, Q, k] int32, top_score float32 or None)."""
+                    with_scores: bool = True, stream=None, index_heads=None):
+    """q [B, H_q, Q, d] float32 CUDA; q_pos [Q] int32 CUDA or None; index_heads
+    = code sets per sequence in the index (H_q, the default, or H_kv for a
+    GQA-shared index).  Returns (top_idx [B, H_q, Q, k] int32, top_score
+    float32 or None)."""
     torch = _torch()
     qp = _dev(q, (torch.float32,), "q")
     B, H_q, Q, d = q.shape
-    need = saki_score_topk_workspace_bytes(B, H_q, Q, N_valid, r, k, sketch)
+    ih = H_q if index_heads is None else int(index_heads)
+    need = saki_score_topk_workspace_bytes(B, H_q, Q, N_valid, r, k, sketch, ih)
     if ws is None:
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
     if top_idx is None:
@@ -220,7 +224,7 @@ def saki_score_topk(index, sketch: str, q, B_q, mu, H_kv: int, N_cap: int, N_val
         top_score = torch.empty((B, H_q, Q, k), dtype=torch.float32, device=q.device)
     pos = _dev(q_pos, (torch.int32,), "q_pos") if q_pos is not None else None
     st = lib().saki_score_topk(
-        _dev(index, (torch.uint8,), "index"), _DTYPES[sketch], B, H_q, int(H_kv), int(N_cap),
+        _dev(index, (torch.uint8,), "index"), _DTYPES[sketch], B, H_q, int(H_kv), ih, int(N_cap),
         int(N_valid), d, int(r), qp, pos, Q, _dev(B_q, (torch.float32,), "B_q"),
         _dev(mu, (torch.float32,), "mu"), int(k), _dev(top_idx, (torch.int32,), "top_idx"),
         _dev(top_score, (torch.float32,), "top_score") if with_scores else None,

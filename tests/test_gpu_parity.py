@@ -157,6 +157,30 @@ def test_decode_split_chunks_and_merge():
             check_head(inp, out, 0, h, 32, mode)
 
 
+@pytest.mark.parametrize("sketch,Q,N", [("bf16", 96, 1500), ("f32", 3, 70_000),
+                                        ("bf16", 1, 150_000)])
+def test_gqa_shared_index_matches_oracle(sketch, Q, N):
+    """A GQA-shared index: one code set per KV head, built from the
+    SAKI_METHOD_SHARED factors, scored by all four query heads of its group
+    (the MFMA path for 96 queries per head; decode shapes take the grouped
+    streaming rows, with the key range split into chunks)."""
+    spec = W.SPECS["decode_1m"].with_(N=N, Q=Q, H_q=8, H_kv=2)
+    inp = W.make_layer(spec)
+    cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32, method="shared")
+    keys, q, mu = _t(inp["keys"]), _t(inp["queries"]), _t(cal["mu"])
+    index = S.saki_build_index(keys, _t(cal["B_k"][::4]), mu, 32, sketch, 2)
+    assert index.numel() == S.saki_index_bytes(1, 2, N, 32, sketch)
+    idx, sc = S.saki_score_topk(index, sketch, q, _t(cal["B_q"]), mu, 2, N, N, 32, k=64,
+                                index_heads=2)
+    torch.cuda.synchronize()
+    out = {"idx": idx.cpu().numpy(), "score": sc.cpu().numpy()}
+    mode = "f32" if sketch == "f32" else "bf16_emul"
+    for g in range(2):
+        oc = O.saki_calibrate_shared(inp["q_cal"][4 * g:4 * g + 4], inp["k_cal"][g], 32)
+        for h in range(4 * g, 4 * g + 4):
+            check_head(inp, out, 0, h, 32, mode, factors=(oc["B_q"], oc["B_k"], oc["mu"]))
+
+
 @pytest.mark.parametrize("k", [1, 10, 64])
 def test_small_k_is_prefix_of_top64(k):
     spec = W.SPECS["single_head_d128"].with_(N=777, Q=33)

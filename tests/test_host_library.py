@@ -25,7 +25,7 @@ def test_exports_every_declared_symbol(lib):
     assert len(names) >= 12
     for n in names:
         assert hasattr(lib, n), n
-    assert S.saki_version() == 1
+    assert S.saki_version() == 2
     assert "workspace" in S.saki_status_string(-3)
 
 
@@ -151,6 +151,24 @@ def test_calibration_with_repeated_singular_values():
     np.testing.assert_allclose(cal["sigma"][0] ** 2, oc["sigma"] ** 2, rtol=0, atol=1e-6 * 5)
 
 
+def test_shared_calibration_matches_oracle():
+    """SAKI_METHOD_SHARED: one map per KV group from the pooled query moment,
+    copied to every head of the group, equal to the oracle's shared map."""
+    spec = W.SPECS["llama31_8b_layer"].with_(N=64, Q=1, q_start=0)
+    inp = W.make_layer(spec)
+    cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32, method="shared")
+    for g in (0, 5):
+        oc = O.saki_calibrate_shared(inp["q_cal"][4 * g:4 * g + 4], inp["k_cal"][g], 32)
+        for h in range(4 * g, 4 * g + 4):
+            M = _m(cal["B_q"][h], cal["B_k"][h])
+            assert np.linalg.norm(M - oc["M"]) <= 2e-6 * np.linalg.norm(oc["M"])
+            np.testing.assert_array_equal(cal["B_k"][h], cal["B_k"][4 * g])
+        sig = oc["sigma"]
+        assert np.max(np.abs(cal["sigma"][4 * g] ** 2 - sig ** 2)) <= 1e-12 * sig[0] ** 2 * spec.d
+    assert S.saki_score_topk_workspace_bytes(1, 32, 4032, 4096, 32, 64, "bf16", 8) > 0
+    assert S.saki_score_topk_workspace_bytes(1, 32, 4032, 4096, 32, 64, "bf16", 5) == 0
+
+
 def test_constant_keys_identity_fallback():
     q = np.random.default_rng(1).standard_normal((1, 64, 16)).astype(np.float32)
     k = np.tile(np.arange(16, dtype=np.float32), (1, 64, 1))
@@ -184,16 +202,20 @@ def test_argument_validation_without_launch(lib):
     assert lib.saki_build_index(P, 0, 1, 3, 2, 64, 128, 32, P, P, 0, P, 1 << 20, 0, 64, None) == ERR_ARG
     assert lib.saki_build_index(P, 7, 1, 1, 1, 64, 128, 32, P, P, 0, P, 1 << 20, 0, 64, None) == ERR_UNSUP
     # score_topk: k out of range, N_valid > N_cap, small workspace, null output
-    args = [P, 0, 1, 1, 1, 256, 256, 128, 32, P, None, 4, P, P]
+    args = [P, 0, 1, 1, 1, 1, 256, 256, 128, 32, P, None, 4, P, P]
     assert lib.saki_score_topk(*args, 65, P, None, P, 1 << 30, None) == ERR_UNSUP
     assert lib.saki_score_topk(*args, 0, P, None, P, 1 << 30, None) == ERR_UNSUP
     assert lib.saki_score_topk(*args, 64, None, None, P, 1 << 30, None) == ERR_ARG
     assert lib.saki_score_topk(*args, 64, P, None, P, 1, None) == ERR_WS
-    bad = [P, 0, 1, 1, 1, 256, 300, 128, 32, P, None, 4, P, P]
+    bad = [P, 0, 1, 1, 1, 1, 256, 300, 128, 32, P, None, 4, P, P]
     assert lib.saki_score_topk(*bad, 64, P, None, P, 1 << 30, None) == ERR_ARG
     # Q == 0 is a no-op that succeeds
-    zero = [P, 0, 1, 1, 1, 256, 256, 128, 32, P, None, 0, P, P]
+    zero = [P, 0, 1, 1, 1, 1, 256, 256, 128, 32, P, None, 0, P, P]
     assert lib.saki_score_topk(*zero, 64, P, None, P, 0, None) == 0
+    # index heads must divide H_q and be a multiple of H_kv (here H_q = 8, H_kv = 2)
+    for ih in (0, 3, 1, 16):
+        gqa = [P, 0, 1, 8, 2, ih, 256, 256, 128, 32, P, None, 4, P, P]
+        assert lib.saki_score_topk(*gqa, 64, P, None, P, 1 << 30, None) == ERR_ARG, ih
     # recall: null hits, bad key dtype
     assert lib.saki_recall(P, 0, P, None, 1, 1, 1, 256, 256, 4, 128, 64, P, None, None, P,
                            1 << 30, None) == ERR_ARG
