@@ -114,6 +114,33 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
                    int* n_clamped, int n_threads);
 
 /*
+ * saki_calibration_moments (GPU) -- the moments saki_calibrate starts from
+ * (Sec. 6, Appendix A), in float64 on the GPU: Sigma_q of every query head
+ * (uncentred), the mean mu and the centred Sigma_k of every KV head, all with
+ * the 1/T normaliser.  Products of the float32 tokens are exact in float64;
+ * only the summation order differs from the host.
+ *
+ *   q_cal    device float [H_q, T, d];  k_cal  device float [H_kv, T, d]
+ *   Sigma_q  device double [H_q, d, d] out (full symmetric matrices)
+ *   Sigma_k  device double [H_kv, d, d] out;  key_mean  device double [H_kv, d] out
+ * Any d in [1, 4096] and T >= 1.
+ */
+int saki_calibration_moments(const float* q_cal, const float* k_cal, int H_q, int H_kv,
+                             int T, int d, double* Sigma_q, double* Sigma_k,
+                             double* key_mean, void* stream);
+
+/*
+ * saki_calibrate_from_moments (host) -- saki_calibrate after its moments:
+ * the same factors from Sigma_q [H_q, d, d], Sigma_k [H_kv, d, d] and
+ * key_mean [H_kv, d] (host float64, e.g. copied back from
+ * saki_calibration_moments).  Arguments and outputs as for saki_calibrate.
+ */
+int saki_calibrate_from_moments(const double* Sigma_q, const double* Sigma_k,
+                                const double* key_mean, int H_q, int H_kv, int d, int r,
+                                int method, double floor_rel, float* B_q, float* B_k,
+                                float* mu, double* sigma, int* n_clamped, int n_threads);
+
+/*
  * saki_weight_svd_factors (host) -- the weight-SVD baseline of Table 1, read
  * as a data-blind truncation of the key projection: B_q = B_k = the top-r left
  * singular vectors of W_K^(g) (eigenvectors of W_K W_K^T), signed as above.

@@ -718,12 +718,20 @@ int saki_sym_eig(int n, const double* A, double* w, double* V) {
   return SAKI_OK;
 }
 
-int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
-                   int T, int d, int r, int method, double floor_rel,
-                   float* B_q, float* B_k, float* mu, double* sigma,
-                   int* n_clamped, int n_threads) {
-  if (!q_cal || !k_cal || !B_q || !B_k || !mu) return SAKI_ERR_ARG;
-  if (H_q <= 0 || H_kv <= 0 || H_q % H_kv != 0 || T <= 0 || d <= 0 || d > 4096 ||
+}  // extern "C"
+
+namespace {
+
+// Both calibration entry points: the moments either come in (Sq_in, Sk_in,
+// mu_in, float64) or are computed here from the calibration tokens.
+int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
+                   const double* Sk_in, const double* mu_in, int H_q, int H_kv, int T, int d,
+                   int r, int method, double floor_rel, float* B_q, float* B_k, float* mu,
+                   double* sigma, int* n_clamped, int n_threads) {
+  const bool given = Sq_in != nullptr;
+  if (!B_q || !B_k || !mu) return SAKI_ERR_ARG;
+  if (given ? (!Sk_in || !mu_in) : (!q_cal || !k_cal)) return SAKI_ERR_ARG;
+  if (H_q <= 0 || H_kv <= 0 || H_q % H_kv != 0 || (!given && T <= 0) || d <= 0 || d > 4096 ||
       r <= 0 || r > d || !(floor_rel >= 0.0))
     return SAKI_ERR_ARG;
   if (method != SAKI_METHOD_OPT && method != SAKI_METHOD_KEY_PCA && method != SAKI_METHOD_SHARED)
@@ -741,19 +749,28 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
     parallel_for(H_kv + (int)sq_all.size(), n_threads, [&](int task) {
       if (task >= H_kv) {
         const int h = task - H_kv;
-        sq_all[h].resize(dd);
-        moment(T, d, q_cal + (size_t)h * T * d, nullptr, sq_all[h].data());
+        if (given) {
+          sq_all[h].assign(Sq_in + (size_t)h * dd, Sq_in + (size_t)(h + 1) * dd);
+        } else {
+          sq_all[h].resize(dd);
+          moment(T, d, q_cal + (size_t)h * T * d, nullptr, sq_all[h].data());
+        }
         return;
       }
       const int g = task;
       KvState& st = kv[g];
-      const float* k = k_cal + (size_t)g * T * d;
-      st.mu.assign(d, 0.0);
-      for (int t = 0; t < T; ++t)
-        for (int i = 0; i < d; ++i) st.mu[i] += (double)k[(size_t)t * d + i];
-      for (int i = 0; i < d; ++i) st.mu[i] /= (double)T;
-      st.sk.resize(dd);
-      moment(T, d, k, st.mu.data(), st.sk.data());
+      if (given) {
+        st.mu.assign(mu_in + (size_t)g * d, mu_in + (size_t)(g + 1) * d);
+        st.sk.assign(Sk_in + (size_t)g * dd, Sk_in + (size_t)(g + 1) * dd);
+      } else {
+        const float* k = k_cal + (size_t)g * T * d;
+        st.mu.assign(d, 0.0);
+        for (int t = 0; t < T; ++t)
+          for (int i = 0; i < d; ++i) st.mu[i] += (double)k[(size_t)t * d + i];
+        for (int i = 0; i < d; ++i) st.mu[i] /= (double)T;
+        st.sk.resize(dd);
+        moment(T, d, k, st.mu.data(), st.sk.data());
+      }
       if (opt) {
         st.L.resize(dd);
         st.chol = unclamped_cholesky(d, st.sk.data(), floor_rel, st.L.data(), true);
@@ -915,6 +932,31 @@ int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
     return SAKI_ERR_NOMEM;
   }
   return SAKI_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int saki_calibrate(const float* q_cal, const float* k_cal, int H_q, int H_kv,
+                   int T, int d, int r, int method, double floor_rel,
+                   float* B_q, float* B_k, float* mu, double* sigma,
+                   int* n_clamped, int n_threads) {
+  if (!q_cal || !k_cal) return SAKI_ERR_ARG;
+  return calibrate_core(q_cal, k_cal, nullptr, nullptr, nullptr, H_q, H_kv, T, d, r, method,
+                        floor_rel, B_q, B_k, mu, sigma, n_clamped, n_threads);
+}
+
+int saki_calibrate_from_moments(const double* Sigma_q, const double* Sigma_k,
+                                const double* key_mean, int H_q, int H_kv, int d, int r,
+                                int method, double floor_rel, float* B_q, float* B_k, float* mu,
+                                double* sigma, int* n_clamped, int n_threads) {
+  if (!Sigma_q || !Sigma_k || !key_mean) return SAKI_ERR_ARG;
+  if (H_q > 0 && H_kv > 0 && d > 0 && d <= 4096)
+    for (size_t i = 0; i < (size_t)H_q * d * d; ++i)
+      if (!std::isfinite(Sigma_q[i])) return SAKI_ERR_NUMERIC;
+  return calibrate_core(nullptr, nullptr, Sigma_q, Sigma_k, key_mean, H_q, H_kv, 0, d, r,
+                        method, floor_rel, B_q, B_k, mu, sigma, n_clamped, n_threads);
 }
 
 int saki_weight_svd_factors(const double* W_K, int H_q, int H_kv, int d, int D,

@@ -1853,6 +1853,62 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void merge_kernel(
   }
 }
 
+// ---------------------------------------------------------------- calibration moments
+
+// grid (ceil(d/16), ceil(d/16), H_q + H_kv), block 256 = 16 x 16.  Work-group
+// (bi, bj, head) with bi <= bj forms the 16 x 16 tile (rows 16 bi.., columns
+// 16 bj..) of that head's moment and writes it and its mirror.  Heads below
+// H_q are query heads (uncentred); the rest are KV heads, centred by their
+// column means, which every work-group computes for its own 32 columns.
+constexpr int kMomTile = 16;
+constexpr int kMomChunk = 64;  // tokens staged per step
+
+__global__ __launch_bounds__(256) void moments_kernel(const float* __restrict__ q_cal,
+                                                      const float* __restrict__ k_cal, int H_q,
+                                                      int T, int d, double* __restrict__ Sq,
+                                                      double* __restrict__ Sk,
+                                                      double* __restrict__ mu_out) {
+  const int bi = blockIdx.x, bj = blockIdx.y, head = blockIdx.z;
+  if (bi > bj) return;  // uniform over the work-group
+  const bool key = head >= H_q;
+  const int hh = key ? head - H_q : head;
+  const float* X = (key ? k_cal : q_cal) + (size_t)hh * T * d;
+  const int tx = threadIdx.x % kMomTile, ty = threadIdx.x / kMomTile;
+  const int i0 = bi * kMomTile, j0 = bj * kMomTile;
+  __shared__ double xi[kMomChunk][kMomTile + 1], xj[kMomChunk][kMomTile + 1];
+  __shared__ double mean[2 * kMomTile];
+  if (threadIdx.x < 2 * kMomTile) {
+    const int c = threadIdx.x < kMomTile ? i0 + threadIdx.x : j0 + threadIdx.x - kMomTile;
+    double m = 0.0;
+    if (key && c < d) {
+      for (int t = 0; t < T; ++t) m += (double)X[(size_t)t * d + c];
+      m /= (double)T;
+    }
+    mean[threadIdx.x] = m;
+  }
+  __syncthreads();
+  double acc = 0.0;
+  for (int t0 = 0; t0 < T; t0 += kMomChunk) {
+    for (int e = threadIdx.x; e < kMomChunk * kMomTile; e += 256) {
+      const int tt = e / kMomTile, c = e % kMomTile, t = t0 + tt;
+      xi[tt][c] = (t < T && i0 + c < d) ? (double)X[(size_t)t * d + i0 + c] - mean[c] : 0.0;
+      xj[tt][c] = (t < T && j0 + c < d) ? (double)X[(size_t)t * d + j0 + c] - mean[kMomTile + c] : 0.0;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int tt = 0; tt < kMomChunk; ++tt) acc = fma(xi[tt][ty], xj[tt][tx], acc);
+    __syncthreads();
+  }
+  const int i = i0 + ty, j = j0 + tx;
+  if (i < d && j < d) {
+    double* S = key ? Sk + (size_t)hh * d * d : Sq + (size_t)hh * d * d;
+    const double v = acc / (double)T;
+    S[(size_t)i * d + j] = v;
+    S[(size_t)j * d + i] = v;
+  }
+  if (key && bi == 0 && ty == 0 && j < d) mu_out[(size_t)hh * d + j] = mean[kMomTile + tx];
+}
+
 // ---------------------------------------------------------------- dispatch helpers
 
 bool launch_ok() { return hipGetLastError() == hipSuccess; }
@@ -2126,6 +2182,19 @@ int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_k
     default: SAKI_SCORE(128); break;
   }
 #undef SAKI_SCORE
+  return launch_ok() ? SAKI_OK : SAKI_ERR_HIP;
+}
+
+int saki_calibration_moments(const float* q_cal, const float* k_cal, int H_q, int H_kv,
+                             int T, int d, double* Sigma_q, double* Sigma_k,
+                             double* key_mean, void* stream) {
+  if (!q_cal || !k_cal || !Sigma_q || !Sigma_k || !key_mean) return SAKI_ERR_ARG;
+  if (H_q <= 0 || H_kv <= 0 || T <= 0 || d <= 0 || d > 4096) return SAKI_ERR_ARG;
+  if ((long long)H_q + H_kv > 65535) return SAKI_ERR_UNSUPPORTED;
+  const unsigned nb = (unsigned)((d + kMomTile - 1) / kMomTile);
+  hipLaunchKernelGGL(moments_kernel, dim3(nb, nb, H_q + H_kv), dim3(256), 0,
+                     reinterpret_cast<hipStream_t>(stream), q_cal, k_cal, H_q, T, d, Sigma_q,
+                     Sigma_k, key_mean);
   return launch_ok() ? SAKI_OK : SAKI_ERR_HIP;
 }
 

@@ -49,6 +49,9 @@ def lib():
         "saki_index_bytes": (sz, [ip, ip, ip, ip, ip]),
         "saki_build_index": (ip, [vp, ip, ip, ip, ip, ip, ip, ip, vp, vp, ip, vp, sz, ip, ip, vp]),
         "saki_index_export": (ip, [vp, ip, ip, ip, ip, ip, vp, vp]),
+        "saki_calibration_moments": (ip, [vp, vp, ip, ip, ip, ip, vp, vp, vp, vp]),
+        "saki_calibrate_from_moments": (ip, [vp, vp, vp, ip, ip, ip, ip, ip, dp, vp, vp, vp, vp,
+                                             vp, ip]),
         "saki_score_topk_workspace_bytes": (sz, [ip, ip, ip, ip, ip, ip, ip, ip]),
         "saki_score_topk": (ip, [vp, ip, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, ip, vp, vp, ip,
                                  vp, vp, vp, sz, vp]),
@@ -106,6 +109,31 @@ def saki_calibrate(q_cal, k_cal, r: int, method: str = "opt", floor_rel: float =
                               mu.ctypes.data, sigma.ctypes.data if with_sigma else None,
                               ncl.ctypes.data, int(n_threads))
     _check("saki_calibrate", st)
+    return {"B_q": B_q, "B_k": B_k, "mu": mu, "sigma": sigma, "n_clamped": ncl}
+
+
+def saki_calibrate_from_moments(Sigma_q, Sigma_k, key_mean, r: int, method: str = "opt",
+                                floor_rel: float = 1e-6, n_threads: int = 0,
+                                with_sigma: bool = True, out=None):
+    """Sigma_q [H_q, d, d], Sigma_k [H_kv, d, d], key_mean [H_kv, d] (float64,
+    host) -> the same dict as saki_calibrate.  `out` may hold preallocated
+    B_q, B_k, mu (and sigma, n_clamped) arrays."""
+    sq, sqp = _host(Sigma_q, np.float64)
+    sk, skp = _host(Sigma_k, np.float64)
+    m, mp = _host(key_mean, np.float64)
+    H_q, d = sq.shape[0], sq.shape[1]
+    H_kv = sk.shape[0]
+    o = out if out is not None else {}
+    B_q = o.get("B_q", np.empty((H_q, d, r), np.float32))
+    B_k = o.get("B_k", np.empty((H_q, d, r), np.float32))
+    mu = o.get("mu", np.empty((H_kv, d), np.float32))
+    sigma = o.get("sigma", np.empty((H_q, d), np.float64)) if with_sigma else None
+    ncl = o.get("n_clamped", np.empty((H_q, 2), np.int32))
+    st = lib().saki_calibrate_from_moments(
+        sqp, skp, mp, H_q, H_kv, d, int(r), _METHODS[method], float(floor_rel),
+        B_q.ctypes.data, B_k.ctypes.data, mu.ctypes.data,
+        sigma.ctypes.data if with_sigma else None, ncl.ctypes.data, int(n_threads))
+    _check("saki_calibrate_from_moments", st)
     return {"B_q": B_q, "B_k": B_k, "mu": mu, "sigma": sigma, "n_clamped": ncl}
 
 
@@ -172,6 +200,30 @@ def _stream(stream):
 def _key_dtype(keys):
     torch = _torch()
     return BF16 if keys.dtype == torch.bfloat16 else F32
+
+
+def saki_calibration_moments(q_cal, k_cal, Sigma_q=None, Sigma_k=None, key_mean=None,
+                             stream=None):
+    """q_cal [H_q, T, d], k_cal [H_kv, T, d] float32 CUDA -> (Sigma_q [H_q, d, d],
+    Sigma_k [H_kv, d, d], key_mean [H_kv, d]) float64 CUDA tensors."""
+    torch = _torch()
+    qp = _dev(q_cal, (torch.float32,), "q_cal")
+    kp = _dev(k_cal, (torch.float32,), "k_cal")
+    H_q, T, d = q_cal.shape
+    H_kv = k_cal.shape[0]
+    dev = q_cal.device
+    if Sigma_q is None:
+        Sigma_q = torch.empty((H_q, d, d), dtype=torch.float64, device=dev)
+    if Sigma_k is None:
+        Sigma_k = torch.empty((H_kv, d, d), dtype=torch.float64, device=dev)
+    if key_mean is None:
+        key_mean = torch.empty((H_kv, d), dtype=torch.float64, device=dev)
+    st = lib().saki_calibration_moments(
+        qp, kp, H_q, H_kv, T, d, _dev(Sigma_q, (torch.float64,), "Sigma_q"),
+        _dev(Sigma_k, (torch.float64,), "Sigma_k"), _dev(key_mean, (torch.float64,), "key_mean"),
+        _stream(stream))
+    _check("saki_calibration_moments", st)
+    return Sigma_q, Sigma_k, key_mean
 
 
 def saki_build_index(keys, B_k, mu, r: int, sketch: str, H_q: int, index=None,

@@ -181,6 +181,32 @@ def test_gqa_shared_index_matches_oracle(sketch, Q, N):
             check_head(inp, out, 0, h, 32, mode, factors=(oc["B_q"], oc["B_k"], oc["mu"]))
 
 
+@pytest.mark.parametrize("T,d", [(512, 128), (77, 40)])
+def test_calibration_moments_on_gpu(T, d):
+    """saki_calibration_moments against the oracle's float64 moments (exact
+    products, so only summation order separates them), and the factors from
+    them against saki_calibrate."""
+    rng = np.random.default_rng(T)
+    q = (rng.standard_normal((6, T, d)) * np.linspace(0.1, 3.0, d)).astype(np.float32)
+    k = (rng.standard_normal((2, T, d)) * np.linspace(2.0, 0.2, d) + 0.5).astype(np.float32)
+    sq, sk, mu = S.saki_calibration_moments(_t(q), _t(k))
+    torch.cuda.synchronize()
+    sq, sk, mu = sq.cpu().numpy(), sk.cpu().numpy(), mu.cpu().numpy()
+    for h in range(6):
+        ref = O.second_moments(q[h], k[h // 3])[0]
+        assert np.max(np.abs(sq[h] - ref)) <= 1e-13 * np.abs(ref).max()
+    for g in range(2):
+        _, ref_k, ref_mu = O.second_moments(q[0], k[g])
+        assert np.max(np.abs(sk[g] - ref_k)) <= 1e-12 * np.abs(ref_k).max()
+        assert np.max(np.abs(mu[g] - ref_mu)) <= 1e-13 * np.abs(ref_mu).max()
+    if d >= 32:
+        a = S.saki_calibrate(q, k, 16)
+        b = S.saki_calibrate_from_moments(sq, sk, mu, 16)
+        M_a = np.einsum("hir,hjr->hij", a["B_q"].astype(np.float64), a["B_k"].astype(np.float64))
+        M_b = np.einsum("hir,hjr->hij", b["B_q"].astype(np.float64), b["B_k"].astype(np.float64))
+        assert np.max(np.abs(M_a - M_b)) <= 1e-5 * np.abs(M_a).max()
+
+
 @pytest.mark.parametrize("k", [1, 10, 64])
 def test_small_k_is_prefix_of_top64(k):
     spec = W.SPECS["single_head_d128"].with_(N=777, Q=33)

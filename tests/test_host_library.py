@@ -169,6 +169,28 @@ def test_shared_calibration_matches_oracle():
     assert S.saki_score_topk_workspace_bytes(1, 32, 4032, 4096, 32, 64, "bf16", 5) == 0
 
 
+@pytest.mark.parametrize("method", ["opt", "shared", "key_pca"])
+def test_calibrate_from_moments_equals_calibrate(method):
+    """saki_calibrate_from_moments on the oracle's float64 moments gives the
+    factors of saki_calibrate on the tokens (same arithmetic after the
+    moments; only their summation order differs)."""
+    spec = W.SPECS["llama31_8b_layer"].with_(N=64, Q=1, q_start=0)
+    inp = W.make_layer(spec)
+    G = spec.H_q // spec.H_kv
+    sq = np.stack([O.second_moments(inp["q_cal"][h], inp["k_cal"][h // G])[0]
+                   for h in range(spec.H_q)])
+    mom = [O.second_moments(inp["q_cal"][0], inp["k_cal"][g]) for g in range(spec.H_kv)]
+    sk = np.stack([m[1] for m in mom])
+    mu = np.stack([m[2] for m in mom])
+    a = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32, method=method)
+    b = S.saki_calibrate_from_moments(sq, sk, mu, 32, method=method)
+    for name in ("B_q", "B_k"):
+        x, y = a[name].astype(np.float64), b[name].astype(np.float64)
+        assert np.max(np.abs(x - y) / np.abs(y).max(axis=1, keepdims=True)) < 1e-5
+    np.testing.assert_allclose(a["mu"], b["mu"], rtol=1e-6, atol=1e-7)
+    np.testing.assert_array_equal(a["n_clamped"], b["n_clamped"])
+
+
 def test_constant_keys_identity_fallback():
     q = np.random.default_rng(1).standard_normal((1, 64, 16)).astype(np.float32)
     k = np.tile(np.arange(16, dtype=np.float32), (1, 64, 1))
