@@ -27,10 +27,16 @@
 #include <immintrin.h>
 
 #include <algorithm>
+#include <unistd.h>
+
 #include <atomic>
+#include <condition_variable>
 #include <cmath>
+#include <cstdint>
 #include <cstring>
+#include <functional>
 #include <limits>
+#include <mutex>
 #include <new>
 #include <thread>
 #include <vector>
@@ -38,6 +44,18 @@
 namespace {
 
 using Mat = std::vector<double>;  // row-major square matrix
+
+// A matrix buffer owned by the calling thread and kept between calls (the
+// pool's workers live on), so the per-head d x d temporaries are not
+// allocated, page-faulted and returned to the system on every call.  Slots
+// 0-1 belong to the per-head calibration steps, 2-3 to sym_eig_top and 4
+// to congruence_lower.
+double* thread_buffer(int slot, size_t n) {
+  thread_local std::vector<double> buf[5];
+  if (buf[slot].size() < n) buf[slot].resize(n);
+  return buf[slot].data();
+}
+
 
 // ---------------------------------------------------------------- AVX2 kernels
 // The library is built for x86-64-v3 hosts (AVX2 + FMA); these helpers keep
@@ -47,6 +65,21 @@ inline double hsum(__m256d v) {
   const __m128d lo = _mm256_castpd256_pd128(v), hi = _mm256_extractf128_pd(v, 1);
   const __m128d s = _mm_add_pd(lo, hi);
   return _mm_cvtsd_f64(_mm_add_sd(s, _mm_unpackhi_pd(s, s)));
+}
+
+// True when every x[i] is finite: x * 0 is NaN exactly for infinities and
+// NaNs, and a NaN survives the sum.
+bool all_finite(const double* x, size_t n) {
+  __m256d s0 = _mm256_setzero_pd(), s1 = _mm256_setzero_pd();
+  const __m256d zero = _mm256_setzero_pd();
+  size_t i = 0;
+  for (; i + 8 <= n; i += 8) {
+    s0 = _mm256_add_pd(s0, _mm256_mul_pd(_mm256_loadu_pd(x + i), zero));
+    s1 = _mm256_add_pd(s1, _mm256_mul_pd(_mm256_loadu_pd(x + i + 4), zero));
+  }
+  double acc = hsum(_mm256_add_pd(s0, s1));
+  for (; i < n; ++i) acc += x[i] * 0.0;
+  return acc == 0.0;
 }
 
 // sum_i a[i] * b[i]
@@ -131,18 +164,19 @@ void matmul(int n, const double* A, const double* B, double* C) {
 // M = L^T W needs k >= i for row i, and only blocks on or below the diagonal
 // are formed before mirroring.
 void congruence_lower(int n, const double* S, const double* L, double* M) {
-  std::vector<double> W((size_t)n * n, 0.0);
+  double* W = thread_buffer(4, (size_t)n * n);
+  std::fill(W, W + (size_t)n * n, 0.0);
   std::fill(M, M + (size_t)n * n, 0.0);
   if (n % 8 == 0) {
     for (int i0 = 0; i0 < n; i0 += 4)
-      for (int j0 = 0; j0 < n; j0 += 8) block4x8(n, S, n, 1, L, W.data(), i0, j0, j0, n);
+      for (int j0 = 0; j0 < n; j0 += 8) block4x8(n, S, n, 1, L, W, i0, j0, j0, n);
     for (int i0 = 0; i0 < n; i0 += 4)
-      for (int j0 = 0; j0 < i0 + 4; j0 += 8) block4x8(n, L, 1, n, W.data(), M, i0, j0, i0, n);
+      for (int j0 = 0; j0 < i0 + 4; j0 += 8) block4x8(n, L, 1, n, W, M, i0, j0, i0, n);
   } else {
     for (int i = 0; i < n; ++i)
-      for (int k = 0; k < n; ++k) axpy(S[(size_t)i * n + k], L + (size_t)k * n, W.data() + (size_t)i * n, k + 1);
+      for (int k = 0; k < n; ++k) axpy(S[(size_t)i * n + k], L + (size_t)k * n, W + (size_t)i * n, k + 1);
     for (int k = 0; k < n; ++k)
-      for (int i = 0; i <= k; ++i) axpy(L[(size_t)k * n + i], W.data() + (size_t)k * n, M + (size_t)i * n, n);
+      for (int i = 0; i <= k; ++i) axpy(L[(size_t)k * n + i], W + (size_t)k * n, M + (size_t)i * n, n);
   }
   for (int i = 0; i < n; ++i)
     for (int j = 0; j < i; ++j) M[(size_t)j * n + i] = M[(size_t)i * n + j];
@@ -376,8 +410,7 @@ bool tridiag_ql(int n, double* diag, double* off, double* zt) {
 // Eigen-decomposition of symmetric A (n x n row-major).  w ascending; vt row j
 // = eigenvector j.  Returns false on non-convergence or non-finite input.
 bool sym_eig_rows(int n, const double* A, double* w, double* vt) {
-  for (size_t i = 0; i < (size_t)n * n; ++i)
-    if (!std::isfinite(A[i])) return false;
+  if (!all_finite(A, (size_t)n * n)) return false;
   Mat a(A, A + (size_t)n * n), q((size_t)n * n), zt((size_t)n * n);
   // symmetrise exactly
   for (int i = 0; i < n; ++i)
@@ -457,54 +490,51 @@ struct ShiftedTridiagLU {
   }
 };
 
-// The eigenvalues with ascending indices idx[0..c) (c <= 8) of the symmetric
-// tridiagonal (diag, off) by bisection on Sturm counts (Golub & Van Loan,
-// Sec. 8.4.1), eight shifts at a time in two 256-bit vectors so that the
-// divisions of independent sequences overlap.  A pivot smaller in magnitude
-// than pivmin is replaced by -pivmin.
+// The eigenvalues with ascending indices idx[0..c) (c <= kBisectShifts) of
+// the symmetric tridiagonal (diag, off) by bisection on Sturm counts (Golub &
+// Van Loan, Sec. 8.4.1): n_halvings halvings of [glo, ghi], kBisectShifts
+// shifts at a time in independent 256-bit vectors so that the divisions of
+// the sequences overlap.  A pivot smaller in magnitude than pivmin is
+// replaced by -pivmin.
+constexpr int kBisectShifts = 16;
 void bisect_eigs(int n, const double* diag, const double* off2, double pivmin, double glo,
-                 double ghi, const int* idx, int c, double* out) {
-  alignas(32) double lo[8], hi[8], kk[8];
-  for (int e = 0; e < 8; ++e) {
-    lo[e] = glo;
-    hi[e] = ghi;
-    kk[e] = e < c ? (double)idx[e] : 0.0;
-  }
-  const __m256d one = _mm256_set1_pd(1.0), half = _mm256_set1_pd(0.5);
+                 double ghi, int n_halvings, const int* idx, int c, double* out) {
+  constexpr int V = kBisectShifts / 4;  // independent 4-wide Sturm sequences
+  alignas(32) double kk[kBisectShifts], res[kBisectShifts];
+  for (int e = 0; e < kBisectShifts; ++e) kk[e] = e < c ? (double)idx[e] : 0.0;
+  const __m256d one = _mm256_set1_pd(1.0), half = _mm256_set1_pd(0.5), zero = _mm256_setzero_pd();
   const __m256d npm = _mm256_set1_pd(-pivmin), pm = _mm256_set1_pd(pivmin);
   const __m256d absmask = _mm256_castsi256_pd(_mm256_set1_epi64x(0x7fffffffffffffffll));
-  __m256d lo0 = _mm256_load_pd(lo), lo1 = _mm256_load_pd(lo + 4);
-  __m256d hi0 = _mm256_load_pd(hi), hi1 = _mm256_load_pd(hi + 4);
-  const __m256d k0 = _mm256_load_pd(kk), k1 = _mm256_load_pd(kk + 4);
-  // the interval halves each step: 64 steps take Gershgorin width to rounding level
-  for (int it = 0; it < 64; ++it) {
-    const __m256d x0 = _mm256_mul_pd(_mm256_add_pd(lo0, hi0), half);
-    const __m256d x1 = _mm256_mul_pd(_mm256_add_pd(lo1, hi1), half);
+  __m256d lo[V], hi[V], k[V], x[V], q[V], cnt[V];
+  for (int v = 0; v < V; ++v) {
+    lo[v] = _mm256_set1_pd(glo);
+    hi[v] = _mm256_set1_pd(ghi);
+    k[v] = _mm256_load_pd(kk + 4 * v);
+  }
+  for (int it = 0; it < n_halvings; ++it) {
     const __m256d d0 = _mm256_set1_pd(diag[0]);
-    __m256d q0 = _mm256_sub_pd(d0, x0), q1 = _mm256_sub_pd(d0, x1);
-    q0 = _mm256_blendv_pd(q0, npm, _mm256_cmp_pd(_mm256_and_pd(q0, absmask), pm, _CMP_LT_OQ));
-    q1 = _mm256_blendv_pd(q1, npm, _mm256_cmp_pd(_mm256_and_pd(q1, absmask), pm, _CMP_LT_OQ));
-    __m256d c0 = _mm256_and_pd(_mm256_cmp_pd(q0, _mm256_setzero_pd(), _CMP_LT_OQ), one);
-    __m256d c1 = _mm256_and_pd(_mm256_cmp_pd(q1, _mm256_setzero_pd(), _CMP_LT_OQ), one);
+    for (int v = 0; v < V; ++v) {
+      x[v] = _mm256_mul_pd(_mm256_add_pd(lo[v], hi[v]), half);
+      q[v] = _mm256_sub_pd(d0, x[v]);
+      q[v] = _mm256_blendv_pd(q[v], npm, _mm256_cmp_pd(_mm256_and_pd(q[v], absmask), pm, _CMP_LT_OQ));
+      cnt[v] = _mm256_and_pd(_mm256_cmp_pd(q[v], zero, _CMP_LT_OQ), one);
+    }
     for (int i = 1; i < n; ++i) {
       const __m256d di = _mm256_set1_pd(diag[i]), ei = _mm256_set1_pd(off2[i - 1]);
-      q0 = _mm256_sub_pd(_mm256_sub_pd(di, x0), _mm256_div_pd(ei, q0));
-      q1 = _mm256_sub_pd(_mm256_sub_pd(di, x1), _mm256_div_pd(ei, q1));
-      q0 = _mm256_blendv_pd(q0, npm, _mm256_cmp_pd(_mm256_and_pd(q0, absmask), pm, _CMP_LT_OQ));
-      q1 = _mm256_blendv_pd(q1, npm, _mm256_cmp_pd(_mm256_and_pd(q1, absmask), pm, _CMP_LT_OQ));
-      c0 = _mm256_add_pd(c0, _mm256_and_pd(_mm256_cmp_pd(q0, _mm256_setzero_pd(), _CMP_LT_OQ), one));
-      c1 = _mm256_add_pd(c1, _mm256_and_pd(_mm256_cmp_pd(q1, _mm256_setzero_pd(), _CMP_LT_OQ), one));
+      for (int v = 0; v < V; ++v) {
+        q[v] = _mm256_sub_pd(_mm256_sub_pd(di, x[v]), _mm256_div_pd(ei, q[v]));
+        q[v] = _mm256_blendv_pd(q[v], npm, _mm256_cmp_pd(_mm256_and_pd(q[v], absmask), pm, _CMP_LT_OQ));
+        cnt[v] = _mm256_add_pd(cnt[v], _mm256_and_pd(_mm256_cmp_pd(q[v], zero, _CMP_LT_OQ), one));
+      }
     }
-    // count(x) <= k: the k-th eigenvalue is >= x
-    const __m256d up0 = _mm256_cmp_pd(c0, k0, _CMP_LE_OQ), up1 = _mm256_cmp_pd(c1, k1, _CMP_LE_OQ);
-    lo0 = _mm256_blendv_pd(lo0, x0, up0);
-    hi0 = _mm256_blendv_pd(x0, hi0, up0);
-    lo1 = _mm256_blendv_pd(lo1, x1, up1);
-    hi1 = _mm256_blendv_pd(x1, hi1, up1);
+    for (int v = 0; v < V; ++v) {  // count(x) <= k: the k-th eigenvalue is >= x
+      const __m256d up = _mm256_cmp_pd(cnt[v], k[v], _CMP_LE_OQ);
+      lo[v] = _mm256_blendv_pd(lo[v], x[v], up);
+      hi[v] = _mm256_blendv_pd(x[v], hi[v], up);
+    }
   }
-  _mm256_store_pd(lo, _mm256_mul_pd(_mm256_add_pd(lo0, hi0), half));
-  _mm256_store_pd(lo + 4, _mm256_mul_pd(_mm256_add_pd(lo1, hi1), half));
-  for (int e = 0; e < c; ++e) out[e] = lo[e];
+  for (int v = 0; v < V; ++v) _mm256_store_pd(res + 4 * v, _mm256_mul_pd(_mm256_add_pd(lo[v], hi[v]), half));
+  for (int e = 0; e < c; ++e) out[e] = res[e];
 }
 
 // The r largest eigenpairs of symmetric A (n x n row-major, read from its
@@ -516,11 +546,12 @@ void bisect_eigs(int n, const double* diag, const double* off2, double pivmin, d
 // clusters of close eigenvalues, and back-transformation by the reflectors.
 // Cost 2n^3 + O(n^2 r) flops instead of the roughly 9n^3 of the full solver.
 bool sym_eig_top(int n, const double* A, int r, double* w, double* vecs, bool all_values) {
-  for (size_t i = 0; i < (size_t)n * n; ++i)
-    if (!std::isfinite(A[i])) return false;
-  Mat a(A, A + (size_t)n * n), hv((size_t)n * n);  // the lower triangle defines A
+  if (!all_finite(A, (size_t)n * n)) return false;
+  double* a = thread_buffer(2, (size_t)n * n);  // the lower triangle defines A
+  double* hv = thread_buffer(3, (size_t)n * n);
+  std::copy(A, A + (size_t)n * n, a);
   std::vector<double> diag(n), off(n), beta(n);
-  householder_tridiag(n, a.data(), diag.data(), off.data(), hv.data(), beta.data());
+  householder_tridiag(n, a, diag.data(), off.data(), hv, beta.data());
   std::vector<double> ev(n);
   if (all_values) {
     std::vector<double> eo(off);
@@ -541,11 +572,18 @@ bool sym_eig_top(int n, const double* A, int r, double* w, double* vecs, bool al
     }
     const double pivmin = std::numeric_limits<double>::min() * std::max(1.0, emax);
     const double pad = 2.0 * std::numeric_limits<double>::epsilon() * std::max(std::fabs(glo), std::fabs(ghi)) + pivmin;
-    for (int m0 = 0; m0 < r; m0 += 8) {
-      int idx[8];
-      const int c = std::min(8, r - m0);
+    // halve the Gershgorin interval down to 2^-46 of the spectrum's scale: the
+    // factors are stored in float32, 2^-46 |T| is far below their rounding
+    const double scale = std::max(std::fabs(glo), std::fabs(ghi));
+    int n_halvings = 0;
+    for (double wdt = (ghi - glo) + 2.0 * pad; wdt > std::ldexp(scale, -46) && n_halvings < 64; wdt *= 0.5)
+      ++n_halvings;
+    for (int m0 = 0; m0 < r; m0 += kBisectShifts) {
+      int idx[kBisectShifts];
+      const int c = std::min(kBisectShifts, r - m0);
       for (int e = 0; e < c; ++e) idx[e] = n - 1 - (m0 + e);  // ascending index of the (m0+e)-th largest
-      bisect_eigs(n, diag.data(), off2.data(), pivmin, glo - pad, ghi + pad, idx, c, ev.data() + m0);
+      bisect_eigs(n, diag.data(), off2.data(), pivmin, glo - pad, ghi + pad, n_halvings, idx, c,
+                  ev.data() + m0);
     }
   }
   std::copy(ev.begin(), ev.begin() + (all_values ? n : r), w);
@@ -603,7 +641,7 @@ bool sym_eig_top(int n, const double* A, int r, double* w, double* vecs, bool al
   std::vector<double> X((size_t)n * r);
   for (int m = 0; m < r; ++m)
     for (int i = 0; i < n; ++i) X[(size_t)i * r + m] = vecs[(size_t)m * n + i];
-  apply_q(n, hv.data(), beta.data(), X.data(), r);
+  apply_q(n, hv, beta.data(), X.data(), r);
   for (int m = 0; m < r; ++m)
     for (int i = 0; i < n; ++i) vecs[(size_t)m * n + i] = X[(size_t)i * r + m];
   return true;
@@ -656,31 +694,133 @@ bool clamped_roots(int n, const double* S, double floor_rel, double* half,
   return true;
 }
 
-// Run fn(i) for i in [0, count) on up to n_threads threads.
+// Worker threads kept for the life of the process.  A calibration call runs
+// two parallel phases over heads; starting threads for each phase would cost
+// tens of microseconds per thread, a large share of a call that takes a few
+// milliseconds.  Jobs are serialised: concurrent callers wait for the pool,
+// and a job started from inside a worker (nesting) runs inline.  The workers
+// are detached and the pool is never destroyed, so process exit does not
+// wait for them; a child of fork() builds its own pool.
+class WorkerPool {
+ public:
+  static WorkerPool& get() {
+    static std::mutex m;
+    static WorkerPool* pool = nullptr;
+    std::lock_guard<std::mutex> lk(m);
+    if (!pool || pool->pid_ != getpid()) pool = new WorkerPool();  // old one leaks after fork
+    return *pool;
+  }
+
+  // fn(i) for i in [0, count) on nt threads (the caller is one of them).
+  // Returns false if some fn(i) threw std::bad_alloc.
+  template <class F>
+  bool run(int count, int nt, F& fn) {
+    if (t_in_worker) return run_inline(count, fn);
+    std::lock_guard<std::mutex> job(job_mutex_);
+    grow(nt - 1);
+    std::atomic<int> next(0);
+    std::atomic<bool> oom(false);
+    Body body = [&]() {
+      for (int i = next.fetch_add(1); i < count; i = next.fetch_add(1)) {
+        try {
+          fn(i);
+        } catch (const std::bad_alloc&) {
+          oom = true;
+        }
+      }
+    };
+    {
+      std::lock_guard<std::mutex> lk(m_);
+      body_ = &body;
+      helpers_ = nt - 1;
+      done_ = 0;
+      ++generation_;
+    }
+    cv_start_.notify_all();
+    t_in_worker = true;
+    body();
+    t_in_worker = false;
+    std::unique_lock<std::mutex> lk(m_);
+    cv_done_.wait(lk, [&] { return done_ == helpers_; });
+    body_ = nullptr;
+    return !oom;
+  }
+
+ private:
+  using Body = std::function<void()>;
+  static thread_local bool t_in_worker;
+
+  WorkerPool() : pid_(getpid()) {}
+
+  template <class F>
+  static bool run_inline(int count, F& fn) {
+    try {
+      for (int i = 0; i < count; ++i) fn(i);
+    } catch (const std::bad_alloc&) {
+      return false;
+    }
+    return true;
+  }
+
+  void grow(int n) {
+    while ((int)n_workers_ < n) {
+      const int id = n_workers_++;
+      std::thread([this, id] { loop(id); }).detach();
+    }
+  }
+
+  void loop(int id) {
+    t_in_worker = true;
+    uint64_t seen = 0;
+    for (;;) {
+      Body* body;
+      {
+        std::unique_lock<std::mutex> lk(m_);
+        cv_start_.wait(lk, [&] { return generation_ != seen; });
+        seen = generation_;
+        if (id >= helpers_) continue;  // not needed for this job
+        body = body_;
+      }
+      (*body)();
+      {
+        std::lock_guard<std::mutex> lk(m_);
+        ++done_;
+      }
+      cv_done_.notify_one();
+    }
+  }
+
+  const pid_t pid_;
+  std::mutex job_mutex_;  // one job at a time
+  std::mutex m_;
+  std::condition_variable cv_start_, cv_done_;
+  Body* body_ = nullptr;
+  int helpers_ = 0, done_ = 0, n_workers_ = 0;
+  uint64_t generation_ = 0;
+};
+
+thread_local bool WorkerPool::t_in_worker = false;
+
+// Run fn(i) for i in [0, count) on up to n_threads threads (0: the host's
+// hardware threads, at most 16).  Throws std::bad_alloc if a task did.
 template <class F>
 void parallel_for(int count, int n_threads, F fn) {
   int nt = n_threads > 0 ? n_threads : (int)std::thread::hardware_concurrency();
   if (n_threads <= 0) nt = std::min(nt, 16);
-  nt = std::max(1, std::min(nt, count));
-  if (nt == 1) {
+  nt = std::max(1, std::min({nt, count, 256}));
+  const bool ok = nt == 1 ? [&] {
     for (int i = 0; i < count; ++i) fn(i);
-    return;
-  }
-  std::atomic<int> next(0);
-  std::vector<std::thread> pool;
-  pool.reserve(nt);
-  for (int t = 0; t < nt; ++t)
-    pool.emplace_back([&]() {
-      for (int i = next.fetch_add(1); i < count; i = next.fetch_add(1)) fn(i);
-    });
-  for (auto& th : pool) th.join();
+    return true;
+  }() : WorkerPool::get().run(count, nt, fn);
+  if (!ok) throw std::bad_alloc();
 }
 
 struct KvState {
   Mat half, ihalf;         // Sigma_k^{1/2}, Sigma_k^{-1/2} (symmetric route)
   Mat L;                   // Cholesky factor of Sigma_k (Cholesky route)
   std::vector<double> mu;  // key mean
-  Mat sk;                  // Sigma_k
+  Mat sk;                  // Sigma_k, when computed here
+  const double* skp = nullptr;  // Sigma_k (sk, or the caller's moment)
   int n_clamped = 0;
   bool chol = false;       // the floor provably does not bind on Sigma_k
   bool ok = false;
@@ -745,23 +885,24 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
     //  computed in the same parallel phase, after the KV heads' tasks)
     std::vector<KvState> kv(H_kv);
     const bool opt = method == SAKI_METHOD_OPT || method == SAKI_METHOD_SHARED;
-    std::vector<Mat> sq_all(opt ? H_q : 0);
-    parallel_for(H_kv + (int)sq_all.size(), n_threads, [&](int task) {
+    // Sigma_q per head: the caller's moments, or computed here
+    std::vector<const double*> sq_of(opt ? H_q : 0);
+    std::vector<Mat> sq_own(opt && !given ? H_q : 0);
+    for (int h = 0; h < (int)sq_of.size(); ++h) sq_of[h] = given ? Sq_in + (size_t)h * dd : nullptr;
+    parallel_for(H_kv + (int)sq_own.size(), n_threads, [&](int task) {
       if (task >= H_kv) {
         const int h = task - H_kv;
-        if (given) {
-          sq_all[h].assign(Sq_in + (size_t)h * dd, Sq_in + (size_t)(h + 1) * dd);
-        } else {
-          sq_all[h].resize(dd);
-          moment(T, d, q_cal + (size_t)h * T * d, nullptr, sq_all[h].data());
-        }
+        sq_own[h].resize(dd);
+        moment(T, d, q_cal + (size_t)h * T * d, nullptr, sq_own[h].data());
+        sq_of[h] = sq_own[h].data();
         return;
       }
       const int g = task;
       KvState& st = kv[g];
       if (given) {
         st.mu.assign(mu_in + (size_t)g * d, mu_in + (size_t)(g + 1) * d);
-        st.sk.assign(Sk_in + (size_t)g * dd, Sk_in + (size_t)(g + 1) * dd);
+        st.skp = Sk_in + (size_t)g * dd;
+        if (!all_finite(st.mu.data(), d) || !all_finite(st.skp, dd)) return;  // st.ok stays false
       } else {
         const float* k = k_cal + (size_t)g * T * d;
         st.mu.assign(d, 0.0);
@@ -770,16 +911,17 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
         for (int i = 0; i < d; ++i) st.mu[i] /= (double)T;
         st.sk.resize(dd);
         moment(T, d, k, st.mu.data(), st.sk.data());
+        st.skp = st.sk.data();
       }
       if (opt) {
         st.L.resize(dd);
-        st.chol = unclamped_cholesky(d, st.sk.data(), floor_rel, st.L.data(), true);
+        st.chol = unclamped_cholesky(d, st.skp, floor_rel, st.L.data(), true);
         if (st.chol) {
           st.ok = true;
         } else {
           st.half.resize(dd);
           st.ihalf.resize(dd);
-          st.ok = clamped_roots(d, st.sk.data(), floor_rel, st.half.data(), st.ihalf.data(),
+          st.ok = clamped_roots(d, st.skp, floor_rel, st.half.data(), st.ihalf.data(),
                                 &st.n_clamped);
         }
       } else {
@@ -794,15 +936,18 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
     // (1/G) sum_h Sigma_q^(h) goes through the per-head steps once, for the
     // group's first head, and the factors are copied to the others
     const bool shared = method == SAKI_METHOD_SHARED;
+    std::vector<Mat> pooled(shared ? H_kv : 0);
     if (shared) {
       parallel_for(H_kv, n_threads, [&](int g) {
-        Mat& pool = sq_all[(size_t)g * G];
+        Mat& pool = pooled[g];
+        pool.assign(sq_of[(size_t)g * G], sq_of[(size_t)g * G] + dd);
         for (int hh = 1; hh < G; ++hh) {
-          const Mat& o = sq_all[(size_t)g * G + hh];
+          const double* o = sq_of[(size_t)g * G + hh];
           for (size_t i = 0; i < dd; ++i) pool[i] += o[i];
         }
         for (size_t i = 0; i < dd; ++i) pool[i] /= (double)G;
       });
+      for (int g = 0; g < H_kv; ++g) sq_of[(size_t)g * G] = pooled[g].data();
     }
     std::atomic<int> failed(0);
     parallel_for(shared ? H_kv : H_q, n_threads, [&](int task) {
@@ -812,7 +957,7 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
       float* bk = B_k + (size_t)h * d * r;
       if (method == SAKI_METHOD_KEY_PCA) {
         std::vector<double> w(d), vt(dd);
-        if (!sym_eig_rows(d, st.sk.data(), w.data(), vt.data())) { failed = 1; return; }
+        if (!sym_eig_rows(d, st.skp, w.data(), vt.data())) { failed = 1; return; }
         for (int m = 0; m < r; ++m) {
           double* v = vt.data() + (size_t)(d - 1 - m) * d;  // m-th largest
           canonical_sign(d, v, nullptr);
@@ -824,16 +969,16 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
         return;
       }
       // Sigma_q (uncentred), from the first phase
-      const Mat& sq = sq_all[h];
+      const double* sq = sq_of[h];
+      if (given && !all_finite(sq, dd)) { failed = 1; return; }
       std::vector<double> sig(d), bqc(d), bkc(d);
-      Mat scratch(dd);
-      if (st.chol && unclamped_cholesky(d, sq.data(), floor_rel, scratch.data(), false)) {
+      if (st.chol && unclamped_cholesky(d, sq, floor_rel, thread_buffer(0, dd), false)) {
         // ---- Cholesky route: M = L^T Sigma_q L, B_q = L v / sqrt(s), B_k = L^-T v sqrt(s)
         const double* L = st.L.data();
-        Mat M(dd);
-        congruence_lower(d, sq.data(), L, M.data());
+        double* M = thread_buffer(1, dd);
+        congruence_lower(d, sq, L, M);
         std::vector<double> w(d), vt((size_t)r * d);
-        if (!sym_eig_top(d, M.data(), r, w.data(), vt.data(), sigma != nullptr)) { failed = 1; return; }
+        if (!sym_eig_top(d, M, r, w.data(), vt.data(), sigma != nullptr)) { failed = 1; return; }
         for (int m = 0; m < (sigma ? d : r); ++m) sig[m] = std::sqrt(std::max(w[m], 0.0));
         // all r columns at once (d x r, row-major): P = L V', X = L^-T V'
         Mat V((size_t)d * r), P((size_t)d * r, 0.0), X((size_t)d * r);
@@ -863,7 +1008,7 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
       // ---- symmetric route: clamped roots of both moments
       Mat qh(dd), qih(dd);
       int nq = 0;
-      if (!clamped_roots(d, sq.data(), floor_rel, qh.data(), qih.data(), &nq)) { failed = 1; return; }
+      if (!clamped_roots(d, sq, floor_rel, qh.data(), qih.data(), &nq)) { failed = 1; return; }
       Mat kh_local, kih_local;
       const double* khalf = st.half.data();
       const double* kihalf = st.ihalf.data();
@@ -871,7 +1016,7 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
       if (st.chol) {  // Sigma_k took the Cholesky route: its roots are needed here only
         kh_local.resize(dd);
         kih_local.resize(dd);
-        if (!clamped_roots(d, st.sk.data(), floor_rel, kh_local.data(), kih_local.data(), &nk)) {
+        if (!clamped_roots(d, st.skp, floor_rel, kh_local.data(), kih_local.data(), &nk)) {
           failed = 1;
           return;
         }
@@ -952,9 +1097,6 @@ int saki_calibrate_from_moments(const double* Sigma_q, const double* Sigma_k,
                                 int method, double floor_rel, float* B_q, float* B_k, float* mu,
                                 double* sigma, int* n_clamped, int n_threads) {
   if (!Sigma_q || !Sigma_k || !key_mean) return SAKI_ERR_ARG;
-  if (H_q > 0 && H_kv > 0 && d > 0 && d <= 4096)
-    for (size_t i = 0; i < (size_t)H_q * d * d; ++i)
-      if (!std::isfinite(Sigma_q[i])) return SAKI_ERR_NUMERIC;
   return calibrate_core(nullptr, nullptr, Sigma_q, Sigma_k, key_mean, H_q, H_kv, 0, d, r,
                         method, floor_rel, B_q, B_k, mu, sigma, n_clamped, n_threads);
 }

@@ -191,6 +191,54 @@ def test_calibrate_from_moments_equals_calibrate(method):
     np.testing.assert_array_equal(a["n_clamped"], b["n_clamped"])
 
 
+def test_calibration_from_concurrent_callers():
+    """Host threads calling the calibration at once share one worker pool:
+    jobs are serialised and each caller gets its own, identical, result."""
+    import threading
+    spec = W.SPECS["llama31_8b_layer"].with_(N=64, Q=1, q_start=0)
+    inp = W.make_layer(spec)
+    ref = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32, n_threads=4)
+    out = [None] * 6
+
+    def work(i):
+        out[i] = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32, n_threads=1 + i % 4)
+
+    ts = [threading.Thread(target=work, args=(i,)) for i in range(len(out))]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    for o in out:
+        for name in ("B_q", "B_k", "mu"):
+            np.testing.assert_array_equal(o[name], ref[name])
+
+
+def _calibrate_in_child(conn):
+    rng = np.random.default_rng(4)
+    q = rng.standard_normal((4, 96, 16)).astype(np.float32)
+    k = rng.standard_normal((2, 96, 16)).astype(np.float32)
+    conn.send(S.saki_calibrate(q, k, 4, n_threads=3)["B_k"])
+    conn.close()
+
+
+def test_calibration_after_fork():
+    """A child forked after the parent started its workers builds its own."""
+    import multiprocessing as mp
+    rng = np.random.default_rng(4)
+    q = rng.standard_normal((4, 96, 16)).astype(np.float32)
+    k = rng.standard_normal((2, 96, 16)).astype(np.float32)
+    ref = S.saki_calibrate(q, k, 4, n_threads=3)["B_k"]  # parent's workers exist now
+    ctx = mp.get_context("fork")
+    a, b = ctx.Pipe(duplex=False)
+    p = ctx.Process(target=_calibrate_in_child, args=(b,))
+    p.start()
+    assert a.poll(60), "child calibration did not finish"
+    got = a.recv()
+    p.join(30)
+    assert p.exitcode == 0
+    np.testing.assert_array_equal(got, ref)
+
+
 def test_constant_keys_identity_fallback():
     q = np.random.default_rng(1).standard_normal((1, 64, 16)).astype(np.float32)
     k = np.tile(np.arange(16, dtype=np.float32), (1, 64, 1))
