@@ -36,6 +36,7 @@
 #include <cstring>
 #include <functional>
 #include <limits>
+#include <memory>
 #include <mutex>
 #include <new>
 #include <thread>
@@ -55,6 +56,56 @@ double* thread_buffer(int slot, size_t n) {
   if (buf[slot].size() < n) buf[slot].resize(n);
   return buf[slot].data();
 }
+
+// Per-call buffers larger than one matrix (a d x d block per head) come
+// from this process-wide cache and go back to it when the call ends, so
+// their pages are touched once, not on every call.  At most four are kept.
+class BufferCache {
+ public:
+  struct Buf {
+    std::unique_ptr<double[]> p;
+    size_t n = 0;
+  };
+  static Buf take(size_t n) {
+    {
+      std::lock_guard<std::mutex> lk(mutex());
+      auto& f = list();
+      for (size_t i = 0; i < f.size(); ++i)
+        if (f[i].n >= n) {
+          Buf b = std::move(f[i]);
+          f.erase(f.begin() + (long)i);
+          return b;
+        }
+    }
+    Buf b;
+    b.p.reset(new double[n]);
+    b.n = n;
+    return b;
+  }
+  static void give(Buf b) {
+    std::lock_guard<std::mutex> lk(mutex());
+    auto& f = list();
+    if (f.size() < 4) f.push_back(std::move(b));
+  }
+
+ private:
+  static std::mutex& mutex() {
+    static std::mutex m;
+    return m;
+  }
+  static std::vector<Buf>& list() {
+    static std::vector<Buf> f;
+    return f;
+  }
+};
+
+// A cached buffer for the lifetime of a scope.
+struct ScopedBuffer {
+  BufferCache::Buf b;
+  explicit ScopedBuffer(size_t n) : b(BufferCache::take(n)) {}
+  ~ScopedBuffer() { BufferCache::give(std::move(b)); }
+  double* data() { return b.p.get(); }
+};
 
 
 // ---------------------------------------------------------------- AVX2 kernels
@@ -537,25 +588,31 @@ void bisect_eigs(int n, const double* diag, const double* off2, double pivmin, d
   for (int e = 0; e < c; ++e) out[e] = res[e];
 }
 
-// The r largest eigenpairs of symmetric A (n x n row-major, read from its
-// lower triangle): w receives all n
-// eigenvalues in descending order, row m of `vecs` (r x n) the unit
-// eigenvector of w[m].  Householder tridiagonalisation, eigenvalues by QL
-// without vectors, then inverse iteration on the tridiagonal for the r
-// vectors (Golub & Van Loan, Sec. 8.2.2 and 8.4), re-orthogonalised within
-// clusters of close eigenvalues, and back-transformation by the reflectors.
-// Cost 2n^3 + O(n^2 r) flops instead of the roughly 9n^3 of the full solver.
-bool sym_eig_top(int n, const double* A, int r, double* w, double* vecs, bool all_values) {
+// Tridiagonal form of symmetric A (n x n row-major, read from its lower
+// triangle) and its reflectors, as householder_tridiag returns them.
+bool tridiag_of(int n, const double* A, double* diag, double* off, double* hv, double* beta) {
   if (!all_finite(A, (size_t)n * n)) return false;
-  double* a = thread_buffer(2, (size_t)n * n);  // the lower triangle defines A
-  double* hv = thread_buffer(3, (size_t)n * n);
+  double* a = thread_buffer(2, (size_t)n * n);
   std::copy(A, A + (size_t)n * n, a);
-  std::vector<double> diag(n), off(n), beta(n);
-  householder_tridiag(n, a, diag.data(), off.data(), hv, beta.data());
+  householder_tridiag(n, a, diag, off, hv, beta);
+  return true;
+}
+
+// The r largest eigenpairs of the symmetric matrix whose tridiagonal form
+// (diag, off) and reflectors (hv, beta) tridiag_of produced: w receives the
+// r largest eigenvalues in descending order (all n with all_values), row m
+// of `vecs` (r x n) the unit eigenvector of w[m].  Eigenvalues by QL without
+// vectors (all_values) or by bisection (only the r largest), then inverse
+// iteration on the tridiagonal for the r vectors (Golub & Van Loan, Sec.
+// 8.2.2 and 8.4), re-orthogonalised within clusters of close eigenvalues,
+// and back-transformation by the reflectors.  With the reduction this costs
+// 2n^3 + O(n^2 r) flops instead of the roughly 9n^3 of the full solver.
+bool top_eigpairs(int n, const double* diag, const double* off, const double* hv,
+                  const double* beta, int r, double* w, double* vecs, bool all_values) {
   std::vector<double> ev(n);
   if (all_values) {
-    std::vector<double> eo(off);
-    std::copy(diag.begin(), diag.end(), ev.begin());
+    std::vector<double> eo(off, off + n);
+    std::copy(diag, diag + n, ev.begin());
     if (!tridiag_ql(n, ev.data(), eo.data(), nullptr)) return false;
     std::sort(ev.begin(), ev.end(), [](double x, double y) { return x > y; });
   } else {  // only the r largest, by bisection
@@ -582,7 +639,7 @@ bool sym_eig_top(int n, const double* A, int r, double* w, double* vecs, bool al
       int idx[kBisectShifts];
       const int c = std::min(kBisectShifts, r - m0);
       for (int e = 0; e < c; ++e) idx[e] = n - 1 - (m0 + e);  // ascending index of the (m0+e)-th largest
-      bisect_eigs(n, diag.data(), off2.data(), pivmin, glo - pad, ghi + pad, n_halvings, idx, c,
+      bisect_eigs(n, diag, off2.data(), pivmin, glo - pad, ghi + pad, n_halvings, idx, c,
                   ev.data() + m0);
     }
   }
@@ -614,7 +671,7 @@ bool sym_eig_top(int n, const double* A, int r, double* w, double* vecs, bool al
       seed = seed * 6364136223846793005ull + 1442695040888963407ull;
       x[i] = (double)(seed >> 11) * (2.0 / 9007199254740992.0) - 1.0;
     }
-    lu.factor(n, diag.data(), off.data(), lambda, tiny);
+    lu.factor(n, diag, off, lambda, tiny);
     int extra = 0;
     bool done = false;
     for (int it = 0; it < 6 && !done; ++it) {
@@ -641,10 +698,19 @@ bool sym_eig_top(int n, const double* A, int r, double* w, double* vecs, bool al
   std::vector<double> X((size_t)n * r);
   for (int m = 0; m < r; ++m)
     for (int i = 0; i < n; ++i) X[(size_t)i * r + m] = vecs[(size_t)m * n + i];
-  apply_q(n, hv, beta.data(), X.data(), r);
+  apply_q(n, hv, beta, X.data(), r);
   for (int m = 0; m < r; ++m)
     for (int i = 0; i < n; ++i) vecs[(size_t)m * n + i] = X[(size_t)i * r + m];
   return true;
+}
+
+// The r largest eigenpairs of symmetric A (n x n row-major, read from its
+// lower triangle); w, vecs and all_values as for top_eigpairs.
+bool sym_eig_top(int n, const double* A, int r, double* w, double* vecs, bool all_values) {
+  double* hv = thread_buffer(3, (size_t)n * n);
+  std::vector<double> diag(n), off(n), beta(n);
+  return tridiag_of(n, A, diag.data(), off.data(), hv, beta.data()) &&
+         top_eigpairs(n, diag.data(), off.data(), hv, beta.data(), r, w, vecs, all_values);
 }
 
 // Flip the sign of row `v` (length n) -- and of `u` if given -- so that its
@@ -881,23 +947,15 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
   try {
     // ---- per KV head: key mean, centred key moment, and either its Cholesky
     //      factor or its clamped symmetric roots
-    // (the uncentred query moments need nothing from the keys: they are
-    //  computed in the same parallel phase, after the KV heads' tasks)
     std::vector<KvState> kv(H_kv);
     const bool opt = method == SAKI_METHOD_OPT || method == SAKI_METHOD_SHARED;
     // Sigma_q per head: the caller's moments, or computed here
     std::vector<const double*> sq_of(opt ? H_q : 0);
     std::vector<Mat> sq_own(opt && !given ? H_q : 0);
     for (int h = 0; h < (int)sq_of.size(); ++h) sq_of[h] = given ? Sq_in + (size_t)h * dd : nullptr;
-    parallel_for(H_kv + (int)sq_own.size(), n_threads, [&](int task) {
-      if (task >= H_kv) {
-        const int h = task - H_kv;
-        sq_own[h].resize(dd);
-        moment(T, d, q_cal + (size_t)h * T * d, nullptr, sq_own[h].data());
-        sq_of[h] = sq_own[h].data();
-        return;
-      }
-      const int g = task;
+    const bool shared = method == SAKI_METHOD_SHARED;
+    std::vector<Mat> pooled(shared ? H_kv : 0);
+    auto kv_task = [&](int g) {
       KvState& st = kv[g];
       if (given) {
         st.mu.assign(mu_in + (size_t)g * d, mu_in + (size_t)(g + 1) * d);
@@ -928,31 +986,123 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
         st.ok = true;
       }
       for (int i = 0; i < d; ++i) mu[(size_t)g * d + i] = (float)st.mu[i];
-    });
-    for (int g = 0; g < H_kv; ++g)
-      if (!kv[g].ok) return SAKI_ERR_NUMERIC;
-
+    };
+    auto qm_task = [&](int h) {  // uncentred query moment from the tokens
+      sq_own[h].resize(dd);
+      moment(T, d, q_cal + (size_t)h * T * d, nullptr, sq_own[h].data());
+      sq_of[h] = sq_own[h].data();
+    };
     // one shared map per KV group: the group's pooled query moment
     // (1/G) sum_h Sigma_q^(h) goes through the per-head steps once, for the
     // group's first head, and the factors are copied to the others
-    const bool shared = method == SAKI_METHOD_SHARED;
-    std::vector<Mat> pooled(shared ? H_kv : 0);
-    if (shared) {
-      parallel_for(H_kv, n_threads, [&](int g) {
-        Mat& pool = pooled[g];
-        pool.assign(sq_of[(size_t)g * G], sq_of[(size_t)g * G] + dd);
-        for (int hh = 1; hh < G; ++hh) {
-          const double* o = sq_of[(size_t)g * G + hh];
-          for (size_t i = 0; i < dd; ++i) pool[i] += o[i];
-        }
-        for (size_t i = 0; i < dd; ++i) pool[i] /= (double)G;
-      });
-      for (int g = 0; g < H_kv; ++g) sq_of[(size_t)g * G] = pooled[g].data();
-    }
+    auto pool_task = [&](int g) {
+      for (int hh = 0; hh < G; ++hh)
+        if (!sq_of[(size_t)g * G + hh]) return;  // a moment failed: sq_of stays unpooled
+      Mat& pool = pooled[g];
+      pool.assign(sq_of[(size_t)g * G], sq_of[(size_t)g * G] + dd);
+      for (int hh = 1; hh < G; ++hh) {
+        const double* o = sq_of[(size_t)g * G + hh];
+        for (size_t i = 0; i < dd; ++i) pool[i] += o[i];
+      }
+      for (size_t i = 0; i < dd; ++i) pool[i] /= (double)G;
+    };
+
+    // One task list, claimed in this order: KV heads, query moments (tokens
+    // given), pooled group moments (shared map), then the per-head factors.
+    // A task waits only for earlier tasks whose results it reads; those are
+    // already claimed by threads that never wait on later tasks, so the
+    // kinds overlap without a barrier and the waits always end.
+    // A head on the Cholesky route takes two tasks: the reduction of M to
+    // tridiagonal form, then its eigenpairs and factor columns (halves of
+    // about equal cost, so that threads slowed by other work on the host
+    // hold up less of the call).
+    const int n_qm = (int)sq_own.size(), n_pool = (int)pooled.size();
+    const int n_pre = H_kv + n_qm + n_pool;
+    const int n_head = shared ? H_kv : H_q;
+    std::unique_ptr<std::atomic<int>[]> done(new std::atomic<int>[n_pre + n_head]);
+    for (int t = 0; t < n_pre + n_head; ++t) done[t].store(0, std::memory_order_relaxed);
+    struct Reduced {  // a head's M in tridiagonal form, between its two tasks
+      std::vector<double> diag, off, beta;
+      bool pending = false;
+    };
+    std::vector<Reduced> red(n_head);
+    ScopedBuffer hv_all(opt ? (size_t)n_head * dd : 1);
+    auto wait_for = [&](int t) {
+      while (done[t].load(std::memory_order_acquire) == 0) _mm_pause();
+    };
+    struct Finish {  // marks a task done however it ends (bad_alloc included)
+      std::atomic<int>& flag;
+      ~Finish() { flag.store(1, std::memory_order_release); }
+    };
     std::atomic<int> failed(0);
-    parallel_for(shared ? H_kv : H_q, n_threads, [&](int task) {
+    // Cholesky route, second half: B_q = L v / sqrt(s), B_k = L^-T v sqrt(s)
+    // for the top-r eigenpairs (s, v) of M = L^T Sigma_q L
+    auto chol_factors = [&](int h, int task) {
+      const Reduced& rd = red[task];
+      const double* L = kv[h / G].L.data();
+      float* bq = B_q + (size_t)h * d * r;
+      float* bk = B_k + (size_t)h * d * r;
+      std::vector<double> sig(d), bqc(d), bkc(d);
+      std::vector<double> w(d), vt((size_t)r * d);
+      if (!top_eigpairs(d, rd.diag.data(), rd.off.data(), hv_all.data() + (size_t)task * dd,
+                        rd.beta.data(), r, w.data(), vt.data(), sigma != nullptr)) {
+        failed = 1;
+        return;
+      }
+      for (int m = 0; m < (sigma ? d : r); ++m) sig[m] = std::sqrt(std::max(w[m], 0.0));
+      // all r columns at once (d x r, row-major): P = L V', X = L^-T V'
+      Mat V((size_t)d * r), P((size_t)d * r, 0.0), X((size_t)d * r);
+      for (int m = 0; m < r; ++m)
+        for (int i = 0; i < d; ++i) V[(size_t)i * r + m] = vt[(size_t)m * d + i];
+      for (int i = 0; i < d; ++i)
+        for (int j = 0; j <= i; ++j) axpy(L[(size_t)i * d + j], V.data() + (size_t)j * r, P.data() + (size_t)i * r, r);
+      for (int i = d - 1; i >= 0; --i) {  // L^T X = V by back substitution, row i of L at a time
+        double* xi = X.data() + (size_t)i * r;
+        const double rl = 1.0 / L[(size_t)i * d + i];
+        for (int m = 0; m < r; ++m) xi[m] = V[(size_t)i * r + m] * rl;
+        for (int j = 0; j < i; ++j) axpy(-L[(size_t)i * d + j], xi, V.data() + (size_t)j * r, r);
+      }
+      for (int m = 0; m < r; ++m) {
+        const double sm = sig[m], rs = std::sqrt(sm);
+        for (int i = 0; i < d; ++i) {
+          bqc[i] = sm > 0.0 ? P[(size_t)i * r + m] / rs : 0.0;
+          bkc[i] = X[(size_t)i * r + m] * rs;
+        }
+        store_pair(d, r, m, bqc.data(), bkc.data(), bq, bk);
+      }
+      if (sigma)
+        for (int m = 0; m < d; ++m) sigma[(size_t)h * d + m] = sig[m];
+      if (n_clamped) { n_clamped[2 * h] = 0; n_clamped[2 * h + 1] = 0; }
+    };
+    parallel_for(n_pre + 2 * n_head, n_threads, [&](int t) {
+      if (t < n_pre) {
+        Finish fin{done[t]};
+        if (t < H_kv) {
+          kv_task(t);
+        } else if (t < H_kv + n_qm) {
+          qm_task(t - H_kv);
+        } else {
+          const int g = t - H_kv - n_qm;
+          if (!given)
+            for (int hh = 0; hh < G; ++hh) wait_for(H_kv + g * G + hh);
+          pool_task(g);
+        }
+        return;
+      }
+      if (t >= n_pre + n_head) {  // second half of a Cholesky-route head
+        const int task = t - n_pre - n_head;
+        wait_for(n_pre + task);
+        if (!red[task].pending) return;
+        const int h = shared ? task * G : task;
+        chol_factors(h, task);
+        return;
+      }
+      const int task = t - n_pre;
+      Finish fin{done[t]};
       const int h = shared ? task * G : task;
+      wait_for(h / G);
       const KvState& st = kv[h / G];
+      if (!st.ok) { failed = 1; return; }
       float* bq = B_q + (size_t)h * d * r;
       float* bk = B_k + (size_t)h * d * r;
       if (method == SAKI_METHOD_KEY_PCA) {
@@ -968,41 +1118,30 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
         if (n_clamped) { n_clamped[2 * h] = 0; n_clamped[2 * h + 1] = 0; }
         return;
       }
-      // Sigma_q (uncentred), from the first phase
-      const double* sq = sq_of[h];
+      // Sigma_q (uncentred): the caller's, this head's moment task, or the pool
+      if (shared)
+        wait_for(H_kv + n_qm + task);
+      else if (!given)
+        wait_for(H_kv + h);
+      const double* sq = shared ? (pooled[task].empty() ? nullptr : pooled[task].data()) : sq_of[h];
+      if (!sq) { failed = 1; return; }
       if (given && !all_finite(sq, dd)) { failed = 1; return; }
       std::vector<double> sig(d), bqc(d), bkc(d);
       if (st.chol && unclamped_cholesky(d, sq, floor_rel, thread_buffer(0, dd), false)) {
-        // ---- Cholesky route: M = L^T Sigma_q L, B_q = L v / sqrt(s), B_k = L^-T v sqrt(s)
-        const double* L = st.L.data();
+        // ---- Cholesky route: M = L^T Sigma_q L, reduced to tridiagonal form here;
+        //      the eigenpairs and columns are the head's second task
         double* M = thread_buffer(1, dd);
-        congruence_lower(d, sq, L, M);
-        std::vector<double> w(d), vt((size_t)r * d);
-        if (!sym_eig_top(d, M, r, w.data(), vt.data(), sigma != nullptr)) { failed = 1; return; }
-        for (int m = 0; m < (sigma ? d : r); ++m) sig[m] = std::sqrt(std::max(w[m], 0.0));
-        // all r columns at once (d x r, row-major): P = L V', X = L^-T V'
-        Mat V((size_t)d * r), P((size_t)d * r, 0.0), X((size_t)d * r);
-        for (int m = 0; m < r; ++m)
-          for (int i = 0; i < d; ++i) V[(size_t)i * r + m] = vt[(size_t)m * d + i];
-        for (int i = 0; i < d; ++i)
-          for (int j = 0; j <= i; ++j) axpy(L[(size_t)i * d + j], V.data() + (size_t)j * r, P.data() + (size_t)i * r, r);
-        for (int i = d - 1; i >= 0; --i) {  // L^T X = V by back substitution, row i of L at a time
-          double* xi = X.data() + (size_t)i * r;
-          const double rl = 1.0 / L[(size_t)i * d + i];
-          for (int m = 0; m < r; ++m) xi[m] = V[(size_t)i * r + m] * rl;
-          for (int j = 0; j < i; ++j) axpy(-L[(size_t)i * d + j], xi, V.data() + (size_t)j * r, r);
+        congruence_lower(d, sq, st.L.data(), M);
+        Reduced& rd = red[task];
+        rd.diag.resize(d);
+        rd.off.resize(d);
+        rd.beta.resize(d);
+        if (!tridiag_of(d, M, rd.diag.data(), rd.off.data(), hv_all.data() + (size_t)task * dd,
+                        rd.beta.data())) {
+          failed = 1;
+          return;
         }
-        for (int m = 0; m < r; ++m) {
-          const double sm = sig[m], rs = std::sqrt(sm);
-          for (int i = 0; i < d; ++i) {
-            bqc[i] = sm > 0.0 ? P[(size_t)i * r + m] / rs : 0.0;
-            bkc[i] = X[(size_t)i * r + m] * rs;
-          }
-          store_pair(d, r, m, bqc.data(), bkc.data(), bq, bk);
-        }
-        if (sigma)
-          for (int m = 0; m < d; ++m) sigma[(size_t)h * d + m] = sig[m];
-        if (n_clamped) { n_clamped[2 * h] = 0; n_clamped[2 * h + 1] = 0; }
+        rd.pending = true;
         return;
       }
       // ---- symmetric route: clamped roots of both moments
