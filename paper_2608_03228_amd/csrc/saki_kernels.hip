@@ -1472,10 +1472,52 @@ __device__ __forceinline__ double lane_dot_f64_g(const void* keys, size_t key_ro
   return acc;
 }
 
-constexpr int kGateCollect = 256;           // keys collected per row
-constexpr int kGateRow = kGateCollect + 1;  // padded LDS row stride
-constexpr int kBatch = 256;                 // keys rescored per wave and batch
-constexpr int kGateWaves = 4;               // waves per 16-row work-group
+constexpr int kGateCap = 64;            // keys one wave collects per row
+constexpr int kGateRow = kGateCap + 1;  // row stride; slot kGateCap absorbs overflow writes
+constexpr int kBatch = 160;             // keys rescored per wave and batch
+constexpr int kGateWaves = 4;           // waves per 16-row work-group
+
+// Float64 partial q.k over dims 32p .. 32p+31 of one key: the four lanes of
+// a quad (p = lane & 3) share a key, and quad_sum_f64 completes the sum.
+// Every load of the lane is issued before its products.
+template <bool KBF>
+__device__ __forceinline__ double quad_dot_f64(const void* keys, size_t key_row,
+                                               const float* __restrict__ qr, int p) {
+  constexpr int D = saki::kHeadDim;
+  float f[32], qv[32];
+  if constexpr (KBF) {
+    const uint4* kr = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(keys) +
+                                                     key_row * D + 32 * p);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) unpack_piece<true>(kr[u], f + 8 * u);
+  } else {
+    const float4* kr = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(keys) +
+                                                       key_row * D + 32 * p);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float4 v = kr[u];
+      f[4 * u] = v.x; f[4 * u + 1] = v.y; f[4 * u + 2] = v.z; f[4 * u + 3] = v.w;
+    }
+  }
+  const float4* q4 = reinterpret_cast<const float4*>(qr + 32 * p);
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const float4 v = q4[u];
+    qv[4 * u] = v.x; qv[4 * u + 1] = v.y; qv[4 * u + 2] = v.z; qv[4 * u + 3] = v.w;
+  }
+  double a0 = 0.0, a1 = 0.0;
+#pragma unroll
+  for (int e = 0; e < 32; e += 2) {
+    a0 = fma((double)qv[e], (double)f[e], a0);
+    a1 = fma((double)qv[e + 1], (double)f[e + 1], a1);
+  }
+  return a0 + a1;
+}
+// The sum over the four lanes of a quad; every lane gets the same bits.
+__device__ __forceinline__ double quad_sum_f64(double v) {
+  v += __longlong_as_double((long long)xor_shfl_u64((uint64_t)__double_as_longlong(v), 1));
+  return v + __longlong_as_double((long long)xor_shfl_u64((uint64_t)__double_as_longlong(v), 2));
+}
 
 // Exact top-k and recall hits in one scan.  A row's candidate list S (k
 // distinct visible keys) gives the gate tau = min over S of a float32 lower
@@ -1493,13 +1535,15 @@ constexpr int kGateWaves = 4;               // waves per 16-row work-group
 //
 // A work-group of four waves owns 16 rows: the waves take four rows each for
 // the gate and the final count, and every fourth key tile of the scan (all
-// 16 rows, shared collection lists), so that the latency of the per-row work
-// is spread over four times as many waves.  A work-group that collects more
-// than 256 keys for a row is flagged for exact_bf16_kernel.  grid: 1-D xcd
-// grid of ceil(Q / 16) * n_chunks * B * H_q work-groups; the flags use the
-// numbering of the two-wave tiers.
+// 16 rows, one collection list per wave and row, filled without atomics: the
+// four lanes of a row append at offsets from a prefix of their counts), so
+// that the latency of the per-row work is spread over four times as many
+// waves.  A work-group in which one wave collects more than 64 keys for a
+// row, or a row has more than 160 others, is flagged for exact_bf16_kernel.
+// grid: 1-D xcd grid of ceil(Q / 16) * n_chunks * B * H_q work-groups; the
+// flags use the numbering of the two-wave tiers.
 template <bool KBF>
-__global__ __launch_bounds__(kGateWaves * kWave) void exact_gate_kernel(
+__global__ __launch_bounds__(kGateWaves * kWave) __attribute__((amdgpu_waves_per_eu(4))) void exact_gate_kernel(
     const void* __restrict__ keys, const uint8_t* __restrict__ khi,
     const uint8_t* __restrict__ klo, const float* __restrict__ knorm, const float* __restrict__ q,
     const int* __restrict__ q_pos, int H_q, int H_kv, int N_cap, int N_valid, int Q,
@@ -1509,12 +1553,13 @@ __global__ __launch_bounds__(kGateWaves * kWave) void exact_gate_kernel(
   constexpr int D = saki::kHeadDim;
   constexpr size_t TB = (size_t)kTile * D * 2;
   using KD = KeysF64;
-  __shared__ int cj[kMR * kGateRow];     // collected keys
+  __shared__ int cj[kGateWaves][kMR * kGateRow];  // keys collected by each scanning wave
   __shared__ uint32_t sl[kMR * kWave];   // candidate lists, sorted descending
-  __shared__ float ss[kMR * kWave];      // float32 score of list entry a
+  __shared__ float ss[kMR * kWave];      // float32 score of sorted entry a
+  __shared__ float se[kMR * kWave];      // and its error radius
   __shared__ float tau_s[kMR];           // gates
   __shared__ int bad_s[kMR];             // invalid lists
-  __shared__ int ccount[kMR];
+  __shared__ int ccount[kGateWaves][kMR];
   __shared__ int wg_fallback;
   __shared__ int bj_m[kGateWaves][kBatch];  // per wave: others' key, exact score, row, S-count
   __shared__ double bsc_m[kGateWaves][kBatch];
@@ -1551,37 +1596,30 @@ __global__ __launch_bounds__(kGateWaves * kWave) void exact_gate_kernel(
   int* bcnt = bcnt_m[wave];
   int* boff = boff_m[wave];
 
-  // query: bf16 hi/lo operands (dims 32kk + 8g .. +7) and norm bound
-  bf16x8_t qh[4], ql[4];
+  // query norm bound (lanes of row qi, dims 32kk + 8g .. +7); the MFMA
+  // operands are formed after the gate
+  const float* qrow = q + (bh * Q + (row_ok ? my_row : row0)) * D;  // a valid row
   float qn;
   {
-    const float* qr = q + (bh * Q + (row_ok ? my_row : row0)) * D;
     float sq = 0.f;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      float fh[8], fl[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float f = row_ok ? qr[32 * kk + 8 * g + e] : 0.f;
-        sq = fmaf(f, f, sq);
-        fh[e] = bf16_round(f);
-        fl[e] = bf16_round(f - fh[e]);
-      }
-      qh[kk] = as_bf16x8(pack_bf16x8(fh));
-      ql[kk] = as_bf16x8(pack_bf16x8(fl));
+      const float4 v0 = *reinterpret_cast<const float4*>(qrow + 32 * kk + 8 * g);
+      const float4 v1 = *reinterpret_cast<const float4*>(qrow + 32 * kk + 8 * g + 4);
+      sq = fmaf(v0.x, v0.x, sq); sq = fmaf(v0.y, v0.y, sq); sq = fmaf(v0.z, v0.z, sq); sq = fmaf(v0.w, v0.w, sq);
+      sq = fmaf(v1.x, v1.x, sq); sq = fmaf(v1.y, v1.y, sq); sq = fmaf(v1.z, v1.z, sq); sq = fmaf(v1.w, v1.w, sq);
     }
-    qn = sqrtf(sum_lane_groups(sq)) * (1.f + 1e-5f);
+    qn = row_ok ? sqrtf(sum_lane_groups(sq)) * (1.f + 1e-5f) : 0.f;
   }
   const float eq = kExactEps3 * qn;
   if (threadIdx.x < kMR) {
-    ccount[threadIdx.x] = 0;
     tau_s[threadIdx.x] = -INFINITY;
     bad_s[threadIdx.x] = 1;
   }
   if (threadIdx.x == 0) wg_fallback = 0;
   __syncthreads();
 
-  // ---- gate of rows wave, wave + 4, ... from their candidate lists
+  // ---- gate, part 1: sort and check the candidate lists of rows wave, wave + 4, ...
   for (int r = wave; r < n_rows; r += kGateWaves) {
     const size_t row = bh * Q + row0 + r;
     const int lim_r = __builtin_amdgcn_readlane(my_lim, r);
@@ -1592,96 +1630,191 @@ __global__ __launch_bounds__(kGateWaves * kWave) void exact_gate_kernel(
     const uint32_t nxt = (uint32_t)__shfl_down((int)key, 1, kWave);
     bad |= lane < kWave - 1 && key == nxt;
     sl[r * kWave + lane] = key;
-    if (__ballot(bad) != 0) continue;  // tau stays -inf: collect every key
-    // float32 scores, 8 lanes per entry (dims 16p .. 16p+15), 8 entries per
-    // step; each sum is at most 12 roundings deep: error <= gamma_12 ||q|| ||k||
+    if (lane == 0) bad_s[r] = __ballot(bad) != 0;  // an invalid list keeps tau = -inf
+  }
+  wave_lds_sync();
+
+  // ---- gate, part 2: tau = min over the list of a float32 lower bound of q.k.
+  //      One flat loop over (row, step): a step scores 8 sorted entries, 8
+  //      lanes per entry (dims 16p .. 16p+15), so each sum is at most 12
+  //      roundings deep (error <= gamma_12 ||q|| ||k||).  The key slice, the
+  //      query slice and the key norm of step u + 1 are loaded while step u
+  //      is computed; pads (k < 64) and the entries of invalid lists read key
+  //      0 and are ignored.
+  {
     const int p = lane & 7, slot = lane >> 3;
-    const float* qr = q + row * D + 16 * p;
-    float qv[16];
+    const int my_rows_g = n_rows > wave ? (n_rows - wave + kGateWaves - 1) / kGateWaves : 0;
+    const int n_steps = my_rows_g * 8;
+    struct Step {
+      float f[16], knv;
+    };
+    auto step_key = [&](int u, bool& use) -> int {
+      const int r = wave + kGateWaves * (u >> 3);
+      const uint32_t kj = sl[r * kWave + ((u & 7) << 3) + slot];
+      use = (kj >> 31) == 0 && bad_s[r] == 0;
+      return use ? (int)kj : 0;
+    };
+    auto load_step = [&](Step& st, int u) {
+      bool use;
+      const int j = step_key(u, use);
+      if constexpr (KBF) {
+        const uint16_t* kr = reinterpret_cast<const uint16_t*>(keys) + (kbase + j) * D + 16 * p;
+        unpack_piece<true>(*reinterpret_cast<const uint4*>(kr), st.f);
+        unpack_piece<true>(*reinterpret_cast<const uint4*>(kr + 8), st.f + 8);
+      } else {
+        const float4* kr = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(keys) +
+                                                           (kbase + j) * D + 16 * p);
 #pragma unroll
-    for (int e4 = 0; e4 < 4; ++e4) {
-      const float4 v = *reinterpret_cast<const float4*>(qr + 4 * e4);
-      qv[4 * e4] = v.x; qv[4 * e4 + 1] = v.y; qv[4 * e4 + 2] = v.z; qv[4 * e4 + 3] = v.w;
-    }
-    const float qn_r = readlane_s(qn, r);
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const float4 v = kr[e4];
+          st.f[4 * e4] = v.x; st.f[4 * e4 + 1] = v.y; st.f[4 * e4 + 2] = v.z; st.f[4 * e4 + 3] = v.w;
+        }
+      }
+      st.knv = kn[j];
+    };
+    // the query slice of the wave's row rr (dims 16p .. 16p+15)
+    auto load_q = [&](float* qv, int rr) {
+      const float4* qr = reinterpret_cast<const float4*>(
+          q + (bh * Q + row0 + wave + kGateWaves * rr) * D + 16 * p);
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const float4 v = qr[e4];
+        qv[4 * e4] = v.x; qv[4 * e4 + 1] = v.y; qv[4 * e4 + 2] = v.z; qv[4 * e4 + 3] = v.w;
+      }
+    };
     float lo = INFINITY;
-#pragma unroll 2
-    for (int a0 = 0; a0 < k; a0 += 8) {
-      const int a = a0 + slot;
-      const int j = __shfl(aj, a < k ? a : 0, kWave);
+    float qcur[16], qnext[16];
+    auto compute_step = [&](const Step& st, int u) {
+      bool use;
+      (void)step_key(u, use);
+      const int r = wave + kGateWaves * (u >> 3), a = ((u & 7) << 3) + slot;
       float s0 = 0.f, s1 = 0.f;
-      if (a < k) {
-        float f[16];
-        if constexpr (KBF) {
-          const uint16_t* kr = reinterpret_cast<const uint16_t*>(keys) + (kbase + j) * D + 16 * p;
-          unpack_piece<true>(*reinterpret_cast<const uint4*>(kr), f);
-          unpack_piece<true>(*reinterpret_cast<const uint4*>(kr + 8), f + 8);
-        } else {
-          const float4* kr = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(keys) +
-                                                             (kbase + j) * D + 16 * p);
 #pragma unroll
-          for (int e4 = 0; e4 < 4; ++e4) {
-            const float4 v = kr[e4];
-            f[4 * e4] = v.x; f[4 * e4 + 1] = v.y; f[4 * e4 + 2] = v.z; f[4 * e4 + 3] = v.w;
-          }
-        }
-#pragma unroll
-        for (int e = 0; e < 16; e += 2) {
-          s0 = fmaf(qv[e], f[e], s0);
-          s1 = fmaf(qv[e + 1], f[e + 1], s1);
-        }
+      for (int e = 0; e < 16; e += 2) {
+        s0 = fmaf(qcur[e], st.f[e], s0);
+        s1 = fmaf(qcur[e + 1], st.f[e + 1], s1);
       }
       float sc = s0 + s1;
       sc += xor_shfl_f32(sc, 1);
       sc += xor_shfl_f32(sc, 2);
       sc += xor_shfl_f32(sc, 4);
-      if (a < k) {
-        if (p == 0) ss[r * kWave + a] = sc;
-        lo = fminf(lo, sc - kTauEps * qn_r * kn[j]);
+      const float ea = kTauEps * readlane_s(qn, r) * st.knv;
+      if (use && p == 0) {
+        ss[r * kWave + a] = sc;
+        se[r * kWave + a] = ea;
       }
+      lo = fminf(lo, use ? sc - ea : INFINITY);
+      if ((u & 7) == 7) {  // the row's last step: its gate, and the next row's query
+        lo = wave_min_f32(lo);
+        if (lane == 0 && bad_s[r] == 0) tau_s[r] = lo;
+        lo = INFINITY;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) qcur[e] = qnext[e];
+        const int rr = (u >> 3) + 2;
+        if (rr < my_rows_g) load_q(qnext, rr);
+      }
+    };
+    Step sa, sb;
+    if (n_steps > 0) {
+      load_q(qcur, 0);
+      if (my_rows_g > 1) load_q(qnext, 1);
+      load_step(sa, 0);
     }
-    lo = wave_min_f32(lo);
-    if (lane == 0) {
-      tau_s[r] = lo;
-      bad_s[r] = 0;
+    for (int u = 0; u < n_steps; u += 2) {  // n_steps is a multiple of 8
+      load_step(sb, u + 1);
+      compute_step(sa, u);
+      load_step(sa, u + 2 < n_steps ? u + 2 : u + 1);
+      compute_step(sb, u + 1);
     }
   }
   __syncthreads();
 
-  // ---- scan (every fourth tile): collect the keys whose upper bound reaches the gate
+  // query MFMA operands: bf16 hi/lo split of dims 32kk + 8g .. +7
+  bf16x8_t qh[4], ql[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    const float4 v0 = *reinterpret_cast<const float4*>(qrow + 32 * kk + 8 * g);
+    const float4 v1 = *reinterpret_cast<const float4*>(qrow + 32 * kk + 8 * g + 4);
+    const float fv[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+    float fh[8], fl[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float f = row_ok ? fv[e] : 0.f;
+      fh[e] = bf16_round(f);
+      fl[e] = bf16_round(f - fh[e]);
+    }
+    qh[kk] = as_bf16x8(pack_bf16x8(fh));
+    ql[kk] = as_bf16x8(pack_bf16x8(fl));
+  }
+
+  // ---- scan (every fourth tile): collect the keys whose upper bound reaches
+  //      the gate into this wave's lists; the four lanes of a row (lane
+  //      groups g) append at offsets from a prefix of their counts
+  int base = 0;  // this wave's entries for row qi so far (same in the row's four lanes)
   {
     const float my_tau = tau_s[qi];
-    for (int t0 = kbeg + wave * kTile; t0 < kend; t0 += kGateWaves * kTile) {
-      const size_t to = hoff + (size_t)(t0 / kTile) * TB;
+    int* my_list = cj[wave] + qi * kGateRow;
+    // a tile is 16 steps (sub-tile s, k-slice kk): each step's hi and lo
+    // pieces come from a four-slot ring, refilled right after use with the
+    // step four ahead (past the last tile: a repeat of a valid address)
+    uint4 rh[4], rl[4];
+    auto load_step = [&](int slot, int t0, int i) {
+      const size_t o = hoff + (size_t)(t0 / kTile) * TB + (size_t)(4 * (i & 3) + g) * kTile * 16 +
+                       (size_t)(16 * (i >> 2) + qi) * 16;
+      rh[slot] = *reinterpret_cast<const uint4*>(khi + o);
+      rl[slot] = *reinterpret_cast<const uint4*>(klo + o);
+    };
+    const int t_first = kbeg + wave * kTile;
+    if (t_first < kend) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) load_step(i, t_first, i);
+    }
+    for (int t0 = t_first; t0 < kend; t0 += kGateWaves * kTile) {
+      const int tn = t0 + kGateWaves * kTile < kend ? t0 + kGateWaves * kTile : t0;
+      uint32_t take = 0;
 #pragma unroll
       for (int sub = 0; sub < 4; ++sub) {
-        const int key = 16 * sub + qi;
+        const int kb = t0 + 16 * sub + 4 * g;
+        const float4 nv = *reinterpret_cast<const float4*>(kn + kb);  // kb < n_tiles_hi * 64
         f32x4_t a = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-          const size_t o = to + (size_t)(4 * kk + g) * kTile * 16 + (size_t)key * 16;
-          const bf16x8_t kh = as_bf16x8(*reinterpret_cast<const uint4*>(khi + o));
-          const bf16x8_t kl = as_bf16x8(*reinterpret_cast<const uint4*>(klo + o));
+          const int i = 4 * sub + kk;
+          const bf16x8_t kh = as_bf16x8(rh[kk]), kl = as_bf16x8(rl[kk]);
           a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, qh[kk], a, 0, 0, 0);
           a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kl, qh[kk], a, 0, 0, 0);
           a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, ql[kk], a, 0, 0, 0);
+          if (i + 4 < 16)
+            load_step(kk, t0, i + 4);
+          else
+            load_step(kk, tn, i - 12);
         }
-        const int kb = t0 + 16 * sub + 4 * g;
-        const float4 nv = *reinterpret_cast<const float4*>(kn + kb);  // kb < n_tiles_hi * 64
         const float nvs[4] = {nv.x, nv.y, nv.z, nv.w};
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int j = kb + v;
-          if (j < my_lim && fmaf(eq, nvs[v], a[v]) >= my_tau) {
-            const int pos = atomicAdd(&ccount[qi], 1);
-            if (pos < kGateCollect) cj[qi * kGateRow + pos] = j;
-          }
-        }
+        for (int v = 0; v < 4; ++v)
+          take |= (kb + v < my_lim && fmaf(eq, nvs[v], a[v]) >= my_tau) ? (1u << (4 * sub + v)) : 0u;
       }
+      if (__ballot(take != 0) == 0) continue;
+      const int c = __popc(take);
+      const int c1 = (int)xor_shfl_u32((uint32_t)c, 16);   // count of lane group g ^ 1
+      const int c2 = (int)xor_shfl_u32((uint32_t)c, 32);   // g ^ 2
+      const int c3 = (int)xor_shfl_u32((uint32_t)c1, 32);  // g ^ 3
+      // entries of the groups below g: g=1: g^1; g=2: g^2, g^3; g=3: g^3, g^2, g^1
+      int pos = base + (g == 1 ? c1 : g == 2 ? c2 + c3 : g == 3 ? c1 + c2 + c3 : 0);
+      base += c + c1 + c2 + c3;
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          if (take & (1u << (4 * sub + v))) {
+            my_list[min(pos, kGateCap)] = t0 + 16 * sub + 4 * g + v;
+            ++pos;
+          }
     }
   }
+  if (lane < kMR) ccount[wave][lane] = base;  // lane r < 16 holds row r
   __syncthreads();
-  bool fallback = __ballot(lane < kMR && ccount[lane % kMR] > kGateCollect) != 0;
+  bool fallback = __ballot(ccount[lane / kMR][lane % kMR] > kGateCap) != 0;
 
   // ---- rows wave, wave + 4, ...: the others C \ S, rescored in batches of whole rows
   int r_done = 0;  // of this wave's rows
@@ -1690,48 +1823,54 @@ __global__ __launch_bounds__(kGateWaves * kWave) void exact_gate_kernel(
     int nb = 0, r_end = r_done;
     for (; r_end < my_rows; ++r_end) {
       const int r = wave + kGateWaves * r_end;
-      const int c = ccount[r];
       const bool rbad = bad_s[r] != 0;
       // others of this row: all of C for an invalid list, else C minus S
       int n_oth = 0, n_in_s = 0;
-      for (int base = 0; base < c; base += kWave) {
-        const int e = base + lane;
-        const int j = e < c ? cj[r * kGateRow + e] : -1;
-        const bool is_s = e < c && !rbad && in_sorted_desc(sl + r * kWave, j);
-        n_in_s += __popcll(__ballot(is_s));
-        n_oth += __popcll(__ballot(e < c && !is_s));
+      for (int w = 0; w < kGateWaves; ++w) {
+        const int c = ccount[w][r];
+        for (int base = 0; base < c; base += kWave) {
+          const int e = base + lane;
+          const int j = e < c ? cj[w][r * kGateRow + e] : -1;
+          const bool is_s = e < c && !rbad && in_sorted_desc(sl + r * kWave, j);
+          n_in_s += __popcll(__ballot(is_s));
+          n_oth += __popcll(__ballot(e < c && !is_s));
+        }
       }
       // every key of a valid list passes the gate (a failed check means a bound
-      // did not hold: hand the rows over rather than trust the result)
-      if (!rbad && n_chunks == 1 && n_in_s != k) {
+      // did not hold: hand the rows over rather than trust the result); a row
+      // whose others do not fit one batch is handed over as well
+      if ((!rbad && n_chunks == 1 && n_in_s != k) || n_oth > kBatch) {
         fallback = true;
         break;
       }
       if (nb + n_oth > kBatch) break;  // this row starts the next batch
       if (lane == 0) boff[r_end - r_done] = nb;
-      for (int base = 0; base < c; base += kWave) {
-        const int e = base + lane;
-        const int j = e < c ? cj[r * kGateRow + e] : -1;
-        const bool other = e < c && (rbad || !in_sorted_desc(sl + r * kWave, j));
-        const uint64_t m = __ballot(other);
-        if (other) {
-          bj[nb + prefix_count(m)] = j;
-          brow[nb + prefix_count(m)] = (unsigned char)r;
+      for (int w = 0; w < kGateWaves; ++w) {
+        const int c = ccount[w][r];
+        for (int base = 0; base < c; base += kWave) {
+          const int e = base + lane;
+          const int j = e < c ? cj[w][r * kGateRow + e] : -1;
+          const bool other = e < c && (rbad || !in_sorted_desc(sl + r * kWave, j));
+          const uint64_t m = __ballot(other);
+          if (other) {
+            bj[nb + prefix_count(m)] = j;
+            brow[nb + prefix_count(m)] = (unsigned char)r;
+          }
+          nb += __popcll(m);
         }
-        nb += __popcll(m);
       }
       if (lane == 0) boff[r_end - r_done + 1] = nb;
     }
     if (fallback) break;
     wave_lds_sync();
 
-    // exact scores of the batch, one key per lane
-    for (int base = 0; base < nb; base += kWave) {
-      const int e = base + lane;
-      if (e < nb) {
-        const size_t row = bh * Q + row0 + brow[e];
-        bsc[e] = lane_dot_f64_g<KBF>(keys, kbase + bj[e], q + row * D);
-      }
+    // exact scores of the batch: four lanes per key, 16 keys per pass
+    for (int base = 0; base < nb; base += kWave / 4) {
+      const int e = base + lane / 4;
+      const int ec = e < nb ? e : nb - 1;  // idle quads repeat the last key
+      const size_t row = bh * Q + row0 + brow[ec];
+      const double sx = quad_sum_f64(quad_dot_f64<KBF>(keys, kbase + bj[ec], q + row * D, lane & 3));
+      if (e < nb && (lane & 3) == 0) bsc[e] = sx;
     }
     wave_lds_sync();
 
@@ -1742,10 +1881,13 @@ __global__ __launch_bounds__(kGateWaves * kWave) void exact_gate_kernel(
       const float* qr = q + row * D;
       const bool rbad = bad_s[r] != 0;
       const int o0 = boff[rr - r_done], o1 = boff[rr - r_done + 1];
-      const int aj = lane < k ? approx[row * k + lane] : -1;
+      // lane a: sorted list entry a (pads, k < 64, have the top bit set)
+      const uint32_t kj = sl[r * kWave + lane];
+      const bool real = (kj >> 31) == 0;
+      const int aj = real ? (int)kj : -1;
       if (ordered) {
         KeyF64 xs = KD::pad();
-        if (!rbad && lane < k && aj >= kbeg && aj < kend)
+        if (!rbad && real && aj >= kbeg && aj < kend)
           xs = KD::make(lane_dot_f64_g<KBF>(keys, kbase + aj, qr), aj);
         wave_sort<KD>(xs);
         for (int base = o0; base < o1; base += kWave) {
@@ -1758,14 +1900,14 @@ __global__ __launch_bounds__(kGateWaves * kWave) void exact_gate_kernel(
       }
       // how many keys of S beat each other o (S's float32 intervals)
       if (!rbad) {
-        const float sa = lane < k ? ss[r * kWave + lane] : 0.f;
-        const float ea = lane < k ? kTauEps * readlane_s(qn, r) * kn[aj] : 0.f;
+        const float sa = real ? ss[r * kWave + lane] : 0.f;
+        const float ea = real ? se[r * kWave + lane] : 0.f;
         const double lo_a = (double)sa - (double)ea, hi_a = (double)sa + (double)ea;
         for (int o = o0; o < o1; ++o) {
           const double so = bsc[o];
           const int jo = bj[o];
-          bool beat = lane < k && lo_a > so;
-          const bool amb = lane < k && !beat && hi_a >= so;
+          bool beat = real && lo_a > so;
+          const bool amb = real && !beat && hi_a >= so;
           if (__ballot(amb) != 0 && amb) {
             const double sx = lane_dot_f64_g<KBF>(keys, kbase + aj, qr);
             beat = sx > so || (sx == so && aj < jo);
