@@ -22,7 +22,7 @@ import numpy as np
 
 __all__ = [
     "second_moments", "clamped_roots", "saki_calibrate", "saki_calibrate_shared",
-    "key_pca_factors",
+    "key_pca_factors", "sap_factors",
     "weight_svd_factors", "score_loss", "codes", "query_sketch", "sketch_scores",
     "direct_scores", "exact_scores", "candidate_limits", "topk_row", "topk_rows",
     "recall_hits", "bf16_round", "f32_round", "score_scale", "predicted_reduction",
@@ -153,6 +153,40 @@ def key_pca_factors(Sigma_k: np.ndarray, r: int) -> np.ndarray:
     w, V = np.linalg.eigh(0.5 * (Sigma_k + Sigma_k.T))
     order = np.argsort(-w, kind="stable")
     return V[:, order[:r]]
+
+
+def _signed_columns(Q: np.ndarray) -> np.ndarray:
+    """Flip each column so that its largest-|.| entry is positive (first
+    index on ties)."""
+    Q = Q.copy()
+    for i in range(Q.shape[1]):
+        j = int(np.argmax(np.abs(Q[:, i])))
+        if Q[j, i] < 0:
+            Q[:, i] = -Q[:, i]
+    return Q
+
+
+def sap_factors(cal: dict, r: int, kind: str) -> np.ndarray:
+    """Span-projector variants of Sec. 6, as the orthonormal basis Q [d, r] of
+    an orthogonal projector P = Q Q^T used with B_q = B_k = Q.
+
+    cal is the output of saki_calibrate (its right singular vectors v_i of
+    C = Sigma_q^{1/2} Sigma_k^{1/2} and the root Sigma_k^{1/2}).
+    kind "svd" (SAP-svd, the raw right-singular span): span{v_1 .. v_r}.
+    kind "map" (SAP-map, the Sigma_k^{1/2}-weighted span, orthonormalised):
+    span{Sigma_k^{1/2} v_1 .. Sigma_k^{1/2} v_r}, which is the range of M_r,
+    orthonormalised by Gram-Schmidt in the order of the singular values (a
+    QR factorisation).  Reading: the paper names both in one line; the basis
+    is fixed by signing each column so that its largest-|.| entry is positive,
+    and the scores do not depend on the basis, only on P."""
+    V = cal["V"][:, :r]
+    if kind == "svd":
+        Q = V
+    elif kind == "map":
+        Q, _ = np.linalg.qr(cal["Sk_half"] @ V)
+    else:
+        raise ValueError(kind)
+    return _signed_columns(Q)
 
 
 def weight_svd_factors(W_K: np.ndarray, r: int) -> np.ndarray:

@@ -325,3 +325,76 @@ def test_shared_map_special_cases():
     np.testing.assert_allclose(O.saki_calibrate_shared(q[None], k, r)["M"], own["M"], atol=1e-12)
     np.testing.assert_allclose(O.saki_calibrate_shared(np.stack([q, q, q]), k, r)["M"], own["M"],
                                atol=1e-12)
+
+
+def _projector(Q):
+    return Q @ Q.T
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_sap_variants_are_the_stated_projectors(seed):
+    """SAP-map and SAP-svd (Sec. 6) are rank-r orthogonal projectors: SAP-map
+    onto the range of M_r (found here from an SVD of M_r itself), SAP-svd the
+    rank-r orthogonal projector that keeps the most of C (Ky Fan: ||C P||_F^2
+    reaches the sum of the r largest squared singular values, and random
+    rank-r projectors stay below it).  Neither beats Proposition 1's optimum."""
+    rng = np.random.default_rng(seed)
+    d, r = 16, 4
+    cal = _calib_from_moments(_spd(rng, d, 1e2), _spd(rng, d, 1e2), r)
+    Lopt = O.score_loss(cal["M"], cal["Sq_half"], cal["Sk_half"])
+    for kind in ("map", "svd"):
+        Q = O.sap_factors(cal, r, kind)
+        P = _projector(Q)
+        np.testing.assert_allclose(Q.T @ Q, np.eye(r), atol=1e-12)
+        np.testing.assert_allclose(P, P.T, atol=1e-12)
+        np.testing.assert_allclose(P @ P, P, atol=1e-12)
+        assert abs(np.trace(P) - r) < 1e-10
+        assert Lopt <= O.score_loss(P, cal["Sq_half"], cal["Sk_half"]) + 1e-12
+    Um, _, _ = np.linalg.svd(cal["M"])
+    np.testing.assert_allclose(_projector(O.sap_factors(cal, r, "map")),
+                               _projector(Um[:, :r]), atol=1e-9)
+    C = cal["Sq_half"] @ cal["Sk_half"]
+    sig = np.linalg.svd(C, compute_uv=False)
+    kept = np.sum((C @ _projector(O.sap_factors(cal, r, "svd"))) ** 2)
+    assert abs(kept - np.sum(sig[:r] ** 2)) <= 1e-10 * np.sum(sig ** 2)
+    for _ in range(300):
+        Qr, _ = np.linalg.qr(rng.standard_normal((d, r)))
+        assert np.sum((C @ _projector(Qr)) ** 2) <= kept + 1e-10
+
+
+def test_sap_variants_special_cases():
+    """Sigma_q = I: both spans are the top-r key eigenvectors (key PCA);
+    Sigma_k = I: both are query PCA; r = d: the identity."""
+    rng = np.random.default_rng(5)
+    d, r = 12, 5
+    Sk = _spd(rng, d, 50.0)
+    cal = _calib_from_moments(np.eye(d), Sk, r)
+    w, V = np.linalg.eigh(Sk)
+    Pk = _projector(V[:, np.argsort(-w)[:r]])
+    for kind in ("map", "svd"):
+        np.testing.assert_allclose(_projector(O.sap_factors(cal, r, kind)), Pk, atol=1e-10)
+    Sq = _spd(rng, d, 50.0)
+    cal = _calib_from_moments(Sq, np.eye(d), r)
+    w, U = np.linalg.eigh(Sq)
+    Pq = _projector(U[:, np.argsort(-w)[:r]])
+    for kind in ("map", "svd"):
+        np.testing.assert_allclose(_projector(O.sap_factors(cal, r, kind)), Pq, atol=1e-10)
+    cal = _calib_from_moments(_spd(rng, d), _spd(rng, d), d)
+    for kind in ("map", "svd"):
+        np.testing.assert_allclose(_projector(O.sap_factors(cal, d, kind)), np.eye(d), atol=1e-10)
+
+
+@pytest.mark.parametrize("layer", [0, 1])
+def test_sap_losses_on_the_generator(layer):
+    """On the single-head generator the exact optimum has the lowest loss
+    (Proposition 1); the order among the span variants and PCA is what Sec. 7
+    reports for real heads (weighted span < raw span, raw span close to PCA),
+    checked here only where it is a theorem."""
+    spec = W.SPECS["single_head_d128"]
+    inp = W.make_layer(spec, layer=layer)
+    cal = O.saki_calibrate(inp["q_cal"][0], inp["k_cal"][0], 32)
+    L = {"opt": O.score_loss(cal["M"], cal["Sq_half"], cal["Sk_half"])}
+    for kind in ("map", "svd"):
+        L[kind] = O.score_loss(_projector(O.sap_factors(cal, 32, kind)), cal["Sq_half"],
+                               cal["Sk_half"])
+    assert L["opt"] <= L["map"] and L["opt"] <= L["svd"]
