@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--k", type=int, default=64)
     ap.add_argument("--shared", action="store_true",
                     help="GQA-shared index: one code set per KV head (pooled query moment)")
+    ap.add_argument("--method", default="opt", choices=["opt", "sap_map", "sap_svd", "key_pca"],
+                    help="factors of the batched layer: the paper's optimum, its span "
+                         "variants (Sec. 6) or the key-PCA baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=4,
                     help="query heads of the CPU-baseline sample (one KV group)")
@@ -359,7 +362,7 @@ def main():
     def factorise(sl):
         h = m_host[sl]
         return S.saki_calibrate_from_moments(h["Sq"].numpy(), h["Sk"].numpy(), h["mu"].numpy(),
-                                             r, with_sigma=False)
+                                             r, method=args.method, with_sigma=False)
     # two pinned staging slots: the host calibrates batch i+1 while the GPU
     # still works on batch i; a slot is rewritten only after its copy finished
     slots = [{n: torch.empty(t.shape, dtype=torch.float32).pin_memory() for n, t in f_dev.items()}
@@ -467,7 +470,7 @@ def main():
         "config": {"workload": spec.name, "H_q": H_q, "H_kv": spec.H_kv, "d": spec.d,
                    "latent_D": spec.D, "N": N, "queries_per_head": spec.Q,
                    "causal": spec.causal, "r": r, "sketch": sk, "k": k, "calib_tokens": spec.T,
-                   "pairs_per_step": pairs},
+                   "factors": args.method, "pairs_per_step": pairs},
         "roofline": roof,
         "cpu_baseline": cpu,
         "stages_ms": stage_ms,

@@ -61,7 +61,9 @@ enum { SAKI_F32 = 0, SAKI_BF16 = 1 };
 enum {
   SAKI_METHOD_OPT = 0,     /* the paper's optimum M_r (Eq. 3-4), one map per query head */
   SAKI_METHOD_KEY_PCA = 1, /* baseline: P = V V^T, top-r eigenvectors of Sigma_k */
-  SAKI_METHOD_SHARED = 2   /* one map per KV group: M_r of the pooled query moment */
+  SAKI_METHOD_SHARED = 2,  /* one map per KV group: M_r of the pooled query moment */
+  SAKI_METHOD_SAP_MAP = 3, /* variant (Sec. 6): orthogonal projector on range(M_r) */
+  SAKI_METHOD_SAP_SVD = 4  /* variant (Sec. 6): orthogonal projector on span(V_r) */
 };
 
 /* Human-readable description of a status code (static storage). */
@@ -96,6 +98,14 @@ int saki_version(void);
  * With SAKI_METHOD_KEY_PCA instead B_q = B_k = the top-r eigenvectors of
  * Sigma_k (each column's largest-magnitude entry positive), sigma = eigenvalues
  * of Sigma_k, descending.
+ * The span variants of Sec. 6 give B_q = B_k = Q, an orthonormal basis of an
+ * orthogonal projector P = Q Q^T, with sigma and n_clamped as for the
+ * optimum: SAKI_METHOD_SAP_SVD takes Q = V_r, the top-r right singular
+ * vectors of C (symmetric clamped roots); SAKI_METHOD_SAP_MAP takes the
+ * Sigma_k^{1/2}-weighted span {Sigma_k^{1/2} v_i} (the range of M_r),
+ * orthonormalised by Gram-Schmidt in the order of the singular values.  Each
+ * column of Q is signed so that its largest-magnitude entry is positive;
+ * scores depend only on P.
  *
  *   q_cal      host float [H_q, T, d]   calibration queries (pre-RoPE)
  *   k_cal      host float [H_kv, T, d]  calibration keys of the same tokens

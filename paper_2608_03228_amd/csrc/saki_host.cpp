@@ -313,6 +313,39 @@ void store_pair(int d, int r, int m, const double* bq, const double* bk, float* 
   }
 }
 
+// Orthonormalise the r vectors stored as the rows of A (r x d) in place, in
+// row order, by modified Gram-Schmidt with each vector orthogonalised twice
+// against the earlier ones; then sign each vector so that its
+// largest-magnitude entry is positive (lowest index on ties).  Returns false
+// when a vector is numerically in the span of the earlier ones.
+bool orthonormal_rows(int d, int r, double* A) {
+  for (int m = 0; m < r; ++m) {
+    double* a = A + (size_t)m * d;
+    const double n0 = std::sqrt(dot(a, a, d));
+    for (int pass = 0; pass < 2; ++pass)
+      for (int p = 0; p < m; ++p) {
+        const double* b = A + (size_t)p * d;
+        axpy(-dot(b, a, d), b, a, d);
+      }
+    const double nrm = std::sqrt(dot(a, a, d));
+    if (!(nrm > 1e-12 * n0) || !std::isfinite(nrm)) return false;
+    for (int i = 0; i < d; ++i) a[i] /= nrm;
+    int jmax = 0;
+    for (int i = 1; i < d; ++i)
+      if (std::fabs(a[i]) > std::fabs(a[jmax])) jmax = i;
+    if (a[jmax] < 0)
+      for (int i = 0; i < d; ++i) a[i] = -a[i];
+  }
+  return true;
+}
+
+// B_q = B_k = Q (d x r, row-major float) from the r basis vectors (rows of Qr).
+void store_basis(int d, int r, const double* Qr, float* Bq, float* Bk) {
+  for (int m = 0; m < r; ++m)
+    for (int i = 0; i < d; ++i)
+      Bq[(size_t)i * r + m] = Bk[(size_t)i * r + m] = (float)Qr[(size_t)m * d + i];
+}
+
 // Householder reduction of symmetric `a` (n x n, lower triangle read and
 // overwritten; the upper triangle is ignored) to tridiagonal
 // form T = Q^T A Q, Q = H_0 H_1 ... H_{n-3} with H_k = I - beta_k v_k v_k^T
@@ -940,7 +973,8 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
   if (H_q <= 0 || H_kv <= 0 || H_q % H_kv != 0 || (!given && T <= 0) || d <= 0 || d > 4096 ||
       r <= 0 || r > d || !(floor_rel >= 0.0))
     return SAKI_ERR_ARG;
-  if (method != SAKI_METHOD_OPT && method != SAKI_METHOD_KEY_PCA && method != SAKI_METHOD_SHARED)
+  if (method != SAKI_METHOD_OPT && method != SAKI_METHOD_KEY_PCA && method != SAKI_METHOD_SHARED &&
+      method != SAKI_METHOD_SAP_MAP && method != SAKI_METHOD_SAP_SVD)
     return SAKI_ERR_UNSUPPORTED;
   const int G = H_q / H_kv;
   const size_t dd = (size_t)d * d;
@@ -948,7 +982,8 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
     // ---- per KV head: key mean, centred key moment, and either its Cholesky
     //      factor or its clamped symmetric roots
     std::vector<KvState> kv(H_kv);
-    const bool opt = method == SAKI_METHOD_OPT || method == SAKI_METHOD_SHARED;
+    // every method but key PCA goes through C = Sigma_q^{1/2} Sigma_k^{1/2}
+    const bool opt = method != SAKI_METHOD_KEY_PCA;
     // Sigma_q per head: the caller's moments, or computed here
     std::vector<const double*> sq_of(opt ? H_q : 0);
     std::vector<Mat> sq_own(opt && !given ? H_q : 0);
@@ -1056,6 +1091,17 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
         for (int i = 0; i < d; ++i) V[(size_t)i * r + m] = vt[(size_t)m * d + i];
       for (int i = 0; i < d; ++i)
         for (int j = 0; j <= i; ++j) axpy(L[(size_t)i * d + j], V.data() + (size_t)j * r, P.data() + (size_t)i * r, r);
+      if (method == SAKI_METHOD_SAP_MAP) {  // column m of P = L V' is Sigma_k^{1/2} v_m
+        Mat Qr((size_t)r * d);
+        for (int m = 0; m < r; ++m)
+          for (int i = 0; i < d; ++i) Qr[(size_t)m * d + i] = P[(size_t)i * r + m];
+        if (!orthonormal_rows(d, r, Qr.data())) { failed = 1; return; }
+        store_basis(d, r, Qr.data(), bq, bk);
+        if (sigma)
+          for (int m = 0; m < d; ++m) sigma[(size_t)h * d + m] = sig[m];
+        if (n_clamped) { n_clamped[2 * h] = 0; n_clamped[2 * h + 1] = 0; }
+        return;
+      }
       for (int i = d - 1; i >= 0; --i) {  // L^T X = V by back substitution, row i of L at a time
         double* xi = X.data() + (size_t)i * r;
         const double rl = 1.0 / L[(size_t)i * d + i];
@@ -1127,7 +1173,9 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
       if (!sq) { failed = 1; return; }
       if (given && !all_finite(sq, dd)) { failed = 1; return; }
       std::vector<double> sig(d), bqc(d), bkc(d);
-      if (st.chol && unclamped_cholesky(d, sq, floor_rel, thread_buffer(0, dd), false)) {
+      // (SAP-svd needs the singular vectors of C with symmetric roots)
+      if (st.chol && method != SAKI_METHOD_SAP_SVD &&
+          unclamped_cholesky(d, sq, floor_rel, thread_buffer(0, dd), false)) {
         // ---- Cholesky route: M = L^T Sigma_q L, reduced to tridiagonal form here;
         //      the eigenpairs and columns are the head's second task
         double* M = thread_buffer(1, dd);
@@ -1174,6 +1222,21 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
       if (sigma)
         for (int m = 0; m < d; ++m) sigma[(size_t)h * d + m] = sig[m];
       if (n_clamped) { n_clamped[2 * h] = nq; n_clamped[2 * h + 1] = nk; }
+      if (method == SAKI_METHOD_SAP_SVD || method == SAKI_METHOD_SAP_MAP) {
+        Mat Qr((size_t)r * d);
+        for (int m = 0; m < r; ++m) {
+          const double* v = vt.data() + (size_t)m * d;
+          double* qm = Qr.data() + (size_t)m * d;
+          if (method == SAKI_METHOD_SAP_SVD) {
+            std::copy(v, v + d, qm);
+          } else {  // Sigma_k^{1/2} v_m
+            for (int i = 0; i < d; ++i) qm[i] = dot(khalf + (size_t)i * d, v, d);
+          }
+        }
+        if (!orthonormal_rows(d, r, Qr.data())) { failed = 1; return; }
+        store_basis(d, r, Qr.data(), bq, bk);
+        return;
+      }
       // top-r pairs: v_m (row of vt), u_m = C v_m / sigma_m
       std::vector<double> u(d);
       for (int m = 0; m < r; ++m) {

@@ -18,9 +18,10 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsaki.so
 _lib = None
 
 F32, BF16 = 0, 1
-METHOD_OPT, METHOD_KEY_PCA, METHOD_SHARED = 0, 1, 2
+METHOD_OPT, METHOD_KEY_PCA, METHOD_SHARED, METHOD_SAP_MAP, METHOD_SAP_SVD = 0, 1, 2, 3, 4
 _DTYPES = {"f32": F32, "bf16": BF16}
-_METHODS = {"opt": METHOD_OPT, "key_pca": METHOD_KEY_PCA, "shared": METHOD_SHARED}
+_METHODS = {"opt": METHOD_OPT, "key_pca": METHOD_KEY_PCA, "shared": METHOD_SHARED,
+            "sap_map": METHOD_SAP_MAP, "sap_svd": METHOD_SAP_SVD}
 
 
 class SakiError(RuntimeError):

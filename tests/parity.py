@@ -34,7 +34,7 @@ def _bf16_ambiguity(exact, abs_sum):
     one bf16 ulp at each element."""
     r = O.bf16_round(exact)
     mag = np.maximum(np.abs(exact), 1e-300)
-    ulp = np.exp2(np.ceil(np.log2(mag)) - 7.0)
+    ulp = np.exp2(np.floor(np.log2(mag)) - 7.0)  # bf16 spacing in [2^e, 2^(e+1)): 2^(e-7)
     dist_mid = np.abs(0.5 * ulp - np.abs(exact - r))
     amb = dist_mid <= AMBIG_REL * abs_sum + 2.0 ** -24 * mag
     return amb, ulp

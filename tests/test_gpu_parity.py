@@ -92,7 +92,7 @@ def test_codes_match_oracle():
                 assert np.max(np.abs(got - exact) / scale) < 1e-5
             else:
                 assert np.all(O.bf16_round(got) == got)  # representable in bf16
-                ulp = np.exp2(np.ceil(np.log2(np.maximum(np.abs(exact), 1e-30))) - 7)
+                ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(exact), 1e-30))) - 7)
                 assert np.all(np.abs(got - exact) <= 0.5 * ulp + 1e-5 * scale)
 
 
@@ -361,8 +361,9 @@ def test_recall_split_chunks_matches_oracle():
 
 
 def test_single_head_recall_table_saki_pca_wsvd():
-    """The single-head workload's recall@64 for SAKI, key PCA and weight SVD,
-    GPU vs oracle: identical hits on every row where the two top-64 sets agree."""
+    """The single-head workload's recall@64 for SAKI, the span variants SAP-map
+    and SAP-svd (Sec. 6), key PCA and weight SVD, GPU vs oracle: identical
+    hits on every row where the two top-64 sets agree."""
     inp = W.make_layer(W.SPECS["single_head_d128"])
     q, keys = inp["queries"][0, 0], inp["keys"][0, 0]
     lim = O.candidate_limits(256, 1024)
@@ -376,8 +377,13 @@ def test_single_head_recall_table_saki_pca_wsvd():
              "wsvd": (wq, wk, cal_pca["mu"])}
     orc_f = {"saki": (oc["B_q"], oc["B_k"], oc["mu"]), "pca": (V, V, oc["mu"]),
              "wsvd": (U, U, oc["mu"])}
+    for kind in ("map", "svd"):
+        c = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32, method="sap_" + kind)
+        lib_f["sap_" + kind] = (c["B_q"], c["B_k"], c["mu"])
+        Q = O.sap_factors(oc, 32, kind)
+        orc_f["sap_" + kind] = (Q, Q, oc["mu"])
     table = {}
-    for name in ("saki", "pca", "wsvd"):
+    for name in ("saki", "sap_map", "sap_svd", "pca", "wsvd"):
         out = gpu_pipeline(inp, 32, "f32", factors=lib_f[name])
         hits, ex = S.saki_recall(out["keys"], out["q"], torch.from_numpy(out["idx"]).to(DEV),
                                  1024)
@@ -392,6 +398,25 @@ def test_single_head_recall_table_saki_pca_wsvd():
         table[name] = (h_g.mean() / 64, h_o.mean() / 64, int((~same).sum()))
     print("recall@64 (gpu, oracle, rows with differing sets):", table)
     assert table["saki"][1] > table["pca"][1] > table["wsvd"][1]
+    assert table["saki"][1] > max(table["sap_map"][1], table["sap_svd"][1])
+
+
+@pytest.mark.parametrize("kind", ["map", "svd"])
+@pytest.mark.parametrize("sketch", ["f32", "bf16"])
+def test_sap_indexes_match_oracle(kind, sketch):
+    """SAP-map / SAP-svd factors from the host library through the GPU index
+    and scorer, against the oracle's scores with the oracle's factors."""
+    spec = W.SPECS["llama31_8b_layer"].with_(N=1000, Q=1000 - 64)
+    inp = W.make_layer(spec)
+    out = gpu_pipeline(inp, 32, sketch, method="sap_" + kind)
+    for h in (0, 13, 30):
+        g = h // 4
+        oc = O.saki_calibrate(inp["q_cal"][h], inp["k_cal"][g], 32)
+        Q = O.sap_factors(oc, 32, kind)
+        np.testing.assert_allclose(out["B_k"][h], Q, atol=1e-6)
+        mode = "f32" if sketch == "f32" else "bf16_emul"
+        n, ex, diff = check_head(inp, out, 0, h, 32, mode, factors=(Q, Q, oc["mu"]))
+        assert diff <= ex, (h, n, ex, diff)
 
 
 def test_determinism():

@@ -169,7 +169,7 @@ def test_shared_calibration_matches_oracle():
     assert S.saki_score_topk_workspace_bytes(1, 32, 4032, 4096, 32, 64, "bf16", 5) == 0
 
 
-@pytest.mark.parametrize("method", ["opt", "shared", "key_pca"])
+@pytest.mark.parametrize("method", ["opt", "shared", "key_pca", "sap_map", "sap_svd"])
 def test_calibrate_from_moments_equals_calibrate(method):
     """saki_calibrate_from_moments on the oracle's float64 moments gives the
     factors of saki_calibrate on the tokens (same arithmetic after the
@@ -237,6 +237,26 @@ def test_calibration_after_fork():
     p.join(30)
     assert p.exitcode == 0
     np.testing.assert_array_equal(got, ref)
+
+
+@pytest.mark.parametrize("kind", ["map", "svd"])
+def test_sap_factors_match_oracle(kind):
+    """SAP-map / SAP-svd bases (Sec. 6) of every head against the oracle's,
+    and the projector they define."""
+    spec = W.SPECS["llama31_8b_layer"].with_(N=64, Q=1, q_start=0)
+    inp = W.make_layer(spec)
+    cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32, method="sap_" + kind)
+    G = spec.H_q // spec.H_kv
+    for h in range(spec.H_q):
+        oc = O.saki_calibrate(inp["q_cal"][h], inp["k_cal"][h // G], 32)
+        Q = O.sap_factors(oc, 32, kind)
+        np.testing.assert_array_equal(cal["B_q"][h], cal["B_k"][h])
+        Bk = cal["B_k"][h].astype(np.float64)
+        assert np.max(np.abs(Bk - Q)) < 1e-6
+        sig = oc["sigma"]
+        assert np.max(np.abs(cal["sigma"][h] ** 2 - sig ** 2)) <= 1e-12 * sig[0] ** 2 * spec.d
+    np.testing.assert_allclose(cal["mu"], inp["k_cal"].astype(np.float64).mean(1), rtol=1e-6,
+                               atol=1e-7)
 
 
 def test_constant_keys_identity_fallback():
