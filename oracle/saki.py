@@ -25,7 +25,8 @@ __all__ = [
     "key_pca_factors", "sap_factors",
     "weight_svd_factors", "score_loss", "codes", "query_sketch", "sketch_scores",
     "direct_scores", "exact_scores", "candidate_limits", "topk_row", "topk_rows",
-    "recall_hits", "bf16_round", "f32_round", "score_scale", "predicted_reduction",
+    "recall_hits", "bf16_round", "f32_round", "fp8_round", "E4M3_MAX", "score_scale",
+    "predicted_reduction",
     "head_group", "index_scores", "PAD_IDX",
 ]
 
@@ -289,6 +290,37 @@ def bf16_round(x: np.ndarray) -> np.ndarray:
     return u.view(np.float32).astype(np.float64)
 
 
+def _e4m3_magnitudes() -> np.ndarray:
+    """The non-negative finite values of the fp8 E4M3 format (OCP: 1 sign, 4
+    exponent bits with bias 7, 3 mantissa bits, subnormals, no infinities;
+    code 0x7F is NaN), indexed by code 0x00 .. 0x7E, ascending."""
+    v = []
+    for code in range(0x7F):
+        e, m = code >> 3, code & 7
+        v.append(m * 2.0 ** -9 if e == 0 else (1.0 + m / 8.0) * 2.0 ** (e - 7))
+    return np.array(v)
+
+
+E4M3_MAX = 448.0
+
+
+def fp8_round(x: np.ndarray) -> np.ndarray:
+    """Storage of a code in fp8 E4M3: round to float32, then to the nearest
+    finite E4M3 value, ties to the even code; magnitudes above 448 saturate to
+    448 (reading: the format has no infinities).  Returned as float64."""
+    f = f32_round(x)
+    a = np.abs(f)
+    vals = _e4m3_magnitudes()
+    hi_i = np.clip(np.searchsorted(vals, a, side="left"), 1, vals.size - 1)
+    lo_v, hi_v = vals[hi_i - 1], vals[hi_i]
+    d_lo, d_hi = a - lo_v, hi_v - a
+    take_hi = (d_hi < d_lo) | ((d_hi == d_lo) & (hi_i % 2 == 0))
+    r = np.where(take_hi, hi_v, lo_v)
+    r = np.where(a >= E4M3_MAX, E4M3_MAX, r)
+    r = np.where(a == 0.0, 0.0, r)
+    return np.copysign(r, f)
+
+
 def score_scale(B_q, B_k, mu, q, keys) -> np.ndarray:
     """Magnitude scale of computing s_hat from (q, k) through the factors:
     S_ij = sum_m (|B_q|^T|q_i|)_m (|B_k|^T|k_j - mu|)_m + |q_i|^T |mu|.
@@ -312,14 +344,17 @@ def predicted_reduction(sigma: np.ndarray, r: int) -> float:
 def index_scores(B_q, B_k, mu, q, keys, sketch: str = "f64"):
     """Scores of one head through the stored index (Eq. 4, Sec. 6), with the
     sketch storage emulated: "f64" keeps exact codes; "f32"/"bf16" round the
-    codes c and the query sketch z to that storage type (the mean term b and
-    the sum stay float64).  Returns (s_hat [Q, N], z, b, c) after rounding."""
+    codes c and the query sketch z to that storage type; "fp8" rounds the
+    codes to fp8 E4M3 and z to bf16 (the mean term b and the sum stay
+    float64).  Returns (s_hat [Q, N], z, b, c) after rounding."""
     c = codes(B_k, mu, keys)
     z, b = query_sketch(B_q, mu, q)
     if sketch == "f32":
         c, z = f32_round(c), f32_round(z)
     elif sketch == "bf16":
         c, z = bf16_round(c), bf16_round(z)
+    elif sketch == "fp8":  # fp8 E4M3 codes, bf16 query sketch
+        c, z = fp8_round(c), bf16_round(z)
     elif sketch != "f64":
         raise ValueError(sketch)
     return sketch_scores(z, b, c), z, b, c

@@ -125,3 +125,28 @@ def test_score_scale_covers_float32_rounding():
     s32 = (z32 @ c32.T + b32[:, None]).astype(np.float64)
     S = O.score_scale(Bq, Bk, mu, q, keys)
     assert np.max(np.abs(s32 - s) / S) < 1e-5
+
+
+def test_fp8_round_matches_torch_e4m3fn():
+    """fp8 E4M3 code storage against torch's float8_e4m3fn conversion (round
+    to nearest even) inside the format's range, subnormals and exact
+    midpoints between neighbouring values included."""
+    rng = np.random.default_rng(4)
+    x = np.concatenate([rng.standard_normal(50000) * 10.0 ** rng.uniform(-4, 2.5, 50000),
+                        rng.uniform(-2.0 ** -6, 2.0 ** -6, 5000)]).astype(np.float32)
+    vals = torch.arange(0, 0x7F, dtype=torch.uint8).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    mids = 0.5 * (vals[1:] + vals[:-1])
+    x = np.concatenate([x, mids, -mids, vals, -vals]).astype(np.float32)
+    x = x[np.abs(x) <= 448.0]
+    want = torch.from_numpy(x).to(torch.float8_e4m3fn).to(torch.float64).numpy()
+    np.testing.assert_array_equal(O.fp8_round(x), want)
+
+
+def test_fp8_format_constants_and_saturation():
+    """Largest finite E4M3 value 448, smallest normal 2^-6, smallest
+    subnormal 2^-9; magnitudes beyond 448 saturate (reading: no infinities)."""
+    x = np.array([448.0, 2.0 ** -6, 2.0 ** -9, 1.0, 1.0625, 1.125, 3.0 * 2 ** -10,
+                  5.0 * 2 ** -11, 449.0, 1e6, -1e6, 0.0])
+    want = np.array([448.0, 2.0 ** -6, 2.0 ** -9, 1.0, 1.0, 1.125, 2.0 ** -8,
+                     2.0 ** -9, 448.0, 448.0, -448.0, 0.0])
+    np.testing.assert_array_equal(O.fp8_round(x), want)
