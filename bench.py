@@ -39,7 +39,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama31_8b_layer")
     ap.add_argument("--r", type=int, default=32)
-    ap.add_argument("--sketch", default="bf16", choices=["bf16", "f32"])
+    ap.add_argument("--sketch", default="bf16", choices=["bf16", "f32", "fp8"])
     ap.add_argument("--k", type=int, default=64)
     ap.add_argument("--shared", action="store_true",
                     help="GQA-shared index: one code set per KV head (pooled query moment)")
@@ -114,7 +114,7 @@ def candidates(spec, N_valid):
 def roofline_terms(spec, r, sketch, k):
     """Algorithmic work per launch of each GPU stage (bytes moved at least once,
     flops of the defined arithmetic)."""
-    es = 2 if sketch == "bf16" else 4
+    es = {"f32": 4, "bf16": 2, "fp8": 1}[sketch]
     rows = spec.batch * spec.H_q * spec.Q
     pairs = candidates(spec, spec.N)
     heads = spec.batch * spec.H_q
@@ -122,8 +122,8 @@ def roofline_terms(spec, r, sketch, k):
         # codes read once per head, queries read once, top-k (idx+score) written once
         "score_topk": {"bytes": heads * spec.N * r * es + rows * spec.d * 4 + rows * k * 8,
                        "flops": 2 * r * pairs,
-                       "peak_flops": PEAK["bf16_TFLOPs"] if sketch == "bf16" else PEAK["fp32_TFLOPs"],
-                       "flop_unit": "bf16" if sketch == "bf16" else "fp32"},
+                       "peak_flops": PEAK["fp32_TFLOPs"] if sketch == "f32" else PEAK["bf16_TFLOPs"],
+                       "flop_unit": "fp32" if sketch == "f32" else "bf16"},
         # keys read once per KV head, codes written once per query head
         "build": {"bytes": spec.batch * spec.H_kv * spec.N * spec.d * 4 + heads * spec.N * r * es,
                   "flops": 2 * spec.d * r * spec.N * heads,
@@ -153,7 +153,7 @@ def cpu_baseline(inp, r, sketch, k, n_heads):
         oc = O.saki_calibrate(inp["q_cal"][h], inp["k_cal"][h // G], r)
         q, keys = inp["queries"][0, h], inp["keys"][0, h // G]
         s_hat, *_ = O.index_scores(oc["B_q"], oc["B_k"], oc["mu"], q, keys,
-                                   "bf16" if sketch == "bf16" else "f32")
+                                   "f32" if sketch == "f32" else sketch)
         approx = O.topk_rows(s_hat, lim, k)
         exact = O.topk_rows(O.exact_scores(q, keys), lim, k)
         O.recall_hits(approx, exact)
@@ -253,7 +253,7 @@ def run_decode(args, spec):
     h = hits.cpu().numpy().astype(np.int64)
     per_head = h.sum(axis=(0, 1, 3)) / (k * Q * n_q)
 
-    es = 2 if sk == "bf16" else 4
+    es = {"f32": 4, "bf16": 2, "fp8": 1}[sk]
     code_bytes = B * IH * N * r * es
     scan_bytes = code_bytes + B * H_q * Q * d * 4 + B * H_q * Q * k * 8
     roof = {"bound": "hbm", "achieved": scan_bytes / (score_ms / 1e3) / 1e9,
@@ -269,7 +269,7 @@ def run_decode(args, spec):
         oc = O.saki_calibrate(inp["q_cal"][0], inp["k_cal"][0], r)
         q0 = decode_queries(spec, args.warmup)[0, 0]
         s_hat, *_ = O.index_scores(oc["B_q"], oc["B_k"], oc["mu"], q0, inp["keys"][0, 0],
-                                   "bf16" if sk == "bf16" else "f32")
+                                   "f32" if sk == "f32" else sk)
         O.topk_rows(s_hat, O.candidate_limits(Q, N), k)
         dtc = time.perf_counter() - t
         cpu = {"value": Q * N / dtc, "unit": "keys/s", "cores": os.cpu_count(), "kind": "oracle",

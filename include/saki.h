@@ -54,8 +54,11 @@ typedef enum {
   SAKI_ERR_NUMERIC = -6      /* eigensolver did not converge / non-finite input */
 } saki_status;
 
-/* Storage type of keys and of key sketches (codes). */
-enum { SAKI_F32 = 0, SAKI_BF16 = 1 };
+/* Storage type of keys (SAKI_F32, SAKI_BF16) and of key sketches (codes: all
+ * three).  SAKI_FP8 is the OCP fp8 E4M3 format (bias 7, 3 mantissa bits,
+ * subnormals, no infinities, largest finite value 448); quantisation
+ * composes with the codes (Sec. 2), halving the bytes of a bf16 index. */
+enum { SAKI_F32 = 0, SAKI_BF16 = 1, SAKI_FP8 = 2 };
 
 /* Rank-r map used by saki_calibrate. */
 enum {
@@ -179,8 +182,10 @@ size_t saki_index_bytes(int B, int H_q, int N_cap, int r, int sketch_dtype);
  * saki_build_index (GPU) -- key codes c_j = B_k^(h)T (k_j - mu_g(h)) (Eq. 4)
  * for every query head h, keys j in [n_begin, n_begin + n_count).  Codes are
  * computed in float32 and stored as sketch_dtype (bf16: round to nearest
- * even).  Codes outside the range are left untouched, so (0, N) builds the
- * whole index and (n, 1) appends one decoded token.
+ * even; fp8: round to the nearest E4M3 value, ties to the even code,
+ * magnitudes above 448 saturating to 448).  Codes outside the range are left
+ * untouched, so (0, N) builds the whole index and (n, 1) appends one decoded
+ * token.
  *
  *   keys    device [B, H_kv, N_cap, d], key_dtype SAKI_F32 or SAKI_BF16
  *   B_k     device float [H_q, d, r];  mu  device float [H_kv, d]
@@ -205,8 +210,8 @@ size_t saki_score_topk_workspace_bytes(int B, int H_q, int index_heads, int Q, i
 
 /*
  * saki_score_topk (GPU) -- Sec. 6: z_i = B_q^T q_i and b_i = q_i^T mu (float32;
- * z rounded to bf16 when sketch_dtype is bf16), scores s_ij = z_i . c_j + b_i
- * accumulated in float32, and the top-k keys per (sequence, head, query).
+ * z rounded to bf16 when sketch_dtype is bf16 or fp8), scores
+ * s_ij = z_i . c_j + b_i with exact products accumulated in float32, and the top-k keys per (sequence, head, query).
  * Query row i sees keys j < N_valid, and with q_pos also only j <= q_pos[i]
  * (causal, inclusive).
  *

@@ -1338,7 +1338,7 @@ int saki_weight_svd_factors(const double* W_K, int H_q, int H_kv, int d, int D,
 
 size_t saki_index_bytes(int B, int H_q, int N_cap, int r, int sketch_dtype) {
   if (B <= 0 || H_q <= 0 || N_cap < 0 || !saki::rank_supported(r) ||
-      (sketch_dtype != SAKI_F32 && sketch_dtype != SAKI_BF16))
+      (sketch_dtype != SAKI_F32 && sketch_dtype != SAKI_BF16 && sketch_dtype != SAKI_FP8))
     return 0;
   return saki::index_bytes(B, H_q, N_cap, r, sketch_dtype);
 }
@@ -1347,7 +1347,7 @@ size_t saki_score_topk_workspace_bytes(int B, int H_q, int index_heads, int Q, i
                                        int r, int k, int sketch_dtype) {
   if (B <= 0 || H_q <= 0 || index_heads <= 0 || H_q % index_heads != 0 || Q < 0 ||
       N_valid < 0 || !saki::rank_supported(r) || k < 1 || k > saki::kMaxK ||
-      (sketch_dtype != SAKI_F32 && sketch_dtype != SAKI_BF16))
+      (sketch_dtype != SAKI_F32 && sketch_dtype != SAKI_BF16 && sketch_dtype != SAKI_FP8))
     return 0;
   return saki::score_plan(B, H_q, index_heads, Q, N_valid, r).ws_bytes;
 }

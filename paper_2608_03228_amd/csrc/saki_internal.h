@@ -13,7 +13,8 @@ constexpr int kTile = 64;      // keys per index tile
 constexpr int kChunkBytes = 16;
 
 inline bool rank_supported(int r) { return r == 16 || r == 32 || r == 64 || r == 128; }
-inline int elem_bytes(int dtype) { return dtype == 1 ? 2 : 4; }
+// bytes per code element: float32 (0), bf16 (1), fp8 E4M3 (2)
+inline int elem_bytes(int dtype) { return dtype == 2 ? 1 : dtype == 1 ? 2 : 4; }
 inline size_t n_tiles(int N) { return ((size_t)N + kTile - 1) / kTile; }
 inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 

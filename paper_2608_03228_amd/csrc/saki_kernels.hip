@@ -47,6 +47,34 @@ __device__ __forceinline__ uint32_t bf16_bits(float x) {
 }
 __device__ __forceinline__ float bf16_round(float x) { return __uint_as_float(bf16_bits(x) << 16); }
 
+// Storage types of the codes (template parameter ST of the index kernels).
+constexpr int kStF32 = SAKI_F32, kStBf16 = SAKI_BF16, kStFp8 = SAKI_FP8;
+template <int ST>
+constexpr int code_bytes() { return ST == kStF32 ? 4 : ST == kStBf16 ? 2 : 1; }
+
+// float32 -> fp8 E4M3 code: round to the nearest E4M3 value (ties to the even
+// code), magnitudes of 448 and more saturate to 448 (finite inputs).
+__device__ __forceinline__ uint32_t e4m3_bits(float x) {
+  const uint32_t sign = (__float_as_uint(x) >> 24) & 0x80u;
+  const float a = fabsf(x);
+  if (!(a < 448.f)) return sign | 0x7Eu;
+  if (a < 0x1p-6f) return sign | (uint32_t)rintf(a * 512.f);  // subnormal: multiples of 2^-9
+  uint32_t u = __float_as_uint(a);
+  u += 0x7FFFFu + ((u >> 20) & 1u);  // round the float32 significand to 3 bits, ties to even
+  u &= 0xFFF00000u;
+  const uint32_t code = (((u >> 23) - 120u) << 3) | ((u >> 20) & 7u);  // rebias 127 -> 7
+  return sign | (code > 0x7Eu ? 0x7Eu : code);
+}
+
+// Four fp8 E4M3 codes (the bytes of w, lowest first) -> two words of bf16
+// pairs.  Exact: an E4M3 value has at most 4 significant bits.
+__device__ __forceinline__ uint2 e4m3x4_to_bf16(uint32_t w) {
+  const auto lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, false);  // bytes 0, 1
+  const auto hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, true);   // bytes 2, 3
+  return uint2{(__float_as_uint(lo[0]) >> 16) | (__float_as_uint(lo[1]) & 0xffff0000u),
+               (__float_as_uint(hi[0]) >> 16) | (__float_as_uint(hi[1]) & 0xffff0000u)};
+}
+
 template <bool BF>
 __device__ __forceinline__ float load_key_elem(const void* p, size_t i) {
   if constexpr (BF) {
@@ -72,6 +100,24 @@ __device__ __forceinline__ void unpack_piece(uint4 v, float* out) {
     out[1] = __uint_as_float(v.y);
     out[2] = __uint_as_float(v.z);
     out[3] = __uint_as_float(v.w);
+  }
+}
+
+// Unpack one 16-byte piece of codes stored as ST into 16 / code_bytes<ST>() floats.
+template <int ST>
+__device__ __forceinline__ void unpack_codes(uint4 v, float* out) {
+  if constexpr (ST == kStFp8) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint2 b = e4m3x4_to_bf16(w[e]);
+      out[4 * e] = __uint_as_float(b.x << 16);
+      out[4 * e + 1] = __uint_as_float(b.x & 0xffff0000u);
+      out[4 * e + 2] = __uint_as_float(b.y << 16);
+      out[4 * e + 3] = __uint_as_float(b.y & 0xffff0000u);
+    }
+  } else {
+    unpack_piece<ST == kStBf16>(v, out);
   }
 }
 
@@ -130,13 +176,13 @@ __device__ __forceinline__ int row_hits(int ej, const int* __restrict__ approx, 
 // ---------------------------------------------------------------- build index
 
 // grid (tiles, H_q, B), block 256.  One tile of 64 keys per workgroup.
-template <int RK, bool KBF, bool SBF>
+template <int RK, bool KBF, int ST>
 __global__ __launch_bounds__(256) void build_index_kernel(
     const void* __restrict__ keys, const float* __restrict__ Bk,
     const float* __restrict__ mu, int H_q, int H_kv, int N_cap, int n_tiles,
     uint8_t* __restrict__ index, int n_begin, int n_end, int tile0) {
   constexpr int D = saki::kHeadDim;
-  constexpr int ES = SBF ? 2 : 4;
+  constexpr int ES = code_bytes<ST>();
   constexpr int CPP = saki::kChunkBytes / ES;  // code elements per piece
   constexpr int NP = RK / CPP;                 // pieces per key
   __shared__ float ks[kTile][D + 1];
@@ -155,7 +201,7 @@ __global__ __launch_bounds__(256) void build_index_kernel(
   }
   for (int i = tid; i < D * RK; i += 256) bk[i / RK][i % RK] = Bk[(size_t)h * D * RK + i];
   __syncthreads();
-  uint8_t* tbase = index + (((size_t)b * H_q + h) * n_tiles + tile) * ((size_t)kTile * RK * (SBF ? 2 : 4));
+  uint8_t* tbase = index + (((size_t)b * H_q + h) * n_tiles + tile) * ((size_t)kTile * RK * ES);
   for (int p = tid; p < kTile * NP; p += 256) {
     const int t = p % kTile, piece = p / kTile;
     const int n = tile * kTile + t;
@@ -169,7 +215,14 @@ __global__ __launch_bounds__(256) void build_index_kernel(
     }
     if (n >= n_begin && n < n_end) {
       uint4 out;
-      if constexpr (SBF) {
+      if constexpr (ST == kStFp8) {
+        uint32_t wv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          wv[e] = e4m3_bits(acc[4 * e]) | (e4m3_bits(acc[4 * e + 1]) << 8) |
+                  (e4m3_bits(acc[4 * e + 2]) << 16) | (e4m3_bits(acc[4 * e + 3]) << 24);
+        out = uint4{wv[0], wv[1], wv[2], wv[3]};
+      } else if constexpr (ST == kStBf16) {
         out.x = bf16_bits(acc[0]) | (bf16_bits(acc[1]) << 16);
         out.y = bf16_bits(acc[2]) | (bf16_bits(acc[3]) << 16);
         out.z = bf16_bits(acc[4]) | (bf16_bits(acc[5]) << 16);
@@ -186,11 +239,11 @@ __global__ __launch_bounds__(256) void build_index_kernel(
 }
 
 // grid (tiles, B*H_q), block 64: codes -> float [B, H_q, N_cap, r].
-template <int RK, bool SBF>
+template <int RK, int ST>
 __global__ __launch_bounds__(64) void export_kernel(const uint8_t* __restrict__ index,
                                                     int n_tiles, int N_cap,
                                                     float* __restrict__ out) {
-  constexpr int ES = SBF ? 2 : 4;
+  constexpr int ES = code_bytes<ST>();
   constexpr int CPP = saki::kChunkBytes / ES;
   constexpr int NP = RK / CPP;
   const int tile = blockIdx.x;
@@ -198,11 +251,11 @@ __global__ __launch_bounds__(64) void export_kernel(const uint8_t* __restrict__ 
   const int t = threadIdx.x;
   const int n = tile * kTile + t;
   if (n >= N_cap) return;
-  const uint8_t* tbase = index + (bh * n_tiles + tile) * ((size_t)kTile * RK * (SBF ? 2 : 4));
+  const uint8_t* tbase = index + (bh * n_tiles + tile) * ((size_t)kTile * RK * ES);
   for (int piece = 0; piece < NP; ++piece) {
     const uint4 v = *reinterpret_cast<const uint4*>(tbase + (size_t)piece * kTile * 16 + (size_t)t * 16);
     float f[CPP];
-    unpack_piece<SBF>(v, f);
+    unpack_codes<ST>(v, f);
     for (int e = 0; e < CPP; ++e) out[(bh * N_cap + n) * RK + piece * CPP + e] = f[e];
   }
 }
@@ -210,8 +263,8 @@ __global__ __launch_bounds__(64) void export_kernel(const uint8_t* __restrict__ 
 // ---------------------------------------------------------------- query sketch
 
 // grid (ceil(Q/16), B*H_q), block 256.  z = B_q^T q (float32, rounded to bf16
-// when the sketches are bf16), b = q^T mu.
-template <int RK, bool SBF>
+// when the codes are bf16 or fp8), b = q^T mu.
+template <int RK, int ST>
 __global__ __launch_bounds__(256) void query_sketch_kernel(
     const float* __restrict__ q, const float* __restrict__ Bq,
     const float* __restrict__ mu, int H_q, int H_kv, int Q, float* __restrict__ z,
@@ -240,7 +293,7 @@ __global__ __launch_bounds__(256) void query_sketch_kernel(
     float acc = 0.f;
     if (m < RK) {
       for (int c = 0; c < D; ++c) acc = fmaf(qs[rr][c], bq[c][m], acc);
-      if (SBF) acc = bf16_round(acc);
+      if (ST != kStF32) acc = bf16_round(acc);
       z[((size_t)bh * Q + i) * RK + m] = acc;
     } else {
       for (int c = 0; c < D; ++c) acc = fmaf(qs[rr][c], ms[c], acc);
@@ -263,14 +316,14 @@ __device__ __forceinline__ bf16x2_t as_bf16x2(uint32_t v) {
 // numbered rho = i * gq + (h % gq) so that one wave's R rows are the heads
 // sharing the codes (for a GQA-shared index) before further queries.  Each
 // wave owns R rows and one key chunk; lane t scores key t of each 64-key tile.
-template <int RK, bool SBF, int R>
+template <int RK, int ST, int R>
 __global__ __launch_bounds__(256) void score_stream_kernel(
     const uint8_t* __restrict__ index, int n_tiles, int N_valid, int Q,
     const int* __restrict__ q_pos, const float* __restrict__ z,
     const float* __restrict__ bvec, int H_q, int gq, int row_blocks, int chunk, int n_chunks,
     int k, int* __restrict__ top_idx, float* __restrict__ top_score,
     uint64_t* __restrict__ part) {
-  constexpr int ES = SBF ? 2 : 4;
+  constexpr int ES = code_bytes<ST>();
   constexpr int CPP = saki::kChunkBytes / ES;
   constexpr int NP = RK / CPP;
   constexpr size_t TB = (size_t)kTile * RK * ES;
@@ -324,9 +377,10 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
     for (int p = 0; p < PF; ++p) v[p] = *reinterpret_cast<const uint4*>(tb + (size_t)p * kTile * 16);
   };
   if (kbeg < kend) load_tile(kbeg, nxt);
-  if constexpr (SBF) {
+  if constexpr (ST != kStF32) {
     // bf16 codes: each 32-bit word holds elements (2e, 2e + 1), scored with
-    // the packed bf16 dot product against the query sketch's pairs
+    // the packed bf16 dot product against the query sketch's pairs; fp8
+    // codes are first widened to such words (exactly)
     // the pairs are the same in every lane: when they fit, scalar registers
     // hold them and the vector registers are left to the key tiles
     constexpr bool kScalarZ = R * RK / 2 <= 64;
@@ -343,15 +397,24 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
       const int j = t0 + lane;
       const uint8_t* tb = hbase + (size_t)(t0 / kTile) * TB;
       uint32_t w[RK / 2];
+      auto put = [&](int p, const uint4& v) {  // piece p -> its words of bf16 pairs
+        if constexpr (ST == kStFp8) {
+          const uint32_t vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-      for (int p = 0; p < PF; ++p) {
-        w[4 * p] = nxt[p].x; w[4 * p + 1] = nxt[p].y; w[4 * p + 2] = nxt[p].z; w[4 * p + 3] = nxt[p].w;
-      }
+          for (int e = 0; e < 4; ++e) {
+            const uint2 bw = e4m3x4_to_bf16(vv[e]);
+            w[8 * p + 2 * e] = bw.x;
+            w[8 * p + 2 * e + 1] = bw.y;
+          }
+        } else {
+          w[4 * p] = v.x; w[4 * p + 1] = v.y; w[4 * p + 2] = v.z; w[4 * p + 3] = v.w;
+        }
+      };
 #pragma unroll
-      for (int p = PF; p < NP; ++p) {
-        const uint4 v = *reinterpret_cast<const uint4*>(tb + (size_t)p * kTile * 16 + (size_t)lane * 16);
-        w[4 * p] = v.x; w[4 * p + 1] = v.y; w[4 * p + 2] = v.z; w[4 * p + 3] = v.w;
-      }
+      for (int p = 0; p < PF; ++p) put(p, nxt[p]);
+#pragma unroll
+      for (int p = PF; p < NP; ++p)
+        put(p, *reinterpret_cast<const uint4*>(tb + (size_t)p * kTile * 16 + (size_t)lane * 16));
       if (t0 + kTile < kend) load_tile(t0 + kTile, nxt);
 #pragma unroll
       for (int r = 0; r < R; ++r) {
@@ -367,11 +430,11 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
       const uint8_t* tb = hbase + (size_t)(t0 / kTile) * TB;
       float c[RK];
 #pragma unroll
-      for (int p = 0; p < PF; ++p) unpack_piece<SBF>(nxt[p], c + p * CPP);
+      for (int p = 0; p < PF; ++p) unpack_codes<ST>(nxt[p], c + p * CPP);
 #pragma unroll
       for (int p = PF; p < NP; ++p) {
         const uint4 v = *reinterpret_cast<const uint4*>(tb + (size_t)p * kTile * 16 + (size_t)lane * 16);
-        unpack_piece<SBF>(v, c + p * CPP);
+        unpack_codes<ST>(v, c + p * CPP);
       }
       if (t0 + kTile < kend) load_tile(t0 + kTile, nxt);
 #pragma unroll
@@ -479,16 +542,20 @@ enum RowMode : int { kModeAll = 0, kModeHist = 1, kModeFallback = 2 };
 
 // Scores of one 64-key tile for the wave's 16 queries: acc[sub][v] is query
 // (lane % 16) against key t0 + 16*sub + 4*(lane/16) + v (without the mean term).
-template <int RK, bool SBF>
+// bf16 and fp8 codes run on the bf16 MFMA (fp8 widened exactly to bf16 in
+// registers), float32 codes on the f32 MFMA.
+template <int RK, int ST>
 struct MfmaScorer {
+  static constexpr bool SBF = ST != kStF32;  // bf16 operands
+  static constexpr bool F8 = ST == kStFp8;
   static constexpr int NKB = (SBF && RK >= 32) ? RK / 32 : 1;
   static constexpr int NKF = SBF ? 1 : RK / 4;
-  static constexpr size_t TB = (size_t)kTile * RK * (SBF ? 2 : 4);
+  static constexpr size_t TB = (size_t)kTile * RK * code_bytes<ST>();
   bf16x8_t zb[NKB];
   i16x4_t zb4;
   float zf[NKF];
 
-  // zs: this lane's query sketch row (RK floats, bf16 values when SBF)
+  // zs: this lane's query sketch row (RK floats, bf16 values for bf16 / fp8 codes)
   __device__ void load_operand(const float* zs, int g) {
     if constexpr (SBF) {
       if constexpr (RK == 16) {
@@ -521,7 +588,17 @@ struct MfmaScorer {
 #pragma unroll
     for (int sub = 0; sub < 4; ++sub) {
       const int key = 16 * sub + qi;
-      if constexpr (SBF && RK == 16) {
+      if constexpr (F8 && RK == 16) {  // dims 4g .. 4g+3: bytes 4g.. of piece 0
+        const uint32_t raw = *reinterpret_cast<const uint32_t*>(tb + (size_t)key * 16 + 4 * g);
+        r.v[sub][0] = uint4{raw, 0u, 0u, 0u};
+      } else if constexpr (F8) {  // dims 32kk + 8g .. +7: piece 2kk + g/2, bytes 8(g%2)..
+#pragma unroll
+        for (int kk = 0; kk < NL; ++kk) {
+          const uint2 raw = *reinterpret_cast<const uint2*>(
+              tb + (size_t)(2 * kk + g / 2) * kTile * 16 + (size_t)key * 16 + (g % 2) * 8);
+          r.v[sub][kk] = uint4{raw.x, raw.y, 0u, 0u};
+        }
+      } else if constexpr (SBF && RK == 16) {
         const uint2 raw = *reinterpret_cast<const uint2*>(tb + (size_t)(g / 2) * kTile * 16 +
                                                          (size_t)key * 16 + (g % 2) * 8);
         r.v[sub][0] = uint4{raw.x, raw.y, 0u, 0u};
@@ -543,7 +620,17 @@ struct MfmaScorer {
 #pragma unroll
     for (int sub = 0; sub < 4; ++sub) {
       f32x4_t a = {0.f, 0.f, 0.f, 0.f};
-      if constexpr (SBF && RK == 16) {
+      if constexpr (F8 && RK == 16) {
+        a = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_i16x4(e4m3x4_to_bf16(r.v[sub][0].x)), zb4,
+                                                     a, 0, 0, 0);
+      } else if constexpr (F8) {
+#pragma unroll
+        for (int kk = 0; kk < NL; ++kk) {
+          const uint2 w0 = e4m3x4_to_bf16(r.v[sub][kk].x), w1 = e4m3x4_to_bf16(r.v[sub][kk].y);
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(uint4{w0.x, w0.y, w1.x, w1.y}),
+                                                      zb[kk], a, 0, 0, 0);
+        }
+      } else if constexpr (SBF && RK == 16) {
         a = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_i16x4(uint2{r.v[sub][0].x, r.v[sub][0].y}),
                                                      zb4, a, 0, 0, 0);
       } else if constexpr (SBF) {
@@ -599,9 +686,9 @@ struct MfmaScorer {
 };
 
 // grid (row_blocks * n_chunks, B*H_q), block 64*waves.  Computes the query
-// sketch itself (z = B_q^T q on the f32 MFMA, rounded to bf16 for bf16
-// sketches; b = q^T mu), then scores and selects as described above.
-template <int RK, bool SBF>
+// sketch itself (z = B_q^T q on the f32 MFMA, rounded to bf16 for bf16 and
+// fp8 codes; b = q^T mu), then scores and selects as described above.
+template <int RK, int ST>
 __global__ __launch_bounds__(128) void score_mfma_kernel(
     const uint8_t* __restrict__ index, int n_tiles, int N_valid, int Q,
     const int* __restrict__ q_pos, const float* __restrict__ q,
@@ -610,7 +697,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
     float* __restrict__ top_score, uint64_t* __restrict__ part) {
   constexpr int D = saki::kHeadDim;
   using KO = KeysF32;
-  using Scorer = MfmaScorer<RK, SBF>;
+  using Scorer = MfmaScorer<RK, ST>;
   // per wave 12.1 KB, used in turn as: z staging [16][RK] floats; histogram
   // [16][kHistRow] ints (pass 2); candidates [16][kSCandRow] (pass 3); or the
   // fallback's score staging [16][64] floats + list and buffer of 8 rows
@@ -663,7 +750,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const float zv = za[mb][v];
-        zs[qi * RK + 16 * mb + 4 * g + v] = SBF ? bf16_round(zv) : zv;
+        zs[qi * RK + 16 * mb + 4 * g + v] = ST != kStF32 ? bf16_round(zv) : zv;
       }
     wave_lds_sync();
     sc.load_operand(zs + qi * RK, g);
@@ -2019,11 +2106,23 @@ __global__ __launch_bounds__(256) void moments_kernel(const float* __restrict__ 
   const int i0 = bi * kMomTile, j0 = bj * kMomTile;
   __shared__ double xi[kMomChunk][kMomTile + 1], xj[kMomChunk][kMomTile + 1];
   __shared__ double mean[2 * kMomTile];
-  if (threadIdx.x < 2 * kMomTile) {
-    const int c = threadIdx.x < kMomTile ? i0 + threadIdx.x : j0 + threadIdx.x - kMomTile;
+  __shared__ double part[8][2 * kMomTile];
+  if (key) {  // column means: 8 threads per column, every eighth token each
+    const int c = threadIdx.x % (2 * kMomTile), sl = threadIdx.x / (2 * kMomTile);
+    const int col = c < kMomTile ? i0 + c : j0 + c - kMomTile;
     double m = 0.0;
-    if (key && c < d) {
-      for (int t = 0; t < T; ++t) m += (double)X[(size_t)t * d + c];
+    if (col < d) {
+#pragma unroll 8
+      for (int t = sl; t < T; t += 8) m += (double)X[(size_t)t * d + col];
+    }
+    part[sl][c] = m;
+  }
+  __syncthreads();
+  if (threadIdx.x < 2 * kMomTile) {
+    double m = 0.0;
+    if (key) {
+#pragma unroll
+      for (int sl = 0; sl < 8; ++sl) m += part[sl][threadIdx.x];
       m /= (double)T;
     }
     mean[threadIdx.x] = m;
@@ -2061,14 +2160,14 @@ dim3 xcd_grid(const saki::Plan& p, int n_bh) {
   return dim3((unsigned)(((total + kXcds - 1) / kXcds) * kXcds));
 }
 
-template <int RK, bool KBF, bool SBF>
+template <int RK, bool KBF, int ST>
 void launch_build(const void* keys, const float* Bk, const float* mu, int B, int H_q,
                   int H_kv, int N_cap, uint8_t* index, int n_begin, int n_end,
                   hipStream_t s) {
   const int t0 = n_begin / kTile;
   const int t1 = (n_end + kTile - 1) / kTile;
   dim3 grid(t1 - t0, H_q, B);
-  hipLaunchKernelGGL((build_index_kernel<RK, KBF, SBF>), grid, dim3(256), 0, s, keys, Bk,
+  hipLaunchKernelGGL((build_index_kernel<RK, KBF, ST>), grid, dim3(256), 0, s, keys, Bk,
                      mu, H_q, H_kv, N_cap, (int)saki::n_tiles(N_cap), index, n_begin,
                      n_end, t0);
 }
@@ -2118,7 +2217,7 @@ saki::Plan one_round(saki::Plan p, K kernel, int groups_per_chunk, int N_valid) 
   return p;
 }
 
-template <int RK, bool SBF>
+template <int RK, int ST>
 void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int index_heads, int N_cap,
                   int N_valid, const float* q, const int* q_pos, int Q, const float* Bq,
                   const float* mu, int k, int* top_idx, float* top_score, uint8_t* ws,
@@ -2126,8 +2225,8 @@ void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int index_head
   const int gq = H_q / index_heads;
   saki::Plan p = p0;
   if (!p.mfma)
-    p = p.rows == 4 ? one_round(p0, score_stream_kernel<RK, SBF, 4>, p0.row_blocks * B * index_heads, N_valid)
-                    : one_round(p0, score_stream_kernel<RK, SBF, 1>, p0.row_blocks * B * index_heads, N_valid);
+    p = p.rows == 4 ? one_round(p0, score_stream_kernel<RK, ST, 4>, p0.row_blocks * B * index_heads, N_valid)
+                    : one_round(p0, score_stream_kernel<RK, ST, 1>, p0.row_blocks * B * index_heads, N_valid);
   float* z = reinterpret_cast<float*>(ws + p.z_off);
   float* bv = reinterpret_cast<float*>(ws + p.b_off);
   const size_t rows = (size_t)B * H_q * Q;
@@ -2136,18 +2235,18 @@ void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int index_head
   dim3 block(kWave * p.waves);
   const int nt = (int)saki::n_tiles(N_cap);
   if (!p.mfma)
-    hipLaunchKernelGGL((query_sketch_kernel<RK, SBF>), dim3((Q + 15) / 16, B * H_q),
+    hipLaunchKernelGGL((query_sketch_kernel<RK, ST>), dim3((Q + 15) / 16, B * H_q),
                        dim3(256), 0, s, q, Bq, mu, H_q, H_kv, Q, z, bv);
   if (p.mfma)
-    hipLaunchKernelGGL((score_mfma_kernel<RK, SBF>), xcd_grid(p, B * H_q), block, 0, s, index,
+    hipLaunchKernelGGL((score_mfma_kernel<RK, ST>), xcd_grid(p, B * H_q), block, 0, s, index,
                        nt, N_valid, Q, q_pos, q, Bq, mu, H_q, H_kv, gq, B * H_q, p.row_blocks,
                        p.chunk, p.n_chunks, k, top_idx, top_score, part);
   else if (p.rows == 4)
-    hipLaunchKernelGGL((score_stream_kernel<RK, SBF, 4>), grid, block, 0, s, index, nt, N_valid,
+    hipLaunchKernelGGL((score_stream_kernel<RK, ST, 4>), grid, block, 0, s, index, nt, N_valid,
                        Q, q_pos, z, bv, H_q, gq, p.row_blocks, p.chunk, p.n_chunks, k, top_idx,
                        top_score, part);
   else
-    hipLaunchKernelGGL((score_stream_kernel<RK, SBF, 1>), grid, block, 0, s, index, nt, N_valid,
+    hipLaunchKernelGGL((score_stream_kernel<RK, ST, 1>), grid, block, 0, s, index, nt, N_valid,
                        Q, q_pos, z, bv, H_q, gq, p.row_blocks, p.chunk, p.n_chunks, k, top_idx,
                        top_score, part);
   if (p.n_chunks > 1)
@@ -2205,7 +2304,8 @@ void launch_recall(const void* keys, const float* q, const int* q_pos, int B, in
                        k, exact_idx, nullptr, approx, hits);
 }
 
-bool dtype_ok(int t) { return t == SAKI_F32 || t == SAKI_BF16; }
+bool dtype_ok(int t) { return t == SAKI_F32 || t == SAKI_BF16; }  // keys
+bool sketch_ok(int t) { return t == SAKI_F32 || t == SAKI_BF16 || t == SAKI_FP8; }
 
 // Common size validation of the GPU entry points.
 int check_common(int B, int H_q, int H_kv, int N_cap, int N_valid, int d) {
@@ -2230,7 +2330,7 @@ int saki_build_index(const void* keys, int key_dtype, int B, int H_q, int H_kv,
   int st = check_common(B, H_q, H_kv, N_cap, 0, d);
   if (st != SAKI_OK) return st;
   if (!keys || !B_k || !mu || !index) return SAKI_ERR_ARG;
-  if (!dtype_ok(key_dtype) || !dtype_ok(sketch_dtype) || !saki::rank_supported(r))
+  if (!dtype_ok(key_dtype) || !sketch_ok(sketch_dtype) || !saki::rank_supported(r))
     return SAKI_ERR_UNSUPPORTED;
   if (n_begin < 0 || n_count < 0 || (long long)n_begin + n_count > N_cap) return SAKI_ERR_ARG;
   if (index_bytes < saki::index_bytes(B, H_q, N_cap, r, sketch_dtype)) return SAKI_ERR_WORKSPACE;
@@ -2238,19 +2338,21 @@ int saki_build_index(const void* keys, int key_dtype, int B, int H_q, int H_kv,
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   uint8_t* ix = reinterpret_cast<uint8_t*>(index);
   const int n_end = n_begin + n_count;
-#define SAKI_BUILD(RK)                                                                   \
-  do {                                                                                   \
-    if (key_dtype == SAKI_BF16) {                                                        \
-      if (sketch_dtype == SAKI_BF16)                                                     \
-        launch_build<RK, true, true>(keys, B_k, mu, B, H_q, H_kv, N_cap, ix, n_begin, n_end, s); \
-      else                                                                               \
-        launch_build<RK, true, false>(keys, B_k, mu, B, H_q, H_kv, N_cap, ix, n_begin, n_end, s); \
-    } else {                                                                             \
-      if (sketch_dtype == SAKI_BF16)                                                     \
-        launch_build<RK, false, true>(keys, B_k, mu, B, H_q, H_kv, N_cap, ix, n_begin, n_end, s); \
-      else                                                                               \
-        launch_build<RK, false, false>(keys, B_k, mu, B, H_q, H_kv, N_cap, ix, n_begin, n_end, s); \
-    }                                                                                    \
+#define SAKI_BUILD_ST(RK, KB)                                                                \
+  do {                                                                                       \
+    if (sketch_dtype == SAKI_FP8)                                                            \
+      launch_build<RK, KB, kStFp8>(keys, B_k, mu, B, H_q, H_kv, N_cap, ix, n_begin, n_end, s);  \
+    else if (sketch_dtype == SAKI_BF16)                                                      \
+      launch_build<RK, KB, kStBf16>(keys, B_k, mu, B, H_q, H_kv, N_cap, ix, n_begin, n_end, s); \
+    else                                                                                     \
+      launch_build<RK, KB, kStF32>(keys, B_k, mu, B, H_q, H_kv, N_cap, ix, n_begin, n_end, s);  \
+  } while (0)
+#define SAKI_BUILD(RK)                         \
+  do {                                         \
+    if (key_dtype == SAKI_BF16)                \
+      SAKI_BUILD_ST(RK, true);                 \
+    else                                       \
+      SAKI_BUILD_ST(RK, false);                \
   } while (0)
   switch (r) {
     case 16: SAKI_BUILD(16); break;
@@ -2259,6 +2361,7 @@ int saki_build_index(const void* keys, int key_dtype, int B, int H_q, int H_kv,
     default: SAKI_BUILD(128); break;
   }
 #undef SAKI_BUILD
+#undef SAKI_BUILD_ST
   return launch_ok() ? SAKI_OK : SAKI_ERR_HIP;
 }
 
@@ -2266,18 +2369,20 @@ int saki_index_export(const void* index, int sketch_dtype, int B, int H_q, int N
                       float* out, void* stream) {
   if (!index || !out || B <= 0 || H_q <= 0 || N_cap < 0) return SAKI_ERR_ARG;
   if ((long long)B * H_q > 65535) return SAKI_ERR_UNSUPPORTED;
-  if (!dtype_ok(sketch_dtype) || !saki::rank_supported(r)) return SAKI_ERR_UNSUPPORTED;
+  if (!sketch_ok(sketch_dtype) || !saki::rank_supported(r)) return SAKI_ERR_UNSUPPORTED;
   if (N_cap == 0) return SAKI_OK;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   dim3 grid((unsigned)saki::n_tiles(N_cap), B * H_q);
   const uint8_t* ix = reinterpret_cast<const uint8_t*>(index);
   const int nt = (int)saki::n_tiles(N_cap);
-#define SAKI_EXPORT(RK)                                                                       \
-  do {                                                                                        \
-    if (sketch_dtype == SAKI_BF16)                                                            \
-      hipLaunchKernelGGL((export_kernel<RK, true>), grid, dim3(64), 0, s, ix, nt, N_cap, out);  \
-    else                                                                                      \
-      hipLaunchKernelGGL((export_kernel<RK, false>), grid, dim3(64), 0, s, ix, nt, N_cap, out); \
+#define SAKI_EXPORT(RK)                                                                          \
+  do {                                                                                           \
+    if (sketch_dtype == SAKI_FP8)                                                                \
+      hipLaunchKernelGGL((export_kernel<RK, kStFp8>), grid, dim3(64), 0, s, ix, nt, N_cap, out);   \
+    else if (sketch_dtype == SAKI_BF16)                                                          \
+      hipLaunchKernelGGL((export_kernel<RK, kStBf16>), grid, dim3(64), 0, s, ix, nt, N_cap, out);  \
+    else                                                                                         \
+      hipLaunchKernelGGL((export_kernel<RK, kStF32>), grid, dim3(64), 0, s, ix, nt, N_cap, out);   \
   } while (0)
   switch (r) {
     case 16: SAKI_EXPORT(16); break;
@@ -2298,7 +2403,7 @@ int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_k
   if (Q < 0) return SAKI_ERR_ARG;
   // a code set serves whole query heads and lies within one KV group
   if (index_heads <= 0 || H_q % index_heads != 0 || index_heads % H_kv != 0) return SAKI_ERR_ARG;
-  if (!dtype_ok(sketch_dtype) || !saki::rank_supported(r) || k < 1 || k > kMaxK)
+  if (!sketch_ok(sketch_dtype) || !saki::rank_supported(r) || k < 1 || k > kMaxK)
     return SAKI_ERR_UNSUPPORTED;
   if (Q == 0) return SAKI_OK;
   if (!index || !q || !B_q || !mu || !top_idx || !ws) return SAKI_ERR_ARG;
@@ -2308,14 +2413,17 @@ int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_k
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const uint8_t* ix = reinterpret_cast<const uint8_t*>(index);
   uint8_t* w = reinterpret_cast<uint8_t*>(ws);
-#define SAKI_SCORE(RK)                                                                        \
-  do {                                                                                        \
-    if (sketch_dtype == SAKI_BF16)                                                            \
-      launch_score<RK, true>(ix, B, H_q, H_kv, index_heads, N_cap, N_valid, q, q_pos, Q, B_q, \
-                             mu, k, top_idx, top_score, w, p, s);                             \
-    else                                                                                      \
-      launch_score<RK, false>(ix, B, H_q, H_kv, index_heads, N_cap, N_valid, q, q_pos, Q, B_q,\
-                              mu, k, top_idx, top_score, w, p, s);                            \
+#define SAKI_SCORE_ST(RK, ST)                                                                 \
+  launch_score<RK, ST>(ix, B, H_q, H_kv, index_heads, N_cap, N_valid, q, q_pos, Q, B_q, mu, k, \
+                       top_idx, top_score, w, p, s)
+#define SAKI_SCORE(RK)                          \
+  do {                                          \
+    if (sketch_dtype == SAKI_FP8)               \
+      SAKI_SCORE_ST(RK, kStFp8);                \
+    else if (sketch_dtype == SAKI_BF16)         \
+      SAKI_SCORE_ST(RK, kStBf16);               \
+    else                                        \
+      SAKI_SCORE_ST(RK, kStF32);                \
   } while (0)
   switch (r) {
     case 16: SAKI_SCORE(16); break;
@@ -2324,6 +2432,7 @@ int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_k
     default: SAKI_SCORE(128); break;
   }
 #undef SAKI_SCORE
+#undef SAKI_SCORE_ST
   return launch_ok() ? SAKI_OK : SAKI_ERR_HIP;
 }
 

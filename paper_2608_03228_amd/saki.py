@@ -17,9 +17,9 @@ import numpy as np
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsaki.so")
 _lib = None
 
-F32, BF16 = 0, 1
+F32, BF16, FP8 = 0, 1, 2
 METHOD_OPT, METHOD_KEY_PCA, METHOD_SHARED, METHOD_SAP_MAP, METHOD_SAP_SVD = 0, 1, 2, 3, 4
-_DTYPES = {"f32": F32, "bf16": BF16}
+_DTYPES = {"f32": F32, "bf16": BF16, "fp8": FP8}
 _METHODS = {"opt": METHOD_OPT, "key_pca": METHOD_KEY_PCA, "shared": METHOD_SHARED,
             "sap_map": METHOD_SAP_MAP, "sap_svd": METHOD_SAP_SVD}
 

@@ -25,6 +25,11 @@ import oracle as O
 
 TOL_F32 = 1e-5
 TOL_BF16_EXACT = 2e-2
+# fp8 E4M3 codes against exact codes: rounding a code costs at most 2^-4 of
+# its magnitude (half of a 3-bit significand step) and z's bf16 rounding 2^-9,
+# so |s_gpu - s_exact| <= (2^-4 + 2^-9 + 2^-4 * 2^-9 + fp32 sum) * S_ij < 0.07 S_ij
+# (codes in the subnormal range below 2^-6 add at most 2^-10 |z_m| each)
+TOL_FP8_EXACT = 7e-2
 AMBIG_REL = 1e-5  # bound on the float32 computation error of one element, relative
                   # to its absolute-value sum
 
@@ -40,23 +45,38 @@ def _bf16_ambiguity(exact, abs_sum):
     return amb, ulp
 
 
+def _fp8_ambiguity(exact, abs_sum):
+    """As _bf16_ambiguity for fp8 E4M3 codes: the spacing is 2^(e-3) in
+    [2^e, 2^(e+1)) for e >= -6 and 2^-9 below 2^-6 (subnormals)."""
+    r = O.fp8_round(exact)
+    mag = np.maximum(np.abs(exact), 1e-300)
+    ulp = np.where(mag < 2.0 ** -6, 2.0 ** -9, np.exp2(np.floor(np.log2(mag)) - 3.0))
+    dist_mid = np.abs(0.5 * ulp - np.abs(exact - r))
+    amb = (dist_mid <= AMBIG_REL * abs_sum + 2.0 ** -24 * mag) & (mag < O.E4M3_MAX)
+    return amb, ulp
+
+
 def oracle_head(B_q, B_k, mu, q, keys, mode: str):
     """Oracle scores and per-score tolerances of one head.
 
     mode: "f32" (exact codes, tol 1e-5), "bf16_exact" (exact codes, tol 2e-2),
-    "bf16_emul" (bf16-rounded codes and z, tol 1e-5 plus ambiguity).
+    "bf16_emul" (bf16-rounded codes and z, tol 1e-5 plus ambiguity),
+    "fp8_exact" (exact codes, tol 7e-2), "fp8_emul" (fp8 codes, bf16 z, tol
+    1e-5 plus ambiguity).
     Returns (s [Q, N], eps [Q, N])."""
     q = np.asarray(q, np.float64)
     keys = np.asarray(keys, np.float64)
     S = O.score_scale(B_q, B_k, mu, q, keys)
-    if mode in ("f32", "bf16_exact"):
+    if mode in ("f32", "bf16_exact", "fp8_exact"):
         s, *_ = O.index_scores(B_q, B_k, mu, q, keys, "f64")
-        return s, (TOL_F32 if mode == "f32" else TOL_BF16_EXACT) * S
-    assert mode == "bf16_emul"
-    s, z, b, c = O.index_scores(B_q, B_k, mu, q, keys, "bf16")
+        tol = {"f32": TOL_F32, "bf16_exact": TOL_BF16_EXACT, "fp8_exact": TOL_FP8_EXACT}[mode]
+        return s, tol * S
+    assert mode in ("bf16_emul", "fp8_emul")
+    s, z, b, c = O.index_scores(B_q, B_k, mu, q, keys, mode[:-5])
     c_ex = O.codes(B_k, mu, keys)
     z_ex, _ = O.query_sketch(B_q, mu, q)
-    amb_c, ulp_c = _bf16_ambiguity(c_ex, np.abs(keys - mu) @ np.abs(B_k))
+    code_amb = _fp8_ambiguity if mode == "fp8_emul" else _bf16_ambiguity
+    amb_c, ulp_c = code_amb(c_ex, np.abs(keys - mu) @ np.abs(B_k))
     amb_z, ulp_z = _bf16_ambiguity(z_ex, np.abs(q) @ np.abs(B_q))
     extra = np.abs(z) @ (amb_c * ulp_c).T + (amb_z * ulp_z) @ np.abs(c).T
     return s, TOL_F32 * S + extra

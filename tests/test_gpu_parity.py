@@ -77,7 +77,7 @@ def test_codes_match_oracle():
     correct rounding of them."""
     spec = W.SPECS["llama31_8b_layer"].with_(N=1000, Q=8, q_start=64)
     inp = W.make_layer(spec)
-    for sketch in ("f32", "bf16"):
+    for sketch in ("f32", "bf16", "fp8"):
         out = gpu_pipeline(inp, 32, sketch, N_valid=1000)
         codes = S.saki_index_export(out["index"], sketch, 1, spec.H_q, 1000, 32)
         codes = codes.cpu().numpy()
@@ -90,6 +90,11 @@ def test_codes_match_oracle():
             got = codes[0, h]
             if sketch == "f32":
                 assert np.max(np.abs(got - exact) / scale) < 1e-5
+            elif sketch == "fp8":
+                assert np.all(O.fp8_round(got) == got)  # representable in E4M3
+                mag = np.maximum(np.abs(exact), 1e-30)
+                ulp = np.where(mag < 2.0 ** -6, 2.0 ** -9, np.exp2(np.floor(np.log2(mag)) - 3))
+                assert np.all(np.abs(got - exact) <= 0.5 * ulp + 1e-5 * scale)
             else:
                 assert np.all(O.bf16_round(got) == got)  # representable in bf16
                 ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(exact), 1e-30))) - 7)
@@ -97,7 +102,7 @@ def test_codes_match_oracle():
 
 
 @pytest.mark.parametrize("r", [16, 32, 64])
-@pytest.mark.parametrize("sketch", ["f32", "bf16"])
+@pytest.mark.parametrize("sketch", ["f32", "bf16", "fp8"])
 def test_llama_layer_causal(r, sketch):
     """One LLaMA-3.1-8B-shaped layer: 32 query / 8 KV heads, N=4096, causal
     rows at positions 64..4095; all rows on the GPU, sampled rows of three
@@ -106,7 +111,8 @@ def test_llama_layer_causal(r, sketch):
     out = gpu_pipeline(inp, r, sketch)
     rng = np.random.default_rng(r)
     rows = np.unique(np.concatenate([[0, 1, 2, 63, 64, 4031], rng.choice(4032, 90, False)]))
-    modes = ["f32"] if sketch == "f32" else ["bf16_emul", "bf16_exact"]
+    modes = {"f32": ["f32"], "bf16": ["bf16_emul", "bf16_exact"],
+             "fp8": ["fp8_emul", "fp8_exact"]}[sketch]
     for h in (0, 13, 31):
         for mode in modes:
             n, ex, diff = check_head(inp, out, 0, h, r, mode, rows=rows)
@@ -151,14 +157,15 @@ def test_decode_split_chunks_and_merge():
     spec = W.SPECS["decode_1m"].with_(N=200_000, H_q=8, H_kv=2)
     inp = W.make_layer(spec)
     assert S.saki_score_topk_workspace_bytes(1, 8, 1, 200_000, 32, 64, "bf16") > 8 * 64 * 8
-    for sketch, mode in (("bf16", "bf16_emul"), ("f32", "f32")):
+    for sketch, mode in (("bf16", "bf16_emul"), ("f32", "f32"), ("fp8", "fp8_emul")):
         out = gpu_pipeline(inp, 32, sketch)
         for h in range(8):
             check_head(inp, out, 0, h, 32, mode)
 
 
 @pytest.mark.parametrize("sketch,Q,N", [("bf16", 96, 1500), ("f32", 3, 70_000),
-                                        ("bf16", 1, 150_000)])
+                                        ("bf16", 1, 150_000), ("fp8", 1, 150_000),
+                                        ("fp8", 40, 3000)])
 def test_gqa_shared_index_matches_oracle(sketch, Q, N):
     """A GQA-shared index: one code set per KV head, built from the
     SAKI_METHOD_SHARED factors, scored by all four query heads of its group
@@ -174,7 +181,7 @@ def test_gqa_shared_index_matches_oracle(sketch, Q, N):
                                 index_heads=2)
     torch.cuda.synchronize()
     out = {"idx": idx.cpu().numpy(), "score": sc.cpu().numpy()}
-    mode = "f32" if sketch == "f32" else "bf16_emul"
+    mode = {"f32": "f32", "bf16": "bf16_emul", "fp8": "fp8_emul"}[sketch]
     for g in range(2):
         oc = O.saki_calibrate_shared(inp["q_cal"][4 * g:4 * g + 4], inp["k_cal"][g], 32)
         for h in range(4 * g, 4 * g + 4):

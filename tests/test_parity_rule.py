@@ -28,3 +28,13 @@ def test_midpoints_are_ambiguous_and_representable_values_are_not():
     amb_mid, _ = _bf16_ambiguity(base + 0.5 * ulp, np.abs(base) * 1e-3)
     amb_rep, _ = _bf16_ambiguity(base, np.abs(base) * 1e-3)
     assert amb_mid.all() and not amb_rep.any()
+
+
+def test_fp8_ulp_is_the_spacing_of_e4m3_values():
+    from tests.parity import _fp8_ambiguity
+    vals = np.array(sorted({abs(float(O.fp8_round(np.float32(v)))) for v in
+                            np.linspace(-448, 448, 20001)} | set(O.fp8_round(
+                                np.exp2(np.linspace(-9, 8.8, 5000))))))
+    vals = vals[vals > 0]
+    _, ulp = _fp8_ambiguity(vals[:-1], vals[:-1])
+    np.testing.assert_array_equal(ulp, np.diff(vals))
