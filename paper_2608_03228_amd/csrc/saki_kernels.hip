@@ -393,7 +393,14 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
                            (__float_as_uint(zs[wave][r][2 * m + 1]) & 0xffff0000u);
         zp[r][m] = kScalarZ ? (uint32_t)__builtin_amdgcn_readfirstlane((int)v) : v;
       }
-    for (int t0 = kbeg; t0 < kend; t0 += kTile) {
+    // with at most 32 bytes of code per key, two tiles are loaded ahead (into
+    // two buffers taken in turn) so that as many bytes are in flight as for
+    // wider codes; otherwise one
+    constexpr int kAhead = NP * 16 <= 32 ? 2 : 1;
+    // one tile: the words of bf16 pairs from `cur` (and the pieces not
+    // prefetched), then `refill` (which may reload cur's registers), then the
+    // dot products
+    auto tile = [&](int t0, const uint4* cur, auto&& refill) {
       const int j = t0 + lane;
       const uint8_t* tb = hbase + (size_t)(t0 / kTile) * TB;
       uint32_t w[RK / 2];
@@ -411,11 +418,11 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
         }
       };
 #pragma unroll
-      for (int p = 0; p < PF; ++p) put(p, nxt[p]);
+      for (int p = 0; p < PF; ++p) put(p, cur[p]);
 #pragma unroll
       for (int p = PF; p < NP; ++p)
         put(p, *reinterpret_cast<const uint4*>(tb + (size_t)p * kTile * 16 + (size_t)lane * 16));
-      if (t0 + kTile < kend) load_tile(t0 + kTile, nxt);
+      refill();
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         float acc = 0.f;
@@ -423,6 +430,18 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
         for (int m = 0; m < RK / 2; ++m) acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(w[m]), as_bf16x2(zp[r][m]), acc, false);
         top.offer(r, j < lim[r] ? acc + bb[r] : -INFINITY, j);
       }
+    };
+    if constexpr (kAhead == 2) {
+      uint4 nxt2[PF];
+      if (kbeg + kTile < kend) load_tile(kbeg + kTile, nxt2);
+      for (int t0 = kbeg; t0 < kend; t0 += 2 * kTile) {
+        tile(t0, nxt, [&] { if (t0 + 2 * kTile < kend) load_tile(t0 + 2 * kTile, nxt); });
+        if (t0 + kTile >= kend) break;
+        tile(t0 + kTile, nxt2, [&] { if (t0 + 3 * kTile < kend) load_tile(t0 + 3 * kTile, nxt2); });
+      }
+    } else {
+      for (int t0 = kbeg; t0 < kend; t0 += kTile)
+        tile(t0, nxt, [&] { if (t0 + kTile < kend) load_tile(t0 + kTile, nxt); });
     }
   } else {
     for (int t0 = kbeg; t0 < kend; t0 += kTile) {
