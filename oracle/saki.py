@@ -27,7 +27,8 @@ __all__ = [
     "direct_scores", "exact_scores", "candidate_limits", "topk_row", "topk_rows",
     "recall_hits", "bf16_round", "f32_round", "fp8_round", "E4M3_MAX", "score_scale",
     "predicted_reduction",
-    "head_group", "index_scores", "PAD_IDX",
+    "head_group", "index_scores", "PAD_IDX", "ROPE_THETA", "rope", "reconstruct_keys",
+    "sparse_attention",
 ]
 
 PAD_IDX = -1
@@ -271,6 +272,54 @@ def recall_hits(approx_idx: np.ndarray, exact_idx: np.ndarray) -> np.ndarray:
         sa = {int(x) for x in a[pos] if x != PAD_IDX}
         se = {int(x) for x in e[pos] if x != PAD_IDX}
         out[pos] = len(sa & se)
+    return out
+
+
+# ---------------------------------------------------------------- reading the winners
+
+ROPE_THETA = 500000.0  # RoPE base of the LLaMA-3.1 models of Sec. 7
+
+
+def rope(x: np.ndarray, pos, theta: float = ROPE_THETA) -> np.ndarray:
+    """Rotary position embedding, rotate-half convention: for m < d/2 the pair
+    (x_m, x_{m + d/2}) is rotated by the angle pos * theta^(-2m/d).  Sec. 3:
+    codes are built from pre-RoPE keys and the rotation is applied after
+    reconstruction.  x [..., d], pos broadcast against x[..., 0]."""
+    x = np.asarray(x, np.float64)
+    d = x.shape[-1]
+    half = d // 2
+    inv = theta ** (-2.0 * np.arange(half, dtype=np.float64) / d)
+    ang = np.asarray(pos, np.float64)[..., None] * inv
+    c, s = np.cos(ang), np.sin(ang)
+    a, b = x[..., :half], x[..., half:]
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+
+
+def reconstruct_keys(B_q: np.ndarray, mu: np.ndarray, c: np.ndarray) -> np.ndarray:
+    """Sec. 6: k_hat = mu + M_r (k - mu) = mu + B_q c from the stored codes c
+    (M_r = B_q B_k^T).  c [N, r] -> [N, d]."""
+    return np.asarray(mu, np.float64) + np.asarray(c, np.float64) @ np.asarray(B_q, np.float64).T
+
+
+def sparse_attention(q, q_pos, keys, values, idx, theta: float = ROPE_THETA) -> np.ndarray:
+    """Attention of each query over the keys its index selected (Sec. 1: the
+    index nominates candidates, exact values are fetched for the winners), in
+    RoPE space: s_j = rope(q, p_q) . rope(k_j, j) / sqrt(d) for the selected j
+    (idx >= 0; a key's position is its index), p = softmax(s), out = sum_j p_j v_j.
+    q [Q, d], q_pos [Q], keys and values [N, d], idx [Q, k] -> [Q, d]."""
+    q = np.asarray(q, np.float64)
+    d = q.shape[-1]
+    out = np.zeros((q.shape[0], d))
+    for i in range(q.shape[0]):
+        sel = np.asarray(idx[i])
+        sel = sel[sel >= 0]
+        if sel.size == 0:
+            continue
+        qr = rope(q[i], q_pos[i], theta)
+        kr = rope(np.asarray(keys, np.float64)[sel], sel, theta)
+        sc = kr @ qr / np.sqrt(d)
+        w = np.exp(sc - sc.max())
+        out[i] = (w / w.sum()) @ np.asarray(values, np.float64)[sel]
     return out
 
 

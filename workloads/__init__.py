@@ -29,7 +29,7 @@ from dataclasses import dataclass
 import numpy as np
 
 BASE_SEED = 20260803
-_PURPOSE = {"wq": 1, "wk": 2, "outliers": 3, "calib": 4, "keys": 5, "queries": 6}
+_PURPOSE = {"wq": 1, "wk": 2, "outliers": 3, "calib": 4, "keys": 5, "queries": 6, "wv": 7}
 _CHUNK = 65536  # rows drawn per call, fixed so that prefixes stay identical
 
 
@@ -126,6 +126,13 @@ def weights(spec: WorkloadSpec, layer: int = 0):
     return wq, wk
 
 
+def value_weights(spec: WorkloadSpec, layer: int = 0):
+    """W_V [H_kv, d, D] (float64), drawn like W_K."""
+    col = np.arange(1, spec.D + 1, dtype=np.float64) ** -0.5
+    return np.stack([rng(spec, "wv", layer, head=g).standard_normal((spec.d, spec.D)) * col
+                     for g in range(spec.H_kv)])
+
+
 def tokens(spec: WorkloadSpec, purpose: str, n: int, layer: int = 0, seq: int = 0,
            step: int = 0) -> np.ndarray:
     """n latent tokens [n, D] (float64), drawn in fixed-size chunks."""
@@ -150,14 +157,15 @@ def _project(x: np.ndarray, w: np.ndarray) -> np.ndarray:
 
 
 def make_layer(spec: WorkloadSpec, layer: int = 0, seqs=None, step: int = 0,
-               with_calib: bool = True) -> dict:
+               with_calib: bool = True, with_values: bool = False) -> dict:
     """All inputs of one layer.
 
     Returns a dict with
       q_cal [H_q, T, d] f32, k_cal [H_kv, T, d] f32 (calibration tokens),
       keys [B, H_kv, N, d] f32, queries [B, H_q, Q, d] f32,
       q_pos int32 [Q] (causal) or None, W_Q [H_q, d, D] and W_K [H_kv, d, D]
-      (float64, for the weight-SVD baseline).
+      (float64, for the weight-SVD baseline); with_values also
+      values [B, H_kv, N, d] f32 = W_V x of the same cached tokens.
     ``seqs`` selects which sequences of the batch to build (default all).
     """
     seqs = list(range(spec.batch)) if seqs is None else list(seqs)
@@ -169,9 +177,14 @@ def make_layer(spec: WorkloadSpec, layer: int = 0, seqs=None, step: int = 0,
         out["k_cal"] = _project(xc, wk)
     keys = np.empty((len(seqs), spec.H_kv, spec.N, spec.d), np.float32)
     queries = np.empty((len(seqs), spec.H_q, spec.Q, spec.d), np.float32)
+    if with_values:
+        wv = value_weights(spec, layer)
+        out["values"] = np.empty((len(seqs), spec.H_kv, spec.N, spec.d), np.float32)
     for bi, s in enumerate(seqs):
         xs = tokens(spec, "keys", spec.N, layer, seq=s)
         keys[bi] = _project(xs, wk)
+        if with_values:
+            out["values"][bi] = _project(xs, wv)
         if spec.causal:
             queries[bi] = _project(xs[spec.q_start:spec.q_start + spec.Q], wq)
         else:
