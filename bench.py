@@ -47,6 +47,8 @@ def parse():
                     help="factors of the batched layer: the paper's optimum, its span "
                          "variants (Sec. 6) or the key-PCA baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-attend", action="store_true",
+                    help="decode: leave out reading the winners (RoPE attention over the top-64)")
     ap.add_argument("--cpu-heads", type=int, default=4,
                     help="query heads of the CPU-baseline sample (one KV group)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -188,10 +190,12 @@ def run_decode(args, spec):
     from paper_2608_03228_amd import saki as S
     r, sk, k = args.r, args.sketch, args.k
     dev = torch.device("cuda:0")
+    attend = not args.no_attend
     t_gen = time.perf_counter()
-    inp = W.make_layer(spec)
+    inp = W.make_layer(spec, with_values=attend)
     t_gen = time.perf_counter() - t_gen
     keys = torch.from_numpy(inp["keys"]).to(dev)
+    values = torch.from_numpy(inp.pop("values")).to(dev) if attend else None
     B, H_kv, N, d = keys.shape
     H_q, Q = spec.H_q, spec.Q
     n_q = args.warmup + args.steps
@@ -216,9 +220,11 @@ def run_decode(args, spec):
     top_sc = torch.empty((n_q, B, H_q, Q, k), dtype=torch.float32, device=dev)
     ev = []
 
+    att_out = torch.empty((B, H_q, Q, d), dtype=torch.float32, device=dev)
+
     def step(s, timed=False):
         if timed:
-            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
             e[0].record()
         S.saki_build_index(keys, Bk, mu, r, sk, IH, index=index, n_begin=N - 1, n_count=1)
         if timed:
@@ -227,6 +233,10 @@ def run_decode(args, spec):
                           top_idx=top_idx[s], top_score=top_sc[s], index_heads=IH)
         if timed:
             e[2].record()
+        if attend:  # read the winners: exact keys and values, RoPE, softmax
+            S.saki_attend(values, qs[s], top_idx[s], N, keys=keys, out=att_out)
+        if timed:
+            e[3].record()
             ev.append(e)
 
     for s in range(args.warmup):
@@ -239,6 +249,7 @@ def run_decode(args, spec):
     dt = (time.perf_counter() - t0) / args.steps
     append_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
     score_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    attend_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
 
     # exact recall of every step (evaluation, outside the timed loop)
     wsr = torch.empty(max(1, S.saki_recall_workspace_bytes(B, H_q, H_kv, Q, N, d, k)),
@@ -284,10 +295,13 @@ def run_decode(args, spec):
         "config": {"workload": spec.name, "H_q": H_q, "H_kv": H_kv, "d": d, "latent_D": spec.D,
                    "N": N, "queries_per_head": Q, "batch": B, "r": r, "sketch": sk, "k": k,
                    "index": "gqa_shared" if args.shared else "per_query_head",
-                   "step": "append one key + score + top-64 (index built once)"},
+                   "step": "append one key + score + top-64" +
+                           (" + RoPE attention over the top-64" if attend else "") +
+                           " (index built once)"},
         "roofline": roof,
         "cpu_baseline": cpu,
         "stages_ms": {"append": append_ms, "score_topk": score_ms,
+                      "attend_top64": attend_ms if attend else None,
                       "build_full_once": build_full_ms, "recall_eval": recall_ms,
                       "input_generation_s": t_gen * 1e3},
         "recall_at_64": {"median_over_heads": float(np.median(per_head)),

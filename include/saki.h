@@ -255,6 +255,46 @@ int saki_recall(const void* keys, int key_dtype, const float* q, const int* q_po
                 int k, const int* approx_idx, int* hits, int* exact_idx,
                 void* ws, size_t ws_bytes, void* stream);
 
+/* Where saki_attend takes the selected keys from. */
+enum {
+  SAKI_KEYS_EXACT = 0,         /* the key cache (exact keys fetched for the winners) */
+  SAKI_KEYS_RECONSTRUCTED = 1  /* mu + B_q c_j from the index codes (Sec. 6) */
+};
+
+/*
+ * saki_attend (GPU) -- reading the index's winners (Sec. 1: the index
+ * nominates candidates and only they are read; Sec. 3 and 6: codes are
+ * pre-RoPE, the rotation is applied after reconstruction).  For every
+ * (sequence, head, query) row, attention over the keys listed in top_idx,
+ * in RoPE space:
+ *   s_j = rope(q_i, pos_i) . rope(key_j, j) / sqrt(d),  p = softmax(s),
+ *   out_i = sum_j p_j v_j,
+ * where key_j is the cached key (SAKI_KEYS_EXACT) or its reconstruction
+ * k_hat_j = mu + M_r (k_j - mu) = mu + B_q c_j from the index codes
+ * (SAKI_KEYS_RECONSTRUCTED).  rope rotates the pairs (x_m, x_{m+d/2}),
+ * m < d/2, by pos * rope_theta^(-2m/d); key j sits at position j, query i at
+ * q_pos[i], or at N_valid - 1 when q_pos is NULL (a decode query attends as
+ * the newest token).  Entries of top_idx < 0 are skipped; a row with none
+ * writes zeros.  Scores and the softmax are float32; the rotation angles are
+ * reduced in float64.
+ *
+ *   keys     device [B, H_kv, N_cap, d] key_dtype (read for SAKI_KEYS_EXACT, else may be NULL)
+ *   values   device float [B, H_kv, N_cap, d]
+ *   index    device index of saki_build_index (read for SAKI_KEYS_RECONSTRUCTED,
+ *            else may be NULL), sketch_dtype and index_heads as for saki_score_topk
+ *   q        device float [B, H_q, Q, d] (pre-RoPE);  q_pos device int [Q] or NULL
+ *   B_q      device float [H_q, d, r];  mu device float [H_kv, d] (reconstruction)
+ *   top_idx  device int [B, H_q, Q, k], k <= 64, entries < N_valid
+ *   out      device float [B, H_q, Q, d]
+ * d must be 128.  Errors: SAKI_ERR_ARG on bad sizes or pointers,
+ * SAKI_ERR_UNSUPPORTED on unsupported d, r, k or dtypes.
+ */
+int saki_attend(const void* keys, int key_dtype, const float* values, const void* index,
+                int sketch_dtype, int key_source, int B, int H_q, int H_kv, int index_heads,
+                int N_cap, int N_valid, int d, int r, const float* q, const int* q_pos, int Q,
+                const float* B_q, const float* mu, const int* top_idx, int k,
+                float rope_theta, float* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -2169,6 +2169,176 @@ __global__ __launch_bounds__(256) void moments_kernel(const float* __restrict__ 
   if (key && bi == 0 && ty == 0 && j < d) mu_out[(size_t)hh * d + j] = mean[kMomTile + tx];
 }
 
+// ---------------------------------------------------------------- reading the winners
+
+__device__ __forceinline__ float wave_sum_f32(float v) {
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) v += xor_shfl_f32(v, m);
+  return v;
+}
+
+// sin and cos of pos * inv (radians): the product and its reduction to
+// [-pi, pi] in float64, the functions in float32.
+__device__ __forceinline__ void rope_sincos(int pos, double inv, float* s, float* c) {
+  constexpr double kTwoPi = 6.283185307179586476925286766559;
+  const double a = (double)pos * inv;
+  const float red = (float)(a - kTwoPi * rint(a / kTwoPi));
+  sincosf(red, s, c);
+}
+
+constexpr int kAttendWaves = 4;
+constexpr int kAttendBatch = 16;  // selected keys whose loads are issued together
+
+// grid (ceil(Q / 4), B * H_q), block 256: one wave per (sequence, head, query)
+// row.  Lane l holds dims l and l + 64 of the rotated query and of each
+// selected key, so that the RoPE pairs (m, m + d/2) stay inside a lane; a
+// key's score is a wave sum.  The row's list is read once (entry e in lane
+// e) and the keys are taken in batches of 16 whose loads (or, for
+// reconstruction, code unpacking into LDS) are issued together.  Lane e ends
+// with entry e's score, then the softmax and the weighted sum of the values.
+template <int RK, bool KBF, int ST, bool RECON>
+__global__ __launch_bounds__(kAttendWaves * kWave) void attend_kernel(
+    const void* __restrict__ keys, const float* __restrict__ values,
+    const uint8_t* __restrict__ index, int n_tiles, int H_q, int H_kv, int index_heads,
+    int N_cap, int N_valid, const float* __restrict__ q, const int* __restrict__ q_pos, int Q,
+    const float* __restrict__ Bq, const float* __restrict__ mu,
+    const int* __restrict__ top_idx, int k, float log_theta, float* __restrict__ out) {
+  constexpr int D = saki::kHeadDim;
+  constexpr int HALF = D / 2;
+  static_assert(HALF == kWave, "one RoPE pair per lane");
+  constexpr int ES = code_bytes<ST>();
+  constexpr int CPP = saki::kChunkBytes / ES;
+  constexpr int NP = RK / CPP;
+  constexpr size_t TB = (size_t)kTile * RK * ES;
+  __shared__ float bq_s[RECON ? D : 1][RECON ? RK + 1 : 1];
+  __shared__ float code_s[kAttendWaves][RECON ? kAttendBatch : 1][RECON ? RK : 1];
+  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const size_t bh = blockIdx.y;
+  const int h = (int)(bh % H_q);
+  const size_t b = bh / H_q;
+  const int g = h / (H_q / H_kv);
+  if constexpr (RECON) {
+    for (int e = threadIdx.x; e < D * RK; e += blockDim.x)
+      bq_s[e / RK][e % RK] = Bq[(size_t)h * D * RK + e];
+    __syncthreads();
+  }
+  const int i = blockIdx.x * kAttendWaves + wave;
+  if (i >= Q) return;  // uniform over the wave, after the work-group barrier
+  const size_t row = bh * Q + i;
+  const size_t kbase = ((size_t)b * H_kv + g) * N_cap;
+  const size_t cset = b * index_heads + h / (H_q / index_heads);
+  const double inv = exp(-(2.0 * lane / D) * (double)log_theta);  // theta^(-2l/d)
+  float qa, qb;
+  {
+    float s, c;
+    rope_sincos(q_pos ? q_pos[i] : N_valid - 1, inv, &s, &c);
+    const float a0 = q[row * D + lane], a1 = q[row * D + lane + HALF];
+    qa = a0 * c - a1 * s;
+    qb = a1 * c + a0 * s;
+  }
+  const int my_j = lane < k ? top_idx[row * k + lane] : -1;
+  const float mu0 = RECON ? mu[(size_t)g * D + lane] : 0.f;
+  const float mu1 = RECON ? mu[(size_t)g * D + lane + HALF] : 0.f;
+  float my_s = -INFINITY;  // lane e: score of list entry e
+  for (int e0 = 0; e0 < k; e0 += kAttendBatch) {
+    int jj[kAttendBatch];
+    float k0[kAttendBatch], k1[kAttendBatch];
+#pragma unroll
+    for (int u = 0; u < kAttendBatch; ++u) {
+      const int e = e0 + u;
+      const int j = e < k ? __builtin_amdgcn_readlane(my_j, e) : -1;
+      jj[u] = j < N_valid ? j : -1;  // entries outside [0, N_valid) are skipped
+    }
+    if constexpr (RECON) {
+      for (int t0 = 0; t0 < kAttendBatch * NP; t0 += kWave) {
+        // lane t0 + lane unpacks piece p of entry e0 + u; the list entry is
+        // read from its lane by every lane of the wave (all lanes active)
+        const int t = t0 + lane;
+        const int u = min(t / NP, kAttendBatch - 1), p = t % NP;
+        int j = __shfl(my_j, min(e0 + u, kWave - 1), kWave);
+        j = j >= 0 && j < N_valid ? j : 0;  // a skipped entry reads key 0
+        if (t < kAttendBatch * NP) {
+          const uint4 v = *reinterpret_cast<const uint4*>(
+              index + (cset * n_tiles + j / kTile) * TB + (size_t)p * kTile * 16 + (size_t)(j % kTile) * 16);
+          float f[CPP];
+          unpack_codes<ST>(v, f);
+#pragma unroll
+          for (int c = 0; c < CPP; ++c) code_s[wave][u][p * CPP + c] = f[c];
+        }
+      }
+      wave_lds_sync();
+#pragma unroll
+      for (int u = 0; u < kAttendBatch; ++u) {
+        k0[u] = mu0;
+        k1[u] = mu1;
+      }
+#pragma unroll 2
+      for (int m = 0; m < RK; ++m) {  // k_hat = mu + B_q c, one code element of all 16 keys at a time
+        const float b0 = bq_s[lane][m], b1 = bq_s[lane + HALF][m];
+#pragma unroll
+        for (int u = 0; u < kAttendBatch; ++u) {
+          const float c = code_s[wave][u][m];
+          k0[u] = fmaf(b0, c, k0[u]);
+          k1[u] = fmaf(b1, c, k1[u]);
+        }
+      }
+      wave_lds_sync();  // the next batch overwrites the codes
+    } else {
+#pragma unroll
+      for (int u = 0; u < kAttendBatch; ++u) {
+        const size_t kr = (kbase + (size_t)max(jj[u], 0)) * D;  // a skipped entry reads key 0
+        k0[u] = load_key_elem<KBF>(keys, kr + lane);
+        k1[u] = load_key_elem<KBF>(keys, kr + lane + HALF);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kAttendBatch; ++u) {
+      float s, c;
+      rope_sincos(max(jj[u], 0), inv, &s, &c);
+      const float kb0 = k0[u] * c - k1[u] * s, kb1 = k1[u] * c + k0[u] * s;
+      const float sc = wave_sum_f32(fmaf(qa, kb0, qb * kb1)) * (1.f / 11.313708498984761f);
+      if (lane == e0 + u && jj[u] >= 0) my_s = sc;
+    }
+  }
+  // softmax over the list (an empty row writes zeros)
+  const float mx = wave_max_f32(my_s);
+  const float p = my_s == -INFINITY ? 0.f : expf(my_s - mx);
+  const float sum = wave_sum_f32(p);
+  float o0 = 0.f, o1 = 0.f;
+  for (int e0 = 0; e0 < k; e0 += kAttendBatch) {
+    float v0[kAttendBatch], v1[kAttendBatch], pe[kAttendBatch];
+#pragma unroll
+    for (int u = 0; u < kAttendBatch; ++u) {
+      const int e = min(e0 + u, kWave - 1);
+      int j = __builtin_amdgcn_readlane(my_j, e);
+      j = j >= 0 && j < N_valid ? j : 0;  // skipped entries have p = 0
+      pe[u] = e0 + u < k ? readlane_s(p, e) : 0.f;
+      const float* vr = values + (kbase + (size_t)j) * D;
+      v0[u] = vr[lane];
+      v1[u] = vr[lane + HALF];
+    }
+#pragma unroll
+    for (int u = 0; u < kAttendBatch; ++u) {
+      o0 = fmaf(pe[u], v0[u], o0);
+      o1 = fmaf(pe[u], v1[u], o1);
+    }
+  }
+  const float isum = sum > 0.f ? 1.f / sum : 0.f;
+  out[row * D + lane] = o0 * isum;
+  out[row * D + lane + HALF] = o1 * isum;
+}
+
+template <int RK, bool KBF, int ST, bool RECON>
+void launch_attend(const void* keys, const float* values, const uint8_t* index, int B, int H_q,
+                   int H_kv, int index_heads, int N_cap, int N_valid, const float* q,
+                   const int* q_pos, int Q, const float* Bq, const float* mu, const int* top_idx,
+                   int k, float rope_theta, float* out, hipStream_t s) {
+  dim3 grid((unsigned)((Q + kAttendWaves - 1) / kAttendWaves), (unsigned)(B * H_q));
+  hipLaunchKernelGGL((attend_kernel<RK, KBF, ST, RECON>), grid, dim3(kAttendWaves * kWave), 0, s,
+                     keys, values, index, (int)saki::n_tiles(N_cap), H_q, H_kv, index_heads, N_cap,
+                     N_valid, q, q_pos, Q, Bq, mu, top_idx, k, logf(rope_theta), out);
+}
+
 // ---------------------------------------------------------------- dispatch helpers
 
 bool launch_ok() { return hipGetLastError() == hipSuccess; }
@@ -2490,6 +2660,60 @@ int saki_recall(const void* keys, int key_dtype, const float* q, const int* q_po
   else
     launch_recall<false>(keys, q, q_pos, B, H_q, H_kv, N_cap, N_valid, Q, k, approx_idx, hits,
                          exact_idx, w, p, s);
+  return launch_ok() ? SAKI_OK : SAKI_ERR_HIP;
+}
+
+int saki_attend(const void* keys, int key_dtype, const float* values, const void* index,
+                int sketch_dtype, int key_source, int B, int H_q, int H_kv, int index_heads,
+                int N_cap, int N_valid, int d, int r, const float* q, const int* q_pos, int Q,
+                const float* B_q, const float* mu, const int* top_idx, int k,
+                float rope_theta, float* out, void* stream) {
+  int st = check_common(B, H_q, H_kv, N_cap, N_valid, d);
+  if (st != SAKI_OK) return st;
+  if (Q < 0 || k < 1 || !(rope_theta > 0.f) || !std::isfinite(rope_theta)) return SAKI_ERR_ARG;
+  if (k > kMaxK) return SAKI_ERR_UNSUPPORTED;
+  const bool recon = key_source == SAKI_KEYS_RECONSTRUCTED;
+  if (key_source != SAKI_KEYS_EXACT && !recon) return SAKI_ERR_ARG;
+  if (Q == 0) return SAKI_OK;
+  if (N_valid < 1 || !values || !q || !top_idx || !out) return SAKI_ERR_ARG;
+  if (recon) {
+    if (!index || !B_q || !mu) return SAKI_ERR_ARG;
+    if (index_heads <= 0 || H_q % index_heads != 0 || index_heads % H_kv != 0) return SAKI_ERR_ARG;
+    if (!sketch_ok(sketch_dtype) || !saki::rank_supported(r)) return SAKI_ERR_UNSUPPORTED;
+  } else {
+    if (!keys) return SAKI_ERR_ARG;
+    if (!dtype_ok(key_dtype)) return SAKI_ERR_UNSUPPORTED;
+  }
+  if ((Q + kAttendWaves - 1) / kAttendWaves > 0x7fffffff) return SAKI_ERR_UNSUPPORTED;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const uint8_t* ix = reinterpret_cast<const uint8_t*>(index);
+#define SAKI_ATTEND(RK, KB, ST, RC)                                                              \
+  launch_attend<RK, KB, ST, RC>(keys, values, ix, B, H_q, H_kv, index_heads, N_cap, N_valid, q, \
+                                q_pos, Q, B_q, mu, top_idx, k, rope_theta, out, s)
+#define SAKI_ATTEND_R(RK)                              \
+  do {                                                 \
+    if (sketch_dtype == SAKI_FP8)                      \
+      SAKI_ATTEND(RK, false, kStFp8, true);            \
+    else if (sketch_dtype == SAKI_BF16)                \
+      SAKI_ATTEND(RK, false, kStBf16, true);           \
+    else                                               \
+      SAKI_ATTEND(RK, false, kStF32, true);            \
+  } while (0)
+  if (!recon) {
+    if (key_dtype == SAKI_BF16)
+      SAKI_ATTEND(32, true, kStF32, false);
+    else
+      SAKI_ATTEND(32, false, kStF32, false);
+  } else {
+    switch (r) {
+      case 16: SAKI_ATTEND_R(16); break;
+      case 32: SAKI_ATTEND_R(32); break;
+      case 64: SAKI_ATTEND_R(64); break;
+      default: SAKI_ATTEND_R(128); break;
+    }
+  }
+#undef SAKI_ATTEND_R
+#undef SAKI_ATTEND
   return launch_ok() ? SAKI_OK : SAKI_ERR_HIP;
 }
 

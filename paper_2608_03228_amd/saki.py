@@ -59,6 +59,8 @@ def lib():
         "saki_recall_workspace_bytes": (sz, [ip, ip, ip, ip, ip, ip, ip]),
         "saki_recall": (ip, [vp, ip, vp, vp, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, vp, vp,
                              sz, vp]),
+        "saki_attend": (ip, [vp, ip, vp, vp, ip, ip, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, ip,
+                             vp, vp, vp, ip, C.c_float, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -310,3 +312,39 @@ def saki_recall(keys, q, approx_idx, N_valid: int, q_pos=None, k: int = 64, ws=N
         _dev(ws, (torch.uint8,), "ws"), ws.numel(), _stream(stream))
     _check("saki_recall", st)
     return hits, (exact_idx if want_exact else None)
+
+
+KEYS_EXACT, KEYS_RECONSTRUCTED = 0, 1
+ROPE_THETA = 500000.0
+
+
+def saki_attend(values, q, top_idx, N_valid: int, keys=None, index=None, sketch: str = "bf16",
+                B_q=None, mu=None, r: int = 32, index_heads=None, q_pos=None,
+                rope_theta: float = ROPE_THETA, out=None, stream=None):
+    """Attention of every (sequence, head, query) row over its listed keys in
+    RoPE space.  values [B, H_kv, N_cap, d] f32, q [B, H_q, Q, d] f32,
+    top_idx [B, H_q, Q, k] int32 (CUDA).  Keys come from `keys` (exact) or,
+    when `keys` is None, are reconstructed as mu + B_q c from `index`.
+    Returns out [B, H_q, Q, d] float32."""
+    torch = _torch()
+    vp_ = _dev(values, (torch.float32,), "values")
+    qp = _dev(q, (torch.float32,), "q")
+    B, H_kv, N_cap, d = values.shape
+    _, H_q, Q, _ = q.shape
+    k = top_idx.shape[-1]
+    if out is None:
+        out = torch.empty((B, H_q, Q, d), dtype=torch.float32, device=q.device)
+    recon = keys is None
+    pos = _dev(q_pos, (torch.int32,), "q_pos") if q_pos is not None else None
+    st = lib().saki_attend(
+        None if recon else _dev(keys, (torch.float32, torch.bfloat16), "keys"),
+        F32 if recon else _key_dtype(keys), vp_,
+        _dev(index, (torch.uint8,), "index") if recon else None, _DTYPES[sketch],
+        KEYS_RECONSTRUCTED if recon else KEYS_EXACT, B, H_q, H_kv,
+        int(index_heads if index_heads is not None else H_q), N_cap, int(N_valid), d, int(r), qp,
+        pos, Q, _dev(B_q, (torch.float32,), "B_q") if recon else None,
+        _dev(mu, (torch.float32,), "mu") if recon else None,
+        _dev(top_idx, (torch.int32,), "top_idx"), int(k), float(rope_theta),
+        _dev(out, (torch.float32,), "out"), _stream(stream))
+    _check("saki_attend", st)
+    return out

@@ -311,6 +311,26 @@ def test_argument_validation_without_launch(lib):
                            1 << 30, None) == ERR_ARG
     assert lib.saki_recall(P, 3, P, None, 1, 1, 1, 256, 256, 4, 128, 64, P, P, None, P,
                            1 << 30, None) == ERR_UNSUP
+    # attend: k > 64, d != 128, bad key source, no valid key, missing index
+    #   (keys, key_dtype, values, index, sketch, source, B, H_q, H_kv, index_heads,
+    #    N_cap, N_valid, d, r, q, q_pos, Q, B_q, mu, top_idx, k, theta, out, stream)
+    def attend(**kw):
+        a = dict(keys=P, key_dtype=0, values=P, index=P, sketch=1, source=0, B=1, H_q=2, H_kv=1,
+                 index_heads=2, N_cap=256, N_valid=256, d=128, r=32, q=P, q_pos=None, Q=4, B_q=P,
+                 mu=P, top_idx=P, k=64, theta=500000.0, out=P)
+        a.update(kw)
+        return lib.saki_attend(*a.values(), None)
+    assert attend(k=65) == ERR_UNSUP
+    assert attend(d=64) == ERR_UNSUP
+    assert attend(source=2) == ERR_ARG
+    assert attend(N_valid=0) == ERR_ARG
+    assert attend(theta=0.0) == ERR_ARG
+    assert attend(keys=None) == ERR_ARG
+    assert attend(source=1, index=None) == ERR_ARG
+    assert attend(source=1, r=48) == ERR_UNSUP
+    assert attend(source=1, index_heads=3) == ERR_ARG
+    assert attend(key_dtype=2) == ERR_UNSUP  # fp8 is a code type, not a key type
+    assert attend(Q=0) == 0
     # calibration: H_q not a multiple of H_kv, r > d, null output
     f = np.zeros((2, 8, 4), np.float32)
     out = np.zeros(64, np.float32)
