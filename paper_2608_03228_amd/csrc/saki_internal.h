@@ -37,6 +37,7 @@ struct Plan {
   int rows = 1;        // query rows per wave
   int waves = 1;       // waves per workgroup
   int row_blocks = 0;  // workgroups along the query axis
+  bool split = false;  // streaming: the waves of a workgroup share rows and take consecutive chunks
   int chunk = kTile;   // keys per chunk (multiple of 64)
   int n_chunks = 1;
   size_t z_off = 0, b_off = 0, part_off = 0, flag_off = 0, ws_bytes = 0;
@@ -76,21 +77,23 @@ inline Plan make_plan(int B, int heads, int Q, int N_valid, int part_entry_bytes
   return p;
 }
 
-// Score path: query sketch z [rows, r] and mean term b [rows] (float32) come
-// first in the workspace, then the partial lists (float score + int index).
+// Score path: the workspace holds the partial lists of a split key axis
+// (float score + int index), at least 256 bytes so that a size of 0 keeps
+// meaning invalid arguments.  Both kernels form the query sketch themselves.
 // The MFMA kernel takes 16 queries of one head per wave; the streaming kernel
 // takes the rows of one code set: the H_q / index_heads heads sharing it,
 // times Q.
-inline Plan score_plan(int B, int H_q, int index_heads, int Q, int N_valid, int r) {
+inline Plan score_plan(int B, int H_q, int index_heads, int Q, int N_valid) {
   const bool mfma = Q >= 16;
   Plan p = mfma ? make_plan(B, H_q, Q, N_valid, 8, true)
                 : make_plan(B, index_heads, (H_q / index_heads) * Q, N_valid, 8, false);
-  const size_t rows_total = (size_t)B * H_q * Q;
-  p.z_off = 0;
-  p.b_off = round_up(rows_total * r * sizeof(float), 256);
-  const size_t base = round_up(p.b_off + rows_total * sizeof(float), 256);
-  if (p.n_chunks > 1) p.part_off = base;
-  p.ws_bytes = base + p.ws_bytes;
+  const int wave_rows = (int)((H_q / index_heads) * (size_t)Q + p.rows - 1) / p.rows;
+  if (!mfma && wave_rows < 4) {  // too few rows to fill a workgroup: its waves split the keys
+    p.split = true;
+    p.waves = 4;
+    p.row_blocks = wave_rows < 1 ? 1 : wave_rows;
+  }
+  if (p.ws_bytes < 256) p.ws_bytes = 256;
   return p;
 }
 

@@ -1,16 +1,19 @@
 // GPU side of libsaki for gfx950 (CDNA4, wave64).
 //
-// Kernels (one launch each, all on the caller's stream):
+// Kernels (all on the caller's stream):
 //   build_index_kernel   key codes c = B_k^T (k - mu) for every query head (Eq. 4)
-//   query_sketch_kernel  z = B_q^T q and b = q^T mu per query row (Sec. 6)
-//   score_mfma_kernel    s = z . c + b on MFMA for blocks of 16 query rows,
-//                        running top-64 per row
-//   score_stream_kernel  the same for few query rows per head (decode): one
-//                        key per lane, float32 dot products, key range split
-//                        into chunks across waves
-//   exact_mfma_kernel    exact float64 q . k (f64 MFMA), top-64, recall hits
-//   exact_stream_kernel  the same with float64 FMAs for few query rows
+//   score_mfma_kernel    z = B_q^T q, b = q^T mu and s = z . c + b on MFMA for
+//                        blocks of 16 query rows, top-64 per row
+//   score_stream_kernel  the same for few query rows per code set (decode):
+//                        one key per lane, key range split into chunks
 //   merge_kernel         reduces per-chunk partial top-64 lists of one row
+//   keys_hi_kernel       bf16 hi/lo split of the keys and their norm bounds
+//   exact_gate_kernel    exact top-64 and recall hits: float32 gate from the
+//                        candidate list, bf16x3 MFMA scan, float64 decisions
+//   exact_bf16_kernel, exact_mfma_kernel  fallback tiers of the same
+//   exact_stream_kernel  exact float64 scores and top-64 for few query rows
+//   moments_kernel       calibration moments in float64
+//   attend_kernel        RoPE attention over the selected keys
 //   export_kernel        debug read-back of the codes
 // Top-k selection is in saki_topk.h.
 
@@ -82,6 +85,18 @@ __device__ __forceinline__ float load_key_elem(const void* p, size_t i) {
     return __uint_as_float((uint32_t)v << 16);
   } else {
     return reinterpret_cast<const float*>(p)[i];
+  }
+}
+
+// Key elements i .. i + 3 (i a multiple of 4) as floats.
+template <bool BF>
+__device__ __forceinline__ float4 load_key4(const void* p, size_t i) {
+  if constexpr (BF) {
+    const uint2 v = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(p) + i);
+    return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                       __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
+  } else {
+    return *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p) + i);
   }
 }
 
@@ -192,14 +207,44 @@ __global__ __launch_bounds__(256) void build_index_kernel(
   const int g = h / (H_q / H_kv);
   const int tid = threadIdx.x;
   const size_t key_base = ((size_t)b * H_kv + g) * N_cap;
-  for (int i = tid; i < kTile * D; i += 256) {
-    const int t = i / D, c = i % D;
-    const int n = tile * kTile + t;
-    float v = 0.f;
-    if (n < N_cap) v = load_key_elem<KBF>(keys, (key_base + n) * D + c) - mu[(size_t)g * D + c];
-    ks[t][c] = v;
+  // stage the centred keys of the tile and B_k with every load issued before
+  // the LDS stores (a one-key append is then one load latency, not dozens);
+  // rows outside [n_begin, n_end) are not written out and stage as zeros.
+  // Thread tid takes dims c .. c + 3 of rows tid / 32 + 8u, and four
+  // consecutive elements of B_k per group.
+  constexpr int KG = kTile * D / 4 / 256;
+  constexpr int BG = D * RK / 4 / 256;
+  static_assert(KG * 1024 == kTile * D && BG * 1024 == D * RK, "staging shape");
+  const int c = (tid * 4) % D;
+  float4 kv[KG], bv[BG];
+#pragma unroll
+  for (int u = 0; u < KG; ++u) {
+    const int n = tile * kTile + (tid * 4 + u * 1024) / D;
+    kv[u] = n >= n_begin && n < n_end ? load_key4<KBF>(keys, (key_base + n) * D + c)
+                                      : make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  for (int i = tid; i < D * RK; i += 256) bk[i / RK][i % RK] = Bk[(size_t)h * D * RK + i];
+#pragma unroll
+  for (int u = 0; u < BG; ++u)
+    bv[u] = *reinterpret_cast<const float4*>(Bk + (size_t)h * D * RK + (size_t)tid * 4 + u * 1024);
+  const float4 m4 = *reinterpret_cast<const float4*>(mu + (size_t)g * D + c);
+#pragma unroll
+  for (int u = 0; u < KG; ++u) {
+    const int t = (tid * 4 + u * 1024) / D;
+    const int n = tile * kTile + t;
+    const bool in = n >= n_begin && n < n_end;
+    ks[t][c] = in ? kv[u].x - m4.x : 0.f;
+    ks[t][c + 1] = in ? kv[u].y - m4.y : 0.f;
+    ks[t][c + 2] = in ? kv[u].z - m4.z : 0.f;
+    ks[t][c + 3] = in ? kv[u].w - m4.w : 0.f;
+  }
+#pragma unroll
+  for (int u = 0; u < BG; ++u) {
+    const int e = tid * 4 + u * 1024;
+    bk[e / RK][e % RK] = bv[u].x;
+    bk[e / RK][e % RK + 1] = bv[u].y;
+    bk[e / RK][e % RK + 2] = bv[u].z;
+    bk[e / RK][e % RK + 3] = bv[u].w;
+  }
   __syncthreads();
   uint8_t* tbase = index + (((size_t)b * H_q + h) * n_tiles + tile) * ((size_t)kTile * RK * ES);
   for (int p = tid; p < kTile * NP; p += 256) {
@@ -260,48 +305,6 @@ __global__ __launch_bounds__(64) void export_kernel(const uint8_t* __restrict__ 
   }
 }
 
-// ---------------------------------------------------------------- query sketch
-
-// grid (ceil(Q/16), B*H_q), block 256.  z = B_q^T q (float32, rounded to bf16
-// when the codes are bf16 or fp8), b = q^T mu.
-template <int RK, int ST>
-__global__ __launch_bounds__(256) void query_sketch_kernel(
-    const float* __restrict__ q, const float* __restrict__ Bq,
-    const float* __restrict__ mu, int H_q, int H_kv, int Q, float* __restrict__ z,
-    float* __restrict__ bout) {
-  constexpr int D = saki::kHeadDim;
-  constexpr int QR = 16;
-  __shared__ float bq[D][RK];
-  __shared__ float qs[QR][D];
-  __shared__ float ms[D];
-  const int bh = blockIdx.y;
-  const int h = bh % H_q;
-  const int g = h / (H_q / H_kv);
-  const int i0 = blockIdx.x * QR;
-  const int tid = threadIdx.x;
-  for (int i = tid; i < D * RK; i += 256) bq[i / RK][i % RK] = Bq[(size_t)h * D * RK + i];
-  for (int i = tid; i < QR * D; i += 256) {
-    const int rr = i / D;
-    qs[rr][i % D] = (i0 + rr < Q) ? q[((size_t)bh * Q + i0 + rr) * D + (i % D)] : 0.f;
-  }
-  if (tid < D) ms[tid] = mu[(size_t)g * D + tid];
-  __syncthreads();
-  for (int o = tid; o < QR * (RK + 1); o += 256) {
-    const int rr = o / (RK + 1), m = o % (RK + 1);
-    const int i = i0 + rr;
-    if (i >= Q) continue;
-    float acc = 0.f;
-    if (m < RK) {
-      for (int c = 0; c < D; ++c) acc = fmaf(qs[rr][c], bq[c][m], acc);
-      if (ST != kStF32) acc = bf16_round(acc);
-      z[((size_t)bh * Q + i) * RK + m] = acc;
-    } else {
-      for (int c = 0; c < D; ++c) acc = fmaf(qs[rr][c], ms[c], acc);
-      bout[(size_t)bh * Q + i] = acc;
-    }
-  }
-}
-
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ bf16x2_t as_bf16x2(uint32_t v) {
   bf16x2_t r;
@@ -316,34 +319,47 @@ __device__ __forceinline__ bf16x2_t as_bf16x2(uint32_t v) {
 // numbered rho = i * gq + (h % gq) so that one wave's R rows are the heads
 // sharing the codes (for a GQA-shared index) before further queries.  Each
 // wave owns R rows and one key chunk; lane t scores key t of each 64-key tile.
+// With `split` (fewer than four waves' worth of rows per code set) the four
+// waves of a work-group share their R rows and take four consecutive chunks.
+// The query sketch of the rows (Sec. 6: z = B_q^T q, rounded to bf16 for bf16
+// and fp8 codes, and b = q^T mu, float32 sums) is formed before the scan: by
+// the four waves together when they share rows (wave w sums dims 32w ..
+// 32w + 31, the four partial sums are added in wave order), otherwise by
+// each wave for its own rows (dims in order).  The first code tiles are
+// requested before the sketch, so that its loads wait under theirs.
 template <int RK, int ST, int R>
 __global__ __launch_bounds__(256) void score_stream_kernel(
     const uint8_t* __restrict__ index, int n_tiles, int N_valid, int Q,
-    const int* __restrict__ q_pos, const float* __restrict__ z,
-    const float* __restrict__ bvec, int H_q, int gq, int row_blocks, int chunk, int n_chunks,
-    int k, int* __restrict__ top_idx, float* __restrict__ top_score,
+    const int* __restrict__ q_pos, const float* __restrict__ q, const float* __restrict__ Bq,
+    const float* __restrict__ mu, int H_q, int H_kv, int gq, int row_blocks, int chunk,
+    int n_chunks, int split, int k, int* __restrict__ top_idx, float* __restrict__ top_score,
     uint64_t* __restrict__ part) {
   constexpr int ES = code_bytes<ST>();
   constexpr int CPP = saki::kChunkBytes / ES;
   constexpr int NP = RK / CPP;
   constexpr size_t TB = (size_t)kTile * RK * ES;
   using KO = KeysF32;
-  __shared__ float zs[kStreamWaves][R][RK];
+  constexpr int D = saki::kHeadDim;
+  constexpr int NO = R * (RK + 1);  // sketch outputs of R rows
+  __shared__ float zs[kStreamWaves][R][RK + 1];  // element RK: the mean term b
+  __shared__ float zpart[kStreamWaves][NO];      // split: partial sums of wave w
   __shared__ uint64_t lmem[kStreamWaves][R][kList];
   __shared__ uint64_t bmem[kStreamWaves][R][kList];
-  const int wave = threadIdx.x / kWave, lane = lane_id();
+  // the wave index is uniform over the wave: say so, so that what depends on
+  // it (the sketch's dim slice, the chunk) stays in scalar registers
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = lane_id();
   const int waves = blockDim.x / kWave;
-  const int rb = blockIdx.x % row_blocks, ch = blockIdx.x / row_blocks;
+  const int rb = blockIdx.x % row_blocks;
+  const int ch = split ? (blockIdx.x / row_blocks) * waves + wave : blockIdx.x / row_blocks;
   const size_t bi = blockIdx.y;  // b * index_heads + code set
   const int index_heads = H_q / gq;
   const size_t b = bi / index_heads;
   const int ih = (int)(bi % index_heads);
   const int n_rho = gq * Q;
-  const int row0 = (rb * waves + wave) * R;
-  if (row0 >= n_rho) return;
+  const int row0 = split ? rb * R : (rb * waves + wave) * R;
+  if (row0 >= n_rho) return;  // never with split (row_blocks = ceil(n_rho / R))
 
   int lim[R];
-  float bb[R];
   size_t flat[R];  // (b * H_q + h) * Q + i of each row
   int kmax = 0;
 #pragma unroll
@@ -355,11 +371,6 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
     flat[r] = (b * H_q + h) * Q + i;
     lim[r] = ok ? row_limit(i, Q, N_valid, q_pos) : 0;
     kmax = lim[r] > kmax ? lim[r] : kmax;
-    bb[r] = ok ? bvec[flat[r]] : 0.f;
-  }
-  for (int i = lane; i < R * RK; i += kWave) {
-    const int r = i / RK;
-    zs[wave][r][i % RK] = (row0 + r < n_rho) ? z[flat[r] * RK + (i % RK)] : 0.f;
   }
   RowLists<KO, R> top;
   top.init(&lmem[wave][0][0], &bmem[wave][0][0]);
@@ -376,7 +387,85 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
 #pragma unroll
     for (int p = 0; p < PF; ++p) v[p] = *reinterpret_cast<const uint4*>(tb + (size_t)p * kTile * 16);
   };
+  // with at most 32 bytes of bf16 or fp8 code per key, two tiles are loaded
+  // ahead (into two buffers taken in turn) so that as many bytes are in
+  // flight as for wider codes; otherwise one
+  constexpr int kAhead = ST != kStF32 && NP * 16 <= 32 ? 2 : 1;
+  uint4 nxt2[PF];
   if (kbeg < kend) load_tile(kbeg, nxt);
+  if (kAhead == 2 && kbeg + kTile < kend) load_tile(kbeg + kTile, nxt2);
+  // the query sketch: output o = r * (RK + 1) + m of the rows in lane o % 64
+  // (m < RK: z_m, m = RK: b), loads taken 16 dims at a time
+  if (split) {
+    constexpr int DS = D / kStreamWaves;
+    static_assert(DS % 16 == 0, "dim slices of whole load groups");
+    for (int o0 = 0; o0 < NO; o0 += kWave) {
+      const int o = o0 + lane;
+      const int r = R == 1 ? 0 : min(o / (RK + 1), R - 1), m = o % (RK + 1);
+      const int rho = row0 + r;
+      const bool rv = rho < n_rho;
+      const int i = rv ? rho / gq : 0;
+      const int h = ih * gq + (rv ? rho % gq : 0);
+      const int stride = m < RK ? RK : 1;
+      const float* qv = q + ((b * H_q + h) * Q + i) * D + wave * DS;
+      const float* col = (m < RK ? Bq + (size_t)h * D * RK + m : mu + (size_t)(h / (H_q / H_kv)) * D) +
+                         (size_t)wave * DS * stride;
+      float acc = 0.f;
+#pragma unroll 1
+      for (int c0 = 0; c0 < DS; c0 += 16) {
+        float qa[16], ba[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          qa[u] = qv[c0 + u];
+          ba[u] = col[(size_t)(c0 + u) * stride];
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) acc = fmaf(qa[u], ba[u], acc);
+      }
+      if (o < NO) zpart[wave][o] = acc;
+    }
+    __syncthreads();
+    for (int o = lane; o < NO; o += kWave) {
+      const int r = o / (RK + 1), m = o % (RK + 1);
+      float v = ((zpart[0][o] + zpart[1][o]) + zpart[2][o]) + zpart[3][o];
+      if (ST != kStF32 && m < RK) v = bf16_round(v);
+      zs[wave][r][m] = row0 + r < n_rho ? v : 0.f;
+    }
+    wave_lds_sync();
+  } else {
+    constexpr int CG = 16;
+    for (int o0 = 0; o0 < NO; o0 += kWave) {
+      const int o = o0 + lane;
+      // with one row per wave the query row is the same in every lane
+      const int r = R == 1 ? 0 : min(o / (RK + 1), R - 1), m = o % (RK + 1);
+      const int rho = row0 + r;
+      const bool rv = rho < n_rho;
+      const bool ok = o < NO && rv;
+      const int i = rv ? rho / gq : 0;
+      const int h = ih * gq + (rv ? rho % gq : 0);
+      const float* qv = q + ((b * H_q + h) * Q + i) * D;
+      const float* col = m < RK ? Bq + (size_t)h * D * RK + m : mu + (size_t)(h / (H_q / H_kv)) * D;
+      const int stride = m < RK ? RK : 1;
+      float acc = 0.f;
+#pragma unroll 1
+      for (int c0 = 0; c0 < D; c0 += CG) {
+        float qa[CG], ba[CG];
+#pragma unroll
+        for (int u = 0; u < CG; ++u) {
+          qa[u] = qv[c0 + u];
+          ba[u] = col[(size_t)(c0 + u) * stride];
+        }
+#pragma unroll
+        for (int u = 0; u < CG; ++u) acc = fmaf(qa[u], ba[u], acc);
+      }
+      if (ST != kStF32 && m < RK) acc = bf16_round(acc);
+      if (o < NO) zs[wave][r][m] = ok ? acc : 0.f;
+    }
+    wave_lds_sync();
+  }
+  float bb[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) bb[r] = zs[wave][r][RK];
   if constexpr (ST != kStF32) {
     // bf16 codes: each 32-bit word holds elements (2e, 2e + 1), scored with
     // the packed bf16 dot product against the query sketch's pairs; fp8
@@ -393,10 +482,6 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
                            (__float_as_uint(zs[wave][r][2 * m + 1]) & 0xffff0000u);
         zp[r][m] = kScalarZ ? (uint32_t)__builtin_amdgcn_readfirstlane((int)v) : v;
       }
-    // with at most 32 bytes of code per key, two tiles are loaded ahead (into
-    // two buffers taken in turn) so that as many bytes are in flight as for
-    // wider codes; otherwise one
-    constexpr int kAhead = NP * 16 <= 32 ? 2 : 1;
     // one tile: the words of bf16 pairs from `cur` (and the pieces not
     // prefetched), then `refill` (which may reload cur's registers), then the
     // dot products
@@ -432,8 +517,6 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
       }
     };
     if constexpr (kAhead == 2) {
-      uint4 nxt2[PF];
-      if (kbeg + kTile < kend) load_tile(kbeg + kTile, nxt2);
       for (int t0 = kbeg; t0 < kend; t0 += 2 * kTile) {
         tile(t0, nxt, [&] { if (t0 + 2 * kTile < kend) load_tile(t0 + 2 * kTile, nxt); });
         if (t0 + kTile >= kend) break;
@@ -467,7 +550,7 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   }
   for (int r = 0; r < R; ++r) {
     top.finish(r);
-    if (row0 + r >= n_rho) continue;
+    if (row0 + r >= n_rho || ch >= n_chunks) continue;  // a split wave past the last chunk
     const uint64_t e = top.entry(r);
     if (n_chunks == 1) {
       if (lane < k) {
@@ -2067,17 +2150,26 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void merge_kernel(
   const int waves = blockDim.x / kWave;
   const size_t row = blockIdx.x;
   if (row >= rows) return;
-  // wave w merges partials w, w + waves, ..., four loads in flight at a time
+  // wave w merges partials w, w + waves, ..., eight at a time; the next
+  // eight are loaded before the current ones are merged
+  constexpr int kLoads = 8;
   K a = KO::pad();
-  for (int c0 = wave; c0 < n_chunks; c0 += 4 * waves) {
-    K b[4];
+  K nb[kLoads];
+  auto load = [&](int c0) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < kLoads; ++u) {
       const int c = c0 + u * waves;
-      b[u] = c < n_chunks ? part[(row * n_chunks + c) * kMaxK + lane] : KO::pad();
+      nb[u] = c < n_chunks ? part[(row * n_chunks + c) * kMaxK + lane] : KO::pad();
     }
+  };
+  if (wave < n_chunks) load(wave);
+  for (int c0 = wave; c0 < n_chunks; c0 += kLoads * waves) {
+    K b[kLoads];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < kLoads; ++u) b[u] = nb[u];
+    if (c0 + kLoads * waves < n_chunks) load(c0 + kLoads * waves);
+#pragma unroll
+    for (int u = 0; u < kLoads; ++u)
       // a partial is sorted: skip it when its best cannot enter the list
       if (KO::gt(KO::readlane(b[u], 0), KO::readlane(a, kWave - 1))) wave_merge<KO>(a, b[u]);
   }
@@ -2186,16 +2278,17 @@ __device__ __forceinline__ void rope_sincos(int pos, double inv, float* s, float
   sincosf(red, s, c);
 }
 
-constexpr int kAttendWaves = 4;
-constexpr int kAttendBatch = 16;  // selected keys whose loads are issued together
+constexpr int kAttendWaves = 4;   // waves per row
+constexpr int kAttendBatch = 16;  // list entries per wave: wave w takes 16w .. 16w + 15
 
-// grid (ceil(Q / 4), B * H_q), block 256: one wave per (sequence, head, query)
-// row.  Lane l holds dims l and l + 64 of the rotated query and of each
-// selected key, so that the RoPE pairs (m, m + d/2) stay inside a lane; a
-// key's score is a wave sum.  The row's list is read once (entry e in lane
-// e) and the keys are taken in batches of 16 whose loads (or, for
-// reconstruction, code unpacking into LDS) are issued together.  Lane e ends
-// with entry e's score, then the softmax and the weighted sum of the values.
+// grid (Q, B * H_q), block 256: one work-group per (sequence, head, query)
+// row, k <= 64.  Lane l holds dims l and l + 64 of the rotated query and of
+// each key, so that the RoPE pairs (m, m + d/2) stay inside a lane, and a
+// key's score is a wave sum.  Each wave gathers its 16 entries' keys (or, for
+// reconstruction, unpacks their codes into LDS and forms mu + B_q c) and
+// values in one round of loads, and keeps the softmax of its entries relative
+// to its own maximum; the four partial results are then rescaled to the
+// row's maximum and added.
 template <int RK, bool KBF, int ST, bool RECON>
 __global__ __launch_bounds__(kAttendWaves * kWave) void attend_kernel(
     const void* __restrict__ keys, const float* __restrict__ values,
@@ -2206,126 +2299,137 @@ __global__ __launch_bounds__(kAttendWaves * kWave) void attend_kernel(
   constexpr int D = saki::kHeadDim;
   constexpr int HALF = D / 2;
   static_assert(HALF == kWave, "one RoPE pair per lane");
+  static_assert(kAttendWaves * kAttendBatch == kWave, "the waves cover a 64-entry list");
   constexpr int ES = code_bytes<ST>();
   constexpr int CPP = saki::kChunkBytes / ES;
   constexpr int NP = RK / CPP;
   constexpr size_t TB = (size_t)kTile * RK * ES;
   __shared__ float bq_s[RECON ? D : 1][RECON ? RK + 1 : 1];
   __shared__ float code_s[kAttendWaves][RECON ? kAttendBatch : 1][RECON ? RK : 1];
+  __shared__ float part_m[kAttendWaves], part_l[kAttendWaves];
+  __shared__ float part_o[kAttendWaves][D];
   const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int i = blockIdx.x;
   const size_t bh = blockIdx.y;
   const int h = (int)(bh % H_q);
   const size_t b = bh / H_q;
   const int g = h / (H_q / H_kv);
-  if constexpr (RECON) {
-    for (int e = threadIdx.x; e < D * RK; e += blockDim.x)
-      bq_s[e / RK][e % RK] = Bq[(size_t)h * D * RK + e];
-    __syncthreads();
-  }
-  const int i = blockIdx.x * kAttendWaves + wave;
-  if (i >= Q) return;  // uniform over the wave, after the work-group barrier
   const size_t row = bh * Q + i;
   const size_t kbase = ((size_t)b * H_kv + g) * N_cap;
   const size_t cset = b * index_heads + h / (H_q / index_heads);
+  const int e0 = wave * kAttendBatch;
+  // lane u < 16: list entry e0 + u (-1 past k)
+  const int my_j = lane < kAttendBatch && e0 + lane < k ? top_idx[row * k + e0 + lane] : -1;
+  if constexpr (RECON) {
+    for (int e = threadIdx.x; e < D * RK; e += blockDim.x)
+      bq_s[e / RK][e % RK] = Bq[(size_t)h * D * RK + e];
+  }
   const double inv = exp(-(2.0 * lane / D) * (double)log_theta);  // theta^(-2l/d)
   float qa, qb;
   {
-    float s, c;
-    rope_sincos(q_pos ? q_pos[i] : N_valid - 1, inv, &s, &c);
+    float sn, cs;
+    rope_sincos(q_pos ? q_pos[i] : N_valid - 1, inv, &sn, &cs);
     const float a0 = q[row * D + lane], a1 = q[row * D + lane + HALF];
-    qa = a0 * c - a1 * s;
-    qb = a1 * c + a0 * s;
+    qa = a0 * cs - a1 * sn;
+    qb = a1 * cs + a0 * sn;
   }
-  const int my_j = lane < k ? top_idx[row * k + lane] : -1;
-  const float mu0 = RECON ? mu[(size_t)g * D + lane] : 0.f;
-  const float mu1 = RECON ? mu[(size_t)g * D + lane + HALF] : 0.f;
-  float my_s = -INFINITY;  // lane e: score of list entry e
-  for (int e0 = 0; e0 < k; e0 += kAttendBatch) {
-    int jj[kAttendBatch];
-    float k0[kAttendBatch], k1[kAttendBatch];
+  int jj[kAttendBatch];
+#pragma unroll
+  for (int u = 0; u < kAttendBatch; ++u) {
+    const int j = __builtin_amdgcn_readlane(my_j, u);
+    jj[u] = j < N_valid ? j : -1;  // entries outside [0, N_valid) are skipped
+  }
+  // keys (or codes) and values of the wave's entries; a skipped entry reads
+  // row 0 and gets weight 0
+  float k0[kAttendBatch], k1[kAttendBatch], v0[kAttendBatch], v1[kAttendBatch];
+#pragma unroll
+  for (int u = 0; u < kAttendBatch; ++u) {
+    const size_t kr = (kbase + (size_t)max(jj[u], 0)) * D;
+    v0[u] = values[kr + lane];
+    v1[u] = values[kr + lane + HALF];
+    if constexpr (!RECON) {
+      k0[u] = load_key_elem<KBF>(keys, kr + lane);
+      k1[u] = load_key_elem<KBF>(keys, kr + lane + HALF);
+    }
+  }
+  if constexpr (RECON) {
+    for (int t0 = 0; t0 < kAttendBatch * NP; t0 += kWave) {
+      // lane t0 + lane unpacks piece p of entry u; the entry is read from
+      // its lane by every lane of the wave (all lanes active)
+      const int t = t0 + lane;
+      const int u = min(t / NP, kAttendBatch - 1), p = t % NP;
+      int j = __shfl(my_j, u, kWave);
+      j = j >= 0 && j < N_valid ? j : 0;
+      if (t < kAttendBatch * NP) {
+        const uint4 v = *reinterpret_cast<const uint4*>(
+            index + (cset * n_tiles + j / kTile) * TB + (size_t)p * kTile * 16 + (size_t)(j % kTile) * 16);
+        float f[CPP];
+        unpack_codes<ST>(v, f);
+#pragma unroll
+        for (int c = 0; c < CPP; ++c) code_s[wave][u][p * CPP + c] = f[c];
+      }
+    }
+    __syncthreads();  // B_q staged by the work-group, codes by the wave
+    const float mu0 = mu[(size_t)g * D + lane], mu1 = mu[(size_t)g * D + lane + HALF];
 #pragma unroll
     for (int u = 0; u < kAttendBatch; ++u) {
-      const int e = e0 + u;
-      const int j = e < k ? __builtin_amdgcn_readlane(my_j, e) : -1;
-      jj[u] = j < N_valid ? j : -1;  // entries outside [0, N_valid) are skipped
+      k0[u] = mu0;
+      k1[u] = mu1;
     }
-    if constexpr (RECON) {
-      for (int t0 = 0; t0 < kAttendBatch * NP; t0 += kWave) {
-        // lane t0 + lane unpacks piece p of entry e0 + u; the list entry is
-        // read from its lane by every lane of the wave (all lanes active)
-        const int t = t0 + lane;
-        const int u = min(t / NP, kAttendBatch - 1), p = t % NP;
-        int j = __shfl(my_j, min(e0 + u, kWave - 1), kWave);
-        j = j >= 0 && j < N_valid ? j : 0;  // a skipped entry reads key 0
-        if (t < kAttendBatch * NP) {
-          const uint4 v = *reinterpret_cast<const uint4*>(
-              index + (cset * n_tiles + j / kTile) * TB + (size_t)p * kTile * 16 + (size_t)(j % kTile) * 16);
-          float f[CPP];
-          unpack_codes<ST>(v, f);
-#pragma unroll
-          for (int c = 0; c < CPP; ++c) code_s[wave][u][p * CPP + c] = f[c];
-        }
-      }
-      wave_lds_sync();
-#pragma unroll
-      for (int u = 0; u < kAttendBatch; ++u) {
-        k0[u] = mu0;
-        k1[u] = mu1;
-      }
 #pragma unroll 2
-      for (int m = 0; m < RK; ++m) {  // k_hat = mu + B_q c, one code element of all 16 keys at a time
-        const float b0 = bq_s[lane][m], b1 = bq_s[lane + HALF][m];
-#pragma unroll
-        for (int u = 0; u < kAttendBatch; ++u) {
-          const float c = code_s[wave][u][m];
-          k0[u] = fmaf(b0, c, k0[u]);
-          k1[u] = fmaf(b1, c, k1[u]);
-        }
-      }
-      wave_lds_sync();  // the next batch overwrites the codes
-    } else {
+    for (int m = 0; m < RK; ++m) {  // k_hat = mu + B_q c, one code element of all 16 keys at a time
+      const float b0 = bq_s[lane][m], b1 = bq_s[lane + HALF][m];
 #pragma unroll
       for (int u = 0; u < kAttendBatch; ++u) {
-        const size_t kr = (kbase + (size_t)max(jj[u], 0)) * D;  // a skipped entry reads key 0
-        k0[u] = load_key_elem<KBF>(keys, kr + lane);
-        k1[u] = load_key_elem<KBF>(keys, kr + lane + HALF);
+        const float cv = code_s[wave][u][m];
+        k0[u] = fmaf(b0, cv, k0[u]);
+        k1[u] = fmaf(b1, cv, k1[u]);
       }
     }
-#pragma unroll
-    for (int u = 0; u < kAttendBatch; ++u) {
-      float s, c;
-      rope_sincos(max(jj[u], 0), inv, &s, &c);
-      const float kb0 = k0[u] * c - k1[u] * s, kb1 = k1[u] * c + k0[u] * s;
-      const float sc = wave_sum_f32(fmaf(qa, kb0, qb * kb1)) * (1.f / 11.313708498984761f);
-      if (lane == e0 + u && jj[u] >= 0) my_s = sc;
-    }
   }
-  // softmax over the list (an empty row writes zeros)
+  float my_s = -INFINITY;  // lane u: score of entry e0 + u
+#pragma unroll
+  for (int u = 0; u < kAttendBatch; ++u) {
+    float sn, cs;
+    rope_sincos(max(jj[u], 0), inv, &sn, &cs);
+    const float kb0 = k0[u] * cs - k1[u] * sn, kb1 = k1[u] * cs + k0[u] * sn;
+    const float sc = wave_sum_f32(fmaf(qa, kb0, qb * kb1)) * (1.f / 11.313708498984761f);
+    if (lane == u && jj[u] >= 0) my_s = sc;
+  }
+  // this wave's softmax terms relative to its own maximum
   const float mx = wave_max_f32(my_s);
-  const float p = my_s == -INFINITY ? 0.f : expf(my_s - mx);
-  const float sum = wave_sum_f32(p);
+  const float pw = my_s == -INFINITY ? 0.f : expf(my_s - mx);
+  const float l = wave_sum_f32(pw);
   float o0 = 0.f, o1 = 0.f;
-  for (int e0 = 0; e0 < k; e0 += kAttendBatch) {
-    float v0[kAttendBatch], v1[kAttendBatch], pe[kAttendBatch];
 #pragma unroll
-    for (int u = 0; u < kAttendBatch; ++u) {
-      const int e = min(e0 + u, kWave - 1);
-      int j = __builtin_amdgcn_readlane(my_j, e);
-      j = j >= 0 && j < N_valid ? j : 0;  // skipped entries have p = 0
-      pe[u] = e0 + u < k ? readlane_s(p, e) : 0.f;
-      const float* vr = values + (kbase + (size_t)j) * D;
-      v0[u] = vr[lane];
-      v1[u] = vr[lane + HALF];
-    }
-#pragma unroll
-    for (int u = 0; u < kAttendBatch; ++u) {
-      o0 = fmaf(pe[u], v0[u], o0);
-      o1 = fmaf(pe[u], v1[u], o1);
-    }
+  for (int u = 0; u < kAttendBatch; ++u) {
+    const float pe = readlane_s(pw, u);
+    o0 = fmaf(pe, v0[u], o0);
+    o1 = fmaf(pe, v1[u], o1);
   }
-  const float isum = sum > 0.f ? 1.f / sum : 0.f;
-  out[row * D + lane] = o0 * isum;
-  out[row * D + lane + HALF] = o1 * isum;
+  if (lane == 0) {
+    part_m[wave] = mx;
+    part_l[wave] = l;
+  }
+  part_o[wave][lane] = o0;
+  part_o[wave][lane + HALF] = o1;
+  __syncthreads();
+  if (wave != 0) return;
+  // rescale to the row's maximum and add (an empty row writes zeros)
+  float M = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < kAttendWaves; ++w) M = fmaxf(M, part_m[w]);
+  float L = 0.f, a0 = 0.f, a1 = 0.f;
+#pragma unroll
+  for (int w = 0; w < kAttendWaves; ++w) {
+    const float f = part_m[w] == -INFINITY ? 0.f : expf(part_m[w] - M);
+    L = fmaf(f, part_l[w], L);
+    a0 = fmaf(f, part_o[w][lane], a0);
+    a1 = fmaf(f, part_o[w][lane + HALF], a1);
+  }
+  const float il = L > 0.f ? 1.f / L : 0.f;
+  out[row * D + lane] = a0 * il;
+  out[row * D + lane + HALF] = a1 * il;
 }
 
 template <int RK, bool KBF, int ST, bool RECON>
@@ -2333,7 +2437,7 @@ void launch_attend(const void* keys, const float* values, const uint8_t* index, 
                    int H_kv, int index_heads, int N_cap, int N_valid, const float* q,
                    const int* q_pos, int Q, const float* Bq, const float* mu, const int* top_idx,
                    int k, float rope_theta, float* out, hipStream_t s) {
-  dim3 grid((unsigned)((Q + kAttendWaves - 1) / kAttendWaves), (unsigned)(B * H_q));
+  dim3 grid((unsigned)Q, (unsigned)(B * H_q));
   hipLaunchKernelGGL((attend_kernel<RK, KBF, ST, RECON>), grid, dim3(kAttendWaves * kWave), 0, s,
                      keys, values, index, (int)saki::n_tiles(N_cap), H_q, H_kv, index_heads, N_cap,
                      N_valid, q, q_pos, Q, Bq, mu, top_idx, k, logf(rope_theta), out);
@@ -2390,13 +2494,14 @@ int resident_groups(K kernel, int threads) {
 // A split-N streaming launch that fills the GPU exactly once: the plan's
 // chunking (which sized the workspace) is coarsened so that the work-groups
 // number at most what the device holds at one time, the chunk count staying
-// within the plan's.
+// within the plan's.  A work-group takes `chunks_per_group` chunks.
 template <class K>
-saki::Plan one_round(saki::Plan p, K kernel, int groups_per_chunk, int N_valid) {
+saki::Plan one_round(saki::Plan p, K kernel, int groups_per_chunk, int chunks_per_group,
+                     int N_valid) {
   if (p.n_chunks <= 1) return p;
   const int slots = resident_groups(kernel, kWave * p.waves);
   if (slots <= 0) return p;
-  const int want = max(1, slots / max(1, groups_per_chunk));
+  const int want = max(1, slots / max(1, groups_per_chunk)) * chunks_per_group;
   const size_t n = N_valid > 0 ? (size_t)N_valid : 1;
   size_t chunk = saki::round_up((n + want - 1) / want, kTile);
   const int n_chunks = (int)((n + chunk - 1) / chunk);
@@ -2413,31 +2518,27 @@ void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int index_head
                   const saki::Plan& p0, hipStream_t s) {
   const int gq = H_q / index_heads;
   saki::Plan p = p0;
+  const int cpg = p0.split ? p0.waves : 1;  // chunks per work-group
   if (!p.mfma)
-    p = p.rows == 4 ? one_round(p0, score_stream_kernel<RK, ST, 4>, p0.row_blocks * B * index_heads, N_valid)
-                    : one_round(p0, score_stream_kernel<RK, ST, 1>, p0.row_blocks * B * index_heads, N_valid);
-  float* z = reinterpret_cast<float*>(ws + p.z_off);
-  float* bv = reinterpret_cast<float*>(ws + p.b_off);
+    p = p.rows == 4 ? one_round(p0, score_stream_kernel<RK, ST, 4>, p0.row_blocks * B * index_heads, cpg, N_valid)
+                    : one_round(p0, score_stream_kernel<RK, ST, 1>, p0.row_blocks * B * index_heads, cpg, N_valid);
   const size_t rows = (size_t)B * H_q * Q;
   uint64_t* part = p.n_chunks > 1 ? reinterpret_cast<uint64_t*>(ws + p.part_off) : nullptr;
-  dim3 grid((unsigned)(p.row_blocks * p.n_chunks), B * index_heads);
+  dim3 grid((unsigned)(p.row_blocks * ((p.n_chunks + cpg - 1) / cpg)), B * index_heads);
   dim3 block(kWave * p.waves);
   const int nt = (int)saki::n_tiles(N_cap);
-  if (!p.mfma)
-    hipLaunchKernelGGL((query_sketch_kernel<RK, ST>), dim3((Q + 15) / 16, B * H_q),
-                       dim3(256), 0, s, q, Bq, mu, H_q, H_kv, Q, z, bv);
   if (p.mfma)
     hipLaunchKernelGGL((score_mfma_kernel<RK, ST>), xcd_grid(p, B * H_q), block, 0, s, index,
                        nt, N_valid, Q, q_pos, q, Bq, mu, H_q, H_kv, gq, B * H_q, p.row_blocks,
                        p.chunk, p.n_chunks, k, top_idx, top_score, part);
   else if (p.rows == 4)
     hipLaunchKernelGGL((score_stream_kernel<RK, ST, 4>), grid, block, 0, s, index, nt, N_valid,
-                       Q, q_pos, z, bv, H_q, gq, p.row_blocks, p.chunk, p.n_chunks, k, top_idx,
-                       top_score, part);
+                       Q, q_pos, q, Bq, mu, H_q, H_kv, gq, p.row_blocks, p.chunk, p.n_chunks,
+                       (int)p.split, k, top_idx, top_score, part);
   else
     hipLaunchKernelGGL((score_stream_kernel<RK, ST, 1>), grid, block, 0, s, index, nt, N_valid,
-                       Q, q_pos, z, bv, H_q, gq, p.row_blocks, p.chunk, p.n_chunks, k, top_idx,
-                       top_score, part);
+                       Q, q_pos, q, Bq, mu, H_q, H_kv, gq, p.row_blocks, p.chunk, p.n_chunks,
+                       (int)p.split, k, top_idx, top_score, part);
   if (p.n_chunks > 1)
     hipLaunchKernelGGL((merge_kernel<KeysF32, false>), dim3((unsigned)rows),
                        dim3(kWave * min(kMergeWaves, p.n_chunks)), 0, s, part, rows, p.n_chunks,
@@ -2596,7 +2697,7 @@ int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_k
     return SAKI_ERR_UNSUPPORTED;
   if (Q == 0) return SAKI_OK;
   if (!index || !q || !B_q || !mu || !top_idx || !ws) return SAKI_ERR_ARG;
-  const saki::Plan p = saki::score_plan(B, H_q, index_heads, Q, N_valid, r);
+  const saki::Plan p = saki::score_plan(B, H_q, index_heads, Q, N_valid);
   if (ws_bytes < p.ws_bytes) return SAKI_ERR_WORKSPACE;
   if ((size_t)p.row_blocks * p.n_chunks > 0x7fffffffu) return SAKI_ERR_UNSUPPORTED;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
