@@ -1750,10 +1750,9 @@ __global__ __launch_bounds__(kGateWaves * kWave) __attribute__((amdgpu_waves_per
   __shared__ int bad_s[kMR];             // invalid lists
   __shared__ int ccount[kGateWaves][kMR];
   __shared__ int wg_fallback;
-  __shared__ int bj_m[kGateWaves][kBatch];  // per wave: others' key, exact score, row, S-count
+  __shared__ int bj_m[kGateWaves][kBatch];  // per wave: others' key, exact score, row
   __shared__ double bsc_m[kGateWaves][kBatch];
   __shared__ unsigned char brow_m[kGateWaves][kBatch];
-  __shared__ int bcnt_m[kGateWaves][kBatch];
   __shared__ int boff_m[kGateWaves][kMR / kGateWaves + 1];
   const int wave = threadIdx.x / kWave, lane = lane_id();
   const int row_blocks = (Q + kMR - 1) / kMR;
@@ -1782,7 +1781,6 @@ __global__ __launch_bounds__(kGateWaves * kWave) __attribute__((amdgpu_waves_per
   int* bj = bj_m[wave];
   double* bsc = bsc_m[wave];
   unsigned char* brow = brow_m[wave];
-  int* bcnt = bcnt_m[wave];
   int* boff = boff_m[wave];
 
   // query norm bound (lanes of row qi, dims 32kk + 8g .. +7); the MFMA
@@ -1824,42 +1822,46 @@ __global__ __launch_bounds__(kGateWaves * kWave) __attribute__((amdgpu_waves_per
   wave_lds_sync();
 
   // ---- gate, part 2: tau = min over the list of a float32 lower bound of q.k.
-  //      One flat loop over (row, step): a step scores 8 sorted entries, 8
-  //      lanes per entry (dims 16p .. 16p+15), so each sum is at most 12
-  //      roundings deep (error <= gamma_12 ||q|| ||k||).  The key slice, the
-  //      query slice and the key norm of step u + 1 are loaded while step u
-  //      is computed; pads (k < 64) and the entries of invalid lists read key
-  //      0 and are ignored.
+  //      Per row of the wave, eight steps of 8 sorted entries, 8 lanes per
+  //      entry (dims 16p .. 16p+15), so each sum is at most 12 roundings deep
+  //      (error <= gamma_12 ||q|| ||k||).  A row's entries and validity are
+  //      read once; the steps take two key buffers in turn, each refilled
+  //      right after use with the step two ahead (the next row's first two
+  //      steps at the end of a row).  Pads (k < 64) and the entries of
+  //      invalid lists read key 0 and are ignored.
   {
     const int p = lane & 7, slot = lane >> 3;
     const int my_rows_g = n_rows > wave ? (n_rows - wave + kGateWaves - 1) / kGateWaves : 0;
-    const int n_steps = my_rows_g * 8;
-    struct Step {
-      float f[16], knv;
-    };
-    auto step_key = [&](int u, bool& use) -> int {
-      const int r = wave + kGateWaves * (u >> 3);
-      const uint32_t kj = sl[r * kWave + ((u & 7) << 3) + slot];
-      use = (kj >> 31) == 0 && bad_s[r] == 0;
-      return use ? (int)kj : 0;
-    };
-    auto load_step = [&](Step& st, int u) {
-      bool use;
-      const int j = step_key(u, use);
-      if constexpr (KBF) {
-        const uint16_t* kr = reinterpret_cast<const uint16_t*>(keys) + (kbase + j) * D + 16 * p;
-        unpack_piece<true>(*reinterpret_cast<const uint4*>(kr), st.f);
-        unpack_piece<true>(*reinterpret_cast<const uint4*>(kr + 8), st.f + 8);
-      } else {
-        const float4* kr = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(keys) +
-                                                           (kbase + j) * D + 16 * p);
+    // row rr of the wave: the key of entry 8u + slot in bit-free form (0 when
+    // unused) and a bit mask of the used entries
+    auto row_keys = [&](int rr, int (&jv)[8]) -> uint32_t {
+      const int r = wave + kGateWaves * rr;
+      const bool ok = bad_s[r] == 0;
+      uint32_t used = 0;
 #pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4) {
-          const float4 v = kr[e4];
-          st.f[4 * e4] = v.x; st.f[4 * e4 + 1] = v.y; st.f[4 * e4 + 2] = v.z; st.f[4 * e4 + 3] = v.w;
-        }
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t kj = sl[r * kWave + 8 * u + slot];
+        const bool use = ok && (kj >> 31) == 0;
+        jv[u] = use ? (int)kj : 0;
+        used |= use ? 1u << u : 0u;
       }
-      st.knv = kn[j];
+      return used;
+    };
+    // a key slice stays in its loaded form (four 16-byte words of float32,
+    // or two of bf16) until it is used
+    auto load_key = [&](uint4* w, float& knv, int j) {
+      if constexpr (KBF) {
+        const uint4* kr = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(keys) +
+                                                         (kbase + j) * D + 16 * p);
+        w[0] = kr[0];
+        w[1] = kr[1];
+      } else {
+        const uint4* kr = reinterpret_cast<const uint4*>(reinterpret_cast<const float*>(keys) +
+                                                         (kbase + j) * D + 16 * p);
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) w[e4] = kr[e4];
+      }
+      knv = kn[j];
     };
     // the query slice of the wave's row rr (dims 16p .. 16p+15)
     auto load_q = [&](float* qv, int rr) {
@@ -1871,49 +1873,77 @@ __global__ __launch_bounds__(kGateWaves * kWave) __attribute__((amdgpu_waves_per
         qv[4 * e4] = v.x; qv[4 * e4 + 1] = v.y; qv[4 * e4 + 2] = v.z; qv[4 * e4 + 3] = v.w;
       }
     };
-    float lo = INFINITY;
-    float qcur[16], qnext[16];
-    auto compute_step = [&](const Step& st, int u) {
-      bool use;
-      (void)step_key(u, use);
-      const int r = wave + kGateWaves * (u >> 3), a = ((u & 7) << 3) + slot;
-      float s0 = 0.f, s1 = 0.f;
+    // the key of entry 8u + slot of row rr if used, else -1
+    auto entry_key = [&](int rr, int u) -> int {
+      const int r = wave + kGateWaves * rr;
+      const uint32_t kj = sl[r * kWave + 8 * u + slot];
+      return bad_s[r] == 0 && (kj >> 31) == 0 ? (int)kj : -1;
+    };
+    if (my_rows_g > 0) {
+      int jv[8];
+      float qcur[16], qnext[16];
+      uint4 ka[KBF ? 2 : 4], kb[KBF ? 2 : 4];
+      float kna, knb;
+      uint32_t used = row_keys(0, jv);
+      load_q(qcur, 0);
+      load_key(ka, kna, jv[0]);
+      load_key(kb, knb, jv[1]);
+      for (int rr = 0; rr < my_rows_g; ++rr) {
+        const int r = wave + kGateWaves * rr;
+        const bool more = rr + 1 < my_rows_g;
+        // the next row's first two keys (pads and invalid lists read key 0)
+        const int n0 = more ? max(entry_key(rr + 1, 0), 0) : 0;
+        const int n1 = more ? max(entry_key(rr + 1, 1), 0) : 0;
+        const float qr_n = readlane_s(qn, r);
+        float lo = INFINITY;
 #pragma unroll
-      for (int e = 0; e < 16; e += 2) {
-        s0 = fmaf(qcur[e], st.f[e], s0);
-        s1 = fmaf(qcur[e + 1], st.f[e + 1], s1);
-      }
-      float sc = s0 + s1;
-      sc += xor_shfl_f32(sc, 1);
-      sc += xor_shfl_f32(sc, 2);
-      sc += xor_shfl_f32(sc, 4);
-      const float ea = kTauEps * readlane_s(qn, r) * st.knv;
-      if (use && p == 0) {
-        ss[r * kWave + a] = sc;
-        se[r * kWave + a] = ea;
-      }
-      lo = fminf(lo, use ? sc - ea : INFINITY);
-      if ((u & 7) == 7) {  // the row's last step: its gate, and the next row's query
+        for (int u = 0; u < 8; ++u) {
+          if (u == 4 && more) load_q(qnext, rr + 1);
+          const uint4* w = (u & 1) ? kb : ka;
+          const float knv = (u & 1) ? knb : kna;
+          float f[16];
+          if constexpr (KBF) {
+            unpack_piece<true>(w[0], f);
+            unpack_piece<true>(w[1], f + 8);
+          } else {
+#pragma unroll
+            for (int e4 = 0; e4 < 4; ++e4) {
+              f[4 * e4] = __uint_as_float(w[e4].x); f[4 * e4 + 1] = __uint_as_float(w[e4].y);
+              f[4 * e4 + 2] = __uint_as_float(w[e4].z); f[4 * e4 + 3] = __uint_as_float(w[e4].w);
+            }
+          }
+          float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+          for (int e = 0; e < 16; e += 2) {
+            s0 = fmaf(qcur[e], f[e], s0);
+            s1 = fmaf(qcur[e + 1], f[e + 1], s1);
+          }
+          float sc = s0 + s1;
+          sc += xor_shfl_f32(sc, 1);
+          sc += xor_shfl_f32(sc, 2);
+          sc += xor_shfl_f32(sc, 4);
+          const float ea = kTauEps * qr_n * knv;
+          const bool use = (used >> u) & 1u;
+          if (use && p == 0) {
+            ss[r * kWave + 8 * u + slot] = sc;
+            se[r * kWave + 8 * u + slot] = ea;
+          }
+          lo = fminf(lo, use ? sc - ea : INFINITY);
+          // refill this buffer with the step two ahead
+          if (u + 2 < 8 || more) {
+            const int j2 = u + 2 < 8 ? jv[u + 2] : (u == 6 ? n0 : n1);
+            if (u & 1) load_key(kb, knb, j2);
+            else load_key(ka, kna, j2);
+          }
+        }
         lo = wave_min_f32(lo);
         if (lane == 0 && bad_s[r] == 0) tau_s[r] = lo;
-        lo = INFINITY;
+        if (more) {
+          used = row_keys(rr + 1, jv);
 #pragma unroll
-        for (int e = 0; e < 16; ++e) qcur[e] = qnext[e];
-        const int rr = (u >> 3) + 2;
-        if (rr < my_rows_g) load_q(qnext, rr);
+          for (int e = 0; e < 16; ++e) qcur[e] = qnext[e];
+        }
       }
-    };
-    Step sa, sb;
-    if (n_steps > 0) {
-      load_q(qcur, 0);
-      if (my_rows_g > 1) load_q(qnext, 1);
-      load_step(sa, 0);
-    }
-    for (int u = 0; u < n_steps; u += 2) {  // n_steps is a multiple of 8
-      load_step(sb, u + 1);
-      compute_step(sa, u);
-      load_step(sa, u + 2 < n_steps ? u + 2 : u + 1);
-      compute_step(sb, u + 1);
     }
   }
   __syncthreads();
@@ -2013,42 +2043,43 @@ __global__ __launch_bounds__(kGateWaves * kWave) __attribute__((amdgpu_waves_per
     for (; r_end < my_rows; ++r_end) {
       const int r = wave + kGateWaves * r_end;
       const bool rbad = bad_s[r] != 0;
-      // others of this row: all of C for an invalid list, else C minus S
-      int n_oth = 0, n_in_s = 0;
+      // others of this row: all of C for an invalid list, else C minus S,
+      // appended in one pass (entries past the batch are not written; a row
+      // that does not fit is taken back and starts the next batch)
+      const int nb0 = nb;
+      int n_in_s = 0;
       for (int w = 0; w < kGateWaves; ++w) {
         const int c = ccount[w][r];
         for (int base = 0; base < c; base += kWave) {
           const int e = base + lane;
           const int j = e < c ? cj[w][r * kGateRow + e] : -1;
           const bool is_s = e < c && !rbad && in_sorted_desc(sl + r * kWave, j);
+          const bool other = e < c && !is_s;
+          const uint64_t m = __ballot(other);
+          const int at = nb + prefix_count(m);
+          if (other && at < kBatch) {
+            bj[at] = j;
+            brow[at] = (unsigned char)r;
+          }
+          nb += __popcll(m);
           n_in_s += __popcll(__ballot(is_s));
-          n_oth += __popcll(__ballot(e < c && !is_s));
         }
       }
       // every key of a valid list passes the gate (a failed check means a bound
       // did not hold: hand the rows over rather than trust the result); a row
       // whose others do not fit one batch is handed over as well
-      if ((!rbad && n_chunks == 1 && n_in_s != k) || n_oth > kBatch) {
+      if ((!rbad && n_chunks == 1 && n_in_s != k) || nb - nb0 > kBatch) {
         fallback = true;
         break;
       }
-      if (nb + n_oth > kBatch) break;  // this row starts the next batch
-      if (lane == 0) boff[r_end - r_done] = nb;
-      for (int w = 0; w < kGateWaves; ++w) {
-        const int c = ccount[w][r];
-        for (int base = 0; base < c; base += kWave) {
-          const int e = base + lane;
-          const int j = e < c ? cj[w][r * kGateRow + e] : -1;
-          const bool other = e < c && (rbad || !in_sorted_desc(sl + r * kWave, j));
-          const uint64_t m = __ballot(other);
-          if (other) {
-            bj[nb + prefix_count(m)] = j;
-            brow[nb + prefix_count(m)] = (unsigned char)r;
-          }
-          nb += __popcll(m);
-        }
+      if (nb > kBatch) {  // this row starts the next batch
+        nb = nb0;
+        break;
       }
-      if (lane == 0) boff[r_end - r_done + 1] = nb;
+      if (lane == 0) {
+        boff[r_end - r_done] = nb0;
+        boff[r_end - r_done + 1] = nb;
+      }
     }
     if (fallback) break;
     wave_lds_sync();
@@ -2087,40 +2118,48 @@ __global__ __launch_bounds__(kGateWaves * kWave) __attribute__((amdgpu_waves_per
         exact_row_out<KD>(xs, row, ch, n_chunks, k, approx, hits, exact_idx, part);
         continue;
       }
-      // how many keys of S beat each other o (S's float32 intervals)
-      if (!rbad) {
-        const float sa = real ? ss[r * kWave + lane] : 0.f;
-        const float ea = real ? se[r * kWave + lane] : 0.f;
-        const double lo_a = (double)sa - (double)ea, hi_a = (double)sa + (double)ea;
-        for (int o = o0; o < o1; ++o) {
-          const double so = bsc[o];
-          const int jo = bj[o];
-          bool beat = real && lo_a > so;
-          const bool amb = real && !beat && hi_a >= so;
-          if (__ballot(amb) != 0 && amb) {
-            const double sx = lane_dot_f64_g<KBF>(keys, kbase + aj, qr);
-            beat = sx > so || (sx == so && aj < jo);
-          }
-          const int cs = __popcll(__ballot(beat));
-          if (lane == 0) bcnt[o] = cs;
-        }
-      }
-      wave_lds_sync();
+      // lane a: S's float32 interval of entry a
+      const float sa = !rbad && real ? ss[r * kWave + lane] : 0.f;
+      const float ea = !rbad && real ? se[r * kWave + lane] : 0.f;
+      const double lo_a = (double)sa - (double)ea, hi_a = (double)sa + (double)ea;
       int in_t = 0, in_ts = 0;
+      // others in blocks of 64, one per lane; the key compared with all of
+      // them is read from its lane
       for (int base = o0; base < o1; base += kWave) {
         const int e = base + lane;
         const bool live = e < o1;
-        const double so = live ? bsc[e] : 0.0;
-        const int jo = live ? bj[e] : 0;
-        int cnt = (live && !rbad) ? bcnt[e] : 0;
-        for (int o2 = o0; o2 < o1; ++o2) {
-          const double s2 = bsc[o2];
-          const int j2 = bj[o2];
-          cnt += (s2 > so || (s2 == so && j2 < jo)) ? 1 : 0;
+        const double so_l = live ? bsc[e] : 0.0;
+        const int jo_l = live ? bj[e] : 0;
+        int cnt = 0;  // keys of C that beat other e
+        if (!rbad) {  // keys of S, through their intervals
+          const int nbk = min(kWave, o1 - base);
+          for (int t = 0; t < nbk; ++t) {
+            const double so = readlane_s(so_l, t);
+            const int jo = __builtin_amdgcn_readlane(jo_l, t);
+            bool beat = real && lo_a > so;
+            const bool amb = real && !beat && hi_a >= so;
+            if (__ballot(amb) != 0 && amb) {
+              const double sx = lane_dot_f64_g<KBF>(keys, kbase + aj, qr);
+              beat = sx > so || (sx == so && aj < jo);
+            }
+            const int cs = __popcll(__ballot(beat));
+            cnt += lane == t ? cs : 0;
+          }
+        }
+        for (int base2 = o0; base2 < o1; base2 += kWave) {  // the other others, exactly
+          const int e2 = base2 + lane;
+          const double s2_l = base2 == base ? so_l : (e2 < o1 ? bsc[e2] : 0.0);
+          const int j2_l = base2 == base ? jo_l : (e2 < o1 ? bj[e2] : 0);
+          const int n2 = min(kWave, o1 - base2);
+          for (int t = 0; t < n2; ++t) {
+            const double s2 = readlane_s(s2_l, t);
+            const int j2 = __builtin_amdgcn_readlane(j2_l, t);
+            cnt += (s2 > so_l || (s2 == so_l && j2 < jo_l)) ? 1 : 0;
+          }
         }
         const bool in = live && cnt < k;
         in_t += __popcll(__ballot(in));
-        in_ts += __popcll(__ballot(in && rbad && in_sorted_desc(sl + r * kWave, jo)));
+        in_ts += __popcll(__ballot(in && rbad && in_sorted_desc(sl + r * kWave, jo_l)));
       }
       if (lane == 0) hits[row] = rbad ? in_ts : k - in_t;
     }
