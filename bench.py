@@ -49,8 +49,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-attend", action="store_true",
                     help="decode: leave out reading the winners (RoPE attention over the top-64)")
-    ap.add_argument("--cpu-heads", type=int, default=4,
-                    help="query heads of the CPU-baseline sample (one KV group)")
+    ap.add_argument("--cpu-heads", type=int, default=16,
+                    help="query heads of the CPU-baseline sample (about 10-15 s of host work)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES (counter scale) and exit")
     return ap.parse_args()
@@ -163,7 +163,8 @@ def cpu_baseline(inp, r, sketch, k, n_heads):
     dt = time.perf_counter() - t0
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     return {"value": n_pairs / dt, "unit": "keys/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"query heads 0-{n_heads - 1} (KV group 0) of layer 0, all {spec.Q} query "
+            "sample": f"query heads 0-{n_heads - 1} (KV groups 0-{(n_heads - 1) // G}) of layer 0, "
+                      f"all {spec.Q} query "
                       f"rows each ({n_pairs} pairs): calibrate+codes+scores+top-{k}+exact "
                       f"top-{k}+recall in float64 numpy; {dt:.1f} s; host os.cpu_count()="
                       f"{os.cpu_count()}, BLAS threads={threads}"}
@@ -360,8 +361,14 @@ def main():
     top_idx = torch.empty((B, H_q, spec.Q, k), dtype=torch.int32, device=dev)
     top_sc = torch.empty((B, H_q, spec.Q, k), dtype=torch.float32, device=dev)
     hits = torch.empty((B, H_q, spec.Q), dtype=torch.int32, device=dev)
-    f_dev = {n: torch.empty(s, dtype=torch.float32, device=dev)
-             for n, s in (("B_q", (H_q, d, r)), ("B_k", (H_q, d, r)), ("mu", (H_kv, d)))}
+    # the factors live in one flat buffer (one upload per step); f_dev are views
+    f_shape = {"B_q": (H_q, d, r), "B_k": (H_q, d, r), "mu": (H_kv, d)}
+    f_off, f_total = {}, 0
+    for n, sh in f_shape.items():
+        f_off[n] = (f_total, f_total + int(np.prod(sh)))
+        f_total = f_off[n][1]
+    f_flat = torch.empty(f_total, dtype=torch.float32, device=dev)
+    f_dev = {n: f_flat[a:b].view(f_shape[n]) for n, (a, b) in f_off.items()}
     # calibration: float64 moments on the GPU (side stream, default priority),
     # copied to pinned host memory; the host factorises them while the GPU
     # still runs the previous batch
@@ -388,14 +395,16 @@ def main():
             m_done[sl] = torch.cuda.Event()
             m_done[sl].record(side)
 
-    def factorise(sl):
+    def factorise(sl, out=None):
         h = m_host[sl]
         return S.saki_calibrate_from_moments(h["Sq"].numpy(), h["Sk"].numpy(), h["mu"].numpy(),
-                                             r, method=args.method, with_sigma=False)
+                                             r, method=args.method, with_sigma=False, out=out)
     # two pinned staging slots: the host calibrates batch i+1 while the GPU
-    # still works on batch i; a slot is rewritten only after its copy finished
-    slots = [{n: torch.empty(t.shape, dtype=torch.float32).pin_memory() for n, t in f_dev.items()}
-             for _ in range(2)]
+    # still works on batch i, writing the factors straight into the slot; a
+    # slot is rewritten only after its copy finished
+    slots = [torch.empty(f_total, dtype=torch.float32).pin_memory() for _ in range(2)]
+    slot_out = [{n: slots[i].numpy()[a:b].reshape(f_shape[n]) for n, (a, b) in f_off.items()}
+                for i in range(2)]
     slot_done = [None, None]
     ev = {}
     n_step = [0]
@@ -407,12 +416,10 @@ def main():
         n_step[0] += 1
         m_done[sl].synchronize()
         enqueue_moments(1 - sl)  # the next batch's moments overlap this one
-        cal = factorise(sl)
         if slot_done[sl] is not None:
             slot_done[sl].synchronize()
-        for n in f_dev:
-            slots[sl][n].numpy()[...] = cal[n]
-            f_dev[n].copy_(slots[sl][n], non_blocking=True)
+        factorise(sl, out=slot_out[sl])
+        f_flat.copy_(slots[sl], non_blocking=True)
         slot_done[sl] = torch.cuda.Event()
         slot_done[sl].record()
         if timed_stages:

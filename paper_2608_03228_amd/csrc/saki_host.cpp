@@ -166,6 +166,27 @@ void axpy2(double a, const double* x, double b, const double* z, double* y, int 
   for (; i < n; ++i) y[i] += a * x[i] + b * z[i];
 }
 
+// One row of a symmetric product from the lower triangle: returns
+// sum_{j<n} a[j] * v[j] and adds vi * a[j] to p[j] (j < n), in one pass.
+double dot_axpy(const double* a, const double* v, double vi, double* p, int n) {
+  const __m256d b = _mm256_set1_pd(vi);
+  __m256d s0 = _mm256_setzero_pd(), s1 = _mm256_setzero_pd();
+  int j = 0;
+  for (; j + 8 <= n; j += 8) {
+    const __m256d a0 = _mm256_loadu_pd(a + j), a1 = _mm256_loadu_pd(a + j + 4);
+    s0 = _mm256_fmadd_pd(a0, _mm256_loadu_pd(v + j), s0);
+    s1 = _mm256_fmadd_pd(a1, _mm256_loadu_pd(v + j + 4), s1);
+    _mm256_storeu_pd(p + j, _mm256_fmadd_pd(b, a0, _mm256_loadu_pd(p + j)));
+    _mm256_storeu_pd(p + j + 4, _mm256_fmadd_pd(b, a1, _mm256_loadu_pd(p + j + 4)));
+  }
+  double acc = hsum(_mm256_add_pd(s0, s1));
+  for (; j < n; ++j) {
+    acc += a[j] * v[j];
+    p[j] += vi * a[j];
+  }
+  return acc;
+}
+
 // sqrt(a^2 + b^2); the plain formula where it cannot over- or underflow.
 inline double hypot2(double a, double b) {
   const double m = std::max(std::fabs(a), std::fabs(b));
@@ -193,6 +214,75 @@ inline void block4x8(int n, const double* A, long sai, long sak, const double* B
     double* ci = C + (size_t)(i0 + a) * n + j0;
     _mm256_storeu_pd(ci, _mm256_add_pd(_mm256_loadu_pd(ci), c[a][0]));
     _mm256_storeu_pd(ci + 4, _mm256_add_pd(_mm256_loadu_pd(ci + 4), c[a][1]));
+  }
+}
+
+// C0[a*ldc + j0 ..+7] += sum_{k in [kb, ke)} A0[a*sai + k*sak] * B[k*ldb + j0 ..+7]
+// for a < 4: one 4 x 8 block of a product whose operands have their own row
+// strides (A0 and C0 point at the block's first row).
+inline void block4x8s(const double* A0, long sai, long sak, const double* B, long ldb,
+                      double* C0, long ldc, int j0, int kb, int ke) {
+  __m256d c[4][2];
+  for (int a = 0; a < 4; ++a) c[a][0] = c[a][1] = _mm256_setzero_pd();
+  for (int k = kb; k < ke; ++k) {
+    const __m256d b0 = _mm256_loadu_pd(B + (size_t)k * ldb + j0);
+    const __m256d b1 = _mm256_loadu_pd(B + (size_t)k * ldb + j0 + 4);
+    for (int a = 0; a < 4; ++a) {
+      const __m256d x = _mm256_broadcast_sd(A0 + a * sai + k * sak);
+      c[a][0] = _mm256_fmadd_pd(x, b0, c[a][0]);
+      c[a][1] = _mm256_fmadd_pd(x, b1, c[a][1]);
+    }
+  }
+  for (int a = 0; a < 4; ++a) {
+    double* ci = C0 + (size_t)a * ldc + j0;
+    _mm256_storeu_pd(ci, _mm256_add_pd(_mm256_loadu_pd(ci), c[a][0]));
+    _mm256_storeu_pd(ci + 4, _mm256_add_pd(_mm256_loadu_pd(ci + 4), c[a][1]));
+  }
+}
+
+// P = L V (d x r, row-major) for lower-triangular L (d x d, upper part zero).
+void lower_times(int d, int r, const double* L, const double* V, double* P) {
+  std::fill(P, P + (size_t)d * r, 0.0);
+  if (d % 4 == 0 && r % 8 == 0) {
+    for (int i0 = 0; i0 < d; i0 += 4)
+      for (int j0 = 0; j0 < r; j0 += 8)
+        block4x8s(L + (size_t)i0 * d, d, 1, V, r, P + (size_t)i0 * r, r, j0, 0, i0 + 4);
+    return;
+  }
+  for (int i = 0; i < d; ++i)
+    for (int j = 0; j <= i; ++j) axpy(L[(size_t)i * d + j], V + (size_t)j * r, P + (size_t)i * r, r);
+}
+
+// X = L^-T V (d x r, row-major): solves L^T X = V for lower-triangular L.
+// Rows are solved from the last, four at a time: the sum over the rows already
+// solved runs through the 4 x 8 block kernel, then the 4 x 4 diagonal block.
+void lower_t_solve(int d, int r, const double* L, const double* V, double* X) {
+  if (d % 4 == 0 && r % 8 == 0) {
+    std::vector<double> T((size_t)4 * r);
+    for (int i0 = d - 4; i0 >= 0; i0 -= 4) {
+      std::fill(T.begin(), T.end(), 0.0);
+      // T[a] = sum_{j >= i0+4} L[j][i0+a] X[j]
+      for (int j0 = 0; j0 < r; j0 += 8)
+        block4x8s(L + i0, 1, d, X, r, T.data(), r, j0, i0 + 4, d);
+      for (int a = 3; a >= 0; --a) {
+        const int i = i0 + a;
+        const double rl = 1.0 / L[(size_t)i * d + i];
+        double* xi = X + (size_t)i * r;
+        for (int m = 0; m < r; ++m) {
+          double v = V[(size_t)i * r + m] - T[(size_t)a * r + m];
+          for (int b = a + 1; b < 4; ++b) v -= L[(size_t)(i0 + b) * d + i] * X[(size_t)(i0 + b) * r + m];
+          xi[m] = v * rl;
+        }
+      }
+    }
+    return;
+  }
+  std::vector<double> W(V, V + (size_t)d * r);
+  for (int i = d - 1; i >= 0; --i) {  // row i of L at a time
+    double* xi = X + (size_t)i * r;
+    const double rl = 1.0 / L[(size_t)i * d + i];
+    for (int m = 0; m < r; ++m) xi[m] = W[(size_t)i * r + m] * rl;
+    for (int j = 0; j < i; ++j) axpy(-L[(size_t)i * d + j], xi, W.data() + (size_t)j * r, r);
   }
 }
 
@@ -376,8 +466,7 @@ void householder_tridiag(int n, double* a, double* diag, double* off, double* hv
     std::fill(p.begin(), p.begin() + m, 0.0);
     for (int i = 0; i < m; ++i) {
       const double* ai = a + (size_t)(k + 1 + i) * n + (k + 1);
-      p[i] += dot(ai, v, i) + ai[i] * v[i];
-      axpy(v[i], ai, p.data(), i);
+      p[i] += dot_axpy(ai, v, v[i], p.data(), i) + ai[i] * v[i];
     }
     for (int i = 0; i < m; ++i) p[i] *= bk;
     const double K = 0.5 * bk * dot(v, p.data(), m);
@@ -1086,11 +1175,10 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
       }
       for (int m = 0; m < (sigma ? d : r); ++m) sig[m] = std::sqrt(std::max(w[m], 0.0));
       // all r columns at once (d x r, row-major): P = L V', X = L^-T V'
-      Mat V((size_t)d * r), P((size_t)d * r, 0.0), X((size_t)d * r);
+      Mat V((size_t)d * r), P((size_t)d * r), X((size_t)d * r);
       for (int m = 0; m < r; ++m)
         for (int i = 0; i < d; ++i) V[(size_t)i * r + m] = vt[(size_t)m * d + i];
-      for (int i = 0; i < d; ++i)
-        for (int j = 0; j <= i; ++j) axpy(L[(size_t)i * d + j], V.data() + (size_t)j * r, P.data() + (size_t)i * r, r);
+      lower_times(d, r, L, V.data(), P.data());
       if (method == SAKI_METHOD_SAP_MAP) {  // column m of P = L V' is Sigma_k^{1/2} v_m
         Mat Qr((size_t)r * d);
         for (int m = 0; m < r; ++m)
@@ -1102,12 +1190,7 @@ int calibrate_core(const float* q_cal, const float* k_cal, const double* Sq_in,
         if (n_clamped) { n_clamped[2 * h] = 0; n_clamped[2 * h + 1] = 0; }
         return;
       }
-      for (int i = d - 1; i >= 0; --i) {  // L^T X = V by back substitution, row i of L at a time
-        double* xi = X.data() + (size_t)i * r;
-        const double rl = 1.0 / L[(size_t)i * d + i];
-        for (int m = 0; m < r; ++m) xi[m] = V[(size_t)i * r + m] * rl;
-        for (int j = 0; j < i; ++j) axpy(-L[(size_t)i * d + j], xi, V.data() + (size_t)j * r, r);
-      }
+      lower_t_solve(d, r, L, V.data(), X.data());  // L^T X = V
       for (int m = 0; m < r; ++m) {
         const double sm = sig[m], rs = std::sqrt(sm);
         for (int i = 0; i < d; ++i) {

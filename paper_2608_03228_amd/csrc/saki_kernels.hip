@@ -1783,6 +1783,36 @@ __global__ __launch_bounds__(kGateWaves * kWave) __attribute__((amdgpu_waves_per
   unsigned char* brow = brow_m[wave];
   int* boff = boff_m[wave];
 
+  // ---- gate, part 1: load, sort and check the candidate lists of rows wave,
+  //      wave + 4, ... (the next row's list is loaded before this one is
+  //      sorted); the owner wave also sets the row's gate to -inf and its
+  //      validity flag (rows past Q count as invalid)
+  {
+    auto list_entry = [&](int r) -> int {
+      return r < n_rows && lane < k ? approx[(bh * Q + row0 + r) * k + lane] : -1;
+    };
+    int aj_next = list_entry(wave);
+#pragma unroll 1
+    for (int r = wave; r < kMR; r += kGateWaves) {
+      const int aj = aj_next;
+      aj_next = list_entry(r + kGateWaves);
+      if (lane == 0) tau_s[r] = -INFINITY;
+      if (r >= n_rows) {
+        if (lane == 0) bad_s[r] = 1;
+        continue;
+      }
+      const int lim_r = __builtin_amdgcn_readlane(my_lim, r);
+      bool bad = lane < k && (aj < 0 || aj >= lim_r);
+      uint32_t key = lane < k ? (uint32_t)aj : (0x80000000u | (uint32_t)lane);
+      wave_sort<KeysU32>(key);
+      const uint32_t nxt = (uint32_t)__shfl_down((int)key, 1, kWave);
+      bad |= lane < kWave - 1 && key == nxt;
+      sl[r * kWave + lane] = key;
+      if (lane == 0) bad_s[r] = __ballot(bad) != 0;  // an invalid list keeps tau = -inf
+    }
+  }
+  if (threadIdx.x == 0) wg_fallback = 0;
+
   // query norm bound (lanes of row qi, dims 32kk + 8g .. +7); the MFMA
   // operands are formed after the gate
   const float* qrow = q + (bh * Q + (row_ok ? my_row : row0)) * D;  // a valid row
@@ -1799,26 +1829,6 @@ __global__ __launch_bounds__(kGateWaves * kWave) __attribute__((amdgpu_waves_per
     qn = row_ok ? sqrtf(sum_lane_groups(sq)) * (1.f + 1e-5f) : 0.f;
   }
   const float eq = kExactEps3 * qn;
-  if (threadIdx.x < kMR) {
-    tau_s[threadIdx.x] = -INFINITY;
-    bad_s[threadIdx.x] = 1;
-  }
-  if (threadIdx.x == 0) wg_fallback = 0;
-  __syncthreads();
-
-  // ---- gate, part 1: sort and check the candidate lists of rows wave, wave + 4, ...
-  for (int r = wave; r < n_rows; r += kGateWaves) {
-    const size_t row = bh * Q + row0 + r;
-    const int lim_r = __builtin_amdgcn_readlane(my_lim, r);
-    const int aj = lane < k ? approx[row * k + lane] : -1;
-    bool bad = lane < k && (aj < 0 || aj >= lim_r);
-    uint32_t key = lane < k ? (uint32_t)aj : (0x80000000u | (uint32_t)lane);
-    wave_sort<KeysU32>(key);
-    const uint32_t nxt = (uint32_t)__shfl_down((int)key, 1, kWave);
-    bad |= lane < kWave - 1 && key == nxt;
-    sl[r * kWave + lane] = key;
-    if (lane == 0) bad_s[r] = __ballot(bad) != 0;  // an invalid list keeps tau = -inf
-  }
   wave_lds_sync();
 
   // ---- gate, part 2: tau = min over the list of a float32 lower bound of q.k.
