@@ -166,7 +166,7 @@ void axpy2(double a, const double* x, double b, const double* z, double* y, int 
   for (; i < n; ++i) y[i] += a * x[i] + b * z[i];
 }
 
-// One row of a symmetric product from the lower triangle: returns
+// One row of a symmetric product over a stored triangle: returns
 // sum_{j<n} a[j] * v[j] and adds vi * a[j] to p[j] (j < n), in one pass.
 double dot_axpy(const double* a, const double* v, double vi, double* p, int n) {
   const __m256d b = _mm256_set1_pd(vi);
@@ -436,49 +436,123 @@ void store_basis(int d, int r, const double* Qr, float* Bq, float* Bk) {
       Bq[(size_t)i * r + m] = Bk[(size_t)i * r + m] = (float)Qr[(size_t)m * d + i];
 }
 
-// Householder reduction of symmetric `a` (n x n, lower triangle read and
-// overwritten; the upper triangle is ignored) to tridiagonal
+// The Householder reflector of x (m entries, contiguous) into v: H = I -
+// beta v v^T maps x to alpha e_0.  Returns beta (0, with v = 0 and alpha = 0,
+// for x = 0).
+double householder_vec(const double* x, int m, double* v, double* alpha_out) {
+  std::copy(x, x + m, v);
+  const double sumsq = dot(v, v, m);
+  const double x0 = v[0];
+  double alpha = std::sqrt(sumsq);
+  *alpha_out = 0.0;
+  if (alpha == 0.0) { std::fill(v, v + m, 0.0); return 0.0; }
+  if (x0 > 0) alpha = -alpha;  // reflect away from x0's sign
+  v[0] = x0 - alpha;
+  const double vv = sumsq - x0 * x0 + v[0] * v[0];
+  if (vv == 0.0) { std::fill(v, v + m, 0.0); return 0.0; }
+  *alpha_out = alpha;
+  return 2.0 / vv;
+}
+
+// One row of the trailing block in the fused pass, from its diagonal (len
+// entries r[t] = a(i, i+t)): r -= vi*w + wi*v (v, w from index i), then the
+// row's part of the next product pn = A v_next over the upper triangle (vn,
+// pn from the row's index in the next block): pn[0] gets the row times vn,
+// pn[t] (t >= 1) gets vn[0] * r[t].
+void update_row_and_product(double* r, const double* v, const double* w, double vi, double wi,
+                            const double* vn, double* pn, int len) {
+  const double vni = vn[0];
+  const double x0 = std::fma(-wi, v[0], std::fma(-vi, w[0], r[0]));
+  r[0] = x0;
+  double acc = x0 * vni;
+  const __m256d nvi = _mm256_set1_pd(-vi), nwi = _mm256_set1_pd(-wi), bn = _mm256_set1_pd(vni);
+  __m256d s0 = _mm256_setzero_pd();
+  int t = 1;
+  for (; t + 4 <= len; t += 4) {
+    const __m256d x = _mm256_fmadd_pd(nwi, _mm256_loadu_pd(v + t),
+                                      _mm256_fmadd_pd(nvi, _mm256_loadu_pd(w + t), _mm256_loadu_pd(r + t)));
+    _mm256_storeu_pd(r + t, x);
+    s0 = _mm256_fmadd_pd(x, _mm256_loadu_pd(vn + t), s0);
+    _mm256_storeu_pd(pn + t, _mm256_fmadd_pd(bn, x, _mm256_loadu_pd(pn + t)));
+  }
+  acc += hsum(s0);
+  for (; t < len; ++t) {
+    const double x = std::fma(-wi, v[t], std::fma(-vi, w[t], r[t]));
+    r[t] = x;
+    acc += x * vn[t];
+    pn[t] += vni * x;
+  }
+  pn[0] += acc;
+}
+
+// Householder reduction of symmetric `a` (n x n, upper triangle read and
+// overwritten; the lower triangle is ignored) to tridiagonal
 // form T = Q^T A Q, Q = H_0 H_1 ... H_{n-3} with H_k = I - beta_k v_k v_k^T
 // acting on indices k+1 .. n-1 (Golub & Van Loan, Sec. 8.3.1).  diag/off
 // receive T's diagonal and sub-diagonal (off[n-1] = 0); row k of `hv` holds
 // v_k in its entries k+1 .. n-1 and beta[k] its factor (0 when H_k = I).
+// The upper triangle keeps every column below the diagonal contiguous (as
+// the row right of it).  Each step's rank-2 update of the trailing block runs
+// in one pass with the next step's product A v_next: the block's first row is
+// updated first, the next reflector is formed from it, then every row is
+// updated and multiplied while it is at hand.
 void householder_tridiag(int n, double* a, double* diag, double* off, double* hv, double* beta) {
   std::fill(hv, hv + (size_t)n * n, 0.0);
   std::fill(beta, beta + n, 0.0);
-  std::vector<double> p(n), w(n);
+  std::vector<double> p(n), w(n), pn(n);
+  auto row = [&](int i) { return a + (size_t)i * n + i; };  // row i from its diagonal
+  double alpha = 0.0;
+  if (n >= 3) beta[0] = householder_vec(row(0) + 1, n - 1, hv + 1, &alpha);
+  bool p_ready = false;  // p holds A22 v_k, accumulated in the previous step's pass
   for (int k = 0; k + 2 < n; ++k) {
-    const int m = n - k - 1;  // length of the column part below the diagonal
-    double* v = hv + (size_t)k * n + (k + 1);
-    for (int i = 0; i < m; ++i) v[i] = a[(size_t)(k + 1 + i) * n + k];
-    const double sumsq = dot(v, v, m);
-    const double x0 = v[0];
-    double alpha = std::sqrt(sumsq);
-    if (alpha == 0.0) { std::fill(v, v + m, 0.0); continue; }  // column already reduced
-    if (x0 > 0) alpha = -alpha;                                // reflect away from x0's sign
-    v[0] = x0 - alpha;
-    const double vv = sumsq - x0 * x0 + v[0] * v[0];
-    if (vv == 0.0) { std::fill(v, v + m, 0.0); continue; }
-    const double bk = 2.0 / vv;
-    beta[k] = bk;
-    // p = beta * A22 v,  K = beta/2 * v.p,  w = p - K v
-    // Only the lower triangle of A22 is kept up to date: row i holds
-    // entries j <= i, and A22 v gathers row i (j < i) and column i (j > i).
-    std::fill(p.begin(), p.begin() + m, 0.0);
-    for (int i = 0; i < m; ++i) {
-      const double* ai = a + (size_t)(k + 1 + i) * n + (k + 1);
-      p[i] += dot_axpy(ai, v, v[i], p.data(), i) + ai[i] * v[i];
+    const int m = n - k - 1;  // order of the trailing block A22 (rows/cols k+1..)
+    const double* v = hv + (size_t)k * n + (k + 1);
+    const double bk = beta[k];
+    const double alpha_k = alpha;
+    if (bk != 0.0) {
+      if (!p_ready) {  // p = A22 v over the upper triangle
+        std::fill(p.begin(), p.begin() + m, 0.0);
+        for (int i = 0; i < m; ++i) {
+          const double* r = row(k + 1 + i);
+          p[i] += r[0] * v[i] + dot_axpy(r + 1, v + i + 1, v[i], p.data() + i + 1, m - i - 1);
+        }
+      }
+      // p = beta A22 v,  K = beta/2 v.p,  w = p - K v
+      for (int i = 0; i < m; ++i) p[i] *= bk;
+      const double K = 0.5 * bk * dot(v, p.data(), m);
+      for (int i = 0; i < m; ++i) w[i] = p[i] - K * v[i];
+      double* r0 = row(k + 1);  // the block's first row
+      for (int t = 0; t < m; ++t) r0[t] = std::fma(-w[0], v[t], std::fma(-v[0], w[t], r0[t]));
     }
-    for (int i = 0; i < m; ++i) p[i] *= bk;
-    const double K = 0.5 * bk * dot(v, p.data(), m);
-    for (int i = 0; i < m; ++i) w[i] = p[i] - K * v[i];
-    // A22 -= v w^T + w v^T (lower triangle)
-    for (int i = 0; i < m; ++i)
-      axpy2(-v[i], w.data(), -w[i], v, a + (size_t)(k + 1 + i) * n + (k + 1), i + 1);
-    // column k now has a single sub-diagonal entry alpha
-    for (int i = 0; i < m; ++i) a[(size_t)(k + 1 + i) * n + k] = (i == 0) ? alpha : 0.0;
+    p_ready = false;
+    const bool next = k + 3 < n;
+    double* vn = next ? hv + (size_t)(k + 1) * n + (k + 2) : nullptr;
+    if (next) beta[k + 1] = householder_vec(row(k + 1) + 1, m - 1, vn, &alpha);
+    const bool fuse = next && beta[k + 1] != 0.0;
+    if (fuse) std::fill(pn.begin(), pn.begin() + (m - 1), 0.0);
+    if (bk != 0.0 || fuse) {
+      for (int i = 1; i < m; ++i) {
+        double* r = row(k + 1 + i);  // entries j = i .. m-1 of the block's row i
+        const int ii = i - 1;        // its row in the next block
+        if (bk != 0.0 && fuse) {
+          update_row_and_product(r, v + i, w.data() + i, v[i], w[i], vn + ii, pn.data() + ii, m - i);
+        } else if (bk != 0.0) {
+          axpy2(-v[i], w.data() + i, -w[i], v + i, r, m - i);
+        } else {
+          pn[ii] += r[0] * vn[ii] + dot_axpy(r + 1, vn + ii + 1, vn[ii], pn.data() + ii + 1, m - i - 1);
+        }
+      }
+      if (fuse) {
+        std::swap(p, pn);
+        p_ready = true;
+      }
+    }
+    // column k below its diagonal (row k right of it) is now alpha e_0
+    double* rk = row(k) + 1;
+    for (int t = 0; t < m; ++t) rk[t] = t == 0 ? alpha_k : 0.0;
   }
   for (int i = 0; i < n; ++i) diag[i] = a[(size_t)i * n + i];
-  for (int i = 0; i + 1 < n; ++i) off[i] = a[(size_t)(i + 1) * n + i];
+  for (int i = 0; i + 1 < n; ++i) off[i] = a[(size_t)i * n + i + 1];
   off[n - 1] = 0.0;
 }
 
@@ -715,7 +789,8 @@ void bisect_eigs(int n, const double* diag, const double* off2, double pivmin, d
 bool tridiag_of(int n, const double* A, double* diag, double* off, double* hv, double* beta) {
   if (!all_finite(A, (size_t)n * n)) return false;
   double* a = thread_buffer(2, (size_t)n * n);
-  std::copy(A, A + (size_t)n * n, a);
+  for (int i = 0; i < n; ++i)  // A's lower triangle, transposed into the upper one
+    for (int j = i; j < n; ++j) a[(size_t)i * n + j] = A[(size_t)j * n + i];
   householder_tridiag(n, a, diag, off, hv, beta);
   return true;
 }

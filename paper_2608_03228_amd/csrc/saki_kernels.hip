@@ -2244,70 +2244,111 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void merge_kernel(
 
 // ---------------------------------------------------------------- calibration moments
 
-// grid (ceil(d/16), ceil(d/16), H_q + H_kv), block 256 = 16 x 16.  Work-group
-// (bi, bj, head) with bi <= bj forms the 16 x 16 tile (rows 16 bi.., columns
-// 16 bj..) of that head's moment and writes it and its mirror.  Heads below
-// H_q are query heads (uncentred); the rest are KV heads, centred by their
-// column means, which every work-group computes for its own 32 columns.
-constexpr int kMomTile = 16;
-constexpr int kMomChunk = 64;  // tokens staged per step
+// grid: (H_q + H_kv) * nb * (nb + 1) / 2 work-groups, nb = ceil(d / 64), block
+// 256.  Work-group (head, block pair bi <= bj) forms the 64 x 64 block (rows
+// 64 bi.., columns 64 bj..) of that head's moment and writes it and its
+// mirror: thread (ty, tx) holds the 4 x 4 outputs of rows 64 bi + 4 ty ..,
+// columns 64 bj + 4 tx .., each a float64 sum over the tokens in order.
+// Heads below H_q are query heads (uncentred); the rest are KV heads, centred
+// by their column means, which every work-group computes for its own 128
+// columns.  Tokens are staged in LDS 32 at a time.
+constexpr int kMomBlk = 64;
+constexpr int kMomChunk = 32;  // tokens staged per step
 
 __global__ __launch_bounds__(256) void moments_kernel(const float* __restrict__ q_cal,
                                                       const float* __restrict__ k_cal, int H_q,
                                                       int T, int d, double* __restrict__ Sq,
                                                       double* __restrict__ Sk,
                                                       double* __restrict__ mu_out) {
-  const int bi = blockIdx.x, bj = blockIdx.y, head = blockIdx.z;
-  if (bi > bj) return;  // uniform over the work-group
+  const int nb = (d + kMomBlk - 1) / kMomBlk;
+  const int npairs = nb * (nb + 1) / 2;
+  const int head = blockIdx.x / npairs;
+  int bi = 0, rem = blockIdx.x % npairs;  // the pair's rank in row-major order of bi <= bj
+  while (rem >= nb - bi) {
+    rem -= nb - bi;
+    ++bi;
+  }
+  const int bj = bi + rem;
   const bool key = head >= H_q;
   const int hh = key ? head - H_q : head;
   const float* X = (key ? k_cal : q_cal) + (size_t)hh * T * d;
-  const int tx = threadIdx.x % kMomTile, ty = threadIdx.x / kMomTile;
-  const int i0 = bi * kMomTile, j0 = bj * kMomTile;
-  __shared__ double xi[kMomChunk][kMomTile + 1], xj[kMomChunk][kMomTile + 1];
-  __shared__ double mean[2 * kMomTile];
-  __shared__ double part[8][2 * kMomTile];
-  if (key) {  // column means: 8 threads per column, every eighth token each
-    const int c = threadIdx.x % (2 * kMomTile), sl = threadIdx.x / (2 * kMomTile);
-    const int col = c < kMomTile ? i0 + c : j0 + c - kMomTile;
+  const int tid = threadIdx.x;
+  const int tx = tid % 16, ty = tid / 16;
+  const int i0 = bi * kMomBlk, j0 = bj * kMomBlk;
+  __shared__ double xi[kMomChunk][kMomBlk], xj[kMomChunk][kMomBlk];
+  __shared__ double mean[2 * kMomBlk];
+  __shared__ double part[2][2 * kMomBlk];
+  // column means (KV heads): two threads per column, even and odd tokens
+  {
+    const int c = tid % (2 * kMomBlk), h = tid / (2 * kMomBlk);
+    const int col = c < kMomBlk ? i0 + c : j0 + c - kMomBlk;
     double m = 0.0;
-    if (col < d) {
-#pragma unroll 8
-      for (int t = sl; t < T; t += 8) m += (double)X[(size_t)t * d + col];
+    if (key && col < d) {
+#pragma unroll 16
+      for (int t = h; t < T; t += 2) m += (double)X[(size_t)t * d + col];
     }
-    part[sl][c] = m;
+    part[h][c] = m;
   }
   __syncthreads();
-  if (threadIdx.x < 2 * kMomTile) {
-    double m = 0.0;
-    if (key) {
+  if (tid < 2 * kMomBlk) mean[tid] = key ? (part[0][tid] + part[1][tid]) / (double)T : 0.0;
+  __syncthreads();
+  double acc[4][4];
 #pragma unroll
-      for (int sl = 0; sl < 8; ++sl) m += part[sl][threadIdx.x];
-      m /= (double)T;
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[a][e] = 0.0;
+  // tokens t0 .. t0 + 31 of both column blocks: element u of this thread is
+  // token t0 + (tid + 256 u) / 64, column (tid + 256 u) % 64; the next chunk's
+  // values are loaded while this one is summed
+  constexpr int kPer = kMomChunk * kMomBlk / 256;
+  float ni[kPer], nj[kPer];
+  auto load_chunk = [&](int t0) {
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = tid + 256 * u, t = t0 + e / kMomBlk, c = e % kMomBlk;
+      ni[u] = (t < T && i0 + c < d) ? X[(size_t)t * d + i0 + c] : 0.f;
+      nj[u] = (t < T && j0 + c < d) ? X[(size_t)t * d + j0 + c] : 0.f;
     }
-    mean[threadIdx.x] = m;
-  }
-  __syncthreads();
-  double acc = 0.0;
+  };
+  load_chunk(0);
   for (int t0 = 0; t0 < T; t0 += kMomChunk) {
-    for (int e = threadIdx.x; e < kMomChunk * kMomTile; e += 256) {
-      const int tt = e / kMomTile, c = e % kMomTile, t = t0 + tt;
-      xi[tt][c] = (t < T && i0 + c < d) ? (double)X[(size_t)t * d + i0 + c] - mean[c] : 0.0;
-      xj[tt][c] = (t < T && j0 + c < d) ? (double)X[(size_t)t * d + j0 + c] - mean[kMomTile + c] : 0.0;
+    // stage the chunk (centred; 0 past T or d), then request the next one
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = tid + 256 * u, tt = e / kMomBlk, c = e % kMomBlk, t = t0 + tt;
+      xi[tt][c] = (t < T && i0 + c < d) ? (double)ni[u] - mean[c] : 0.0;
+      xj[tt][c] = (t < T && j0 + c < d) ? (double)nj[u] - mean[kMomBlk + c] : 0.0;
+    }
+    if (t0 + kMomChunk < T) load_chunk(t0 + kMomChunk);
+    __syncthreads();
+#pragma unroll 4
+    for (int tt = 0; tt < kMomChunk; ++tt) {
+      double va[4], vb[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        va[a] = xi[tt][4 * ty + a];
+        vb[a] = xj[tt][4 * tx + a];
+      }
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[a][e] = fma(va[a], vb[e], acc[a][e]);
     }
     __syncthreads();
-#pragma unroll 8
-    for (int tt = 0; tt < kMomChunk; ++tt) acc = fma(xi[tt][ty], xj[tt][tx], acc);
-    __syncthreads();
   }
-  const int i = i0 + ty, j = j0 + tx;
-  if (i < d && j < d) {
-    double* S = key ? Sk + (size_t)hh * d * d : Sq + (size_t)hh * d * d;
-    const double v = acc / (double)T;
-    S[(size_t)i * d + j] = v;
-    S[(size_t)j * d + i] = v;
-  }
-  if (key && bi == 0 && ty == 0 && j < d) mu_out[(size_t)hh * d + j] = mean[kMomTile + tx];
+  double* S = key ? Sk + (size_t)hh * d * d : Sq + (size_t)hh * d * d;
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int i = i0 + 4 * ty + a, j = j0 + 4 * tx + e;
+      if (i < d && j < d) {
+        const double v = acc[a][e] / (double)T;
+        S[(size_t)i * d + j] = v;
+        S[(size_t)j * d + i] = v;
+      }
+    }
+  if (key && bi == 0 && tid < kMomBlk && j0 + tid < d) mu_out[(size_t)hh * d + j0 + tid] = mean[kMomBlk + tid];
 }
 
 // ---------------------------------------------------------------- reading the winners
@@ -2781,8 +2822,8 @@ int saki_calibration_moments(const float* q_cal, const float* k_cal, int H_q, in
   if (!q_cal || !k_cal || !Sigma_q || !Sigma_k || !key_mean) return SAKI_ERR_ARG;
   if (H_q <= 0 || H_kv <= 0 || T <= 0 || d <= 0 || d > 4096) return SAKI_ERR_ARG;
   if ((long long)H_q + H_kv > 65535) return SAKI_ERR_UNSUPPORTED;
-  const unsigned nb = (unsigned)((d + kMomTile - 1) / kMomTile);
-  hipLaunchKernelGGL(moments_kernel, dim3(nb, nb, H_q + H_kv), dim3(256), 0,
+  const long long nb = (d + kMomBlk - 1) / kMomBlk;
+  hipLaunchKernelGGL(moments_kernel, dim3((unsigned)((H_q + H_kv) * (nb * (nb + 1) / 2))), dim3(256), 0,
                      reinterpret_cast<hipStream_t>(stream), q_cal, k_cal, H_q, T, d, Sigma_q,
                      Sigma_k, key_mean);
   return launch_ok() ? SAKI_OK : SAKI_ERR_HIP;
