@@ -54,6 +54,27 @@ def test_sym_eig_degenerate_and_graded():
     np.testing.assert_array_equal(w, [1.0, 2.0, 3.0])
 
 
+@pytest.mark.parametrize("n", [4, 9, 33, 128])
+def test_sym_eig_structured_matrices(n):
+    """Matrices whose Householder reduction meets columns that are already
+    reduced part-way (a zero or diagonal matrix, a block-diagonal one, a
+    low-rank one): eigenvalues, residuals and orthogonality as for dense ones."""
+    rng = np.random.default_rng(100 + n)
+    A = rng.standard_normal((n, n))
+    A = A + A.T
+    blocks = A.copy()
+    blocks[n // 2:, :n // 2] = 0.0
+    blocks[:n // 2, n // 2:] = 0.0
+    B = rng.standard_normal((n, 2))
+    for M in (np.zeros((n, n)), np.diag(rng.standard_normal(n)), blocks, B @ B.T):
+        w, V = S.saki_sym_eig(M)
+        ref = np.linalg.eigvalsh(M)
+        scale = max(np.abs(ref).max(), 1.0)
+        assert np.max(np.abs(w - ref)) <= 1e-13 * n * scale
+        assert np.max(np.abs(M @ V - V * w)) <= 1e-13 * n * scale
+        np.testing.assert_allclose(V.T @ V, np.eye(n), atol=1e-13 * n)
+
+
 def _m(B_q, B_k):
     return B_q.astype(np.float64) @ B_k.astype(np.float64).T
 
