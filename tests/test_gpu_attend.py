@@ -135,3 +135,49 @@ def test_attend_full_rank_reconstruction_is_exact_attention():
         extra = np.stack([qn[i] * dk[idx[0, h, i]] / np.sqrt(128) for i in range(2)])
         _check(a[0, h], inp["queries"][0, h], np.full(2, N - 1), keys, inp["values"][0, 0],
                idx[0, h], extra)
+
+
+def test_attend_sequences_groups_short_and_skipped_lists():
+    """Two sequences and two KV groups; lists of 40 entries (the work-group's
+    last wave has none), one of 5 (only the first wave), one empty row (zeros),
+    and entries at or past N_valid (skipped); exact keys and the GQA-shared
+    index's reconstruction (float32 codes)."""
+    spec = W.SPECS["decode_1m"].with_(N=1200, H_q=4, H_kv=2, Q=3, batch=2)
+    inp = W.make_layer(spec, with_values=True)
+    N_cap, N_valid, k, G = 1200, 1100, 40, 2
+    rng = np.random.default_rng(7)
+    idx = np.stack([rng.choice(N_cap, k, replace=False) for _ in range(2 * 4 * 3)])
+    idx = idx.reshape(2, 4, 3, k).astype(np.int32)
+    idx[0, 1, 0, :] = -1   # an empty row
+    idx[1, 2, 1, 5:] = -1  # five entries
+    visible = np.where(idx < N_valid, idx, -1)  # what the oracle attends over
+    keys, values, q = inp["keys"], inp["values"], inp["queries"]
+    pos = np.full(3, N_valid - 1)
+    out = S.saki_attend(_t(values), _t(q), _t(idx, torch.int32), N_valid,
+                        keys=_t(keys)).cpu().numpy()
+    for b in range(2):
+        for h in range(4):
+            g = h // G
+            if b == 0 and h == 1:
+                assert np.all(out[b, h, 0] == 0.0)
+                rows = [1, 2]
+            else:
+                rows = [0, 1, 2]
+            _check(out[b, h, rows], q[b, h, rows], pos[rows], keys[b, g], values[b, g],
+                   visible[b, h, rows])
+    # the GQA-shared index: one code set per KV head, read by its G query heads
+    cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32, method="shared")
+    index = S.saki_build_index(_t(keys), _t(cal["B_k"][::G]), _t(cal["mu"]), 32, "f32", 2)
+    out2 = S.saki_attend(_t(values), _t(q), _t(idx, torch.int32), N_valid, index=index,
+                         sketch="f32", B_q=_t(cal["B_q"]), mu=_t(cal["mu"]), r=32,
+                         index_heads=2).cpu().numpy()
+    assert np.all(out2[0, 1, 0] == 0.0)
+    for g in range(2):
+        oc = O.saki_calibrate_shared(inp["q_cal"][G * g:G * g + G], inp["k_cal"][g], 32)
+        for b in range(2):
+            c = O.f32_round(O.codes(oc["B_k"], oc["mu"], keys[b, g]))
+            khat = O.reconstruct_keys(oc["B_q"], oc["mu"], c)
+            for h in range(G * g, G * g + G):
+                rows = [1, 2] if (b == 0 and h == 1) else [0, 1, 2]
+                _check(out2[b, h, rows], q[b, h, rows], pos[rows], khat, values[b, g],
+                       visible[b, h, rows])
