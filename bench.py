@@ -61,6 +61,12 @@ def parse():
 # flagged)
 STAGE_KERNEL = {"build": "build_index_kernel", "score_topk": "score_mfma_kernel",
                 "recall": "exact_gate_kernel"}
+# template instance launched for each stage (r, sketch) as rocprofv3 names it
+STAGE_INSTANCE = {
+    "build": lambda r, sk: f"build_index_kernel<{r}, false, {({'f32': 0, 'bf16': 1, 'fp8': 2})[sk]}>",
+    "score_topk": lambda r, sk: f"score_mfma_kernel<{r}, {({'f32': 0, 'bf16': 1, 'fp8': 2})[sk]}>",
+    "recall": lambda r, sk: "exact_gate_kernel<false>",
+}
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_03228_amd", "csrc", "saki_kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.md")
 
@@ -71,10 +77,11 @@ def kernel_source_digest():
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(kernel, workload):
+def measured_traffic(kernel, workload, instance):
     """HBM bytes per launch of `kernel` on `workload` from the committed
     rocprofv3 FETCH_SIZE / WRITE_SIZE summary (scaled by a plain copy of
-    known size), or None when no row matches the current kernel source."""
+    known size), or None when no row matches the current kernel source and
+    the template instance the run launches (sketch type, rows per wave)."""
     try:
         lines = open(TRAFFIC_FILE).read().splitlines()
     except OSError:
@@ -82,7 +89,8 @@ def measured_traffic(kernel, workload):
     digest = kernel_source_digest()
     for ln in lines:
         cells = [c.strip() for c in ln.strip().strip("|").split("|")]
-        if len(cells) >= 6 and cells[0] == kernel and cells[1] == workload and cells[2] == digest:
+        if (len(cells) >= 7 and cells[0] == kernel and cells[1] == workload and cells[2] == digest
+                and cells[6].startswith(f"`{instance}`")):
             try:
                 return float(cells[5])
             except ValueError:
@@ -284,7 +292,11 @@ def run_decode(args, spec):
     roof = {"bound": "hbm", "achieved": scan_bytes / (score_ms / 1e3) / 1e9,
             "peak": PEAK["hbm_GBps"], "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = measured_traffic("score_stream_kernel", spec.name)
+    # the profiled decode run: per-query-head index (one row per wave)
+    st = {"f32": 0, "bf16": 1, "fp8": 2}[sk]
+    rows_per_wave = 4 if (H_q // IH) * Q >= 4 else 1
+    roof["traffic"] = measured_traffic("score_stream_kernel", spec.name,
+                                       f"score_stream_kernel<{r}, {st}, {rows_per_wave}>")
     roof["kernel"] = "score_topk"
     roof["work"] = {"bytes": scan_bytes, "code_bytes": code_bytes}
 
@@ -482,7 +494,10 @@ def main():
         roof = {"bound": "mfma", "achieved": t["flops"] / sec / 1e12, "peak": t["peak_flops"],
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = measured_traffic(STAGE_KERNEL[dom], spec.name)
+    # the profiled batched run: the paper's factors and fp32 keys (the recall
+    # kernel's traffic depends on how good the candidate lists are)
+    roof["traffic"] = (measured_traffic(STAGE_KERNEL[dom], spec.name, STAGE_INSTANCE[dom](r, sk))
+                       if args.method == "opt" and k == 64 else None)
     roof["kernel"] = dom
     roof["work"] = {"bytes": t["bytes"], "flops": t["flops"], "flop_dtype": t["flop_unit"]}
     others = {}
