@@ -737,51 +737,101 @@ struct ShiftedTridiagLU {
   }
 };
 
-// The eigenvalues with ascending indices idx[0..c) (c <= kBisectShifts) of
-// the symmetric tridiagonal (diag, off) by bisection on Sturm counts (Golub &
-// Van Loan, Sec. 8.4.1): n_halvings halvings of [glo, ghi], kBisectShifts
-// shifts at a time in independent 256-bit vectors so that the divisions of
-// the sequences overlap.  A pivot smaller in magnitude than pivmin is
-// replaced by -pivmin.
+// Sturm counts of the symmetric tridiagonal (diag, off2 = off^2): cnt[e] =
+// the number of eigenvalues below x[e] for the kBisectShifts points, in
+// independent 4-wide sequences so that their divisions overlap (Golub & Van
+// Loan, Sec. 8.4.1).  A pivot smaller in magnitude than pivmin is replaced by
+// -pivmin.
 constexpr int kBisectShifts = 16;
-void bisect_eigs(int n, const double* diag, const double* off2, double pivmin, double glo,
-                 double ghi, int n_halvings, const int* idx, int c, double* out) {
-  constexpr int V = kBisectShifts / 4;  // independent 4-wide Sturm sequences
-  alignas(32) double kk[kBisectShifts], res[kBisectShifts];
-  for (int e = 0; e < kBisectShifts; ++e) kk[e] = e < c ? (double)idx[e] : 0.0;
-  const __m256d one = _mm256_set1_pd(1.0), half = _mm256_set1_pd(0.5), zero = _mm256_setzero_pd();
+void sturm_counts(int n, const double* diag, const double* off2, double pivmin, const double* x,
+                  int* cnt_out) {
+  constexpr int V = kBisectShifts / 4;
+  const __m256d one = _mm256_set1_pd(1.0), zero = _mm256_setzero_pd();
   const __m256d npm = _mm256_set1_pd(-pivmin), pm = _mm256_set1_pd(pivmin);
   const __m256d absmask = _mm256_castsi256_pd(_mm256_set1_epi64x(0x7fffffffffffffffll));
-  __m256d lo[V], hi[V], k[V], x[V], q[V], cnt[V];
+  __m256d xv[V], q[V], cnt[V];
+  const __m256d d0 = _mm256_set1_pd(diag[0]);
   for (int v = 0; v < V; ++v) {
-    lo[v] = _mm256_set1_pd(glo);
-    hi[v] = _mm256_set1_pd(ghi);
-    k[v] = _mm256_load_pd(kk + 4 * v);
+    xv[v] = _mm256_loadu_pd(x + 4 * v);
+    q[v] = _mm256_sub_pd(d0, xv[v]);
+    q[v] = _mm256_blendv_pd(q[v], npm, _mm256_cmp_pd(_mm256_and_pd(q[v], absmask), pm, _CMP_LT_OQ));
+    cnt[v] = _mm256_and_pd(_mm256_cmp_pd(q[v], zero, _CMP_LT_OQ), one);
   }
-  for (int it = 0; it < n_halvings; ++it) {
-    const __m256d d0 = _mm256_set1_pd(diag[0]);
+  for (int i = 1; i < n; ++i) {
+    const __m256d di = _mm256_set1_pd(diag[i]), ei = _mm256_set1_pd(off2[i - 1]);
     for (int v = 0; v < V; ++v) {
-      x[v] = _mm256_mul_pd(_mm256_add_pd(lo[v], hi[v]), half);
-      q[v] = _mm256_sub_pd(d0, x[v]);
+      q[v] = _mm256_sub_pd(_mm256_sub_pd(di, xv[v]), _mm256_div_pd(ei, q[v]));
       q[v] = _mm256_blendv_pd(q[v], npm, _mm256_cmp_pd(_mm256_and_pd(q[v], absmask), pm, _CMP_LT_OQ));
-      cnt[v] = _mm256_and_pd(_mm256_cmp_pd(q[v], zero, _CMP_LT_OQ), one);
+      cnt[v] = _mm256_add_pd(cnt[v], _mm256_and_pd(_mm256_cmp_pd(q[v], zero, _CMP_LT_OQ), one));
     }
-    for (int i = 1; i < n; ++i) {
-      const __m256d di = _mm256_set1_pd(diag[i]), ei = _mm256_set1_pd(off2[i - 1]);
-      for (int v = 0; v < V; ++v) {
-        q[v] = _mm256_sub_pd(_mm256_sub_pd(di, x[v]), _mm256_div_pd(ei, q[v]));
-        q[v] = _mm256_blendv_pd(q[v], npm, _mm256_cmp_pd(_mm256_and_pd(q[v], absmask), pm, _CMP_LT_OQ));
-        cnt[v] = _mm256_add_pd(cnt[v], _mm256_and_pd(_mm256_cmp_pd(q[v], zero, _CMP_LT_OQ), one));
+  }
+  alignas(32) double c[kBisectShifts];
+  for (int v = 0; v < V; ++v) _mm256_store_pd(c + 4 * v, cnt[v]);
+  for (int e = 0; e < kBisectShifts; ++e) cnt_out[e] = (int)c[e];
+}
+
+// The eigenvalues with ascending indices i_lo .. n-1 (the n - i_lo largest)
+// of the symmetric tridiagonal (diag, off2), by multisection on Sturm counts
+// over [glo, ghi) (count(glo) = 0, count(ghi) = n).  A bracket [a, b) with
+// counts ca = count(a), cb = count(b) holds eigenvalues ca .. cb-1.  Each
+// round spends the kBisectShifts evaluation points on the open brackets that
+// hold wanted eigenvalues: several points per bracket, equally spaced, while
+// fewer brackets are open, one (the midpoint) once there are more.  A bracket
+// no wider than tol closes, and its eigenvalues take its midpoint.  out[i -
+// i_lo] receives eigenvalue i.
+void multisect_eigs(int n, const double* diag, const double* off2, double pivmin, double glo,
+                    double ghi, double tol, int i_lo, double* out) {
+  struct Bracket {
+    double a, b;
+    int ca, cb;
+  };
+  std::vector<Bracket> open{{glo, ghi, 0, n}}, act;
+  while (!open.empty()) {
+    act.clear();
+    for (const Bracket& B : open) {
+      const int t0 = std::max(B.ca, i_lo), t1 = B.cb;  // wanted eigenvalues in the bracket
+      if (t0 >= t1) continue;
+      if (B.b - B.a <= tol) {
+        for (int i = t0; i < t1; ++i) out[i - i_lo] = 0.5 * (B.a + B.b);
+        continue;
+      }
+      act.push_back(B);
+    }
+    open.clear();
+    for (size_t s = 0; s < act.size(); s += kBisectShifts) {
+      const int m = (int)std::min<size_t>(kBisectShifts, act.size() - s);
+      const int per = kBisectShifts / m;  // points per bracket this round
+      alignas(32) double x[kBisectShifts];
+      int cnt[kBisectShifts];
+      int np = 0;
+      for (int j = 0; j < m; ++j) {
+        const Bracket& B = act[s + j];
+        for (int u = 1; u <= per; ++u) x[np++] = B.a + (B.b - B.a) * ((double)u / (per + 1));
+      }
+      for (int e = np; e < kBisectShifts; ++e) x[e] = x[0];  // unused lanes
+      sturm_counts(n, diag, off2, pivmin, x, cnt);
+      for (int j = 0, e = 0; j < m; ++j) {
+        const Bracket& B = act[s + j];
+        double a = B.a;
+        int ca = B.ca;
+        bool stuck = false;
+        for (int u = 0; u < per; ++u, ++e) {
+          if (!(x[e] > a && x[e] < B.b)) stuck = true;  // no room left between doubles
+          const int c = std::min(std::max(cnt[e], ca), B.cb);  // counts rise with x
+          if (!stuck) {
+            open.push_back({a, x[e], ca, c});
+            a = x[e];
+            ca = c;
+          }
+        }
+        if (stuck) {  // close what is left at its midpoint
+          for (int i = std::max(ca, i_lo); i < B.cb; ++i) out[i - i_lo] = 0.5 * (a + B.b);
+        } else {
+          open.push_back({a, B.b, ca, B.cb});
+        }
       }
     }
-    for (int v = 0; v < V; ++v) {  // count(x) <= k: the k-th eigenvalue is >= x
-      const __m256d up = _mm256_cmp_pd(cnt[v], k[v], _CMP_LE_OQ);
-      lo[v] = _mm256_blendv_pd(lo[v], x[v], up);
-      hi[v] = _mm256_blendv_pd(x[v], hi[v], up);
-    }
   }
-  for (int v = 0; v < V; ++v) _mm256_store_pd(res + 4 * v, _mm256_mul_pd(_mm256_add_pd(lo[v], hi[v]), half));
-  for (int e = 0; e < c; ++e) out[e] = res[e];
 }
 
 // Tridiagonal form of symmetric A (n x n row-major, read from its lower
@@ -826,19 +876,13 @@ bool top_eigpairs(int n, const double* diag, const double* off, const double* hv
     }
     const double pivmin = std::numeric_limits<double>::min() * std::max(1.0, emax);
     const double pad = 2.0 * std::numeric_limits<double>::epsilon() * std::max(std::fabs(glo), std::fabs(ghi)) + pivmin;
-    // halve the Gershgorin interval down to 2^-46 of the spectrum's scale: the
-    // factors are stored in float32, 2^-46 |T| is far below their rounding
+    // narrow the Gershgorin interval down to 2^-46 of the spectrum's scale:
+    // the factors are stored in float32, 2^-46 |T| is far below their rounding
     const double scale = std::max(std::fabs(glo), std::fabs(ghi));
-    int n_halvings = 0;
-    for (double wdt = (ghi - glo) + 2.0 * pad; wdt > std::ldexp(scale, -46) && n_halvings < 64; wdt *= 0.5)
-      ++n_halvings;
-    for (int m0 = 0; m0 < r; m0 += kBisectShifts) {
-      int idx[kBisectShifts];
-      const int c = std::min(kBisectShifts, r - m0);
-      for (int e = 0; e < c; ++e) idx[e] = n - 1 - (m0 + e);  // ascending index of the (m0+e)-th largest
-      bisect_eigs(n, diag, off2.data(), pivmin, glo - pad, ghi + pad, n_halvings, idx, c,
-                  ev.data() + m0);
-    }
+    const double tol = std::ldexp(scale, -46);
+    std::vector<double> asc(r);  // eigenvalues n-r .. n-1 in ascending index order
+    multisect_eigs(n, diag, off2.data(), pivmin, glo - pad, ghi + pad, tol, n - r, asc.data());
+    for (int m = 0; m < r; ++m) ev[m] = asc[r - 1 - m];  // descending
   }
   std::copy(ev.begin(), ev.begin() + (all_values ? n : r), w);
 
