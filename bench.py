@@ -292,11 +292,17 @@ def run_decode(args, spec):
     roof = {"bound": "hbm", "achieved": scan_bytes / (score_ms / 1e3) / 1e9,
             "peak": PEAK["hbm_GBps"], "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    # the profiled decode run: per-query-head index (one row per wave)
+    # the kernel the library runs for this shape: 16 or more queries per head
+    # take the MFMA kernels (one pass over the codes from 16,384 keys on),
+    # fewer the streaming kernel with 1 or 4 rows per wave
     st = {"f32": 0, "bf16": 1, "fp8": 2}[sk]
-    rows_per_wave = 4 if (H_q // IH) * Q >= 4 else 1
-    roof["traffic"] = measured_traffic("score_stream_kernel", spec.name,
-                                       f"score_stream_kernel<{r}, {st}, {rows_per_wave}>")
+    if Q >= 16:
+        kern = "score_scan_kernel" if N >= 16384 else "score_mfma_kernel"
+        inst = f"{kern}<{r}, {st}>"
+    else:
+        kern = "score_stream_kernel"
+        inst = f"{kern}<{r}, {st}, {4 if (H_q // IH) * Q >= 4 else 1}>"
+    roof["traffic"] = measured_traffic(kern, spec.name, inst)
     roof["kernel"] = "score_topk"
     roof["work"] = {"bytes": scan_bytes, "code_bytes": code_bytes}
 

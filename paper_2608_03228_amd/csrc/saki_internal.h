@@ -11,6 +11,8 @@ constexpr int kHeadDim = 128;  // d on the GPU path
 constexpr int kMaxK = 64;      // top-k lists hold 64 entries, one per wave lane
 constexpr int kTile = 64;      // keys per index tile
 constexpr int kChunkBytes = 16;
+constexpr int kScanWaves = 1;          // waves per work-group of the one-pass MFMA scoring kernel
+constexpr int kScanMinKeys = 16384;    // rows at least this long take it
 
 inline bool rank_supported(int r) { return r == 16 || r == 32 || r == 64 || r == 128; }
 // bytes per code element: float32 (0), bf16 (1), fp8 E4M3 (2)
@@ -38,6 +40,8 @@ struct Plan {
   int waves = 1;       // waves per workgroup
   int row_blocks = 0;  // workgroups along the query axis
   bool split = false;  // streaming: the waves of a workgroup share rows and take consecutive chunks
+  bool scan = false;   // MFMA rows scored in one pass (row_blocks: 16-row blocks, one per wave;
+                       // with a split key axis z_off: chunk gates, flag_off: rows to redo)
   int chunk = kTile;   // keys per chunk (multiple of 64)
   int n_chunks = 1;
   size_t z_off = 0, b_off = 0, part_off = 0, flag_off = 0, ws_bytes = 0;
@@ -79,14 +83,26 @@ inline Plan make_plan(int B, int heads, int Q, int N_valid, int part_entry_bytes
 
 // Score path: the workspace holds the partial lists of a split key axis
 // (float score + int index), at least 256 bytes so that a size of 0 keeps
-// meaning invalid arguments.  Both kernels form the query sketch themselves.
-// The MFMA kernel takes 16 queries of one head per wave; the streaming kernel
-// takes the rows of one code set: the H_q / index_heads heads sharing it,
-// times Q.
+// meaning invalid arguments.  Every kernel forms the query sketch itself.
+// The MFMA kernels take 16 queries of one head per wave (the one-pass kernel
+// when the rows are long); the streaming kernel takes the rows of one code
+// set: the H_q / index_heads heads sharing it, times Q.
 inline Plan score_plan(int B, int H_q, int index_heads, int Q, int N_valid) {
   const bool mfma = Q >= 16;
   Plan p = mfma ? make_plan(B, H_q, Q, N_valid, 8, true)
                 : make_plan(B, index_heads, (H_q / index_heads) * Q, N_valid, 8, false);
+  if (mfma && N_valid >= kScanMinKeys) {
+    p.scan = true;
+    p.waves = kScanWaves;
+    p.row_blocks = (Q + 15) / 16;
+    if (p.n_chunks > 1) {  // per (row, chunk) gate of a chunk that kept too few keys; per-row redo flags
+      const size_t rows_total = (size_t)B * H_q * Q;
+      p.z_off = round_up(p.ws_bytes, 256);
+      p.flag_off = round_up(p.z_off + rows_total * p.n_chunks * sizeof(float), 256);
+      p.flag_count = rows_total;
+      p.ws_bytes = round_up(p.flag_off + rows_total * sizeof(int), 256);
+    }
+  }
   const int wave_rows = (int)((H_q / index_heads) * (size_t)Q + p.rows - 1) / p.rows;
   if (!mfma && wave_rows < 4) {  // too few rows to fill a workgroup: its waves split the keys
     p.split = true;

@@ -4,6 +4,8 @@
 //   build_index_kernel   key codes c = B_k^T (k - mu) for every query head (Eq. 4)
 //   score_mfma_kernel    z = B_q^T q, b = q^T mu and s = z . c + b on MFMA for
 //                        blocks of 16 query rows, top-64 per row
+//   score_scan_kernel    the same in one pass over the codes for long rows
+//                        (batches of decode queries), running top-64 per row
 //   score_stream_kernel  the same for few query rows per code set (decode):
 //                        one key per lane, key range split into chunks
 //   merge_kernel         reduces per-chunk partial top-64 lists of one row
@@ -656,6 +658,7 @@ struct MfmaScorer {
   bf16x8_t zb[NKB];
   i16x4_t zb4;
   float zf[NKF];
+  float init = 0.f;  // accumulator start (this lane's query column)
 
   // zs: this lane's query sketch row (RK floats, bf16 values for bf16 / fp8 codes)
   __device__ void load_operand(const float* zs, int g) {
@@ -721,7 +724,7 @@ struct MfmaScorer {
   __device__ __forceinline__ void mma(const Raw& r, f32x4_t acc[4]) const {
 #pragma unroll
     for (int sub = 0; sub < 4; ++sub) {
-      f32x4_t a = {0.f, 0.f, 0.f, 0.f};
+      f32x4_t a = {init, init, init, init};
       if constexpr (F8 && RK == 16) {
         a = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_i16x4(e4m3x4_to_bf16(r.v[sub][0].x)), zb4,
                                                      a, 0, 0, 0);
@@ -785,7 +788,92 @@ struct MfmaScorer {
       }
     }
   }
+
+  // body(t0, acc) for every tile of [t_beg, t_end) in order, with the loads
+  // of the next two tiles in flight while one is scored (three register
+  // buffers taken in turn) when a tile's operands fit in 32 registers;
+  // otherwise as for_tiles.  Loads past the last tile are clamped to it.
+  template <class F>
+  __device__ __forceinline__ void for_tiles_deep(const uint8_t* hbase, int t_beg, int t_end,
+                                                 int qi, int g, F&& body) const {
+    if constexpr (kPrefetch) {
+      if (t_beg >= t_end) return;
+      const int last = t_beg + ((t_end - 1 - t_beg) / kTile) * kTile;
+      auto at = [&](int t) { return hbase + (size_t)(min(t, last) / kTile) * TB; };
+      Raw ra, rb, rc;
+      load(at(t_beg), qi, g, ra);
+      load(at(t_beg + kTile), qi, g, rb);
+      for (int t0 = t_beg; t0 < t_end; t0 += 3 * kTile) {
+        load(at(t0 + 2 * kTile), qi, g, rc);
+        f32x4_t acc[4];
+        mma(ra, acc);
+        body(t0, acc);
+        if (t0 + kTile >= t_end) break;
+        load(at(t0 + 3 * kTile), qi, g, ra);
+        mma(rb, acc);
+        body(t0 + kTile, acc);
+        if (t0 + 2 * kTile >= t_end) break;
+        load(at(t0 + 4 * kTile), qi, g, rb);
+        mma(rc, acc);
+        body(t0 + 2 * kTile, acc);
+      }
+    } else {
+      for_tiles(hbase, t_beg, t_end, kTile, qi, g, body);
+    }
+  }
 };
+
+// The query sketch of a wave's 16 rows (lane (qi, g) = lane % 16, lane / 16)
+// on the f32 MFMA: D[m][qi] = sum_c B_q[c][m] q[qi][c] with lane group g
+// feeding dims c = 4s + g, rounded to bf16 for bf16 and fp8 codes and staged
+// through zs (16 x RK floats of LDS) into the scorer's operand.  Returns
+// b = q . mu of row qi (the same in its four lanes).  qr: row qi's query (any
+// valid row when !row_ok, whose query counts as zero).
+template <int RK, int ST>
+__device__ __forceinline__ float mfma_query_sketch(const float* __restrict__ qr, bool row_ok,
+                                                   const float* __restrict__ bq,
+                                                   const float* __restrict__ mr, float* zs, int qi,
+                                                   int g, MfmaScorer<RK, ST>& sc) {
+  constexpr int D = saki::kHeadDim;
+  f32x4_t za[RK / 16];
+#pragma unroll
+  for (int mb = 0; mb < RK / 16; ++mb) za[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float bp = 0.f;
+  // the loads of SB steps are issued together, then their products taken
+  constexpr int SB = RK <= 32 ? 16 : RK <= 64 ? 8 : 4;
+#pragma unroll 1
+  for (int s0 = 0; s0 < D / 4; s0 += SB) {
+    float qa[SB], ma[SB], ba[SB][RK / 16];
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      const int c = 4 * (s0 + u) + g;
+      qa[u] = qr[c];
+      ma[u] = mr[c];
+#pragma unroll
+      for (int mb = 0; mb < RK / 16; ++mb) ba[u][mb] = bq[c * RK + 16 * mb + qi];
+    }
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      const float qv = row_ok ? qa[u] : 0.f;
+      bp = fmaf(qv, ma[u], bp);
+#pragma unroll
+      for (int mb = 0; mb < RK / 16; ++mb)
+        za[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(ba[u][mb], qv, za[mb], 0, 0, 0);
+    }
+  }
+  const float b = sum_lane_groups(bp);
+#pragma unroll
+  for (int mb = 0; mb < RK / 16; ++mb)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const float zv = za[mb][v];
+      zs[qi * RK + 16 * mb + 4 * g + v] = ST != kStF32 ? bf16_round(zv) : zv;
+    }
+  wave_lds_sync();
+  sc.load_operand(zs + qi * RK, g);
+  wave_lds_sync();
+  return b;
+}
 
 // grid (row_blocks * n_chunks, B*H_q), block 64*waves.  Computes the query
 // sketch itself (z = B_q^T q on the f32 MFMA, rounded to bf16 for bf16 and
@@ -826,38 +914,11 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
   uint64_t* cand = cand_mem[wave];
   int* hist = reinterpret_cast<int*>(cand);
 
-  // ---- query sketch: D[m][qi] = sum_c B_q[c][m] q[qi][c], lane group g feeds c = 4s + g
-  float my_b;
+  // ---- query sketch
   Scorer sc;
-  {
-    const float* qr = q + (bh * Q + (row_ok ? my_row : row0)) * D;
-    const float* bq = Bq + (size_t)h * D * RK;
-    const float* mr = mu + (size_t)gkv * D;
-    f32x4_t za[RK / 16];
-#pragma unroll
-    for (int mb = 0; mb < RK / 16; ++mb) za[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    float bp = 0.f;
-    for (int s = 0; s < D / 4; ++s) {
-      const int c = 4 * s + g;
-      const float qv = row_ok ? qr[c] : 0.f;
-      bp = fmaf(qv, mr[c], bp);
-#pragma unroll
-      for (int mb = 0; mb < RK / 16; ++mb)
-        za[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(bq[c * RK + 16 * mb + qi], qv, za[mb], 0, 0, 0);
-    }
-    my_b = sum_lane_groups(bp);
-    float* zs = reinterpret_cast<float*>(cand);  // [16][RK]
-#pragma unroll
-    for (int mb = 0; mb < RK / 16; ++mb)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float zv = za[mb][v];
-        zs[qi * RK + 16 * mb + 4 * g + v] = ST != kStF32 ? bf16_round(zv) : zv;
-      }
-    wave_lds_sync();
-    sc.load_operand(zs + qi * RK, g);
-    wave_lds_sync();
-  }
+  const float my_b = mfma_query_sketch<RK, ST>(q + (bh * Q + (row_ok ? my_row : row0)) * D, row_ok,
+                                               Bq + (size_t)h * D * RK, mu + (size_t)gkv * D,
+                                               reinterpret_cast<float*>(cand), qi, g, sc);
   // the head's code set: one per query head (gq = 1) or per group of gq heads
   const size_t code_set = (bh / H_q) * (H_q / gq) + h / gq;
   const uint8_t* hbase = index + code_set * n_tiles * Scorer::TB;
@@ -1061,6 +1122,256 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
       }
     }
     wave_lds_sync();
+  }
+}
+
+// ---------------------------------------------------------------- sketch scoring, MFMA, one pass
+
+// Long rows (a batch of decode queries over a long cache) read each code once.
+// A wave scores its 16 query rows against one key chunk on the MFMA (the
+// layout of MfmaScorer, the mean term b folded into the accumulator) and
+// keeps a running top-64 per row: a sorted 64-entry list and a 64-slot
+// buffer of unsorted candidates, both in LDS.  A score is a candidate when it
+// beats the row's threshold; a buffer that would overflow is sorted and
+// merged into the list, which raises the threshold to the list's 64th score.
+// Tiles are visited in increasing key order and buffers are flushed only
+// between tiles, so a later key that merely ties the threshold ranks below
+// every list entry: the strict test loses nothing.
+//
+// The threshold starts at a gate read off a sample of the chunk (8 tiles
+// spread over it): the least, over the row's four lanes, of each lane's best
+// (several chunks) or second-best (one chunk) sampled score.  The gate only
+// bounds which keys are kept: a row whose list ends with 64 entries above it
+// holds the exact top-64 of the chunk.  A row that kept fewer (the gate was
+// above its 64th score) still holds every key of the chunk above the gate.
+// With one chunk per row the wave scans such rows again without a gate.
+// With several, it records the gate in `gates` (-inf for rows that need
+// none) and merge_kernel checks that the row's merged k-th score lies above
+// every recorded gate, which makes the merged list exact; rows that fail the
+// check are flagged, and a second launch of this kernel with `only` = the
+// flags rescans the whole key range of just those rows (its waves without a
+// flagged row exit at once).  A chunk's gate sits near its 100th-best key
+// while the merged k-th score sits near each chunk's (64 / chunks)-th best,
+// so the check passes unless the scores are placed adversarially; with one
+// chunk the rescan costs the wave a second pass, hence the lower gate.
+//
+// grid: 8 * ceil(ceil(units / kScanWaves) / 8) work-groups (XCD-ordered, as
+// for xcd_logical_block), units = n_bh * wave_rows * n_chunks, one unit
+// (head, 16-row block, chunk) per wave, chunks fastest.
+using saki::kScanWaves;
+constexpr int kScanBuf = 64;            // candidate slots per row
+constexpr int kScanSample = 8;          // sampled tiles per chunk
+constexpr int kScanGateKeys = 16 * kTile;  // rows with fewer keys in the chunk start ungated
+
+template <int RK, int ST>
+__global__ __launch_bounds__(kScanWaves * kWave) void score_scan_kernel(
+    const uint8_t* __restrict__ index, int n_tiles, int N_valid, int Q,
+    const int* __restrict__ q_pos, const float* __restrict__ q, const float* __restrict__ Bq,
+    const float* __restrict__ mu, int H_q, int H_kv, int gq, int n_bh, int wave_rows, int chunk,
+    int n_chunks, int k, int* __restrict__ top_idx, float* __restrict__ top_score,
+    uint64_t* __restrict__ part, float* __restrict__ gates, const int* __restrict__ only) {
+  constexpr int D = saki::kHeadDim;
+  using KO = KeysF32;
+  using K = KO::K;
+  using Scorer = MfmaScorer<RK, ST>;
+  __shared__ K list_mem[kScanWaves][kMR * kList];
+  __shared__ K buf_mem[kScanWaves][kMR * kScanBuf];  // first the sketch staging [16][RK] floats
+  static_assert(kMR * RK * sizeof(float) <= kMR * kScanBuf * sizeof(K), "sketch staging fits");
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = lane_id();
+  const long long units = (long long)n_bh * wave_rows * n_chunks;
+  const long long lb = xcd_logical_block((units + kScanWaves - 1) / kScanWaves);
+  if (lb < 0) return;
+  const long long unit = lb * kScanWaves + wave;
+  if (unit >= units) return;
+  const int ch = (int)(unit % n_chunks);
+  const int wr = (int)((unit / n_chunks) % wave_rows);
+  const size_t bh = (size_t)(unit / ((long long)n_chunks * wave_rows));
+  const int h = (int)(bh % H_q);
+  const int qi = lane % 16, g = lane / 16;
+  const int row0 = wr * kMR;
+  const int my_row = row0 + qi;
+  const bool row_ok = my_row < Q;
+  // with `only`, the rows to redo (a wave with none has nothing to do)
+  const bool want = row_ok && (!only || only[bh * Q + my_row] != 0);
+  if (only && __ballot(want) == 0) return;
+  const int my_lim = row_limit(my_row, Q, N_valid, q_pos);
+  const int kmax = wave_max_i(my_lim);
+  const int kmin = wave_min_i(row_ok ? my_lim : INT_MAX);
+  const int kbeg = ch * chunk;
+  const int kend = min(kbeg + chunk, kmax);
+  K* list = list_mem[wave];
+  K* buf = buf_mem[wave];
+
+  const size_t code_set = (bh / H_q) * (H_q / gq) + h / gq;
+  const uint8_t* hbase = index + code_set * n_tiles * Scorer::TB;
+  // the gate's sample: every stride-th tile of the chunk, at most kScanSample;
+  // the first kSA of them are requested before the query sketch is formed
+  const int n_row = row_ok ? max(0, min(my_lim, kend) - kbeg) : 0;
+  const bool gated = !only && wave_max_i(n_row) >= kScanGateKeys;
+  const int stride = max(1, (kend - kbeg) / (kTile * kScanSample)) * kTile;
+  const int n_samp = gated ? min(kScanSample, (kend - kbeg + stride - 1) / stride) : 0;
+  constexpr int kSA = Scorer::NL == 1 ? 4 : Scorer::kPrefetch ? 2 : 1;
+  Scorer sc;
+  typename Scorer::Raw sraw[kSA];
+  auto sample_at = [&](int i) { return hbase + (size_t)((kbeg + i * stride) / kTile) * Scorer::TB; };
+#pragma unroll
+  for (int u = 0; u < kSA; ++u)
+    if (u < n_samp) sc.load(sample_at(u), qi, g, sraw[u]);
+
+  sc.init = mfma_query_sketch<RK, ST>(q + (bh * Q + (row_ok ? my_row : row0)) * D, row_ok,
+                                      Bq + (size_t)h * D * RK, mu + (size_t)(h / (H_q / H_kv)) * D,
+                                      reinterpret_cast<float*>(buf), qi, g, sc);
+#pragma unroll 1
+  for (int r = 0; r < kMR; ++r) list[r * kList + lane] = KO::pad();
+
+  // ---- the gate
+  float tau = -INFINITY;
+  if (gated) {
+    float m1 = -INFINITY, m2 = -INFINITY;
+    for (int i0 = 0; i0 < n_samp; i0 += kSA) {
+#pragma unroll
+      for (int u = 0; u < kSA; ++u) {
+        const int i = i0 + u;
+        if (i >= n_samp) break;
+        f32x4_t acc[4];
+        sc.mma(sraw[u], acc);
+        if (i + kSA < n_samp) sc.load(sample_at(i + kSA), qi, g, sraw[u]);
+        const int t0 = kbeg + i * stride;
+#pragma unroll
+        for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const float x = t0 + 16 * sub + 4 * g + v < my_lim ? acc[sub][v] : -INFINITY;
+            m2 = fmaxf(m2, fminf(m1, x));
+            m1 = fmaxf(m1, x);
+          }
+      }
+    }
+    // several chunks: the least of the four lanes' best sampled scores (at
+    // least 4 sampled keys reach it; a chunk that keeps fewer than 64 keys
+    // costs only the merged check); one chunk: of their second best (8 keys)
+    float m = n_chunks > 1 ? m1 : m2;
+    m = fminf(m, xor_shfl_f32(m, 16));
+    m = fminf(m, xor_shfl_f32(m, 32));
+    if (n_row >= kScanGateKeys) tau = m;
+  }
+
+  // ---- the scan
+  float thr = want ? tau : INFINITY;  // row qi's threshold (the same in its four lanes)
+  int base = 0;                       // row qi's buffered candidates
+  auto flush = [&](int r) {
+    wave_lds_sync();
+    const int c = __builtin_amdgcn_readlane(base, r);  // lane r: row r, lane group 0
+    K b = lane < c ? buf[r * kScanBuf + lane] : KO::pad();
+    wave_sort<KO>(b);
+    K a = list[r * kList + lane];
+    wave_merge<KO>(a, b);
+    list[r * kList + lane] = a;
+    const float t = KO::score(KO::readlane(a, kWave - 1));
+    if (qi == r) {
+      thr = fmaxf(thr, t);
+      base = 0;
+    }
+    wave_lds_sync();
+  };
+  auto scan = [&]() {
+    sc.for_tiles_deep(hbase, kbeg, kend, qi, g, [&](int t0, f32x4_t* acc) {
+      uint32_t take = 0;
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) take |= (acc[sub][v] > thr ? 1u : 0u) << (4 * sub + v);
+      if (t0 + kTile > kmin) {  // a tile crossing some row's limit
+#pragma unroll
+        for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (t0 + 16 * sub + 4 * g + v >= my_lim) take &= ~(1u << (4 * sub + v));
+      }
+      if (__ballot(take != 0) == 0) return;
+      // the four lanes of a row append at offsets from a prefix of their counts
+      int c = __popc(take);
+      int c1 = (int)xor_shfl_u32((uint32_t)c, 16);   // lane group g ^ 1
+      int c2 = (int)xor_shfl_u32((uint32_t)c, 32);   // g ^ 2
+      int c3 = (int)xor_shfl_u32((uint32_t)c1, 32);  // g ^ 3
+      uint64_t full = __ballot(base + c + c1 + c2 + c3 > kScanBuf) & 0xffffull;
+      if (full) {
+        do {
+          flush(__builtin_ctzll(full));
+          full &= full - 1;
+        } while (full);
+#pragma unroll
+        for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (!(acc[sub][v] > thr)) take &= ~(1u << (4 * sub + v));
+        c = __popc(take);
+        c1 = (int)xor_shfl_u32((uint32_t)c, 16);
+        c2 = (int)xor_shfl_u32((uint32_t)c, 32);
+        c3 = (int)xor_shfl_u32((uint32_t)c1, 32);
+      }
+      int pos = base + (g == 1 ? c1 : g == 2 ? c2 + c3 : g == 3 ? c1 + c2 + c3 : 0);
+      base += c + c1 + c2 + c3;
+      // a lane rarely holds more than one or two candidates of a tile: take
+      // them one per round, lowest element first, each picked out of the 16
+      // scores by the bits of its element number
+      while (__ballot(take != 0)) {
+        const int e = __builtin_ctz(take | 0x10000u);
+        // bit masks of e's bits: (m & x) | (~m & y) picks x where the bit is set
+        const uint32_t m0 = 0u - (uint32_t)(e & 1), m1 = 0u - (uint32_t)((e >> 1) & 1);
+        const uint32_t m2 = 0u - (uint32_t)((e >> 2) & 1), m3 = 0u - (uint32_t)((e >> 3) & 1);
+        auto pick = [](uint32_t m, uint32_t x, uint32_t y) { return (m & x) | (~m & y); };
+        uint32_t s8[8], s4[4], s2[2];
+#pragma unroll
+        for (int m = 0; m < 8; ++m)
+          s8[m] = pick(m0, __float_as_uint(acc[m >> 1][(2 * m + 1) & 3]), __float_as_uint(acc[m >> 1][(2 * m) & 3]));
+#pragma unroll
+        for (int m = 0; m < 4; ++m) s4[m] = pick(m1, s8[2 * m + 1], s8[2 * m]);
+#pragma unroll
+        for (int m = 0; m < 2; ++m) s2[m] = pick(m2, s4[2 * m + 1], s4[2 * m]);
+        const float sv = __uint_as_float(pick(m3, s2[1], s2[0]));
+        if (take) {
+          buf[qi * kScanBuf + pos] = KO::make(sv, t0 + 16 * (e >> 2) + 4 * g + (e & 3));
+          ++pos;
+          take &= take - 1;
+        }
+      }
+    });
+    uint64_t left = __ballot(base > 0) & 0xffffull;
+    while (left) {
+      flush(__builtin_ctzll(left));
+      left &= left - 1;
+    }
+  };
+  scan();
+  // rows whose gate kept fewer than 64 keys of the chunk
+  wave_lds_sync();
+  const bool short_row = tau > -INFINITY && KO::index(list[qi * kList + kList - 1]) == kPadIdx;
+  if (n_chunks > 1) {
+    if (g == 0 && row_ok) gates[(bh * Q + my_row) * n_chunks + ch] = short_row ? tau : -INFINITY;
+  } else if (__ballot(short_row) != 0) {  // one chunk: again, ungated; the other rows are done
+    for (uint64_t m = __ballot(short_row) & 0xffffull; m; m &= m - 1)
+      list[__builtin_ctzll(m) * kList + lane] = KO::pad();
+    thr = short_row ? -INFINITY : INFINITY;
+    wave_lds_sync();
+    scan();
+    wave_lds_sync();
+  }
+
+  for (int r = 0; r < kMR; ++r) {
+    const int i = row0 + r;
+    if (i >= Q) break;
+    if (!__builtin_amdgcn_readlane((int)want, r)) continue;
+    const K e = list[r * kList + lane];
+    if (n_chunks == 1) {
+      if (lane < k) {
+        const size_t o = (bh * Q + i) * k + lane;
+        top_idx[o] = out_index<KO>(e);
+        if (top_score) top_score[o] = KO::score(e);
+      }
+    } else {
+      part[((bh * Q + i) * n_chunks + ch) * kMaxK + lane] = e;
+    }
   }
 }
 
@@ -2192,7 +2503,8 @@ template <class KO, bool RECALL>
 __global__ __launch_bounds__(kMergeWaves * kWave) void merge_kernel(
     const typename KO::K* __restrict__ part, size_t rows, int n_chunks, int k,
     int* __restrict__ out_idx, float* __restrict__ out_score,
-    const int* __restrict__ approx, int* __restrict__ hits) {
+    const int* __restrict__ approx, int* __restrict__ hits,
+    const float* __restrict__ gates = nullptr, int* __restrict__ redo = nullptr) {
   using K = typename KO::K;
   __shared__ K lists[kMergeWaves][kWave];
   const int wave = threadIdx.x / kWave, lane = lane_id();
@@ -2238,6 +2550,15 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void merge_kernel(
     if (lane < k) {
       out_idx[row * k + lane] = j;
       if (out_score) out_score[row * k + lane] = (float)KO::score(a);
+    }
+    if (gates) {  // score_scan_kernel's chunks that kept only the keys above a gate
+      float gmax = -INFINITY;
+      for (int c = lane; c < n_chunks; c += kWave) gmax = fmaxf(gmax, gates[row * n_chunks + c]);
+      gmax = wave_max_f32(gmax);
+      // exact when every recorded gate lies below the k-th score: keys a gate
+      // left out score at most the gate
+      const float sk = (float)KO::score(KO::readlane(a, k - 1));
+      if (lane == 0) redo[row] = (gmax == -INFINITY || sk > gmax) ? 0 : 1;
     }
   }
 }
@@ -2583,13 +2904,20 @@ int resident_groups(K kernel, int threads) {
 
 // A split-N streaming launch that fills the GPU exactly once: the plan's
 // chunking (which sized the workspace) is coarsened so that the work-groups
-// number at most what the device holds at one time, the chunk count staying
-// within the plan's.  A work-group takes `chunks_per_group` chunks.
+// number at most what the device holds at one time (or, given
+// max_waves_per_simd, at most that many waves per SIMD), the chunk count
+// staying within the plan's.  A work-group takes `chunks_per_group` chunks.
 template <class K>
 saki::Plan one_round(saki::Plan p, K kernel, int groups_per_chunk, int chunks_per_group,
-                     int N_valid) {
+                     int N_valid, int max_waves_per_simd = 0) {
   if (p.n_chunks <= 1) return p;
-  const int slots = resident_groups(kernel, kWave * p.waves);
+  int slots = resident_groups(kernel, kWave * p.waves);
+  if (max_waves_per_simd > 0 && slots > 0) {  // at most this many waves on each of a CU's 4 SIMDs
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
+      slots = min(slots, cus * 4 * max_waves_per_simd / p.waves);
+  }
   if (slots <= 0) return p;
   const int want = max(1, slots / max(1, groups_per_chunk)) * chunks_per_group;
   const size_t n = N_valid > 0 ? (size_t)N_valid : 1;
@@ -2608,6 +2936,36 @@ void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int index_head
                   const saki::Plan& p0, hipStream_t s) {
   const int gq = H_q / index_heads;
   saki::Plan p = p0;
+  if (p.scan) {
+    const long long wr = p0.row_blocks, per_chunk = wr * B * H_q;
+    // two waves per SIMD: VALU-heavy waves of equal work, none waiting on a third
+    p = one_round(p0, score_scan_kernel<RK, ST>, (int)((per_chunk + kScanWaves - 1) / kScanWaves), 1,
+                  N_valid, 2);
+    const int nt = (int)saki::n_tiles(N_cap);
+    auto launch = [&](int chunk, int n_chunks, uint64_t* part, float* gates, const int* only) {
+      const long long groups = (per_chunk * n_chunks + kScanWaves - 1) / kScanWaves;
+      hipLaunchKernelGGL((score_scan_kernel<RK, ST>), dim3((unsigned)(((groups + kXcds - 1) / kXcds) * kXcds)),
+                         dim3(kScanWaves * kWave), 0, s, index, nt, N_valid, Q, q_pos, q, Bq, mu, H_q,
+                         H_kv, gq, B * H_q, (int)wr, chunk, n_chunks, k, top_idx, top_score, part,
+                         gates, only);
+    };
+    if (p.n_chunks == 1) {
+      launch(p.chunk, 1, nullptr, nullptr, nullptr);
+      return;
+    }
+    // chunks, their merge with the gate check, then the flagged rows over all keys
+    uint64_t* part = reinterpret_cast<uint64_t*>(ws + p.part_off);
+    float* gates = reinterpret_cast<float*>(ws + p.z_off);
+    int* redo = reinterpret_cast<int*>(ws + p.flag_off);
+    launch(p.chunk, p.n_chunks, part, gates, nullptr);
+    const size_t rows = (size_t)B * H_q * Q;
+    // one wave per row: its loads of eight partial lists at a time are in
+    // flight together, and few chunks leave little to split further
+    hipLaunchKernelGGL((merge_kernel<KeysF32, false>), dim3((unsigned)rows), dim3(kWave), 0, s, part,
+                       rows, p.n_chunks, k, top_idx, top_score, nullptr, nullptr, gates, redo);
+    launch((int)saki::round_up((size_t)N_valid, kTile), 1, nullptr, nullptr, redo);
+    return;
+  }
   const int cpg = p0.split ? p0.waves : 1;  // chunks per work-group
   if (!p.mfma)
     p = p.rows == 4 ? one_round(p0, score_stream_kernel<RK, ST, 4>, p0.row_blocks * B * index_heads, cpg, N_valid)
@@ -2790,6 +3148,9 @@ int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_k
   const saki::Plan p = saki::score_plan(B, H_q, index_heads, Q, N_valid);
   if (ws_bytes < p.ws_bytes) return SAKI_ERR_WORKSPACE;
   if ((size_t)p.row_blocks * p.n_chunks > 0x7fffffffu) return SAKI_ERR_UNSUPPORTED;
+  // the one-pass kernel's 1-D grid: one wave per (head, row block, chunk)
+  if (p.scan && (size_t)B * H_q * p.row_blocks * p.n_chunks * kWave >= 0xffffffffu)
+    return SAKI_ERR_UNSUPPORTED;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const uint8_t* ix = reinterpret_cast<const uint8_t*>(index);
   uint8_t* w = reinterpret_cast<uint8_t*>(ws);

@@ -165,12 +165,13 @@ def test_decode_split_chunks_and_merge():
 
 @pytest.mark.parametrize("sketch,Q,N", [("bf16", 96, 1500), ("f32", 3, 70_000),
                                         ("bf16", 1, 150_000), ("fp8", 1, 150_000),
-                                        ("fp8", 40, 3000)])
+                                        ("fp8", 40, 3000), ("bf16", 16, 20_000)])
 def test_gqa_shared_index_matches_oracle(sketch, Q, N):
     """A GQA-shared index: one code set per KV head, built from the
     SAKI_METHOD_SHARED factors, scored by all four query heads of its group
-    (the MFMA path for 96 queries per head; decode shapes take the grouped
-    streaming rows, with the key range split into chunks)."""
+    (the MFMA path for 96 queries per head, its one-pass kernel for 16
+    queries over 20,000 keys; decode shapes take the grouped streaming rows,
+    with the key range split into chunks)."""
     spec = W.SPECS["decode_1m"].with_(N=N, Q=Q, H_q=8, H_kv=2)
     inp = W.make_layer(spec)
     cal = S.saki_calibrate(inp["q_cal"], inp["k_cal"], 32, method="shared")
