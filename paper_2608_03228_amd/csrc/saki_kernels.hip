@@ -1139,21 +1139,22 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
 // every list entry: the strict test loses nothing.
 //
 // The threshold starts at a gate read off a sample of the chunk (8 tiles
-// spread over it): the least, over the row's four lanes, of each lane's best
-// (several chunks) or second-best (one chunk) sampled score.  The gate only
-// bounds which keys are kept: a row whose list ends with 64 entries above it
-// holds the exact top-64 of the chunk.  A row that kept fewer (the gate was
-// above its 64th score) still holds every key of the chunk above the gate.
-// With one chunk per row the wave scans such rows again without a gate.
-// With several, it records the gate in `gates` (-inf for rows that need
-// none) and merge_kernel checks that the row's merged k-th score lies above
-// every recorded gate, which makes the merged list exact; rows that fail the
-// check are flagged, and a second launch of this kernel with `only` = the
-// flags rescans the whole key range of just those rows (its waves without a
-// flagged row exit at once).  A chunk's gate sits near its 100th-best key
-// while the merged k-th score sits near each chunk's (64 / chunks)-th best,
-// so the check passes unless the scores are placed adversarially; with one
-// chunk the rescan costs the wave a second pass, hence the lower gate.
+// spread over it): the least, over the row's four lanes, of each lane's
+// second-best sampled score, so that at least 8 sampled keys reach it.  The
+// gate only bounds which keys are kept: a row whose list ends with 64
+// entries above it holds the exact top-64 of the chunk.  A row that kept
+// fewer (the gate was above its 64th score) still holds every key of the
+// chunk above the gate.  With one chunk per row the wave scans such rows
+// again without a gate.  With several, it records the gate in `gates` (-inf
+// for rows that need none) and merge_kernel checks that the row's merged
+// k-th score lies above every recorded gate, which makes the merged list
+// exact.  Rows that fail the check are flagged; a second launch of this
+// kernel with `only` = the flags rescans their chunks without a gate (its
+// waves without a flagged row exit at once) and a second merge of just those
+// rows follows.  A chunk's gate sits near its 200th-best key while the
+// merged k-th score sits near each chunk's (64 / chunks)-th best, so rows
+// fail only when several of their best keys fall in one chunk's sample (the
+// queries of a sequence can share a few dominant keys).
 //
 // grid: 8 * ceil(ceil(units / kScanWaves) / 8) work-groups (XCD-ordered, as
 // for xcd_logical_block), units = n_bh * wave_rows * n_chunks, one unit
@@ -1247,10 +1248,9 @@ __global__ __launch_bounds__(kScanWaves * kWave) void score_scan_kernel(
           }
       }
     }
-    // several chunks: the least of the four lanes' best sampled scores (at
-    // least 4 sampled keys reach it; a chunk that keeps fewer than 64 keys
-    // costs only the merged check); one chunk: of their second best (8 keys)
-    float m = n_chunks > 1 ? m1 : m2;
+    // the least of the four lanes' second-best sampled scores: at least 8
+    // sampled keys reach it
+    float m = m2;
     m = fminf(m, xor_shfl_f32(m, 16));
     m = fminf(m, xor_shfl_f32(m, 32));
     if (n_row >= kScanGateKeys) tau = m;
@@ -1348,7 +1348,7 @@ __global__ __launch_bounds__(kScanWaves * kWave) void score_scan_kernel(
   wave_lds_sync();
   const bool short_row = tau > -INFINITY && KO::index(list[qi * kList + kList - 1]) == kPadIdx;
   if (n_chunks > 1) {
-    if (g == 0 && row_ok) gates[(bh * Q + my_row) * n_chunks + ch] = short_row ? tau : -INFINITY;
+    if (g == 0 && want) gates[(bh * Q + my_row) * n_chunks + ch] = short_row ? tau : -INFINITY;
   } else if (__ballot(short_row) != 0) {  // one chunk: again, ungated; the other rows are done
     for (uint64_t m = __ballot(short_row) & 0xffffull; m; m &= m - 1)
       list[__builtin_ctzll(m) * kList + lane] = KO::pad();
@@ -2497,6 +2497,9 @@ __global__ __launch_bounds__(kGateWaves * kWave) __attribute__((amdgpu_waves_per
 // grid (rows), block 64 * waves (waves <= kMergeWaves): the waves of a row's
 // work-group merge interleaved subsets of its sorted partial lists, then wave
 // 0 merges their lists.  RECALL: the row is an exact list -> exact_idx and hits.
+// gates / redo: the gate check of score_scan_kernel's chunks (a row whose
+// k-th score does not lie above every recorded gate gets redo = 1, else 0);
+// only: merge just the rows flagged there.
 constexpr int kMergeWaves = 8;
 
 template <class KO, bool RECALL>
@@ -2504,13 +2507,15 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void merge_kernel(
     const typename KO::K* __restrict__ part, size_t rows, int n_chunks, int k,
     int* __restrict__ out_idx, float* __restrict__ out_score,
     const int* __restrict__ approx, int* __restrict__ hits,
-    const float* __restrict__ gates = nullptr, int* __restrict__ redo = nullptr) {
+    const float* __restrict__ gates = nullptr, int* __restrict__ redo = nullptr,
+    const int* __restrict__ only = nullptr) {
   using K = typename KO::K;
   __shared__ K lists[kMergeWaves][kWave];
   const int wave = threadIdx.x / kWave, lane = lane_id();
   const int waves = blockDim.x / kWave;
   const size_t row = blockIdx.x;
   if (row >= rows) return;
+  if (only && only[row] == 0) return;  // the rows a rescan redid, nothing else
   // wave w merges partials w, w + waves, ..., eight at a time; the next
   // eight are loaded before the current ones are merged
   constexpr int kLoads = 8;
@@ -2963,7 +2968,11 @@ void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int index_head
     // flight together, and few chunks leave little to split further
     hipLaunchKernelGGL((merge_kernel<KeysF32, false>), dim3((unsigned)rows), dim3(kWave), 0, s, part,
                        rows, p.n_chunks, k, top_idx, top_score, nullptr, nullptr, gates, redo);
-    launch((int)saki::round_up((size_t)N_valid, kTile), 1, nullptr, nullptr, redo);
+    // the flagged rows' chunks again without a gate, and their merge
+    launch(p.chunk, p.n_chunks, part, gates, redo);
+    hipLaunchKernelGGL((merge_kernel<KeysF32, false>), dim3((unsigned)rows), dim3(kWave), 0, s, part,
+                       rows, p.n_chunks, k, top_idx, top_score, nullptr, nullptr, nullptr, nullptr,
+                       redo);
     return;
   }
   const int cpg = p0.split ? p0.waves : 1;  // chunks per work-group

@@ -47,28 +47,38 @@ def test_scan_positions_n_valid_and_small_k():
         check_head(inp, out, 0, h, 32, "bf16_emul", k=10, N_valid=N_valid)
 
 
-def _spiked(inp, rows_spikes):
-    """Replace keys by spikes: for each (row, positions) pair, keys at those
-    positions become mu + a u with u = M^T q_row (M = B_q B_k^T of head 0), a
-    chosen so that they score about ten times the largest ordinary score for
-    that row, each a little apart.  Returns the new inputs after checking on
-    the oracle that each spike outscores every ordinary key for its row."""
+def _planted(inp, plants):
+    """Replace keys: for each (row, positions, scores) triple, the keys at
+    those positions become mu + a u with u = M^T q_row (M = B_q B_k^T of head
+    0), a chosen so that each scores the given value for that row (on the
+    oracle's float64 scores).  Returns the new inputs and head 0's scores."""
     keys = inp["keys"].copy()
     Bq, Bk, mu = oracle_factors(inp, 0, 32)
     M = Bq @ Bk.T
     q = inp["queries"][0, 0].astype(np.float64)
-    s0, *_ = O.index_scores(Bq, Bk, mu, q, keys[0, 0])
-    big = 10.0 * np.abs(s0).max()
-    for i, pos in rows_spikes:
+    for i, pos, score in plants:
         u = M.T @ q[i]
-        for m, j in enumerate(pos):
-            keys[0, 0, j] = (mu + big * (1.0 + 0.01 * m) / np.linalg.norm(u) ** 2 * u).astype(np.float32)
+        for j, sc in zip(pos, score):
+            a = (sc - q[i] @ mu) / (u @ u)
+            keys[0, 0, j] = (mu + a * u).astype(np.float32)
     s1, *_ = O.index_scores(Bq, Bk, mu, q, keys[0, 0])
+    return dict(inp, keys=keys), s1
+
+
+def _spiked(inp, rows_spikes):
+    """Spikes: keys that score about ten times the largest ordinary score for
+    their row, each a little apart; checks on the oracle that each outscores
+    every ordinary key for its row."""
+    Bq, Bk, mu = oracle_factors(inp, 0, 32)
+    s0, *_ = O.index_scores(Bq, Bk, mu, inp["queries"][0, 0], inp["keys"][0, 0])
+    big = 10.0 * np.abs(s0).max()
+    out, s1 = _planted(inp, [(i, pos, big * (1.0 + 0.01 * np.arange(len(pos))))
+                             for i, pos in rows_spikes])
     every = np.concatenate([p for _, p in rows_spikes])
-    plain = np.setdiff1d(np.arange(keys.shape[2]), every)
+    plain = np.setdiff1d(np.arange(s1.shape[1]), every)
     for i, pos in rows_spikes:
         assert s1[i, pos].min() > s1[i, plain].max()
-    return dict(inp, keys=keys)
+    return out
 
 
 def _sampled(chunk0, tile, g, v):
@@ -77,14 +87,35 @@ def _sampled(chunk0, tile, g, v):
     return chunk0 + 256 * tile + 4 * g + v
 
 
-def test_scan_chunk_gates_above_their_64th_score():
-    """Keys placed so that the sampled tiles of two chunks hold, for rows
-    0..3, eight keys that score far above every other key: the gate read off
-    the sample then keeps fewer than 64 keys of the chunk for those rows.  The
-    other chunks hold plenty of keys above it, so the merged lists pass the
-    check and are exact.  (16 rows of one head over 16,384 keys are cut into
-    chunks of 2,048 keys, sampled every 256 keys; lane group g of a row
-    samples keys 4g .. 4g + 3 of each 16 of a tile.)"""
+def test_scan_short_chunks_pass_the_merged_check():
+    """Row 0's sampled keys in the first tile of chunks 0 and 5 are replaced
+    by keys that score near its 90th-best score, two per lane group: the gate
+    of those chunks sits there, so they keep fewer than 64 keys, while more
+    than 64 keys of the row lie above it and the merged list passes the
+    check.  (16 rows of one head over 16,384 keys are cut into chunks of
+    2,048 keys, sampled every 256 keys; lane group g of a row samples keys
+    4g .. 4g + 3 of each 16 of a tile.)"""
+    spec = W.SPECS["qwen25_7b_decode"].with_(N=16_384, Q=16, H_q=2, H_kv=1, batch=1)
+    inp = W.make_layer(spec)
+    Bq, Bk, mu = oracle_factors(inp, 0, 32)
+    s0, *_ = O.index_scores(Bq, Bk, mu, inp["queries"][0, 0], inp["keys"][0, 0])
+    top = np.sort(s0[0])[::-1]
+    pos = np.array([_sampled(2048 * c, 0, g, v) for c in (0, 5) for g in range(4) for v in range(2)])
+    inp, s1 = _planted(inp, [(0, pos, np.linspace(top[95], top[85], len(pos)))])
+    for c in (0, 5):
+        assert np.sum(s1[0, 2048 * c:2048 * (c + 1)] > s1[0, pos].min()) < 64
+    assert np.sum(s1[0] > s1[0, pos].max()) >= 64
+    for sketch in ("f32", "bf16"):
+        out = gpu_pipeline(inp, 32, sketch)
+        for h in range(2):
+            check_head(inp, out, 0, h, 32, MODE[sketch])
+
+
+def test_scan_spikes_in_two_chunks_are_rescanned():
+    """Rows 0..3 get eight keys each, in the sampled tiles of chunks 0 and 5,
+    that score far above every other key: those chunks' gates sit on them, no
+    other key lies above, and the rows fail the merged check, so their chunks
+    are scanned again without a gate."""
     spec = W.SPECS["qwen25_7b_decode"].with_(N=16_384, Q=16, H_q=2, H_kv=1, batch=1)
     inp = W.make_layer(spec)
     spikes = [(i, np.array([_sampled(2048 * c, i, g, v) for c in (0, 5) for g in range(4)
@@ -100,7 +131,7 @@ def test_scan_rows_failing_the_merged_check_are_rescanned():
     """Row 0's 64 best keys are spikes, eight in the sampled tiles of every
     chunk: each chunk keeps only its spikes above its gate, and the merged
     64th score (the lowest spike) does not lie above every chunk's gate, so
-    the row is flagged and rescanned over all keys without a gate."""
+    the row is flagged and its chunks are scanned again without a gate."""
     spec = W.SPECS["qwen25_7b_decode"].with_(N=16_384, Q=16, H_q=2, H_kv=1, batch=1)
     inp = W.make_layer(spec)
     pos = np.array([_sampled(2048 * c, c % 8, g, v) for c in range(8) for g in range(4)
