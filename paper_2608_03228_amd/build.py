@@ -22,6 +22,10 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 # Packed FP32 instructions are disabled for all device code.
 NO_PACKED_FP32 = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# MFMA results are written to the architectural VGPRs rather than the
+# accumulation registers, which saves a copy of every result the kernels
+# inspect (the selection passes read each score).
+MFMA_VGPR = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 
 
 def _run(cmd, verbose):
@@ -38,7 +42,7 @@ def build(verbose: bool = True) -> str:
     _run(["g++", "-O3", "-std=c++17", "-fPIC", "-march=x86-64-v3", "-pthread",
           "-Wall", "-Wextra", "-I", INCLUDE, "-I", CSRC, "-c",
           os.path.join(CSRC, "saki_host.cpp"), "-o", host_o], verbose)
-    _run([HIPCC, "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", *NO_PACKED_FP32,
+    _run([HIPCC, "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", *NO_PACKED_FP32, *MFMA_VGPR,
           "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, "saki_kernels.hip"),
           "-o", dev_o], verbose)
     tmp = LIB + ".tmp"
