@@ -680,60 +680,71 @@ bool sym_eig_rows(int n, const double* A, double* w, double* vt) {
   return true;
 }
 
-// LU factorisation with partial pivoting of T - lambda I for the symmetric
-// tridiagonal T (diag, off); pivots smaller than `tiny` are replaced by
-// +-tiny, as inverse iteration requires, and stored as reciprocals.
-struct ShiftedTridiagLU {
-  std::vector<double> rdg, du, du2, dl;
-  std::vector<unsigned char> swap;
-  explicit ShiftedTridiagLU(int n) : rdg(n), du(n), du2(n), dl(n), swap(n) {}
+// LU factorisation with partial pivoting of T - lambda_l I for four shifts
+// at once, one per AVX2 lane, for the symmetric tridiagonal T (diag, off).
+// Each lane takes the steps of the one-shift factorisation, its row exchange
+// chosen by a blend; pivots smaller than `tiny` are replaced by +-tiny, as
+// inverse iteration requires, and stored as reciprocals.
+struct ShiftedTridiagLU4 {
+  // row i of each array: its four lanes at [4i, 4i + 4)
+  std::vector<double> rdg, du, du2, dl, sw;
+  explicit ShiftedTridiagLU4(int n) : rdg(4 * n), du(4 * n), du2(4 * n), dl(4 * n), sw(4 * n) {}
+  static __m256d ld(const std::vector<double>& v, int i) { return _mm256_loadu_pd(v.data() + 4 * i); }
+  static void st(std::vector<double>& v, int i, __m256d x) { _mm256_storeu_pd(v.data() + 4 * i, x); }
 
-  void factor(int n, const double* diag, const double* off, double lambda, double tiny) {
-    double* dg = rdg.data();
-    for (int i = 0; i < n; ++i) dg[i] = diag[i] - lambda;
-    for (int i = 0; i + 1 < n; ++i) { du[i] = off[i]; dl[i] = off[i]; }
+  void factor(int n, const double* diag, const double* off, const double* lambda, double tiny) {
+    const __m256d lam = _mm256_loadu_pd(lambda), vtiny = _mm256_set1_pd(tiny);
+    const __m256d absmask = _mm256_castsi256_pd(_mm256_set1_epi64x(0x7fffffffffffffffll));
+    const __m256d zero = _mm256_setzero_pd();
+    std::vector<double>& dg = rdg;
+    for (int i = 0; i < n; ++i) st(dg, i, _mm256_sub_pd(_mm256_set1_pd(diag[i]), lam));
+    for (int i = 0; i + 1 < n; ++i) st(du, i, _mm256_set1_pd(off[i]));
+    st(du, n - 1, zero);
+    st(du2, n - 1, zero);
+    st(dl, n - 1, zero);
+    st(sw, n - 1, zero);
     for (int i = 0; i + 1 < n; ++i) {
-      du2[i] = 0.0;
-      if (std::fabs(dg[i]) >= std::fabs(dl[i])) {
-        swap[i] = 0;
-        const double piv = dg[i] != 0.0 ? dg[i] : tiny;
-        const double f = dl[i] / piv;
-        dl[i] = f;
-        dg[i + 1] -= f * du[i];
-      } else {  // rows i and i+1 change places
-        swap[i] = 1;
-        const double f = dg[i] / dl[i];
-        dg[i] = dl[i];
-        dl[i] = f;
-        const double t = du[i];
-        du[i] = dg[i + 1];
-        dg[i + 1] = t - f * dg[i + 1];
-        if (i + 2 < n) {
-          du2[i] = du[i + 1];
-          du[i + 1] = -f * du[i + 1];
-        }
+      const __m256d a = ld(dg, i), o = _mm256_set1_pd(off[i]), d1 = ld(dg, i + 1), t = ld(du, i);
+      // exchange rows i and i+1 where |dg_i| < |off_i|
+      const __m256d s = _mm256_cmp_pd(_mm256_and_pd(a, absmask), _mm256_and_pd(o, absmask), _CMP_LT_OQ);
+      const __m256d piv = _mm256_blendv_pd(a, vtiny, _mm256_cmp_pd(a, zero, _CMP_EQ_OQ));
+      const __m256d f = _mm256_div_pd(_mm256_blendv_pd(o, a, s), _mm256_blendv_pd(piv, o, s));
+      st(dl, i, f);
+      st(dg, i, _mm256_blendv_pd(a, o, s));
+      st(du, i, _mm256_blendv_pd(t, d1, s));
+      st(dg, i + 1, _mm256_blendv_pd(_mm256_fnmadd_pd(f, t, d1), _mm256_fnmadd_pd(f, d1, t), s));
+      if (i + 2 < n) {
+        const __m256d u1 = ld(du, i + 1);
+        st(du2, i, _mm256_and_pd(s, u1));
+        st(du, i + 1, _mm256_blendv_pd(u1, _mm256_sub_pd(zero, _mm256_mul_pd(f, u1)), s));
+      } else {
+        st(du2, i, zero);
       }
+      st(sw, i, s);
     }
+    const __m256d one = _mm256_set1_pd(1.0);
     for (int i = 0; i < n; ++i) {
-      if (std::fabs(dg[i]) < tiny) dg[i] = dg[i] < 0.0 ? -tiny : tiny;
-      dg[i] = 1.0 / dg[i];
+      const __m256d x = ld(dg, i);
+      const __m256d small = _mm256_cmp_pd(_mm256_and_pd(x, absmask), vtiny, _CMP_LT_OQ);
+      const __m256d tt = _mm256_blendv_pd(vtiny, _mm256_sub_pd(zero, vtiny), _mm256_cmp_pd(x, zero, _CMP_LT_OQ));
+      st(dg, i, _mm256_div_pd(one, _mm256_blendv_pd(x, tt, small)));
     }
   }
 
-  // b <- (T - lambda I)^{-1} b
+  // b <- (T - lambda_l I)^{-1} b in each lane (b[4i + l]: lane l's element i)
   void solve(int n, double* b) const {
+    auto bl = [&](int i) { return _mm256_loadu_pd(b + 4 * i); };
+    auto bs = [&](int i, __m256d x) { _mm256_storeu_pd(b + 4 * i, x); };
     for (int i = 0; i + 1 < n; ++i) {  // L y = P b
-      if (swap[i]) {
-        const double t = b[i] - dl[i] * b[i + 1];
-        b[i] = b[i + 1];
-        b[i + 1] = t;
-      } else {
-        b[i + 1] -= dl[i] * b[i];
-      }
+      const __m256d bi = bl(i), bi1 = bl(i + 1), s = ld(sw, i), l = ld(dl, i);
+      bs(i, _mm256_blendv_pd(bi, bi1, s));
+      bs(i + 1, _mm256_blendv_pd(_mm256_fnmadd_pd(l, bi, bi1), _mm256_fnmadd_pd(l, bi1, bi), s));
     }
-    b[n - 1] *= rdg[n - 1];  // U x = y
-    if (n > 1) b[n - 2] = (b[n - 2] - du[n - 2] * b[n - 1]) * rdg[n - 2];
-    for (int i = n - 3; i >= 0; --i) b[i] = (b[i] - du[i] * b[i + 1] - du2[i] * b[i + 2]) * rdg[i];
+    bs(n - 1, _mm256_mul_pd(bl(n - 1), ld(rdg, n - 1)));  // U x = y
+    if (n > 1) bs(n - 2, _mm256_mul_pd(_mm256_fnmadd_pd(ld(du, n - 2), bl(n - 1), bl(n - 2)), ld(rdg, n - 2)));
+    for (int i = n - 3; i >= 0; --i)
+      bs(i, _mm256_mul_pd(_mm256_fnmadd_pd(ld(du2, i), bl(i + 2), _mm256_fnmadd_pd(ld(du, i), bl(i + 1), bl(i))),
+                          ld(rdg, i)));
   }
 };
 
@@ -894,46 +905,94 @@ bool top_eigpairs(int n, const double* diag, const double* off, const double* hv
   const double cluster_gap = 1e-3 * tnorm;  // re-orthogonalise closer eigenvalues
   const double tiny = eps * tnorm;
   const double converged = std::sqrt(0.1 / n);
-  std::vector<double> x(n);
-  ShiftedTridiagLU lu(n);
-  int cluster_begin = 0;
-  double shift_prev = 0.0;
-  uint64_t seed = 0x9E3779B97F4A7C15ull;
-  for (int m = 0; m < r; ++m) {
-    double lambda = ev[m];
-    if (m > 0) {
-      if (shift_prev - lambda > cluster_gap) cluster_begin = m;
-      // equal eigenvalues get distinct shifts so the iterations separate them
-      const double sep = 10.0 * eps * std::max(std::fabs(shift_prev), tnorm * eps);
-      if (lambda > shift_prev - sep) lambda = shift_prev - sep;
-    }
-    shift_prev = lambda;
-    for (int i = 0; i < n; ++i) {  // fixed pseudo-random start in [-1, 1)
-      seed = seed * 6364136223846793005ull + 1442695040888963407ull;
-      x[i] = (double)(seed >> 11) * (2.0 / 9007199254740992.0) - 1.0;
-    }
-    lu.factor(n, diag, off, lambda, tiny);
-    int extra = 0;
-    bool done = false;
-    for (int it = 0; it < 6 && !done; ++it) {
-      double l1 = 0.0;
-      for (int i = 0; i < n; ++i) l1 += std::fabs(x[i]);
-      // start small: a converged solve then grows by about 1 / (eps n)
-      const double scale = n * tnorm * eps / l1;
-      for (int i = 0; i < n; ++i) x[i] *= scale;
-      lu.solve(n, x.data());
-      for (int p = cluster_begin; p < m; ++p) {  // against earlier vectors of the cluster
-        const double* vp = vecs + (size_t)p * n;  // still in the tridiagonal basis
-        axpy(-dot(vp, x.data(), n), vp, x.data(), n);
+  // shifts, clusters and start vectors of the r vectors, in order
+  std::vector<double> shift(r), start((size_t)r * n);
+  std::vector<int> cbeg(r);
+  {
+    int cluster_begin = 0;
+    double shift_prev = 0.0;
+    uint64_t seed = 0x9E3779B97F4A7C15ull;
+    for (int m = 0; m < r; ++m) {
+      double lambda = ev[m];
+      if (m > 0) {
+        if (shift_prev - lambda > cluster_gap) cluster_begin = m;
+        // equal eigenvalues get distinct shifts so the iterations separate them
+        const double sep = 10.0 * eps * std::max(std::fabs(shift_prev), tnorm * eps);
+        if (lambda > shift_prev - sep) lambda = shift_prev - sep;
       }
-      double amax = 0.0;
-      for (int i = 0; i < n; ++i) amax = std::max(amax, std::fabs(x[i]));
-      if (!std::isfinite(amax) || amax == 0.0) return false;
-      if (amax >= converged && ++extra >= 2) done = true;
+      shift_prev = lambda;
+      shift[m] = lambda;
+      cbeg[m] = cluster_begin;
+      for (int i = 0; i < n; ++i) {  // fixed pseudo-random start in [-1, 1)
+        seed = seed * 6364136223846793005ull + 1442695040888963407ull;
+        start[(size_t)m * n + i] = (double)(seed >> 11) * (2.0 / 9007199254740992.0) - 1.0;
+      }
     }
-    const double nrm = std::sqrt(dot(x.data(), x.data(), n));
-    double* vm = vecs + (size_t)m * n;
-    for (int i = 0; i < n; ++i) vm[i] = x[i] / nrm;
+  }
+  // four vectors at a time, one per lane of the factorisation and solve; a
+  // vector is re-orthogonalised after each solve against the finished
+  // vectors of its cluster and against the earlier lanes of its group (block
+  // Gram-Schmidt), and is kept once it has converged
+  ShiftedTridiagLU4 lu(n);
+  std::vector<double> xb((size_t)4 * n);
+  std::vector<double> x4((size_t)4 * n);  // lane l's vector at x4[l * n ...]
+  for (int m0 = 0; m0 < r; m0 += 4) {
+    const int nl = std::min(4, r - m0);
+    double lam[4];
+    for (int l = 0; l < 4; ++l) lam[l] = l < nl ? shift[m0 + l] : shift[m0] + (l + 1) * tnorm;  // idle lanes: any shift
+    lu.factor(n, diag, off, lam, tiny);
+    for (int l = 0; l < 4; ++l)
+      std::copy(start.begin() + (size_t)(m0 + std::min(l, nl - 1)) * n,
+                start.begin() + (size_t)(m0 + std::min(l, nl - 1) + 1) * n, x4.begin() + (size_t)l * n);
+    int extra[4] = {0, 0, 0, 0};
+    bool done[4];
+    for (int l = 0; l < 4; ++l) done[l] = l >= nl;
+    auto finish = [&](int l) {
+      const double* xl = x4.data() + (size_t)l * n;
+      const double nrm = std::sqrt(dot(xl, xl, n));
+      double* vm = vecs + (size_t)(m0 + l) * n;
+      for (int i = 0; i < n; ++i) vm[i] = xl[i] / nrm;
+    };
+    for (int it = 0; it < 6; ++it) {
+      if (done[0] && done[1] && done[2] && done[3]) break;
+      for (int l = 0; l < 4; ++l) {  // start small: a converged solve then grows by about 1 / (eps n)
+        double* xl = x4.data() + (size_t)l * n;
+        double l1 = 0.0;
+        for (int i = 0; i < n; ++i) l1 += std::fabs(xl[i]);
+        const double sc = l1 > 0.0 ? n * tnorm * eps / l1 : 1.0;
+        for (int i = 0; i < n; ++i) xl[i] *= sc;
+      }
+      for (int i = 0; i < n; ++i)
+        for (int l = 0; l < 4; ++l) xb[(size_t)4 * i + l] = x4[(size_t)l * n + i];
+      lu.solve(n, xb.data());
+      for (int l = 0; l < 4; ++l)
+        if (!done[l])
+          for (int i = 0; i < n; ++i) x4[(size_t)l * n + i] = xb[(size_t)4 * i + l];
+      for (int l = 0; l < nl; ++l) {
+        if (done[l]) continue;
+        double* xl = x4.data() + (size_t)l * n;
+        const int m = m0 + l;
+        for (int p = cbeg[m]; p < m; ++p) {
+          if (p < m0 || done[p - m0]) {  // a finished unit vector, still in the tridiagonal basis
+            const double* vp = vecs + (size_t)p * n;
+            axpy(-dot(vp, xl, n), vp, xl, n);
+          } else {  // an earlier lane of this group, not yet finished
+            const double* xp = x4.data() + (size_t)(p - m0) * n;
+            const double pp = dot(xp, xp, n);
+            if (pp > 0.0) axpy(-dot(xp, xl, n) / pp, xp, xl, n);
+          }
+        }
+        double amax = 0.0;
+        for (int i = 0; i < n; ++i) amax = std::max(amax, std::fabs(xl[i]));
+        if (!std::isfinite(amax) || amax == 0.0) return false;
+        if (amax >= converged && ++extra[l] >= 2) {
+          done[l] = true;
+          finish(l);
+        }
+      }
+    }
+    for (int l = 0; l < nl; ++l)
+      if (!done[l]) finish(l);
   }
   // back to the basis of A, all r vectors at once (n x r, then transposed)
   std::vector<double> X((size_t)n * r);
