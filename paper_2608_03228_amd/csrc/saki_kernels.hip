@@ -645,7 +645,8 @@ constexpr int kSCandRow = kSCollect + 1;
 enum RowMode : int { kModeAll = 0, kModeHist = 1, kModeFallback = 2 };
 
 // Scores of one 64-key tile for the wave's 16 queries: acc[sub][v] is query
-// (lane % 16) against key t0 + 16*sub + 4*(lane/16) + v (without the mean term).
+// (lane % 16) against key t0 + 16*sub + 4*(lane/16) + v, plus `init` (the
+// kernels set it to the row's mean term b).
 // bf16 and fp8 codes run on the bf16 MFMA (fp8 widened exactly to bf16 in
 // registers), float32 codes on the f32 MFMA.
 template <int RK, int ST>
@@ -916,9 +917,11 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
 
   // ---- query sketch
   Scorer sc;
+  // the scorer's accumulators start at b, so that scores come out whole
   const float my_b = mfma_query_sketch<RK, ST>(q + (bh * Q + (row_ok ? my_row : row0)) * D, row_ok,
                                                Bq + (size_t)h * D * RK, mu + (size_t)gkv * D,
                                                reinterpret_cast<float*>(cand), qi, g, sc);
+  sc.init = my_b;
   // the head's code set: one per query head (gq = 1) or per group of gq heads
   const size_t code_set = (bh / H_q) * (H_q / gq) + h / gq;
   const uint8_t* hbase = index + code_set * n_tiles * Scorer::TB;
@@ -935,7 +938,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const bool in = t0 + 16 * sub + 4 * g + v < my_lim;
-          const float x = in ? acc[sub][v] : 0.f;
+          const float x = in ? acc[sub][v] - my_b : 0.f;  // moments of z . c, not shifted by b
           sum += x;
           sumsq = fmaf(x, x, sumsq);
           cnt += in ? 1.f : 0.f;
@@ -981,7 +984,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
       for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const float x = fmaf(acc[sub][v] + my_b, inv_w, off);
+          const float x = fmaf(acc[sub][v], inv_w, off);
           int bin = (int)fminf(x, x_hi);
           bin = (hmode && x >= 1.f) ? bin : trash;
           if (need_mask && t0 + 16 * sub + 4 * g + v >= my_lim) bin = trash;
@@ -1029,7 +1032,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
       for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
         for (int v = 0; v < 4; ++v)
-          take |= (fmaf(acc[sub][v] + my_b, inv_w, off) >= gate) ? (1u << (4 * sub + v)) : 0u;
+          take |= (fmaf(acc[sub][v], inv_w, off) >= gate) ? (1u << (4 * sub + v)) : 0u;
       if (t0 + kTile > kmin) {  // a tile crossing some row's causal limit
 #pragma unroll
         for (int sub = 0; sub < 4; ++sub)
@@ -1052,7 +1055,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
         for (int v = 0; v < 4; ++v)
           if (take & (1u << (4 * sub + v))) {
             if (pos < kSCollect)
-              cand[qi * kSCandRow + pos] = KO::make(acc[sub][v] + my_b, t0 + 16 * sub + 4 * g + v);
+              cand[qi * kSCandRow + pos] = KO::make(acc[sub][v], t0 + 16 * sub + 4 * g + v);
             ++pos;
           }
     });
@@ -1092,7 +1095,7 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
     sc.for_tiles(hbase, kbeg, kend, kTile, qi, g, [&](int t0, f32x4_t* acc) {
 #pragma unroll
       for (int sub = 0; sub < 4; ++sub) {
-        const f32x4_t sv = acc[sub] + my_b;
+        const f32x4_t sv = acc[sub];
         *reinterpret_cast<f32x4_t*>(&stage[qi * kTile + ((16 * sub + 4 * g) ^ (qi << 2))]) = sv;
       }
       wave_lds_sync();
