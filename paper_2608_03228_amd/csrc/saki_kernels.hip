@@ -2498,12 +2498,14 @@ __global__ __launch_bounds__(kGateWaves * kWave) __attribute__((amdgpu_waves_per
 // ---------------------------------------------------------------- merge of partials
 
 // grid (rows), block 64 * waves (waves <= kMergeWaves): the waves of a row's
-// work-group merge interleaved subsets of its sorted partial lists, then wave
-// 0 merges their lists.  RECALL: the row is an exact list -> exact_idx and hits.
+// work-group merge interleaved subsets of its sorted partial lists, then
+// their lists are merged pairwise in a tree (wave w takes wave w + s's list at
+// stride s = 1, 2, 4, ...).  RECALL: the row is an exact list -> exact_idx and
+// hits.
 // gates / redo: the gate check of score_scan_kernel's chunks (a row whose
 // k-th score does not lie above every recorded gate gets redo = 1, else 0);
 // only: merge just the rows flagged there.
-constexpr int kMergeWaves = 8;
+constexpr int kMergeWaves = 16;
 
 template <class KO, bool RECALL>
 __global__ __launch_bounds__(kMergeWaves * kWave) void merge_kernel(
@@ -2544,11 +2546,17 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void merge_kernel(
   }
   lists[wave][lane] = a;
   __syncthreads();
-  if (wave != 0) return;
-  for (int w = 1; w < waves; ++w) {
-    const K b = lists[w][lane];
-    if (KO::gt(KO::readlane(b, 0), KO::readlane(a, kWave - 1))) wave_merge<KO>(a, b);
+  for (int st = 1; st < waves; st *= 2) {  // uniform trip count: every wave reaches each barrier
+    const bool active = wave % (2 * st) == 0 && wave + st < waves;
+    if (active) {
+      const K b = lists[wave + st][lane];
+      if (KO::gt(KO::readlane(b, 0), KO::readlane(a, kWave - 1))) wave_merge<KO>(a, b);
+    }
+    __syncthreads();
+    if (active) lists[wave][lane] = a;
+    __syncthreads();
   }
+  if (wave != 0) return;
   const int j = out_index<KO>(a);
   if constexpr (RECALL) {
     if (out_idx && lane < k) out_idx[row * k + lane] = j;
