@@ -860,7 +860,8 @@ bool tridiag_of(int n, const double* A, double* diag, double* off, double* hv, d
 // (diag, off) and reflectors (hv, beta) tridiag_of produced: w receives the
 // r largest eigenvalues in descending order (all n with all_values), row m
 // of `vecs` (r x n) the unit eigenvector of w[m].  Eigenvalues by QL without
-// vectors (all_values) or by bisection (only the r largest), then inverse
+// vectors (all_values) or by multisection on Sturm counts (only the r
+// largest), then inverse
 // iteration on the tridiagonal for the r vectors (Golub & Van Loan, Sec.
 // 8.2.2 and 8.4), re-orthogonalised within clusters of close eigenvalues,
 // and back-transformation by the reflectors.  With the reduction this costs
@@ -873,7 +874,7 @@ bool top_eigpairs(int n, const double* diag, const double* off, const double* hv
     std::copy(diag, diag + n, ev.begin());
     if (!tridiag_ql(n, ev.data(), eo.data(), nullptr)) return false;
     std::sort(ev.begin(), ev.end(), [](double x, double y) { return x > y; });
-  } else {  // only the r largest, by bisection
+  } else {  // only the r largest, by multisection
     std::vector<double> off2(n, 0.0);
     double glo = diag[0], ghi = diag[0], emax = 0.0;
     for (int i = 0; i < n; ++i) {
