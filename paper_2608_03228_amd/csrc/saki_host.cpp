@@ -861,10 +861,10 @@ bool tridiag_of(int n, const double* A, double* diag, double* off, double* hv, d
 // r largest eigenvalues in descending order (all n with all_values), row m
 // of `vecs` (r x n) the unit eigenvector of w[m].  Eigenvalues by QL without
 // vectors (all_values) or by multisection on Sturm counts (only the r
-// largest), then inverse
-// iteration on the tridiagonal for the r vectors (Golub & Van Loan, Sec.
-// 8.2.2 and 8.4), re-orthogonalised within clusters of close eigenvalues,
-// and back-transformation by the reflectors.  With the reduction this costs
+// largest), then inverse iteration on the tridiagonal for the r vectors
+// (Golub & Van Loan, Sec. 8.2.2 and 8.4), four shifts at a time,
+// re-orthogonalised within clusters of close eigenvalues, and
+// back-transformation by the reflectors.  With the reduction this costs
 // 2n^3 + O(n^2 r) flops instead of the roughly 9n^3 of the full solver.
 bool top_eigpairs(int n, const double* diag, const double* off, const double* hv,
                   const double* beta, int r, double* w, double* vecs, bool all_values) {
