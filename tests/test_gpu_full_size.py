@@ -138,3 +138,21 @@ def test_full_sweep_one_launch():
         n, ex, diff = check_head(inp, out, 0, h, 32, "bf16_emul", rows=rows)
         _log(f"head {h}: rows {n} exempt {ex} differing {diff}")
     _check_recall(out, inp, [(0, h, rows) for h in heads], spec.N, 32, want_exact_too=False)
+
+
+def test_six_chunk_merges_score_and_recall():
+    """8 sequences x 48 query heads x 16 queries over 12,000 keys: both the
+    MFMA score path and the MFMA recall path cut the key axis into six chunks
+    (384 row blocks), so each row's merge runs six waves and its tree has an
+    odd level.  Sampled heads checked against the oracle, with the oracle's
+    lists given to the recall."""
+    spec = W.SPECS["qwen25_7b_decode"].with_(N=12_000, Q=16, H_q=48, H_kv=4, batch=8)
+    inp = W.make_layer(spec)
+    _log("inputs generated")
+    assert S.saki_score_topk_workspace_bytes(8, 48, 16, 12_000, 32, 64, "bf16") >= 8 * 48 * 16 * 6 * 64 * 8
+    out = gpu_pipeline(inp, 32, "bf16")
+    samples = [(0, 0), (3, 25), (7, 47)]
+    for b, h in samples:
+        n, ex, diff = check_head(inp, out, b, h, 32, "bf16_emul")
+        _log(f"b{b} h{h}: rows {n} exempt {ex} differing {diff}")
+    _check_recall(out, inp, [(b, h, np.arange(16)) for b, h in samples], 12_000, 32)
