@@ -300,6 +300,30 @@ def test_size_helpers():
     assert S.saki_recall_workspace_bytes(1, 32, 8, 1, 1 << 20, 64, 64) == 0
 
 
+def test_scan_workspace_holds_lists_gates_and_flags():
+    """16 or more queries per head over at least 16,384 keys take the one-pass
+    MFMA scan: with the key axis in chunks its workspace holds, per row, a
+    64-entry partial list (8 B each) and a gate (4 B) per chunk, and a redo
+    flag (4 B).  The chunk count is the planner's (one per 2,048 waves' worth
+    of rows, chunks of at least 2,048 keys), so the bound below follows from
+    the sizes alone."""
+    B, H, Q, N = 8, 28, 16, 131_072
+    rows = B * H * Q
+    waves = B * H * (Q // 16)                   # one 16-row block per head
+    want = -(-2048 // waves)                    # chunks per row for 2,048 waves
+    chunk = max(2048, -(-(-(-N // want)) // 64) * 64)
+    chunks = -(-N // chunk)
+    assert chunks == 10
+    ws = S.saki_score_topk_workspace_bytes(B, H, Q, N, 32, 64, "bf16")
+    assert ws >= rows * chunks * (64 * 8 + 4) + rows * 4
+    # one row block of one head over 16,384 keys: 8 chunks of 2,048 keys
+    ws1 = S.saki_score_topk_workspace_bytes(1, 1, 16, 16_384, 32, 64, "bf16")
+    assert ws1 >= 16 * 8 * (64 * 8 + 4) + 16 * 4
+    # enough rows that every row block scans its keys in one chunk: no partial
+    # lists, gates or flags (the minimum workspace)
+    assert S.saki_score_topk_workspace_bytes(1, 16, 2048, 16_384, 32, 64, "bf16") == 256
+
+
 def test_argument_validation_without_launch(lib):
     """Invalid arguments are rejected before anything touches the GPU."""
     P = C.c_void_p(1)  # never dereferenced: validation fails first
