@@ -26,7 +26,8 @@ __all__ = [
     "weight_svd_factors", "score_loss", "codes", "query_sketch", "sketch_scores",
     "direct_scores", "exact_scores", "candidate_limits", "topk_row", "topk_rows",
     "recall_hits", "bf16_round", "f32_round", "fp8_round", "E4M3_MAX", "score_scale",
-    "predicted_reduction",
+    "norm_scale",
+    "predicted_reduction", "measured_reduction", "population_reduction",
     "head_group", "index_scores", "PAD_IDX", "ROPE_THETA", "rope", "reconstruct_keys",
     "sparse_attention",
 ]
@@ -383,11 +384,59 @@ def score_scale(B_q, B_k, mu, q, keys) -> np.ndarray:
     return zq @ ck.T + (aq @ np.abs(mu))[:, None]
 
 
+def norm_scale(B_q, B_k, mu, q, keys) -> np.ndarray:
+    """Scale of the sketch-score tolerances: ||z_i||_2 ||c_j||_2 + |b_i| with the
+    exact z_i = B_q^T q_i, c_j = B_k^T (k_j - mu) and b_i = q_i^T mu (Sec. 6).
+    By Cauchy-Schwarz it bounds |s_hat_ij|, so a relative tolerance on it is a
+    relative tolerance on the score's own magnitude.  [Q, d], [N, d] -> [Q, N]."""
+    z, b = query_sketch(B_q, mu, q)
+    c = codes(B_k, mu, keys)
+    return (np.linalg.norm(z, axis=1)[:, None] * np.linalg.norm(c, axis=1)[None, :]
+            + np.abs(b)[:, None])
+
+
 def predicted_reduction(sigma: np.ndarray, r: int) -> float:
     """Predicted relative score-MSE reduction of the rank-r map (Remark 2,
     Appendix C): 1 - sum_{i>r} sigma_i^2 / sum_i sigma_i^2."""
     s2 = np.asarray(sigma, np.float64) ** 2
     return float(1.0 - s2[r:].sum() / s2.sum())
+
+
+def measured_reduction(q, keys, M, mu, q_pos=None):
+    """Measured relative score-MSE reduction of the map M (Appendix C):
+    1 - sum (q^T (I - M)(k - mu))^2 / sum (q^T (k - mu))^2 over (query, key)
+    pairs, keys centred by the calibration mean, pre-RoPE.  The denominator is
+    the error of the rank-0 map, which keeps only the mean term.
+
+    With q_pos None the pairs are (q_i, k_i), one to one (independent pairs
+    when the rows are independent draws); the delta-method standard error of
+    the ratio is returned with it.  With q_pos, every causal pair j <= q_pos[i]
+    counts, and the standard error is None.  q [n, d], keys [n or N, d]."""
+    q = np.asarray(q, np.float64)
+    kc = np.asarray(keys, np.float64) - np.asarray(mu, np.float64)
+    res = kc - kc @ np.asarray(M, np.float64).T  # (I - M)(k - mu), row-wise
+    if q_pos is None:
+        base = np.einsum("nd,nd->n", q, kc)
+        err = np.einsum("nd,nd->n", q, res)
+        a, b = np.mean(err ** 2), np.mean(base ** 2)
+        se = np.sqrt(np.var(err ** 2 - (a / b) * base ** 2) / q.shape[0]) / b
+        return float(1.0 - a / b), float(se)
+    mask = np.arange(kc.shape[0])[None, :] <= np.asarray(q_pos)[:, None]
+    base = q @ kc.T
+    err = q @ res.T
+    return float(1.0 - np.sum(err[mask] ** 2) / np.sum(base[mask] ** 2)), None
+
+
+def population_reduction(M, mu, Sigma_q, Sigma_k) -> float:
+    """The reduction measured_reduction converges to on independent pairs
+    (Eq. 2 with the population moments): queries with second moment Sigma_q,
+    zero-mean keys with covariance Sigma_k, centred by mu, so the keys' second
+    moment about mu is Sigma_k + mu mu^T:
+    1 - tr((I - M)^T Sigma_q (I - M) K) / tr(Sigma_q K), K = Sigma_k + mu mu^T."""
+    d = np.asarray(M).shape[0]
+    K = np.asarray(Sigma_k, np.float64) + np.outer(mu, mu)
+    E = np.eye(d) - np.asarray(M, np.float64)
+    return float(1.0 - np.trace(E.T @ Sigma_q @ E @ K) / np.trace(Sigma_q @ K))
 
 
 def index_scores(B_q, B_k, mu, q, keys, sketch: str = "f64"):

@@ -63,6 +63,28 @@ def _check_recall(out, inp, samples, N, r, want_exact_too=True, factors=None):
              f"(mean {np.mean([want[k][1].mean() for k in want]) / 64:.4f})")
 
 
+def _check_own_recall(out, inp, samples, N, r, factors=None):
+    """saki_recall over the GPU's own sketch lists: on the sampled rows (whose
+    sets equal the oracle's, asserted by the caller) the hits, their integer
+    total and the recall printed to four decimals equal the oracle's."""
+    hits, _ = S.saki_recall(out["keys"], out["q"], _t(out["idx"], torch.int32), N,
+                            q_pos=out["pos"], want_exact=False)
+    torch.cuda.synchronize()
+    hits = hits.cpu().numpy()
+    got = want = n_rows = 0
+    for b, h, rows in samples:
+        fac = factors(h) if factors is not None else None
+        ap, ex = _oracle_lists(inp, b, h, r, rows, N, fac)
+        wh = O.recall_hits(ap, ex)
+        np.testing.assert_array_equal(hits[b, h, rows], wh)
+        got += int(hits[b, h, rows].sum())
+        want += int(wh.sum())
+        n_rows += len(rows)
+    assert got == want and f"{got / (64 * n_rows):.4f}" == f"{want / (64 * n_rows):.4f}"
+    _log(f"recall of the GPU's own lists on {n_rows} sampled rows: {got} hits, "
+         f"{got / (64 * n_rows):.4f} (oracle {want}, {want / (64 * n_rows):.4f})")
+
+
 def test_full_llama_layer():
     """LLaMA-3.1-8B-shaped layer as the bench runs it: 32 query / 8 KV heads,
     N = 4096, causal rows 64..4095, bf16 codes at r = 32, one build, one
@@ -73,10 +95,12 @@ def test_full_llama_layer():
     _log("layer scored")
     rng = np.random.default_rng(11)
     rows = np.unique(np.concatenate([[0, 1, 63, 64, 2047, spec.Q - 1],
-                                     rng.choice(spec.Q, 40, False)]))
+                                     rng.choice(spec.Q, 200, False)]))
     for h in (0, 13, 31):
         n, ex, diff = check_head(inp, out, 0, h, 32, "bf16_emul", rows=rows)
         _log(f"h{h}: rows {n} exempt {ex} differing {diff}")
+        assert diff == 0 and ex <= 0.1 * n
+    _check_own_recall(out, inp, [(0, h, rows) for h in (0, 13, 31)], spec.N, 32)
     _check_recall(out, inp, [(0, h, rows) for h in (0, 13, 31)], spec.N, 32)
 
 
@@ -92,6 +116,8 @@ def test_full_decode_1m():
     for h in (0, 13, 31):
         n, ex, diff = check_head(inp, out, 0, h, 32, "bf16_emul")
         _log(f"h{h}: exempt {ex} differing {diff}")
+        assert diff == 0
+    _check_own_recall(out, inp, [(0, h, np.arange(spec.Q)) for h in (0, 13, 31)], spec.N, 32)
     _check_recall(out, inp, [(0, h, np.arange(spec.Q)) for h in (0, 31)], spec.N, 32)
 
 
@@ -108,6 +134,8 @@ def test_full_qwen_decode_layer():
     for b, h in samples:
         n, ex, diff = check_head(inp, out, b, h, 32, "bf16_emul")
         _log(f"b{b} h{h}: rows {n} exempt {ex} differing {diff}")
+        assert diff == 0
+    _check_own_recall(out, inp, [(b, h, np.arange(spec.Q)) for b, h in samples], spec.N, 32)
     _check_recall(out, inp, [(b, h, np.arange(spec.Q)) for b, h in samples[:2]], spec.N, 32,
                   want_exact_too=False)
 
@@ -137,6 +165,8 @@ def test_full_sweep_one_launch():
     for h in heads:
         n, ex, diff = check_head(inp, out, 0, h, 32, "bf16_emul", rows=rows)
         _log(f"head {h}: rows {n} exempt {ex} differing {diff}")
+        assert diff == 0
+    _check_own_recall(out, inp, [(0, h, rows) for h in heads], spec.N, 32)
     _check_recall(out, inp, [(0, h, rows) for h in heads], spec.N, 32, want_exact_too=False)
 
 
@@ -155,4 +185,5 @@ def test_six_chunk_merges_score_and_recall():
     for b, h in samples:
         n, ex, diff = check_head(inp, out, b, h, 32, "bf16_emul")
         _log(f"b{b} h{h}: rows {n} exempt {ex} differing {diff}")
+        assert diff == 0
     _check_recall(out, inp, [(b, h, np.arange(16)) for b, h in samples], 12_000, 32)

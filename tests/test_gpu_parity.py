@@ -5,7 +5,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from tests.parity import check_rows, oracle_head
+from tests.parity import AMBIG_REL, check_rows, oracle_head
 
 torch = pytest.importorskip("torch")
 S = pytest.importorskip("paper_2608_03228_amd.saki")
@@ -69,7 +69,7 @@ def test_single_head_f32_full():
     out = gpu_pipeline(inp, 32, "f32")
     n, ex, diff = check_head(inp, out, 0, 0, 32, "f32")
     print(f"rows {n} exempt {ex} differing {diff}")
-    assert n == 256 and diff <= ex
+    assert n == 256 and diff == 0
 
 
 def test_codes_match_oracle():
@@ -88,17 +88,17 @@ def test_codes_match_oracle():
             exact = kc @ Bk
             scale = np.abs(kc) @ np.abs(Bk)
             got = codes[0, h]
-            if sketch == "f32":
-                assert np.max(np.abs(got - exact) / scale) < 1e-5
+            if sketch == "f32":  # the computation error bound the bf16 parity rule assumes
+                assert np.max(np.abs(got - exact) / scale) < AMBIG_REL
             elif sketch == "fp8":
                 assert np.all(O.fp8_round(got) == got)  # representable in E4M3
                 mag = np.maximum(np.abs(exact), 1e-30)
                 ulp = np.where(mag < 2.0 ** -6, 2.0 ** -9, np.exp2(np.floor(np.log2(mag)) - 3))
-                assert np.all(np.abs(got - exact) <= 0.5 * ulp + 1e-5 * scale)
+                assert np.all(np.abs(got - exact) <= 0.5 * ulp + AMBIG_REL * scale)
             else:
                 assert np.all(O.bf16_round(got) == got)  # representable in bf16
                 ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(exact), 1e-30))) - 7)
-                assert np.all(np.abs(got - exact) <= 0.5 * ulp + 1e-5 * scale)
+                assert np.all(np.abs(got - exact) <= 0.5 * ulp + AMBIG_REL * scale)
 
 
 @pytest.mark.parametrize("r", [16, 32, 64])
@@ -369,9 +369,12 @@ def test_recall_split_chunks_matches_oracle():
 
 
 def test_single_head_recall_table_saki_pca_wsvd():
-    """The single-head workload's recall@64 for SAKI, the span variants SAP-map
-    and SAP-svd (Sec. 6), key PCA and weight SVD, GPU vs oracle: identical
-    hits on every row where the two top-64 sets agree."""
+    """The single-head workload's recall@64 for SAKI, key PCA and weight SVD
+    (the reported table), GPU vs oracle: every row's top-64 set equals the
+    oracle's, so the hits, their integer totals and the recall printed to
+    four decimals are identical.  The span variants SAP-map and SAP-svd
+    (Sec. 6) may swap keys on tie-exempt rows (checked by the parity rule);
+    their hits are identical on every row whose sets agree."""
     inp = W.make_layer(W.SPECS["single_head_d128"])
     q, keys = inp["queries"][0, 0], inp["keys"][0, 0]
     lim = O.candidate_limits(256, 1024)
@@ -397,16 +400,25 @@ def test_single_head_recall_table_saki_pca_wsvd():
                                  1024)
         np.testing.assert_array_equal(ex.cpu().numpy()[0, 0], ex_o)
         Bq, Bk, mu = orc_f[name]
+        n, n_ex, diff = check_head(inp, out, 0, 0, 32, "f32", factors=orc_f[name])
         s_hat, *_ = O.index_scores(Bq, Bk, mu, q, keys)
         ap_o = O.topk_rows(s_hat, lim)
         h_o = O.recall_hits(ap_o, ex_o)
         h_g = hits.cpu().numpy()[0, 0]
         same = np.array([set(a) == set(b) for a, b in zip(out["idx"][0, 0], ap_o)])
         np.testing.assert_array_equal(h_g[same], h_o[same])
-        table[name] = (h_g.mean() / 64, h_o.mean() / 64, int((~same).sum()))
-    print("recall@64 (gpu, oracle, rows with differing sets):", table)
-    assert table["saki"][1] > table["pca"][1] > table["wsvd"][1]
-    assert table["saki"][1] > max(table["sap_map"][1], table["sap_svd"][1])
+        if name in ("saki", "pca", "wsvd"):
+            # the reported table: every set equal, so identical hits and recall
+            assert diff == 0, (name, n_ex, diff)
+            assert int(h_g.sum()) == int(h_o.sum())
+            assert f"{h_g.sum() / (64 * 256):.4f}" == f"{h_o.sum() / (64 * 256):.4f}"
+        table[name] = (f"{h_g.sum() / (64 * 256):.4f}", int(h_g.sum()), int(h_o.sum()), n_ex,
+                       diff)
+    print("recall@64 (GPU 4 decimals, GPU hits, oracle hits, tie-exempt rows, differing rows):",
+          table)
+    hit = {name: v[2] for name, v in table.items()}
+    assert hit["saki"] > hit["pca"] > hit["wsvd"]
+    assert hit["saki"] > max(hit["sap_map"], hit["sap_svd"])
 
 
 @pytest.mark.parametrize("kind", ["map", "svd"])

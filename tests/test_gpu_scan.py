@@ -31,6 +31,7 @@ def test_scan_matches_oracle(sketch, r, Q, N, batch):
         for h in range(2):
             n, ex, diff = check_head(inp, out, b, h, r, MODE[sketch])
             print(f"b{b} h{h}: rows {n} exempt {ex} differing {diff}")
+            assert diff == 0
 
 
 def test_scan_positions_n_valid_and_small_k():

@@ -9,6 +9,7 @@ import pytest
 import torch
 
 import oracle as O
+import workloads as W
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_2x2.json")
 
@@ -125,6 +126,35 @@ def test_score_scale_covers_float32_rounding():
     s32 = (z32 @ c32.T + b32[:, None]).astype(np.float64)
     S = O.score_scale(Bq, Bk, mu, q, keys)
     assert np.max(np.abs(s32 - s) / S) < 1e-5
+
+
+def test_norm_scale_covers_float32_on_the_layer():
+    """The parity scale T_ij = ||z|| ||c|| + |b| on SAKI's own factors (LLaMA-
+    shaped layer, head 0, 400 causal rows): float32 codes, query sketches and
+    scores (factors rounded to float32, as the library stores them) stay
+    within 1e-5 T_ij of the float64 scores, and each float32 code and sketch
+    element within tests.parity.AMBIG_REL times its absolute-value sum of
+    the exact one, the bounds the GPU parity tests rely on.  The magnitude
+    scale S_ij of the factored computation is far larger (cancellation in
+    B_q^T q and B_k^T (k - mu))."""
+    from tests.parity import AMBIG_REL
+    spec = W.SPECS["llama31_8b_layer"].with_(H_q=4, H_kv=1)
+    inp = W.make_layer(spec)
+    cal = O.saki_calibrate(inp["q_cal"][0], inp["k_cal"][0], 32)
+    Bq, Bk, mu = cal["B_q"], cal["B_k"], cal["mu"]
+    q = inp["queries"][0, 0][-400:].astype(np.float64)
+    keys = inp["keys"][0, 0].astype(np.float64)
+    s, z, b, c = O.index_scores(Bq, Bk, mu, q, keys)
+    f = np.float32
+    c32 = ((keys.astype(f) - mu.astype(f)) @ Bk.astype(f)).astype(np.float64)
+    z32 = (q.astype(f) @ Bq.astype(f)).astype(np.float64)
+    b32 = (q.astype(f) @ mu.astype(f)).astype(np.float64)
+    s32 = z32 @ c32.T + b32[:, None]
+    T = O.norm_scale(Bq, Bk, mu, q, keys)
+    assert np.max(np.abs(s32 - s) / T) < 1e-5
+    assert np.max(np.abs(c32 - c) / (np.abs(keys - mu) @ np.abs(Bk))) < AMBIG_REL
+    assert np.max(np.abs(z32 - z) / (np.abs(q) @ np.abs(Bq))) < AMBIG_REL
+    assert np.median(O.score_scale(Bq, Bk, mu, q, keys) / T) > 50
 
 
 def test_fp8_round_matches_torch_e4m3fn():
