@@ -32,8 +32,10 @@
  *   - Ranking: top-k lists are sorted by score descending, ties broken by the
  *     lower key index.  Rows with fewer than k candidates are padded with
  *     index -1 and score -INFINITY.
- *   - No global mutable state: calls on different streams may run
- *     concurrently.
+ *   - Shared state: a process-wide cache of kernel occupancies and a host
+ *     worker pool (both behind mutexes), and the static scratch array of
+ *     saki_score_topk_noalloc.  Every other call works only on the caller's
+ *     buffers, so calls on different streams may run concurrently.
  */
 #ifndef SAKI_H
 #define SAKI_H
@@ -234,6 +236,30 @@ int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_k
                     const int* q_pos, int Q, const float* B_q, const float* mu,
                     int k, int* top_idx, float* top_score, void* ws,
                     size_t ws_bytes, void* stream);
+
+/*
+ * saki_score_topk_noalloc (GPU) -- for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, kernels and results as saki_score_topk,
+ * without the workspace: the split-key partial lists, chunk gates and redo
+ * flags live in a static device array of saki_noalloc_scratch_bytes()
+ * (32 MiB) that each GPU the library runs on holds until the process ends.
+ * Nothing is allocated.  Returns SAKI_ERR_WORKSPACE when the call needs
+ * more (saki_score_topk_workspace_bytes(...) > saki_noalloc_scratch_bytes()),
+ * SAKI_ERR_HIP when the array's device address cannot be obtained.  Every
+ * call on a GPU uses that GPU's one array: calls that overlap in time on the
+ * same GPU (different streams, or host threads) race and must be serialised
+ * by the caller.  The array keeps the last call's contents; each call writes
+ * every entry it reads before reading it.
+ */
+int saki_score_topk_noalloc(const void* index, int sketch_dtype, int B, int H_q, int H_kv,
+                            int index_heads, int N_cap, int N_valid, int d, int r,
+                            const float* q, const int* q_pos, int Q, const float* B_q,
+                            const float* mu, int k, int* top_idx, float* top_score,
+                            void* stream);
+
+/* Bytes of the static scratch array behind saki_score_topk_noalloc. */
+size_t saki_noalloc_scratch_bytes(void);
 
 /* Workspace for saki_recall with these sizes (bytes; 0 on bad arguments). */
 size_t saki_recall_workspace_bytes(int B, int H_q, int H_kv, int Q, int N_valid, int d, int k);

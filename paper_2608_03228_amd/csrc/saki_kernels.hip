@@ -3075,6 +3075,95 @@ int check_common(int B, int H_q, int H_kv, int N_cap, int N_valid, int d) {
   return SAKI_OK;
 }
 
+// Scratch memory of the allocation-free score entry point: a static device
+// array, one copy per GPU the library runs on (held until the process
+// ends).  In host code `scratch` names a host-side stand-in, never the
+// device memory: the device address comes from hipGetSymbolAddress, taken
+// once per device with that device current, and only that address is
+// passed to kernels.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+
+}  // namespace
+
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array (*out), or an error.
+int scratch_address(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return SAKI_ERR_HIP;
+  }
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+      (void)hipGetLastError();
+      return SAKI_ERR_HIP;
+    }
+    scratch_ptr[dev] = ptr;
+  }
+  *out = scratch_ptr[dev];
+  return SAKI_OK;
+}
+
+// saki_score_topk with ws == NULL meaning the static scratch array (whose
+// size the caller passes as ws_bytes).
+int score_topk_impl(const void* index, int sketch_dtype, int B, int H_q, int H_kv,
+                    int index_heads, int N_cap, int N_valid, int d, int r, const float* q,
+                    const int* q_pos, int Q, const float* B_q, const float* mu, int k,
+                    int* top_idx, float* top_score, void* ws, size_t ws_bytes, void* stream) {
+  int st = check_common(B, H_q, H_kv, N_cap, N_valid, d);
+  if (st != SAKI_OK) return st;
+  if (Q < 0) return SAKI_ERR_ARG;
+  // a code set serves whole query heads and lies within one KV group
+  if (index_heads <= 0 || H_q % index_heads != 0 || index_heads % H_kv != 0) return SAKI_ERR_ARG;
+  if (!sketch_ok(sketch_dtype) || !saki::rank_supported(r) || k < 1 || k > kMaxK)
+    return SAKI_ERR_UNSUPPORTED;
+  if (Q == 0) return SAKI_OK;
+  if (!index || !q || !B_q || !mu || !top_idx) return SAKI_ERR_ARG;
+  const saki::Plan p = saki::score_plan(B, H_q, index_heads, Q, N_valid);
+  if (ws_bytes < p.ws_bytes) return SAKI_ERR_WORKSPACE;
+  if (!ws) {  // the static scratch array, resolved only once the sizes fit it
+    const int sst = scratch_address(&ws);
+    if (sst != SAKI_OK) return sst;
+  }
+  if ((size_t)p.row_blocks * p.n_chunks > 0x7fffffffu) return SAKI_ERR_UNSUPPORTED;
+  // the one-pass kernel's 1-D grid: one wave per (head, row block, chunk)
+  if (p.scan && (size_t)B * H_q * p.row_blocks * p.n_chunks * kWave >= 0xffffffffu)
+    return SAKI_ERR_UNSUPPORTED;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const uint8_t* ix = reinterpret_cast<const uint8_t*>(index);
+  uint8_t* w = reinterpret_cast<uint8_t*>(ws);
+#define SAKI_SCORE_ST(RK, ST)                                                                 \
+  launch_score<RK, ST>(ix, B, H_q, H_kv, index_heads, N_cap, N_valid, q, q_pos, Q, B_q, mu, k, \
+                       top_idx, top_score, w, p, s)
+#define SAKI_SCORE(RK)                          \
+  do {                                          \
+    if (sketch_dtype == SAKI_FP8)               \
+      SAKI_SCORE_ST(RK, kStFp8);                \
+    else if (sketch_dtype == SAKI_BF16)         \
+      SAKI_SCORE_ST(RK, kStBf16);               \
+    else                                        \
+      SAKI_SCORE_ST(RK, kStF32);                \
+  } while (0)
+  switch (r) {
+    case 16: SAKI_SCORE(16); break;
+    case 32: SAKI_SCORE(32); break;
+    case 64: SAKI_SCORE(64); break;
+    default: SAKI_SCORE(128); break;
+  }
+#undef SAKI_SCORE
+#undef SAKI_SCORE_ST
+  return launch_ok() ? SAKI_OK : SAKI_ERR_HIP;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------- C ABI
@@ -3156,46 +3245,22 @@ int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_k
                     int index_heads, int N_cap, int N_valid, int d, int r, const float* q,
                     const int* q_pos, int Q, const float* B_q, const float* mu, int k,
                     int* top_idx, float* top_score, void* ws, size_t ws_bytes, void* stream) {
-  int st = check_common(B, H_q, H_kv, N_cap, N_valid, d);
-  if (st != SAKI_OK) return st;
-  if (Q < 0) return SAKI_ERR_ARG;
-  // a code set serves whole query heads and lies within one KV group
-  if (index_heads <= 0 || H_q % index_heads != 0 || index_heads % H_kv != 0) return SAKI_ERR_ARG;
-  if (!sketch_ok(sketch_dtype) || !saki::rank_supported(r) || k < 1 || k > kMaxK)
-    return SAKI_ERR_UNSUPPORTED;
-  if (Q == 0) return SAKI_OK;
-  if (!index || !q || !B_q || !mu || !top_idx || !ws) return SAKI_ERR_ARG;
-  const saki::Plan p = saki::score_plan(B, H_q, index_heads, Q, N_valid);
-  if (ws_bytes < p.ws_bytes) return SAKI_ERR_WORKSPACE;
-  if ((size_t)p.row_blocks * p.n_chunks > 0x7fffffffu) return SAKI_ERR_UNSUPPORTED;
-  // the one-pass kernel's 1-D grid: one wave per (head, row block, chunk)
-  if (p.scan && (size_t)B * H_q * p.row_blocks * p.n_chunks * kWave >= 0xffffffffu)
-    return SAKI_ERR_UNSUPPORTED;
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const uint8_t* ix = reinterpret_cast<const uint8_t*>(index);
-  uint8_t* w = reinterpret_cast<uint8_t*>(ws);
-#define SAKI_SCORE_ST(RK, ST)                                                                 \
-  launch_score<RK, ST>(ix, B, H_q, H_kv, index_heads, N_cap, N_valid, q, q_pos, Q, B_q, mu, k, \
-                       top_idx, top_score, w, p, s)
-#define SAKI_SCORE(RK)                          \
-  do {                                          \
-    if (sketch_dtype == SAKI_FP8)               \
-      SAKI_SCORE_ST(RK, kStFp8);                \
-    else if (sketch_dtype == SAKI_BF16)         \
-      SAKI_SCORE_ST(RK, kStBf16);               \
-    else                                        \
-      SAKI_SCORE_ST(RK, kStF32);                \
-  } while (0)
-  switch (r) {
-    case 16: SAKI_SCORE(16); break;
-    case 32: SAKI_SCORE(32); break;
-    case 64: SAKI_SCORE(64); break;
-    default: SAKI_SCORE(128); break;
-  }
-#undef SAKI_SCORE
-#undef SAKI_SCORE_ST
-  return launch_ok() ? SAKI_OK : SAKI_ERR_HIP;
+  if (!ws) return SAKI_ERR_ARG;
+  return score_topk_impl(index, sketch_dtype, B, H_q, H_kv, index_heads, N_cap, N_valid, d, r,
+                         q, q_pos, Q, B_q, mu, k, top_idx, top_score, ws, ws_bytes, stream);
 }
+
+int saki_score_topk_noalloc(const void* index, int sketch_dtype, int B, int H_q, int H_kv,
+                            int index_heads, int N_cap, int N_valid, int d, int r,
+                            const float* q, const int* q_pos, int Q, const float* B_q,
+                            const float* mu, int k, int* top_idx, float* top_score,
+                            void* stream) {
+  return score_topk_impl(index, sketch_dtype, B, H_q, H_kv, index_heads, N_cap, N_valid, d, r,
+                         q, q_pos, Q, B_q, mu, k, top_idx, top_score, nullptr, kScratchBytes,
+                         stream);
+}
+
+size_t saki_noalloc_scratch_bytes(void) { return kScratchBytes; }
 
 int saki_calibration_moments(const float* q_cal, const float* k_cal, int H_q, int H_kv,
                              int T, int d, double* Sigma_q, double* Sigma_k,

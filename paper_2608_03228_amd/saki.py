@@ -56,6 +56,9 @@ def lib():
         "saki_score_topk_workspace_bytes": (sz, [ip, ip, ip, ip, ip, ip, ip, ip]),
         "saki_score_topk": (ip, [vp, ip, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, ip, vp, vp, ip,
                                  vp, vp, vp, sz, vp]),
+        "saki_score_topk_noalloc": (ip, [vp, ip, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, ip, vp,
+                                         vp, ip, vp, vp, vp]),
+        "saki_noalloc_scratch_bytes": (sz, []),
         "saki_recall_workspace_bytes": (sz, [ip, ip, ip, ip, ip, ip, ip]),
         "saki_recall": (ip, [vp, ip, vp, vp, ip, ip, ip, ip, ip, ip, ip, ip, vp, vp, vp, vp,
                              sz, vp]),
@@ -286,6 +289,31 @@ def saki_score_topk(index, sketch: str, q, B_q, mu, H_kv: int, N_cap: int, N_val
         _dev(ws, (torch.uint8,), "ws"), ws.numel(), _stream(stream))
     _check("saki_score_topk", st)
     return top_idx, (top_score if with_scores else None)
+
+
+def saki_noalloc_scratch_bytes() -> int:
+    return int(lib().saki_noalloc_scratch_bytes())
+
+
+def saki_score_topk_noalloc(index, sketch: str, q, B_q, mu, H_kv: int, N_cap: int,
+                            N_valid: int, r: int, top_idx, top_score=None, q_pos=None,
+                            k: int = 64, stream=None, index_heads=None):
+    """saki_score_topk without a workspace (the library's static scratch
+    array): the caller passes the outputs top_idx [B, H_q, Q, k] int32 and
+    top_score float32 (or None)."""
+    torch = _torch()
+    qp = _dev(q, (torch.float32,), "q")
+    B, H_q, Q, d = q.shape
+    ih = H_q if index_heads is None else int(index_heads)
+    pos = _dev(q_pos, (torch.int32,), "q_pos") if q_pos is not None else None
+    st = lib().saki_score_topk_noalloc(
+        _dev(index, (torch.uint8,), "index"), _DTYPES[sketch], B, H_q, int(H_kv), ih, int(N_cap),
+        int(N_valid), d, int(r), qp, pos, Q, _dev(B_q, (torch.float32,), "B_q"),
+        _dev(mu, (torch.float32,), "mu"), int(k), _dev(top_idx, (torch.int32,), "top_idx"),
+        _dev(top_score, (torch.float32,), "top_score") if top_score is not None else None,
+        _stream(stream))
+    _check("saki_score_topk_noalloc", st)
+    return top_idx, top_score
 
 
 def saki_recall(keys, q, approx_idx, N_valid: int, q_pos=None, k: int = 64, ws=None,

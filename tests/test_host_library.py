@@ -351,6 +351,17 @@ def test_argument_validation_without_launch(lib):
     for ih in (0, 3, 1, 16):
         gqa = [P, 0, 1, 8, 2, ih, 256, 256, 128, 32, P, None, 4, P, P]
         assert lib.saki_score_topk(*gqa, 64, P, None, P, 1 << 30, None) == ERR_ARG, ih
+    # the allocation-free variant: same validation; a call needing more than
+    # its static scratch array fails before the array is touched
+    na = [P, 0, 1, 1, 1, 1, 256, 256, 128, 32, P, None, 4, P, P]
+    assert lib.saki_score_topk_noalloc(*na, 65, P, None, None) == ERR_UNSUP
+    assert lib.saki_score_topk_noalloc(*na, 64, None, None, None) == ERR_ARG
+    # 2,047 heads x 16 queries over 16,384 keys: two key chunks per row, whose
+    # partial lists, gates and flags need just over 32 MiB
+    need = S.saki_score_topk_workspace_bytes(1, 2047, 16, 16_384, 32, 64, "bf16")
+    assert need > S.saki_noalloc_scratch_bytes() == 32 << 20
+    over = [P, 1, 1, 2047, 1, 2047, 16_384, 16_384, 128, 32, P, None, 16, P, P]
+    assert lib.saki_score_topk_noalloc(*over, 64, P, None, None) == ERR_WS
     # recall: null hits, bad key dtype
     assert lib.saki_recall(P, 0, P, None, 1, 1, 1, 256, 256, 4, 128, 64, P, None, None, P,
                            1 << 30, None) == ERR_ARG
