@@ -74,11 +74,11 @@ def log(msg):
 
 # the kernel that dominates each stage, and the template instance launched
 # for (r, sketch) as rocprofv3 names it
-STAGE_KERNEL = {"build": "build_index_kernel", "score_topk": "score_mfma_kernel",
+STAGE_KERNEL = {"build": "build_index_kernel", "score_topk": "score_batch_kernel",
                 "recall": "exact_gate_kernel"}
 STAGE_INSTANCE = {
     "build": lambda r, sk: f"build_index_kernel<{r}, false, {({'f32': 0, 'bf16': 1, 'fp8': 2})[sk]}>",
-    "score_topk": lambda r, sk: f"score_mfma_kernel<{r}, {({'f32': 0, 'bf16': 1, 'fp8': 2})[sk]}>",
+    "score_topk": lambda r, sk: f"score_batch_kernel<{r}, {({'f32': 0, 'bf16': 1, 'fp8': 2})[sk]}>",
     "recall": lambda r, sk: "exact_gate_kernel<false>",
 }
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_03228_amd", "csrc", "saki_kernels.hip")
@@ -386,7 +386,7 @@ def run_batched(inp, r, sk, k, steps, warmup, method="opt"):
 
 
 def score_roofline(res, spec, r, sk, k, method):
-    """The headline roofline: the score_topk stage (score_mfma_kernel
+    """The headline roofline: the score_topk stage (score_batch_kernel
     dominates it), 2 r flops per allowed pair against the sketch dtype's MFMA
     peak."""
     t = res["terms"]["score_topk"]
@@ -496,7 +496,7 @@ def run_decode(spec, r, sk, k, steps, warmup, shared=False, attend=True, cpu=Fal
     # fewer the streaming kernel with 1 or 4 rows per wave
     st = {"f32": 0, "bf16": 1, "fp8": 2}[sk]
     if Q >= 16:
-        kern = "score_scan_kernel" if N >= 16384 else "score_mfma_kernel"
+        kern = "score_scan_kernel" if N >= 16384 else "score_batch_kernel"
         inst = f"{kern}<{r}, {st}>"
     else:
         kern = "score_stream_kernel"

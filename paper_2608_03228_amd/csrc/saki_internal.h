@@ -13,6 +13,8 @@ constexpr int kTile = 64;      // keys per index tile
 constexpr int kChunkBytes = 16;
 constexpr int kScanWaves = 1;          // waves per work-group of the one-pass MFMA scoring kernel
 constexpr int kScanMinKeys = 16384;    // rows at least this long take it
+constexpr int kBatchMaxChunk = 4096;   // keys per chunk of the two-pass MFMA scoring kernel
+constexpr int kBatchWaves = 4;         // its waves per work-group (16 rows each)
 
 inline bool rank_supported(int r) { return r == 16 || r == 32 || r == 64 || r == 128; }
 // bytes per code element: float32 (0), bf16 (1), fp8 E4M3 (2)
@@ -102,6 +104,17 @@ inline Plan score_plan(int B, int H_q, int index_heads, int Q, int N_valid) {
       p.flag_count = rows_total;
       p.ws_bytes = round_up(p.flag_off + rows_total * sizeof(int), 256);
     }
+  }
+  if (mfma && !p.scan) {  // the two-pass kernel: chunks of at most kBatchMaxChunk keys
+    p.waves = kBatchWaves;
+    p.row_blocks = ((Q + 15) / 16 + kBatchWaves - 1) / kBatchWaves;
+    const size_t n = N_valid > 0 ? (size_t)N_valid : 1;
+    if ((size_t)p.chunk > (size_t)kBatchMaxChunk) {
+      p.chunk = kBatchMaxChunk;
+      p.n_chunks = (int)((n + kBatchMaxChunk - 1) / kBatchMaxChunk);
+    }
+    p.part_off = 0;
+    p.ws_bytes = p.n_chunks > 1 ? round_up((size_t)B * H_q * Q * p.n_chunks * kMaxK * 8, 256) : 0;
   }
   const int wave_rows = (int)((H_q / index_heads) * (size_t)Q + p.rows - 1) / p.rows;
   if (!mfma && wave_rows < 4) {  // too few rows to fill a workgroup: its waves split the keys

@@ -2,8 +2,9 @@
 //
 // Kernels (all on the caller's stream):
 //   build_index_kernel   key codes c = B_k^T (k - mu) for every query head (Eq. 4)
-//   score_mfma_kernel    z = B_q^T q, b = q^T mu and s = z . c + b on MFMA for
-//                        blocks of 16 query rows, top-64 per row
+//   score_batch_kernel   z = B_q^T q, b = q^T mu and s = z . c + b on MFMA for
+//                        blocks of 16 query rows, top-64 per row (two passes:
+//                        block maxima and a threshold, then the candidates)
 //   score_scan_kernel    the same in one pass over the codes for long rows
 //                        (batches of decode queries), running top-64 per row
 //   score_stream_kernel  the same for few query rows per code set (decode):
@@ -25,6 +26,7 @@
 #include <mutex>
 #include <tuple>
 
+#include <cfloat>
 #include <climits>
 #include <cmath>
 #include <cstdint>
@@ -571,25 +573,9 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
 // Query blocks of 16 rows per wave, the column count of the 16x16 MFMA tiles.
 // A = 16 keys of the current tile (rows), B = the wave's 16 queries (columns),
 // so each lane holds scores of one query (lane % 16) against 16 keys of every
-// 64-key tile.
-//
-// Selection runs in three cheap passes over the keys instead of one pass with
-// many sort/merge flushes (scores are recomputed by MFMA in every pass, which
-// costs far less than sorting):
-//   1. moments: per row, mean and variance of its scores in this key chunk;
-//   2. histogram: 64 bins around the predicted 64th score
-//      mean + sd * Phi^-1(1 - 64/n) (bins from 2 sd below to 1 sd above it;
-//      scores below the range are not counted, bin 63 takes everything above);
-//      the highest bin b* whose count from the top reaches 64 gives a gate
-//      that at least 64 and at most 128 candidates pass;
-//   3. collect: the gated candidates go to a per-row LDS buffer, which is
-//      sorted once at the end (bitonic, 64 or 128 entries).
-// The gate only decides which keys are sorted, never their order, so the
-// result is the exact top-64 whenever the gate admits >= 64 keys, which the
-// histogram counts guarantee.  Rows with at most 128 candidates skip the
-// histogram and collect everything.  When the prediction misses (fewer than
-// 64 counted scores in range, more than 128 gated, or zero variance) the wave
-// redoes its rows with the online selection of saki_topk.h.
+// 64-key tile.  The scorer and the query-sketch prologue below serve the
+// batched kernel (score_batch_kernel), the one-pass kernel for long rows
+// (score_scan_kernel) and the exact-recall kernels.
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
@@ -640,8 +626,6 @@ constexpr float kWinLo = 1.25f;   // histogram window around the predicted 64th 
 constexpr float kWinHi = 0.75f;
 constexpr int kCandRow = kCollect + 1;  // padded row strides (LDS bank spread)
 constexpr int kHistRow = kBins + 5;  // 64 bins, 4 private overflow slots, 1 pad
-constexpr int kSCollect = 96;            // candidates per row in score_mfma_kernel
-constexpr int kSCandRow = kSCollect + 1;
 enum RowMode : int { kModeAll = 0, kModeHist = 1, kModeFallback = 2 };
 
 // Scores of one 64-key tile for the wave's 16 queries: acc[sub][v] is query
@@ -876,222 +860,408 @@ __device__ __forceinline__ float mfma_query_sketch(const float* __restrict__ qr,
   return b;
 }
 
-// grid (row_blocks * n_chunks, B*H_q), block 64*waves.  Computes the query
-// sketch itself (z = B_q^T q on the f32 MFMA, rounded to bf16 for bf16 and
-// fp8 codes; b = q^T mu), then scores and selects as described above.
+// ---------------------------------------------------------------- sketch scoring, MFMA, block-maximum gate
+
+// score_batch_kernel: four independent waves per work-group, each with a
+// block of 16 query rows and that block's keys of one chunk (at most 4,096
+// keys), and the exact top-64 per row in two passes over the codes (the MFMA
+// recomputes the scores in the second):
+//   A. each lane records the maxima of its keys in blocks of 8 (rows of at
+//      least 2,048 keys), 4 (1,024), 2 (512) or 1 key, so that a row with
+//      at least 256 keys has at least 256 blocks and one with fewer has one
+//      block per key.  A maximum is stored as the top 16 bits of its
+//      ordered float32 bits, which rounds it down.
+//   threshold: per row, a histogram of the stored maxima over 64 equal bins
+//      of score around the predicted 64th largest (from their mean and
+//      spread and a normal quantile; moved above or below when the crossing
+//      falls outside) gives tau, the lower edge of the bin below the highest
+//      bin whose count from the top reaches 64.  At least 64 blocks then
+//      have a maximum >= tau, so at least 64 keys score >= tau and all of
+//      the row's top-64 do; with 256 blocks or more about 64-90 keys pass.
+//   B. every key that scores >= tau goes to its lane's candidate slots (40
+//      per lane, 160 per row), and the row's count is checked to be >= 64.
+// The candidates are then sorted by a bitonic network that holds 16 entries
+// per lane, and the best 64 are kept.  A row whose candidates overflow its
+// slots (many equal scores) or fall short sends its wave to the online
+// selection of saki_topk.h.
+
+constexpr int kBWaves = saki::kBatchWaves;  // independent waves per work-group
+constexpr int kBEnt = 512;                 // block-maximum entries per row
+constexpr int kBBins = 64;                 // histogram bins per row
+constexpr int kBSlots = 40;                // candidate slots per lane
+constexpr int kBWaveBytes = kMR * 4 * kBSlots * 8;  // 20 KiB of LDS per wave
+static_assert(saki::kBatchMaxChunk / 8 <= kBEnt, "a chunk's 8-key blocks fit");
+static_assert(kMR * kBEnt * 2 + kMR * kBBins * 4 <= kBWaveBytes, "entries and bins fit");
+static_assert(kMR * kTile * 4 + 2 * (kMR / 2) * kList * 8 <= kBWaveBytes, "fallback fits");
+
+// Top 16 bits of the ordered float32 bits: rounds down, finite values map to
+// 0x0080 and above, and -inf (a masked key) to 0.
+__device__ __forceinline__ uint32_t ord16(float x) {
+  return x == -INFINITY ? 0u : (ord_f32(x) >> 16);
+}
+// The float an entry stands for (at most the maximum it was taken from).
+__device__ __forceinline__ float unord16(uint32_t v) { return unord_f32(v << 16); }
+
+// Bitonic sort of one row's 64 entries held 16 per lane by the row's four
+// lanes (lane groups g = lane / 16): entry e = 16 g + i is x[i] of lane group
+// g.  Leaves the entries in descending order of e.
+template <class KO>
+__device__ __forceinline__ void sort64_x16(typename KO::K (&x)[16], int g) {
+  using K = typename KO::K;
+#pragma unroll
+  for (int k = 2; k <= 64; k <<= 1) {
+#pragma unroll
+    for (int m = k >> 1; m > 0; m >>= 1) {
+      if (m >= 16) {  // partner in lane group g ^ (m / 16): lane xor m
+        const bool lower = (g & (m >> 4)) == 0;
+        const bool desc = k == 64 || (g & (k >> 4)) == 0;
+        const bool keep_better = lower == desc;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const K o = KO::shfl_xor(x[i], m);
+          x[i] = KO::sel(KO::gt(x[i], o) == keep_better, x[i], o);
+        }
+      } else {  // partner in the same lane
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          if (i & m) continue;
+          const int j = i | m;
+          const bool desc = k >= 64 ? true : k >= 16 ? (g & (k >> 4)) == 0 : (i & k) == 0;
+          const K a = x[i], b = x[j];
+          const bool sw = KO::gt(a, b) != desc;  // the lower position takes the better when descending
+          x[i] = KO::sel(sw, b, a);
+          x[j] = KO::sel(sw, a, b);
+        }
+      }
+    }
+  }
+}
+
+// x <- the best 64 of x and y (both sorted descending as left by sort64_x16).
+template <class KO>
+__device__ __forceinline__ void merge64_x16(typename KO::K (&x)[16], const typename KO::K (&y)[16],
+                                            int g) {
+  using K = typename KO::K;
+  // entry e against y's entry 63 - e = 16 (3 - g) + (15 - i): lane group g ^ 3
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const K r = KO::shfl_xor(KO::shfl_xor(y[15 - i], 16), 32);
+    x[i] = KO::sel(KO::gt(r, x[i]), r, x[i]);
+  }
+  // x is now bitonic: half-cleaners, all descending
+#pragma unroll
+  for (int m = 32; m >= 16; m >>= 1) {
+    const bool lower = (g & (m >> 4)) == 0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const K o = KO::shfl_xor(x[i], m);
+      x[i] = KO::sel(KO::gt(x[i], o) == lower, x[i], o);
+    }
+  }
+#pragma unroll
+  for (int m = 8; m > 0; m >>= 1) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if (i & m) continue;
+      const int j = i | m;
+      const K a = x[i], b = x[j];
+      const bool sw = KO::gt(b, a);
+      x[i] = KO::sel(sw, b, a);
+      x[j] = KO::sel(sw, a, b);
+    }
+  }
+}
+
+// grid: 1-D, 8 * ceil(groups * n_chunks * n_bh / 8) work-groups of kBWaves
+// waves; work-group (bh, chunk, group) takes the 16-row blocks 4 * group ..
+// 4 * group + 3 of (sequence, head) bh, the longest causal rows first.
 template <int RK, int ST>
-__global__ __launch_bounds__(128) void score_mfma_kernel(
+__global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
     const uint8_t* __restrict__ index, int n_tiles, int N_valid, int Q,
     const int* __restrict__ q_pos, const float* __restrict__ q,
     const float* __restrict__ Bq, const float* __restrict__ mu, int H_q, int H_kv, int gq,
-    int n_bh, int row_blocks, int chunk, int n_chunks, int k, int* __restrict__ top_idx,
+    int n_bh, int groups, int chunk, int n_chunks, int k, int* __restrict__ top_idx,
     float* __restrict__ top_score, uint64_t* __restrict__ part) {
   constexpr int D = saki::kHeadDim;
   using KO = KeysF32;
+  using K = uint64_t;
   using Scorer = MfmaScorer<RK, ST>;
-  // per wave 12.1 KB, used in turn as: z staging [16][RK] floats; histogram
-  // [16][kHistRow] ints (pass 2); candidates [16][kSCandRow] (pass 3); or the
-  // fallback's score staging [16][64] floats + list and buffer of 8 rows
-  __shared__ uint64_t cand_mem[kMfmaWaves][kMR * kSCandRow];
-  __shared__ int ccount[kMfmaWaves][kMR];
+  __shared__ __align__(16) uint8_t lds_mem[kBWaves][kBWaveBytes];
   const int wave = threadIdx.x / kWave, lane = lane_id();
-  const int waves = blockDim.x / kWave;
-  const long long lb = xcd_logical_block((long long)row_blocks * n_chunks * n_bh);
+  const long long lb = xcd_logical_block((long long)groups * n_chunks * n_bh);
   if (lb < 0) return;
-  const int rb = (int)(lb % row_blocks), ch = (int)((lb / row_blocks) % n_chunks);
-  const size_t bh = (size_t)(lb / ((long long)row_blocks * n_chunks));
+  const int gb = groups - 1 - (int)(lb % groups);
+  const int ch = (int)((lb / groups) % n_chunks);
+  const size_t bh = (size_t)(lb / ((long long)groups * n_chunks));
   const int h = (int)(bh % H_q);
   const int gkv = h / (H_q / H_kv);
-  const int row0 = (rb * waves + wave) * kMR;
-  if (row0 >= Q) return;
+  const int row0 = (gb * kBWaves + wave) * kMR;
+  if (row0 >= Q) return;  // the waves never synchronise with each other
   const int qi = lane % 16, g = lane / 16;
   const int my_row = row0 + qi;
   const bool row_ok = my_row < Q;
-  const int my_lim = row_limit(my_row, Q, N_valid, q_pos);
+  const int my_lim = row_limit(my_row, Q, N_valid, q_pos);  // 0 for rows past Q
   const int kmax = wave_max_i(my_lim);
-  const int kmin = wave_min_i(row_ok ? my_lim : INT_MAX);
+  const int kmin = wave_min_i(my_lim);
   const int kbeg = ch * chunk;
   const int kend = min(kbeg + chunk, kmax);
-  uint64_t* cand = cand_mem[wave];
-  int* hist = reinterpret_cast<int*>(cand);
+  uint8_t* wl = lds_mem[wave];
 
   // ---- query sketch
   Scorer sc;
-  // the scorer's accumulators start at b, so that scores come out whole
   const float my_b = mfma_query_sketch<RK, ST>(q + (bh * Q + (row_ok ? my_row : row0)) * D, row_ok,
                                                Bq + (size_t)h * D * RK, mu + (size_t)gkv * D,
-                                               reinterpret_cast<float*>(cand), qi, g, sc);
-  sc.init = my_b;
-  // the head's code set: one per query head (gq = 1) or per group of gq heads
+                                               reinterpret_cast<float*>(wl), qi, g, sc);
+  sc.init = my_b;  // the accumulators start at b: scores come out whole
   const size_t code_set = (bh / H_q) * (H_q / gq) + h / gq;
   const uint8_t* hbase = index + code_set * n_tiles * Scorer::TB;
 
-  // ---- pass 1: moments of this lane's row over a sample of the chunk's
-  //      tiles (every stride-th tile, at least kSampleTiles of them)
-  const int n_row = row_ok ? max(0, min(my_lim, kend) - kbeg) : 0;
-  const int stride = max(1, (kend - kbeg) / (kTile * kSampleTiles));
-  float sum = 0.f, sumsq = 0.f, cnt = 0.f;
-  if (wave_max_i(n_row) > kSCollect) {
-    sc.for_tiles(hbase, kbeg, kend, stride * kTile, qi, g, [&](int t0, f32x4_t* acc) {
+  // keys past a row's limit score -inf (tiles crossing some row's limit only)
+  auto mask_tile = [&](int t0, f32x4_t* acc) {
+    if (t0 + kTile > kmin) {
 #pragma unroll
       for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const bool in = t0 + 16 * sub + 4 * g + v < my_lim;
-          const float x = in ? acc[sub][v] - my_b : 0.f;  // moments of z . c, not shifted by b
-          sum += x;
-          sumsq = fmaf(x, x, sumsq);
-          cnt += in ? 1.f : 0.f;
-        }
-    });
-    sum = sum_lane_groups(sum);
-    sumsq = sum_lane_groups(sumsq);
-    cnt = sum_lane_groups(cnt);
-  }
-  int mode = kModeAll;
-  float inv_w = 0.f, off = 0.f;
-  if (n_row > kSCollect) {
-    const float mean = sum / cnt;
-    const float var = fmaxf(sumsq / cnt - mean * mean, 0.f);
-    const float sd = sqrtf(var);
-    if (cnt > 0.f && sd > 0.f && isfinite(sd) && isfinite(mean)) {
-      // bins from kWinLo sd below to kWinHi sd above the predicted 64th score
-      const float t_hat = my_b + mean + sd * normal_upper_quantile((float)kList / (float)n_row);
-      const float lo = t_hat - kWinLo * sd;
-      inv_w = (float)(kBins - 2) / ((kWinLo + kWinHi) * sd);
-      off = 1.f - lo * inv_w;  // bin(s) = fmaf(s, inv_w, off): below 1 = out of range
-      mode = kModeHist;
+        for (int v = 0; v < 4; ++v)
+          if (t0 + 16 * sub + 4 * g + v >= my_lim) acc[sub][v] = -INFINITY;
+    }
+  };
+
+  // ---- pass A: block maxima of this lane's keys
+  const int n_row = max(0, min(my_lim, kend) - kbeg);
+  const int row_tiles = (n_row + kTile - 1) / kTile;
+  // entries of one lane per tile: 2, 4, 8 or 16 blocks of 8, 4, 2 or 1 keys
+  const int lane_ent = n_row >= 2048 ? 2 : n_row >= 1024 ? 4 : n_row >= 512 ? 8 : 16;
+  // row qi's entries and histogram bins have their 16-byte groups permuted
+  // (word offset xor 4 qi), so that the rows' accesses spread over the banks
+  uint32_t* ent = reinterpret_cast<uint32_t*>(wl) + qi * (kBEnt / 2);
+  const int sw = 4 * qi;
+  float bsum = 0.f, bsq = 0.f, bmax = -INFINITY, bmin = INFINITY, bcnt = 0.f;
+  auto stat = [&](float x) {  // x: a block maximum (-inf: no key of the row)
+    const bool ok = x != -INFINITY;
+    const float y = ok ? x : 0.f;
+    bcnt += ok ? 1.f : 0.f;
+    bsum += y;
+    bsq = fmaf(y, y, bsq);
+    bmax = fmaxf(bmax, x);
+    bmin = ok ? fminf(bmin, x) : bmin;
+  };
+  sc.for_tiles_deep(hbase, kbeg, kend, qi, g, [&](int t0, f32x4_t* acc) {
+    mask_tile(t0, acc);
+    const int tl = (t0 - kbeg) / kTile;
+    if (tl >= row_tiles) return;  // nothing of this row: no entries
+    float m2[8];  // maxima of the pairs (sub, v = 0..1), (sub, v = 2..3)
+#pragma unroll
+    for (int sub = 0; sub < 4; ++sub) {
+      m2[2 * sub] = fmaxf(acc[sub][0], acc[sub][1]);
+      m2[2 * sub + 1] = fmaxf(acc[sub][2], acc[sub][3]);
+    }
+    const int wo = (tl * 4 * lane_ent + g * lane_ent) / 2;  // this lane's first word
+    if (lane_ent == 2) {
+      const float a = fmaxf(fmaxf(m2[0], m2[1]), fmaxf(m2[2], m2[3]));
+      const float b = fmaxf(fmaxf(m2[4], m2[5]), fmaxf(m2[6], m2[7]));
+      ent[wo ^ sw] = ord16(a) | (ord16(b) << 16);
+      stat(a);
+      stat(b);
+    } else if (lane_ent == 4) {
+      uint32_t u[4];
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub) {
+        const float m4 = fmaxf(m2[2 * sub], m2[2 * sub + 1]);
+        u[sub] = ord16(m4);
+        stat(m4);
+      }
+      *reinterpret_cast<uint2*>(ent + (wo ^ sw)) = uint2{u[0] | (u[1] << 16), u[2] | (u[3] << 16)};
+    } else if (lane_ent == 8) {
+      uint32_t u[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        u[j] = ord16(m2[j]);
+        stat(m2[j]);
+      }
+      *reinterpret_cast<uint4*>(ent + (wo ^ sw)) =
+          uint4{u[0] | (u[1] << 16), u[2] | (u[3] << 16), u[4] | (u[5] << 16), u[6] | (u[7] << 16)};
     } else {
-      mode = kModeFallback;
-    }
-  }
-
-  // ---- pass 2: histogram of the rows in histogram mode
-  const bool any_hist = __ballot(mode == kModeHist) != 0;
-  float gate = -INFINITY;  // bin value (>= 1) a score must reach to be collected
-  if (any_hist) {
-    for (int i = lane; i < kMR * kHistRow; i += kWave) hist[i] = 0;
-    wave_lds_sync();
-    // every score adds to a bin; scores below the window, masked keys and rows
-    // not in histogram mode go to the lane's own slot (kBins + g), which no
-    // other lane touches and which is never read
-    const float x_hi = (float)(kBins - 1);
-    const int trash = kBins + g;
-    const bool hmode = mode == kModeHist;
-    sc.for_tiles(hbase, kbeg, kend, kTile, qi, g, [&](int t0, f32x4_t* acc) {
-      const bool need_mask = t0 + kTile > kmin;
+      uint32_t u[16];
 #pragma unroll
       for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const float x = fmaf(acc[sub][v], inv_w, off);
-          int bin = (int)fminf(x, x_hi);
-          bin = (hmode && x >= 1.f) ? bin : trash;
-          if (need_mask && t0 + 16 * sub + 4 * g + v >= my_lim) bin = trash;
-          atomicAdd(&hist[qi * kHistRow + bin], 1);
+          u[4 * sub + v] = ord16(acc[sub][v]);
+          stat(acc[sub][v]);
         }
-    });
-    wave_lds_sync();
-    // per row: the highest bin whose count from the top reaches 64
-    for (int r = 0; r < kMR; ++r) {
-      if (__builtin_amdgcn_readlane(mode, r) != kModeHist) continue;
-      int x = hist[r * kHistRow + (kBins - 1 - lane)];  // lane i: bin 63 - i
-      if (lane == kBins - 1) x = 0;                  // bin 0 is never counted
-#pragma unroll
-      for (int d = 1; d < kWave; d <<= 1) {
-        const int t = __shfl_up(x, d, kWave);
-        if (lane >= d) x += t;
-      }
-      const uint64_t reach = __ballot(x >= kList);
-      int new_mode = kModeHist;
-      float bstar = 0.f;
-      if (reach == 0) {
-        new_mode = kModeFallback;
-      } else {
-        const int l = __builtin_ctzll(reach);
-        if (__builtin_amdgcn_readlane(x, l) > kSCollect) new_mode = kModeFallback;
-        bstar = (float)(kBins - 1 - l);
-      }
-      if (qi == r) {
-        mode = new_mode;
-        gate = bstar;
-      }
+      *reinterpret_cast<uint4*>(ent + (wo ^ sw)) =
+          uint4{u[0] | (u[1] << 16), u[2] | (u[3] << 16), u[4] | (u[5] << 16), u[6] | (u[7] << 16)};
+      *reinterpret_cast<uint4*>(ent + ((wo + 4) ^ sw)) = uint4{u[8] | (u[9] << 16), u[10] | (u[11] << 16),
+                                                             u[12] | (u[13] << 16), u[14] | (u[15] << 16)};
+    }
+  });
+  wave_lds_sync();
+
+  // ---- threshold per row
+  bsum = sum_lane_groups(bsum);
+  bsq = sum_lane_groups(bsq);
+  bcnt = sum_lane_groups(bcnt);
+  bmax = fmaxf(bmax, xor_shfl_f32(bmax, 16));
+  bmax = fmaxf(bmax, xor_shfl_f32(bmax, 32));
+  bmin = fminf(bmin, xor_shfl_f32(bmin, 16));
+  bmin = fminf(bmin, xor_shfl_f32(bmin, 32));
+  const int n_ent = row_tiles * 4 * lane_ent;
+  float tau = -FLT_MAX;  // rows with fewer than 64 blocks keep every key
+  bool done = bcnt < (float)kList;
+  float lo = 0.f, hi = 0.f;
+  if (!done) {
+    const float mean = bsum / bcnt;
+    const float sd = sqrtf(fmaxf(bsq / bcnt - mean * mean, 0.f));
+    const float tail = (float)kList / bcnt;  // in (0, 1]
+    const float zq = tail <= 0.5f ? normal_upper_quantile(tail)
+                                  : (tail < 1.f ? -normal_upper_quantile(1.f - tail) : -4.f);
+    const float pred = mean + sd * zq;  // predicted 64th largest maximum
+    lo = fmaxf(pred - 1.5f * sd, bmin);
+    hi = fminf(pred + 0.5f * sd, bmax);
+    if (!(hi > lo)) {  // all maxima (nearly) equal
+      tau = bmin;
+      done = true;
     }
   }
-
-  if (__ballot(mode == kModeFallback) == 0) {
-    // ---- pass 3: collect the gated candidates; the four lanes of a row
-    //      (lane groups g) append at offsets from a prefix of their counts
-    int base = 0;  // the row's entries so far (same in its four lanes)
-    wave_lds_sync();  // the histogram's reads are done: its space takes candidates
-    sc.for_tiles(hbase, kbeg, kend, kTile, qi, g, [&](int t0, f32x4_t* acc) {
-      // the same bin test as the histogram (rows that collect everything have
-      // inv_w = off = 0 and gate = -inf)
-      uint32_t take = 0;
+  uint32_t* hist = reinterpret_cast<uint32_t*>(wl + kMR * kBEnt * 2) + qi * kBBins;  // bin b at word b ^ sw
+  for (int round = 0; __ballot(!done) != 0; ++round) {
 #pragma unroll
-      for (int sub = 0; sub < 4; ++sub)
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          take |= (fmaf(acc[sub][v], inv_w, off) >= gate) ? (1u << (4 * sub + v)) : 0u;
-      if (t0 + kTile > kmin) {  // a tile crossing some row's causal limit
-#pragma unroll
-        for (int sub = 0; sub < 4; ++sub)
-#pragma unroll
-          for (int v = 0; v < 4; ++v)
-            if (t0 + 16 * sub + 4 * g + v >= my_lim) take &= ~(1u << (4 * sub + v));
-      }
-      if (__ballot(take != 0) == 0) return;
-      const int c = __popc(take);
-      const int c1 = (int)xor_shfl_u32((uint32_t)c, 16);   // count of lane group g ^ 1
-      const int c2 = (int)xor_shfl_u32((uint32_t)c, 32);   // g ^ 2
-      const int c3 = (int)xor_shfl_u32((uint32_t)c1, 32);  // g ^ 3
-      // entries of the groups below g: g=1: group 0 = g^1; g=2: groups 0, 1 =
-      // g^2, g^3; g=3: groups 0, 1, 2 = g^3, g^2, g^1
-      int pos = base + (g == 1 ? c1 : g == 2 ? c2 + c3 : g == 3 ? c1 + c2 + c3 : 0);
-      base += c + c1 + c2 + c3;
-#pragma unroll
-      for (int sub = 0; sub < 4; ++sub)
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          if (take & (1u << (4 * sub + v))) {
-            if (pos < kSCollect)
-              cand[qi * kSCandRow + pos] = KO::make(acc[sub][v], t0 + 16 * sub + 4 * g + v);
-            ++pos;
-          }
-    });
-    if (lane < kMR) ccount[wave][lane] = base;  // lane r < 16 is row r, group 0
+    for (int u = 0; u < 4; ++u)
+      *reinterpret_cast<uint4*>(hist + ((16 * g + 4 * u) ^ sw)) = uint4{0u, 0u, 0u, 0u};
     wave_lds_sync();
-    for (int r = 0; r < kMR; ++r) {
-      const int i = row0 + r;
-      if (i >= Q) break;
-      const int c = min(ccount[wave][r], kSCollect);
-      uint64_t a = lane < c ? cand[r * kSCandRow + lane] : KO::pad();
-      wave_sort<KO>(a);
-      if (c > kList) {
-        uint64_t b2 = lane + kList < c ? cand[r * kSCandRow + kList + lane] : KO::pad();
-        wave_sort<KO>(b2);
-        wave_merge<KO>(a, b2);
+    const float inv_w = (float)(kBBins - 1) / (hi - lo);  // bins 0..62 over [lo, hi), 63 above
+    if (!done) {
+      for (int e0 = 8 * g; e0 < n_ent; e0 += 32) {  // this lane's quarter of the row's entries
+        const uint4 w = *reinterpret_cast<const uint4*>(ent + ((e0 / 2) ^ sw));
+        const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const uint32_t v = (ww[u / 2] >> (16 * (u % 2))) & 0xffffu;
+          const float x = (unord16(v) - lo) * inv_w;
+          if (v != 0u && x >= 0.f) atomicAdd(&hist[(int)fminf(x, (float)(kBBins - 1)) ^ sw], 1u);
+        }
       }
+    }
+    wave_lds_sync();
+    // bins 16 g .. 16 g + 15 of this lane's row: counts from the top
+    uint32_t c[16];
+    {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint4 t = *reinterpret_cast<const uint4*>(hist + ((16 * g + 4 * u) ^ sw));
+        c[4 * u] = t.x;
+        c[4 * u + 1] = t.y;
+        c[4 * u + 2] = t.z;
+        c[4 * u + 3] = t.w;
+      }
+    }
+    uint32_t run = 0;
+#pragma unroll
+    for (int i = 15; i >= 0; --i) {
+      run += c[i];
+      c[i] = run;
+    }
+    const uint32_t t1 = xor_shfl_u32(run, 16), t2 = xor_shfl_u32(run, 32), t3 = xor_shfl_u32(t1, 32);
+    // totals of the lane groups above g (groups g ^ 1, g ^ 2, g ^ 3 hold t1, t2, t3)
+    const uint32_t above = g == 0 ? t1 + t2 + t3 : g == 1 ? t2 + t3 : g == 2 ? t1 : 0u;
+    int n_ge = 0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) n_ge += (c[i] + above >= (uint32_t)kList) ? 1 : 0;
+    int b = n_ge > 0 ? 16 * g + n_ge - 1 : -1;
+    b = max(b, (int)xor_shfl_u32((uint32_t)b, 16));
+    b = max(b, (int)xor_shfl_u32((uint32_t)b, 32));
+    if (!done) {
+      const float w = (hi - lo) / (float)(kBBins - 1);
+      if (round >= 3) {  // no usable window: keep every key (the count check decides)
+        done = true;
+      } else if (b < 0) {  // the 64th largest maximum lies below the window
+        hi = lo;
+        lo = bmin;
+        done = !(hi > lo);
+      } else if (b == kBBins - 1 && hi < bmax) {  // or above it
+        lo = hi;
+        hi = bmax;
+      } else {
+        // one bin lower than the crossing: rounding in the bin index never
+        // puts a maximum below tau
+        tau = lo + (float)(b - 1) * w;
+        done = true;
+      }
+    }
+    wave_lds_sync();
+  }
+
+  // ---- pass B: candidates, every key scoring >= tau
+  // slots hold (score bits, key) as they are found (slot j of every lane in
+  // one 512-byte row, so that the lanes' writes spread over the banks);
+  // ordered keys are formed when they are sorted
+  uint2* cand = reinterpret_cast<uint2*>(wl) + lane;
+  int cnt = 0;
+  sc.for_tiles_deep(hbase, kbeg, kend, qi, g, [&](int t0, f32x4_t* acc) {
+    mask_tile(t0, acc);
+    const int kb = t0 + 4 * g;
+#pragma unroll
+    for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (acc[sub][v] >= tau) {
+          cand[min(cnt, kBSlots - 1) * kWave] = uint2{__float_as_uint(acc[sub][v]), (uint32_t)(kb + 16 * sub + v)};
+          ++cnt;
+        }
+  });
+
+  // the row's candidates: at least 64 unless every key of the row is one
+  int row_cnt = cnt + (int)xor_shfl_u32((uint32_t)cnt, 16);
+  row_cnt += (int)xor_shfl_u32((uint32_t)row_cnt, 32);
+  const bool short_row = tau > -FLT_MAX && row_cnt < kList;
+  if (__ballot(cnt > kBSlots || short_row) == 0) {
+    // ---- sort the candidates, keep the best 64
+    wave_lds_sync();
+    auto slot = [&](int j) {
+      const uint2 c = cand[min(j, kBSlots - 1) * kWave];
+      return j < min(cnt, kBSlots) ? KO::make(__uint_as_float(c.x), (int)c.y) : KO::pad();
+    };
+    K x[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) x[i] = slot(i);
+    sort64_x16<KO>(x, g);
+    // the slots past the first 16 of each lane, 16 at a time
+#pragma unroll 1
+    for (int set = 1; 16 * set < kBSlots && __ballot(cnt > 16 * set) != 0; ++set) {
+      K y[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) y[i] = slot(16 * set + i);
+      sort64_x16<KO>(y, g);
+      merge64_x16<KO>(x, y, g);
+    }
+    if (row_ok) {
+      const size_t rw = bh * Q + my_row;
       if (n_chunks == 1) {
-        if (lane < k) {
-          const size_t o = (bh * Q + i) * k + lane;
-          top_idx[o] = out_index<KO>(a);
-          if (top_score) top_score[o] = KO::score(a);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int e = 16 * g + i;
+          if (e < k) {
+            top_idx[rw * k + e] = out_index<KO>(x[i]);
+            if (top_score) top_score[rw * k + e] = KO::score(x[i]);
+          }
         }
       } else {
-        part[((bh * Q + i) * n_chunks + ch) * kMaxK + lane] = a;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) part[(rw * n_chunks + ch) * kMaxK + 16 * g + i] = x[i];
       }
     }
     return;
   }
 
-  // ---- fallback: online selection over the chunk (rare), in two halves of
-  //      8 rows so that the lists fit the wave's LDS
-  float* stage = reinterpret_cast<float*>(cand);  // [16][64], key column swizzled
+  // ---- fallback: online selection over the chunk, in two halves of 8 rows
+  wave_lds_sync();
+  float* stage = reinterpret_cast<float*>(wl);  // [16][64], key column swizzled
+  K* lists = reinterpret_cast<K*>(wl + kMR * kTile * 4);
   constexpr int kHalf = kMR / 2;
   for (int half = 0; half < 2; ++half) {
     RowLists<KO, kHalf> top;
-    top.init(cand + kMR * kTile / 2, cand + kMR * kTile / 2 + kHalf * kList);
+    top.init(lists, lists + kHalf * kList);
     sc.for_tiles(hbase, kbeg, kend, kTile, qi, g, [&](int t0, f32x4_t* acc) {
 #pragma unroll
       for (int sub = 0; sub < 4; ++sub) {
@@ -1113,15 +1283,15 @@ __global__ __launch_bounds__(128) void score_mfma_kernel(
       top.finish(rr);
       const int i = row0 + kHalf * half + rr;
       if (i >= Q) continue;
-      const uint64_t e = top.entry(rr);
+      const K e = top.entry(rr);
+      const size_t rw = bh * Q + i;
       if (n_chunks == 1) {
         if (lane < k) {
-          const size_t o = (bh * Q + i) * k + lane;
-          top_idx[o] = out_index<KO>(e);
-          if (top_score) top_score[o] = KO::score(e);
+          top_idx[rw * k + lane] = out_index<KO>(e);
+          if (top_score) top_score[rw * k + lane] = KO::score(e);
         }
       } else {
-        part[((bh * Q + i) * n_chunks + ch) * kMaxK + lane] = e;
+        part[(rw * n_chunks + ch) * kMaxK + lane] = e;
       }
     }
     wave_lds_sync();
@@ -1462,7 +1632,8 @@ __global__ __launch_bounds__(256) void exact_stream_kernel(
 
 // Exact float64 scores on the f64 MFMA (16x16x4).  Lane group g feeds dims
 // 32g .. 32g+31 of its key and query, one per k-step.  The f64 MFMA returns
-// D[g + 4v][lane % 16] in register v.  grid and block as for score_mfma_kernel.
+// D[g + 4v][lane % 16] in register v.  grid (row_blocks * n_chunks, B*H_q) via
+// xcd_grid, two waves of 16 rows per work-group.
 template <bool KBF>
 __global__ __launch_bounds__(128) void exact_mfma_kernel(
     const void* __restrict__ keys, const float* __restrict__ q,
@@ -1607,14 +1778,14 @@ __global__ __launch_bounds__(256) void keys_hi_kernel(const void* __restrict__ k
 // a3 = q_h.k_h + q_h.k_l + q_l.k_h miss q.k by the dropped terms (at most about
 // 3 * 2^-16 sum|q_i k_i|) plus float32 accumulation (at most 384 * 2^-24 of the
 // same sum), so |a3 - q.k| <= E = kExactEps3 * ||q|| ||k|| with 40% margin.
-// The three passes of score_mfma_kernel run on these intervals: moments of the
+// Three passes run on these intervals: moments of the
 // single product q_h.k_h (only a prediction), a histogram of the lower bounds
 // a3 - E, and a gate on the upper bounds a3 + E at the bin where the
 // lower-bound count reaches 64: every key whose exact score can reach the 64th
 // exact score passes it.  Gated keys are rescored in float64 (float32 inputs,
 // so every product is exact) and sorted.  A wave whose rows miss the
 // prediction or gate more than 128 keys is flagged and redone by
-// exact_mfma_kernel.  grid/block as score_mfma_kernel.
+// exact_mfma_kernel.  grid/block as exact_mfma_kernel.
 constexpr float kExactEps3 = 1e-4f;
 
 template <bool KBF>
@@ -2996,9 +3167,9 @@ void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int index_head
   dim3 block(kWave * p.waves);
   const int nt = (int)saki::n_tiles(N_cap);
   if (p.mfma)
-    hipLaunchKernelGGL((score_mfma_kernel<RK, ST>), xcd_grid(p, B * H_q), block, 0, s, index,
-                       nt, N_valid, Q, q_pos, q, Bq, mu, H_q, H_kv, gq, B * H_q, p.row_blocks,
-                       p.chunk, p.n_chunks, k, top_idx, top_score, part);
+    hipLaunchKernelGGL((score_batch_kernel<RK, ST>), xcd_grid(p, B * H_q), dim3(kBWaves * kWave), 0,
+                       s, index, nt, N_valid, Q, q_pos, q, Bq, mu, H_q, H_kv, gq, B * H_q,
+                       p.row_blocks, p.chunk, p.n_chunks, k, top_idx, top_score, part);
   else if (p.rows == 4)
     hipLaunchKernelGGL((score_stream_kernel<RK, ST, 4>), grid, block, 0, s, index, nt, N_valid,
                        Q, q_pos, q, Bq, mu, H_q, H_kv, gq, p.row_blocks, p.chunk, p.n_chunks,
