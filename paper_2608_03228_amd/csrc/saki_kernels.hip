@@ -42,6 +42,12 @@ using saki::kMaxK;
 using saki::kTile;
 using namespace saki_dev;
 
+// MFMA operand and accumulator vectors
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+
 constexpr int kStreamWaves = 4;  // waves per workgroup, streaming kernels
 constexpr int kMfmaWaves = 2;    // waves per workgroup, MFMA kernels
 constexpr int kMR = 16;          // query rows per wave on the MFMA kernels
@@ -194,95 +200,119 @@ __device__ __forceinline__ int row_hits(int ej, const int* __restrict__ approx, 
 
 // ---------------------------------------------------------------- build index
 
-// grid (tiles, H_q, B), block 256.  One tile of 64 keys per workgroup.
+// Key codes c_j = B_k^T (k_j - mu) on the float32 MFMA (16x16x4).  A
+// work-group takes up to 1,024 keys of one KV head (16-key groups, 8 per
+// wave) and computes their codes for every query head of the group,
+// so each key is read once (a short range, a decode append, takes one query
+// head per work-group instead, so that the heads' factors load in parallel).
+// For a group of 16 keys and a block of 16 code dimensions the MFMA forms
+// D[m][key] = sum_c B_k[c][m] (k - mu)[key][c] in 32 steps of 4 dimensions;
+// the dimensions are taken in the order in which each lane's float4 loads
+// hold them (lane (key qi, group kg) loads dims 16 s + 4 kg .. + 3 of its key,
+// which are step 4 s + j's dimension 16 s + 4 kg + j), so the keys go from
+// registers straight into the B operand.  B_k of up to
+// kBuildLdsFloats / (128 (r + 4)) heads
+// at a time sits in LDS with rows of r + 4 floats (the four dimension groups of
+// a step start 0 and 16 banks apart).  Lane (qi, kg) ends with dims
+// m0 + 4 kg .. + 3 of key qi: one 16-byte float32 piece, half a bf16 piece or
+// a quarter of an fp8 piece.  Centring is float32 (k - mu) before the
+// product, as the paper writes it.
+constexpr int kBuildKeys = 1024;        // keys per work-group
+constexpr int kBuildSplitKeys = 256;    // ranges up to this many keys: one query head per work-group
+constexpr int kBuildLdsFloats = 18432;  // 72 KiB: B_k of up to 4 heads at r = 32
+template <int RK>
+constexpr int build_heads_lds() { return kBuildLdsFloats / (saki::kHeadDim * (RK + 4)); }
+
+// grid (ceil(keys / kBuildKeys), H_kv or H_q (per_head), B), block 64 *
+// kBuildWaves; keys [k0, n_end) with k0 = n_begin rounded down to 16.
+constexpr int kBuildWaves = 8;
 template <int RK, bool KBF, int ST>
-__global__ __launch_bounds__(256) void build_index_kernel(
+__global__ __launch_bounds__(kBuildWaves * kWave) void build_index_kernel(
     const void* __restrict__ keys, const float* __restrict__ Bk,
     const float* __restrict__ mu, int H_q, int H_kv, int N_cap, int n_tiles,
-    uint8_t* __restrict__ index, int n_begin, int n_end, int tile0) {
+    uint8_t* __restrict__ index, int n_begin, int n_end, int per_head) {
   constexpr int D = saki::kHeadDim;
   constexpr int ES = code_bytes<ST>();
-  constexpr int CPP = saki::kChunkBytes / ES;  // code elements per piece
-  constexpr int NP = RK / CPP;                 // pieces per key
-  __shared__ float ks[kTile][D + 1];
-  __shared__ float bk[D][RK];
-  const int tile = tile0 + blockIdx.x;
-  const int h = blockIdx.y, b = blockIdx.z;
-  const int g = h / (H_q / H_kv);
-  const int tid = threadIdx.x;
+  constexpr int RS = RK + 4;  // LDS row stride of B_k (floats)
+  constexpr int HB = build_heads_lds<RK>();
+  static_assert(HB >= 1, "one head of B_k fits");
+  constexpr size_t TB = (size_t)kTile * RK * ES;  // bytes of one 64-key tile
+  constexpr int NM = RK / 16;
+  __shared__ float bks[HB * D * RS];
+  const int G = H_q / H_kv;
+  const int g = per_head ? (int)blockIdx.y / G : (int)blockIdx.y, b = blockIdx.z;
+  const int h_first = per_head ? (int)blockIdx.y : g * G;  // query heads [h_first, h_end)
+  const int h_end = per_head ? h_first + 1 : h_first + G;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int qi = lane % 16, kg = lane / 16;
+  const int k0 = (n_begin / 16) * 16 + blockIdx.x * kBuildKeys;
   const size_t key_base = ((size_t)b * H_kv + g) * N_cap;
-  // stage the centred keys of the tile and B_k with every load issued before
-  // the LDS stores (a one-key append is then one load latency, not dozens);
-  // rows outside [n_begin, n_end) are not written out and stage as zeros.
-  // Thread tid takes dims c .. c + 3 of rows tid / 32 + 8u, and four
-  // consecutive elements of B_k per group.
-  constexpr int KG = kTile * D / 4 / 256;
-  constexpr int BG = D * RK / 4 / 256;
-  static_assert(KG * 1024 == kTile * D && BG * 1024 == D * RK, "staging shape");
-  const int c = (tid * 4) % D;
-  float4 kv[KG], bv[BG];
+  float4 m4[8];  // mu at this lane's dims 16 s + 4 kg .. + 3
 #pragma unroll
-  for (int u = 0; u < KG; ++u) {
-    const int n = tile * kTile + (tid * 4 + u * 1024) / D;
-    kv[u] = n >= n_begin && n < n_end ? load_key4<KBF>(keys, (key_base + n) * D + c)
-                                      : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
+  for (int s = 0; s < 8; ++s)
+    m4[s] = *reinterpret_cast<const float4*>(mu + (size_t)g * D + 16 * s + 4 * kg);
+  // (k - mu) of key n at dims 16 s + 4 kg + j, step t = 4 s + j (zero outside the range)
+  auto load_keys = [&](int n, bool ok, float* kf) {
 #pragma unroll
-  for (int u = 0; u < BG; ++u)
-    bv[u] = *reinterpret_cast<const float4*>(Bk + (size_t)h * D * RK + (size_t)tid * 4 + u * 1024);
-  const float4 m4 = *reinterpret_cast<const float4*>(mu + (size_t)g * D + c);
-#pragma unroll
-  for (int u = 0; u < KG; ++u) {
-    const int t = (tid * 4 + u * 1024) / D;
-    const int n = tile * kTile + t;
-    const bool in = n >= n_begin && n < n_end;
-    ks[t][c] = in ? kv[u].x - m4.x : 0.f;
-    ks[t][c + 1] = in ? kv[u].y - m4.y : 0.f;
-    ks[t][c + 2] = in ? kv[u].z - m4.z : 0.f;
-    ks[t][c + 3] = in ? kv[u].w - m4.w : 0.f;
-  }
-#pragma unroll
-  for (int u = 0; u < BG; ++u) {
-    const int e = tid * 4 + u * 1024;
-    bk[e / RK][e % RK] = bv[u].x;
-    bk[e / RK][e % RK + 1] = bv[u].y;
-    bk[e / RK][e % RK + 2] = bv[u].z;
-    bk[e / RK][e % RK + 3] = bv[u].w;
-  }
-  __syncthreads();
-  uint8_t* tbase = index + (((size_t)b * H_q + h) * n_tiles + tile) * ((size_t)kTile * RK * ES);
-  for (int p = tid; p < kTile * NP; p += 256) {
-    const int t = p % kTile, piece = p / kTile;
-    const int n = tile * kTile + t;
-    float acc[CPP];
-#pragma unroll
-    for (int e = 0; e < CPP; ++e) acc[e] = 0.f;
-    for (int c = 0; c < D; ++c) {
-      const float kv = ks[t][c];
-#pragma unroll
-      for (int e = 0; e < CPP; ++e) acc[e] = fmaf(kv, bk[c][piece * CPP + e], acc[e]);
+    for (int s = 0; s < 8; ++s) {
+      const float4 kv = ok ? load_key4<KBF>(keys, (key_base + n) * D + 16 * s + 4 * kg)
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+      kf[4 * s] = ok ? kv.x - m4[s].x : 0.f;
+      kf[4 * s + 1] = ok ? kv.y - m4[s].y : 0.f;
+      kf[4 * s + 2] = ok ? kv.z - m4[s].z : 0.f;
+      kf[4 * s + 3] = ok ? kv.w - m4[s].w : 0.f;
     }
-    if (n >= n_begin && n < n_end) {
-      uint4 out;
-      if constexpr (ST == kStFp8) {
-        uint32_t wv[4];
+  };
+  auto store = [&](int n, int h, const f32x4_t* acc) {
+    uint8_t* tb = index + (((size_t)b * H_q + h) * n_tiles + n / kTile) * TB;
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          wv[e] = e4m3_bits(acc[4 * e]) | (e4m3_bits(acc[4 * e + 1]) << 8) |
-                  (e4m3_bits(acc[4 * e + 2]) << 16) | (e4m3_bits(acc[4 * e + 3]) << 24);
-        out = uint4{wv[0], wv[1], wv[2], wv[3]};
+    for (int mc = 0; mc < NM; ++mc) {
+      const int m = 16 * mc + 4 * kg;  // first code dim of this lane
+      uint8_t* dst = tb + (size_t)(m * ES / 16) * kTile * 16 + (size_t)(n % kTile) * 16 + (m * ES) % 16;
+      const f32x4_t v = acc[mc];
+      if constexpr (ST == kStFp8) {
+        *reinterpret_cast<uint32_t*>(dst) = e4m3_bits(v[0]) | (e4m3_bits(v[1]) << 8) |
+                                            (e4m3_bits(v[2]) << 16) | (e4m3_bits(v[3]) << 24);
       } else if constexpr (ST == kStBf16) {
-        out.x = bf16_bits(acc[0]) | (bf16_bits(acc[1]) << 16);
-        out.y = bf16_bits(acc[2]) | (bf16_bits(acc[3]) << 16);
-        out.z = bf16_bits(acc[4]) | (bf16_bits(acc[5]) << 16);
-        out.w = bf16_bits(acc[6]) | (bf16_bits(acc[7]) << 16);
+        *reinterpret_cast<uint2*>(dst) =
+            uint2{bf16_bits(v[0]) | (bf16_bits(v[1]) << 16), bf16_bits(v[2]) | (bf16_bits(v[3]) << 16)};
       } else {
-        out.x = __float_as_uint(acc[0]);
-        out.y = __float_as_uint(acc[1]);
-        out.z = __float_as_uint(acc[2]);
-        out.w = __float_as_uint(acc[3]);
+        *reinterpret_cast<uint4*>(dst) = uint4{__float_as_uint(v[0]), __float_as_uint(v[1]),
+                                               __float_as_uint(v[2]), __float_as_uint(v[3])};
       }
-      *reinterpret_cast<uint4*>(tbase + (size_t)piece * kTile * 16 + (size_t)t * 16) = out;
+    }
+  };
+  for (int h0 = h_first; h0 < h_end; h0 += HB) {
+    const int nh = min(HB, h_end - h0);
+    __syncthreads();  // the previous heads' reads are done
+    for (int e = tid * 4; e < nh * D * RK; e += kBuildWaves * kWave * 4) {
+      const float4 v = *reinterpret_cast<const float4*>(Bk + (size_t)h0 * D * RK + e);
+      const int hh = e / (D * RK), c = (e / RK) % D, m = e % RK;
+      *reinterpret_cast<float4*>(&bks[(hh * D + c) * RS + m]) = v;
+    }
+    __syncthreads();
+    for (int grp = wave; grp < kBuildKeys / 16; grp += kBuildWaves) {
+      const int n0 = k0 + 16 * grp;
+      if (n0 >= n_end) break;  // wave-uniform
+      const int n = n0 + qi;
+      const bool ok = n >= n_begin && n < n_end;
+      float kf[32];
+      load_keys(n, ok, kf);
+      for (int hh = 0; hh < nh; ++hh) {
+        const float* bh = &bks[hh * D * RS];
+        f32x4_t acc[NM];
+#pragma unroll
+        for (int mc = 0; mc < NM; ++mc) acc[mc] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int st = 0; st < 32; ++st) {
+          const int c = 16 * (st / 4) + 4 * kg + st % 4;
+#pragma unroll
+          for (int mc = 0; mc < NM; ++mc)
+            acc[mc] = __builtin_amdgcn_mfma_f32_16x16x4f32(bh[c * RS + 16 * mc + qi], kf[st], acc[mc],
+                                                           0, 0, 0);
+        }
+        if (ok) store(n, h0 + hh, acc);
+      }
     }
   }
 }
@@ -577,10 +607,6 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
 // batched kernel (score_batch_kernel), the one-pass kernel for long rows
 // (score_scan_kernel) and the exact-recall kernels.
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef short i16x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
   bf16x8_t r;
@@ -3055,12 +3081,12 @@ template <int RK, bool KBF, int ST>
 void launch_build(const void* keys, const float* Bk, const float* mu, int B, int H_q,
                   int H_kv, int N_cap, uint8_t* index, int n_begin, int n_end,
                   hipStream_t s) {
-  const int t0 = n_begin / kTile;
-  const int t1 = (n_end + kTile - 1) / kTile;
-  dim3 grid(t1 - t0, H_q, B);
-  hipLaunchKernelGGL((build_index_kernel<RK, KBF, ST>), grid, dim3(256), 0, s, keys, Bk,
-                     mu, H_q, H_kv, N_cap, (int)saki::n_tiles(N_cap), index, n_begin,
-                     n_end, t0);
+  const int k0 = (n_begin / 16) * 16;
+  const int groups = (n_end - k0 + kBuildKeys - 1) / kBuildKeys;
+  const int per_head = n_end - n_begin <= kBuildSplitKeys ? 1 : 0;
+  dim3 grid(groups, per_head ? H_q : H_kv, B);
+  hipLaunchKernelGGL((build_index_kernel<RK, KBF, ST>), grid, dim3(kBuildWaves * kWave), 0, s, keys, Bk, mu, H_q,
+                     H_kv, N_cap, (int)saki::n_tiles(N_cap), index, n_begin, n_end, per_head);
 }
 
 // Work-groups of `kernel` (block `threads`) resident on the whole current
