@@ -206,7 +206,11 @@ int saki_build_index(const void* keys, int key_dtype, int B, int H_q, int H_kv,
 int saki_index_export(const void* index, int sketch_dtype, int B, int H_q,
                       int N_cap, int r, float* out, void* stream);
 
-/* Workspace for saki_score_topk with these sizes (bytes; 0 on bad arguments). */
+/* Workspace for saki_score_topk with these sizes (bytes; 0 on bad arguments):
+ * the partial lists of a split key axis and, for Q >= 16 with N_valid below
+ * 16,384 (the two-pass kernel), the query sketches z (r bf16 values per row,
+ * r floats for float32 codes) and b (one float per row) of all B * H_q * Q
+ * rows, formed by one kernel before the scoring kernel reads them. */
 size_t saki_score_topk_workspace_bytes(int B, int H_q, int index_heads, int Q, int N_valid,
                                        int r, int k, int sketch_dtype);
 
@@ -241,8 +245,8 @@ int saki_score_topk(const void* index, int sketch_dtype, int B, int H_q, int H_k
  * saki_score_topk_noalloc (GPU) -- for callers that cannot allocate device
  * memory (code under HIP graph capture, tight serving loops, harnesses that
  * forbid hipMalloc).  Same arguments, kernels and results as saki_score_topk,
- * without the workspace: the split-key partial lists, chunk gates and redo
- * flags live in a static device array of saki_noalloc_scratch_bytes()
+ * without the workspace: the split-key partial lists, chunk gates, redo
+ * flags and query sketches live in a static device array of saki_noalloc_scratch_bytes()
  * (32 MiB) that each GPU the library runs on holds until the process ends.
  * Nothing is allocated.  Returns SAKI_ERR_WORKSPACE when the call needs
  * more (saki_score_topk_workspace_bytes(...) > saki_noalloc_scratch_bytes()),

@@ -1611,7 +1611,7 @@ size_t saki_score_topk_workspace_bytes(int B, int H_q, int index_heads, int Q, i
       N_valid < 0 || !saki::rank_supported(r) || k < 1 || k > saki::kMaxK ||
       (sketch_dtype != SAKI_F32 && sketch_dtype != SAKI_BF16 && sketch_dtype != SAKI_FP8))
     return 0;
-  return saki::score_plan(B, H_q, index_heads, Q, N_valid).ws_bytes;
+  return saki::score_plan(B, H_q, index_heads, Q, N_valid, r, sketch_dtype).ws_bytes;
 }
 
 size_t saki_recall_workspace_bytes(int B, int H_q, int H_kv, int Q, int N_valid, int d, int k) {

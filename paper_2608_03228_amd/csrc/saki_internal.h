@@ -85,11 +85,14 @@ inline Plan make_plan(int B, int heads, int Q, int N_valid, int part_entry_bytes
 
 // Score path: the workspace holds the partial lists of a split key axis
 // (float score + int index), at least 256 bytes so that a size of 0 keeps
-// meaning invalid arguments.  Every kernel forms the query sketch itself.
-// The MFMA kernels take 16 queries of one head per wave (the one-pass kernel
-// when the rows are long); the streaming kernel takes the rows of one code
-// set: the H_q / index_heads heads sharing it, times Q.
-inline Plan score_plan(int B, int H_q, int index_heads, int Q, int N_valid) {
+// meaning invalid arguments.  The MFMA kernels take 16 queries of one head per
+// wave (the one-pass kernel when the rows are long); the streaming kernel
+// takes the rows of one code set: the H_q / index_heads heads sharing it,
+// times Q.  The two-pass MFMA kernel reads the query sketches z (r values per
+// row: bf16 for bf16 and fp8 codes (dtype 1, 2), float32 for float32 codes)
+// at z_off and b = q . mu (one float per row) at b_off, written by a kernel
+// before it; the other kernels form the sketch themselves.
+inline Plan score_plan(int B, int H_q, int index_heads, int Q, int N_valid, int r, int dtype) {
   const bool mfma = Q >= 16;
   Plan p = mfma ? make_plan(B, H_q, Q, N_valid, 8, true)
                 : make_plan(B, index_heads, (H_q / index_heads) * Q, N_valid, 8, false);
@@ -113,8 +116,11 @@ inline Plan score_plan(int B, int H_q, int index_heads, int Q, int N_valid) {
       p.chunk = kBatchMaxChunk;
       p.n_chunks = (int)((n + kBatchMaxChunk - 1) / kBatchMaxChunk);
     }
+    const size_t rows_total = (size_t)B * H_q * Q;
     p.part_off = 0;
-    p.ws_bytes = p.n_chunks > 1 ? round_up((size_t)B * H_q * Q * p.n_chunks * kMaxK * 8, 256) : 0;
+    p.z_off = p.n_chunks > 1 ? round_up(rows_total * p.n_chunks * kMaxK * 8, 256) : 0;
+    p.b_off = round_up(p.z_off + rows_total * r * (dtype == 0 ? 4 : 2), 256);
+    p.ws_bytes = round_up(p.b_off + rows_total * sizeof(float), 256);
   }
   const int wave_rows = (int)((H_q / index_heads) * (size_t)Q + p.rows - 1) / p.rows;
   if (!mfma && wave_rows < 4) {  // too few rows to fill a workgroup: its waves split the keys

@@ -166,16 +166,24 @@ __device__ __forceinline__ long long xcd_logical_block(long long total) {
   return logical < total ? logical : -1;
 }
 
+// Wave-wide max / min, returned in a scalar register (every lane holds the
+// same value after the butterfly), so that what is derived from it stays on
+// the scalar unit.
 __device__ __forceinline__ int wave_max_i(int v) {
 #pragma unroll
   for (int m = kWave / 2; m > 0; m >>= 1) v = max(v, __shfl_xor(v, m, kWave));
-  return v;
+  return __builtin_amdgcn_readfirstlane(v);
 }
 __device__ __forceinline__ int wave_min_i(int v) {
 #pragma unroll
   for (int m = kWave / 2; m > 0; m >>= 1) v = min(v, __shfl_xor(v, m, kWave));
-  return v;
+  return __builtin_amdgcn_readfirstlane(v);
 }
+
+// max / min of floats as v_maximum3_f32 / v_minimum3_f32 (a NaN operand gives
+// NaN; scores are never NaN), without the quieting moves fmaxf / fminf need.
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+__device__ __forceinline__ float vmin(float a, float b) { return __builtin_elementwise_minimum(a, b); }
 
 // Final list entry of a row -> output index / score.
 template <class KO>
@@ -691,6 +699,29 @@ struct MfmaScorer {
     }
   }
 
+  // zr: this lane's query sketch row as query_sketch_kernel writes it (RK
+  // bf16 values for bf16 / fp8 codes, RK floats for float32 codes)
+  __device__ void load_operand_row(const uint8_t* zr, int g) {
+    if constexpr (SBF) {
+      if constexpr (RK == 16) {
+        zb4 = as_i16x4(*reinterpret_cast<const uint2*>(zr + 8 * g));
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < NKB; ++kk)
+          zb[kk] = as_bf16x8(*reinterpret_cast<const uint4*>(zr + 2 * (32 * kk + 8 * g)));
+      }
+    } else {
+#pragma unroll
+      for (int m = 0; m < RK / 16; ++m) {
+        const float4 v = *reinterpret_cast<const float4*>(zr + 4 * (4 * (g + 4 * m)));
+        zf[4 * m] = v.x;
+        zf[4 * m + 1] = v.y;
+        zf[4 * m + 2] = v.z;
+        zf[4 * m + 3] = v.w;
+      }
+    }
+  }
+
   // raw operands of one tile: NL 16-byte loads per 16-key sub-block
   static constexpr int NL = SBF ? (RK == 16 ? 1 : RK / 32) : RK / 16;
   struct Raw {
@@ -801,32 +832,29 @@ struct MfmaScorer {
   }
 
   // body(t0, acc) for every tile of [t_beg, t_end) in order, with the loads
-  // of the next two tiles in flight while one is scored (three register
-  // buffers taken in turn) when a tile's operands fit in 32 registers;
+  // of the next DEPTH - 1 tiles in flight while one is scored (a ring of
+  // DEPTH register buffers) when a tile's operands fit in 32 registers;
   // otherwise as for_tiles.  Loads past the last tile are clamped to it.
-  template <class F>
+  template <int DEPTH = 3, class F>
   __device__ __forceinline__ void for_tiles_deep(const uint8_t* hbase, int t_beg, int t_end,
                                                  int qi, int g, F&& body) const {
     if constexpr (kPrefetch) {
       if (t_beg >= t_end) return;
       const int last = t_beg + ((t_end - 1 - t_beg) / kTile) * kTile;
       auto at = [&](int t) { return hbase + (size_t)(min(t, last) / kTile) * TB; };
-      Raw ra, rb, rc;
-      load(at(t_beg), qi, g, ra);
-      load(at(t_beg + kTile), qi, g, rb);
-      for (int t0 = t_beg; t0 < t_end; t0 += 3 * kTile) {
-        load(at(t0 + 2 * kTile), qi, g, rc);
-        f32x4_t acc[4];
-        mma(ra, acc);
-        body(t0, acc);
-        if (t0 + kTile >= t_end) break;
-        load(at(t0 + 3 * kTile), qi, g, ra);
-        mma(rb, acc);
-        body(t0 + kTile, acc);
-        if (t0 + 2 * kTile >= t_end) break;
-        load(at(t0 + 4 * kTile), qi, g, rb);
-        mma(rc, acc);
-        body(t0 + 2 * kTile, acc);
+      Raw r[DEPTH];
+#pragma unroll
+      for (int d = 0; d + 1 < DEPTH; ++d) load(at(t_beg + d * kTile), qi, g, r[d]);
+      for (int t0 = t_beg;; t0 += DEPTH * kTile) {
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+          const int t = t0 + d * kTile;
+          load(at(t + (DEPTH - 1) * kTile), qi, g, r[(d + DEPTH - 1) % DEPTH]);
+          f32x4_t acc[4];
+          mma(r[d], acc);
+          body(t, acc);
+          if (t + kTile >= t_end) return;
+        }
       }
     } else {
       for_tiles(hbase, t_beg, t_end, kTile, qi, g, body);
@@ -886,16 +914,110 @@ __device__ __forceinline__ float mfma_query_sketch(const float* __restrict__ qr,
   return b;
 }
 
+// ---------------------------------------------------------------- query sketches of a batch of rows
+
+// query_sketch_kernel: z = B_q^T q and b = q . mu (equation (5): the query
+// side of the factored score) of every row, written once so that the
+// two-pass scoring kernel loads each wave's 16 rows as one contiguous block.
+// z is rounded to bf16 for bf16 and fp8 codes (the MFMA operand) and kept in
+// float32 for float32 codes; row layout zq[(bh * Q + i) * RK + m], b[bh * Q + i].
+// The f32 MFMA forms D[m][qi] = sum_c B_q[c][m] q[qi][c]: lane (qi, g) loads
+// q[qi][16j + 4g .. 16j + 4g + 3] for j = 0..7 as float4 (each row read as
+// 64-byte runs) and feeds dims c = 16j + 4g + e at step 4j + e.  B_q of the
+// head waits in LDS in that operand order, one float4 per (j, mb) and lane.
+// grid: 1-D, work-group (bh, part) covers rows [part * kQsRows, ...) of (b, h).
+constexpr int kQsWaves = 4;
+constexpr int kQsRows = 1024;
+
+template <int RK, int ST>
+__global__ __launch_bounds__(kQsWaves * kWave) void query_sketch_kernel(
+    const float* __restrict__ q, const float* __restrict__ Bq, const float* __restrict__ mu,
+    int Q, int H_q, int H_kv, int n_bh, int parts, uint8_t* __restrict__ zq,
+    float* __restrict__ bout) {
+  constexpr int D = saki::kHeadDim;
+  constexpr int MB = RK / 16;
+  __shared__ __align__(16) float bl[D * RK];
+  const long long lb = xcd_logical_block((long long)n_bh * parts);
+  if (lb < 0) return;
+  const size_t bh = (size_t)(lb / parts);
+  const int part = (int)(lb % parts);
+  const int h = (int)(bh % H_q);
+  const int gkv = h / (H_q / H_kv);
+  // B_q[h] (row-major D x RK) -> bl[((j * MB + mb) * 64 + 16 g + qi) * 4 + e]
+  // = B_q[16j + 4g + e][16mb + qi]
+  const float* bsrc = Bq + (size_t)h * D * RK;
+  for (int i = threadIdx.x; i < D * RK; i += kQsWaves * kWave) {
+    const int c = i / RK, m = i % RK;
+    bl[(((c / 16) * MB + m / 16) * 64 + 16 * ((c % 16) / 4) + m % 16) * 4 + c % 4] = bsrc[i];
+  }
+  __syncthreads();
+  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int qi = lane % 16, g = lane / 16;
+  const float* mr = mu + (size_t)gkv * D;
+  float4 mv[8];  // this lane's dims of mu
+#pragma unroll
+  for (int j = 0; j < 8; ++j) mv[j] = *reinterpret_cast<const float4*>(mr + 16 * j + 4 * g);
+  const int r_end = min(Q, (part + 1) * kQsRows);
+  for (int row0 = part * kQsRows + wave * kMR; row0 < r_end; row0 += kQsWaves * kMR) {
+    const int row = row0 + qi;
+    const bool ok = row < r_end;
+    const float* qr = q + (bh * Q + (ok ? row : row0)) * D;
+    float4 qv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      qv[j] = *reinterpret_cast<const float4*>(qr + 16 * j + 4 * g);
+      if (!ok) qv[j] = float4{0.f, 0.f, 0.f, 0.f};
+    }
+    float bp = 0.f;
+    f32x4_t za[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) za[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      bp = fmaf(qv[j].x, mv[j].x, bp);
+      bp = fmaf(qv[j].y, mv[j].y, bp);
+      bp = fmaf(qv[j].z, mv[j].z, bp);
+      bp = fmaf(qv[j].w, mv[j].w, bp);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const float4 a = *reinterpret_cast<const float4*>(bl + ((j * MB + mb) * 64 + lane) * 4);
+        za[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, qv[j].x, za[mb], 0, 0, 0);
+        za[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, qv[j].y, za[mb], 0, 0, 0);
+        za[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, qv[j].z, za[mb], 0, 0, 0);
+        za[mb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, qv[j].w, za[mb], 0, 0, 0);
+      }
+    }
+    const float b = sum_lane_groups(bp);
+    if (!ok) continue;
+    const size_t base = (bh * Q + row) * RK;
+    // lane (qi, g) holds z[row][16mb + 4g + v], v = 0..3
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      if constexpr (ST != kStF32) {
+        const uint2 u{bf16_bits(za[mb][0]) | (bf16_bits(za[mb][1]) << 16),
+                      bf16_bits(za[mb][2]) | (bf16_bits(za[mb][3]) << 16)};
+        *reinterpret_cast<uint2*>(zq + (base + 16 * mb + 4 * g) * 2) = u;
+      } else {
+        *reinterpret_cast<float4*>(zq + (base + 16 * mb + 4 * g) * 4) =
+            float4{za[mb][0], za[mb][1], za[mb][2], za[mb][3]};
+      }
+    }
+    if (g == 0) bout[bh * Q + row] = b;
+  }
+}
+
 // ---------------------------------------------------------------- sketch scoring, MFMA, block-maximum gate
 
 // score_batch_kernel: four independent waves per work-group, each with a
 // block of 16 query rows and that block's keys of one chunk (at most 4,096
 // keys), and the exact top-64 per row in two passes over the codes (the MFMA
-// recomputes the scores in the second):
-//   A. each lane records the maxima of its keys in blocks of 8 (rows of at
-//      least 2,048 keys), 4 (1,024), 2 (512) or 1 key, so that a row with
-//      at least 256 keys has at least 256 blocks and one with fewer has one
-//      block per key.  A maximum is stored as the top 16 bits of its
+// recomputes the scores in the second).  Rows are ranked by s' = z . c: b is
+// the same for all keys of a row and is added to the 64 kept scores.
+//   A. each lane records the maxima of its keys in blocks of 8, 4, 2 or 1
+//      keys, the size set by the wave's longest row (at least 2,048, 1,024,
+//      512 keys, or fewer), so that a row of at least about 256 keys has
+//      about 256 blocks or more and the rows of a wave below 512 keys have
+//      one block per key.  A maximum is stored as the top 16 bits of its
 //      ordered float32 bits, which rounds it down.
 //   threshold: per row, a histogram of the stored maxima over 64 equal bins
 //      of score around the predicted 64th largest (from their mean and
@@ -904,17 +1026,20 @@ __device__ __forceinline__ float mfma_query_sketch(const float* __restrict__ qr,
 //      bin whose count from the top reaches 64.  At least 64 blocks then
 //      have a maximum >= tau, so at least 64 keys score >= tau and all of
 //      the row's top-64 do; with 256 blocks or more about 64-90 keys pass.
-//   B. every key that scores >= tau goes to its lane's candidate slots (40
-//      per lane, 160 per row), and the row's count is checked to be >= 64.
+//      A row with fewer than 64 blocks keeps every key.
+//   B. every key that scores >= tau goes to its lane's candidate slots (39
+//      per lane usable, 156 per row), and the row's count is checked to be
+//      >= 64.
 // The candidates are then sorted by a bitonic network that holds 16 entries
 // per lane, and the best 64 are kept.  A row whose candidates overflow its
-// slots (many equal scores) or fall short sends its wave to the online
-// selection of saki_topk.h.
+// slots (many equal scores, or rows of very different lengths in one wave)
+// or fall short sends its wave to the online selection of saki_topk.h.
 
 constexpr int kBWaves = saki::kBatchWaves;  // independent waves per work-group
 constexpr int kBEnt = 512;                 // block-maximum entries per row
 constexpr int kBBins = 64;                 // histogram bins per row
 constexpr int kBSlots = 40;                // candidate slots per lane
+constexpr int kBDepth = 3;                 // code tiles whose loads are in flight, plus one
 constexpr int kBWaveBytes = kMR * 4 * kBSlots * 8;  // 20 KiB of LDS per wave
 static_assert(saki::kBatchMaxChunk / 8 <= kBEnt, "a chunk's 8-key blocks fit");
 static_assert(kMR * kBEnt * 2 + kMR * kBBins * 4 <= kBWaveBytes, "entries and bins fit");
@@ -927,6 +1052,13 @@ __device__ __forceinline__ uint32_t ord16(float x) {
 }
 // The float an entry stands for (at most the maximum it was taken from).
 __device__ __forceinline__ float unord16(uint32_t v) { return unord_f32(v << 16); }
+// ord16(a) | ord16(b) << 16 for finite a and b.
+__device__ __forceinline__ uint32_t pack_ord16(float a, float b) {
+  const uint32_t ua = __float_as_uint(a), ub = __float_as_uint(b);
+  const uint32_t oa = ua ^ ((uint32_t)((int32_t)ua >> 31) | 0x80000000u);
+  const uint32_t ob = ub ^ ((uint32_t)((int32_t)ub >> 31) | 0x80000000u);
+  return __builtin_amdgcn_perm(ob, oa, 0x07060302u);  // bytes 2, 3 of oa, then of ob
+}
 
 // Bitonic sort of one row's 64 entries held 16 per lane by the row's four
 // lanes (lane groups g = lane / 16): entry e = 16 g + i is x[i] of lane group
@@ -1004,10 +1136,10 @@ __device__ __forceinline__ void merge64_x16(typename KO::K (&x)[16], const typen
 template <int RK, int ST>
 __global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
     const uint8_t* __restrict__ index, int n_tiles, int N_valid, int Q,
-    const int* __restrict__ q_pos, const float* __restrict__ q,
-    const float* __restrict__ Bq, const float* __restrict__ mu, int H_q, int H_kv, int gq,
-    int n_bh, int groups, int chunk, int n_chunks, int k, int* __restrict__ top_idx,
-    float* __restrict__ top_score, uint64_t* __restrict__ part) {
+    const int* __restrict__ q_pos, const uint8_t* __restrict__ zq,
+    const float* __restrict__ zb, int H_q, int gq, int n_bh, int groups, int chunk,
+    int n_chunks, int k, int* __restrict__ top_idx, float* __restrict__ top_score,
+    uint64_t* __restrict__ part) {
   constexpr int D = saki::kHeadDim;
   using KO = KeysF32;
   using K = uint64_t;
@@ -1020,7 +1152,6 @@ __global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
   const int ch = (int)((lb / groups) % n_chunks);
   const size_t bh = (size_t)(lb / ((long long)groups * n_chunks));
   const int h = (int)(bh % H_q);
-  const int gkv = h / (H_q / H_kv);
   const int row0 = (gb * kBWaves + wave) * kMR;
   if (row0 >= Q) return;  // the waves never synchronise with each other
   const int qi = lane % 16, g = lane / 16;
@@ -1033,12 +1164,13 @@ __global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
   const int kend = min(kbeg + chunk, kmax);
   uint8_t* wl = lds_mem[wave];
 
-  // ---- query sketch
+  // ---- query sketch, formed by query_sketch_kernel.  b = q . mu is the same
+  // for every key of a row, so the selection ranks s' = z . c (accumulators
+  // starting at zero) and b is added to the 64 scores that are kept.
   Scorer sc;
-  const float my_b = mfma_query_sketch<RK, ST>(q + (bh * Q + (row_ok ? my_row : row0)) * D, row_ok,
-                                               Bq + (size_t)h * D * RK, mu + (size_t)gkv * D,
-                                               reinterpret_cast<float*>(wl), qi, g, sc);
-  sc.init = my_b;  // the accumulators start at b: scores come out whole
+  const size_t zrow = bh * Q + (row_ok ? my_row : row0);
+  sc.load_operand_row(zq + zrow * RK * (ST != kStF32 ? 2 : 4), g);
+  const float my_b = zb[zrow];
   const size_t code_set = (bh / H_q) * (H_q / gq) + h / gq;
   const uint8_t* hbase = index + code_set * n_tiles * Scorer::TB;
 
@@ -1056,8 +1188,11 @@ __global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
   // ---- pass A: block maxima of this lane's keys
   const int n_row = max(0, min(my_lim, kend) - kbeg);
   const int row_tiles = (n_row + kTile - 1) / kTile;
-  // entries of one lane per tile: 2, 4, 8 or 16 blocks of 8, 4, 2 or 1 keys
-  const int lane_ent = n_row >= 2048 ? 2 : n_row >= 1024 ? 4 : n_row >= 512 ? 8 : 16;
+  // entries of one lane per tile: 2, 4, 8 or 16 blocks of 8, 4, 2 or 1 keys,
+  // by the wave's longest row (kend - kbeg keys), so that no row has more
+  // than kBEnt entries
+  const int n_wave = kend - kbeg;
+  const int lane_ent = n_wave >= 2048 ? 2 : n_wave >= 1024 ? 4 : n_wave >= 512 ? 8 : 16;
   // row qi's entries and histogram bins have their 16-byte groups permuted
   // (word offset xor 4 qi), so that the rows' accesses spread over the banks
   uint32_t* ent = reinterpret_cast<uint32_t*>(wl) + qi * (kBEnt / 2);
@@ -1069,23 +1204,50 @@ __global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
     bcnt += ok ? 1.f : 0.f;
     bsum += y;
     bsq = fmaf(y, y, bsq);
-    bmax = fmaxf(bmax, x);
-    bmin = ok ? fminf(bmin, x) : bmin;
+    bmax = vmax(bmax, x);
+    bmin = ok ? vmin(bmin, x) : bmin;
   };
-  sc.for_tiles_deep(hbase, kbeg, kend, qi, g, [&](int t0, f32x4_t* acc) {
-    mask_tile(t0, acc);
+  sc.template for_tiles_deep<kBDepth>(hbase, kbeg, kend, qi, g, [&](int t0, f32x4_t* acc) {
     const int tl = (t0 - kbeg) / kTile;
+    const int wo = (tl * 4 * lane_ent + g * lane_ent) / 2;  // this lane's first word
+    if (t0 + kTile <= kmin && lane_ent <= 4) {
+      // every key of the tile lies below every row's limit: no -inf
+      if (lane_ent == 2) {
+        const float a = vmax(vmax(vmax(acc[0][0], acc[0][1]), vmax(acc[0][2], acc[0][3])),
+                             vmax(vmax(acc[1][0], acc[1][1]), vmax(acc[1][2], acc[1][3])));
+        const float b = vmax(vmax(vmax(acc[2][0], acc[2][1]), vmax(acc[2][2], acc[2][3])),
+                             vmax(vmax(acc[3][0], acc[3][1]), vmax(acc[3][2], acc[3][3])));
+        ent[wo ^ sw] = pack_ord16(a, b);
+        bsum += a + b;
+        bsq = fmaf(a, a, fmaf(b, b, bsq));
+        bmax = vmax(bmax, vmax(a, b));
+        bmin = vmin(bmin, vmin(a, b));
+        bcnt += 2.f;
+      } else {
+        float m4[4];
+#pragma unroll
+        for (int sub = 0; sub < 4; ++sub)
+          m4[sub] = vmax(vmax(acc[sub][0], acc[sub][1]), vmax(acc[sub][2], acc[sub][3]));
+        *reinterpret_cast<uint2*>(ent + (wo ^ sw)) = uint2{pack_ord16(m4[0], m4[1]), pack_ord16(m4[2], m4[3])};
+        bsum += (m4[0] + m4[1]) + (m4[2] + m4[3]);
+        bsq = fmaf(m4[0], m4[0], fmaf(m4[1], m4[1], fmaf(m4[2], m4[2], fmaf(m4[3], m4[3], bsq))));
+        bmax = vmax(vmax(bmax, vmax(m4[0], m4[1])), vmax(m4[2], m4[3]));
+        bmin = vmin(vmin(bmin, vmin(m4[0], m4[1])), vmin(m4[2], m4[3]));
+        bcnt += 4.f;
+      }
+      return;
+    }
+    mask_tile(t0, acc);
     if (tl >= row_tiles) return;  // nothing of this row: no entries
     float m2[8];  // maxima of the pairs (sub, v = 0..1), (sub, v = 2..3)
 #pragma unroll
     for (int sub = 0; sub < 4; ++sub) {
-      m2[2 * sub] = fmaxf(acc[sub][0], acc[sub][1]);
-      m2[2 * sub + 1] = fmaxf(acc[sub][2], acc[sub][3]);
+      m2[2 * sub] = vmax(acc[sub][0], acc[sub][1]);
+      m2[2 * sub + 1] = vmax(acc[sub][2], acc[sub][3]);
     }
-    const int wo = (tl * 4 * lane_ent + g * lane_ent) / 2;  // this lane's first word
     if (lane_ent == 2) {
-      const float a = fmaxf(fmaxf(m2[0], m2[1]), fmaxf(m2[2], m2[3]));
-      const float b = fmaxf(fmaxf(m2[4], m2[5]), fmaxf(m2[6], m2[7]));
+      const float a = vmax(vmax(m2[0], m2[1]), vmax(m2[2], m2[3]));
+      const float b = vmax(vmax(m2[4], m2[5]), vmax(m2[6], m2[7]));
       ent[wo ^ sw] = ord16(a) | (ord16(b) << 16);
       stat(a);
       stat(b);
@@ -1093,7 +1255,7 @@ __global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
       uint32_t u[4];
 #pragma unroll
       for (int sub = 0; sub < 4; ++sub) {
-        const float m4 = fmaxf(m2[2 * sub], m2[2 * sub + 1]);
+        const float m4 = vmax(m2[2 * sub], m2[2 * sub + 1]);
         u[sub] = ord16(m4);
         stat(m4);
       }
@@ -1219,34 +1381,52 @@ __global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
   }
 
   // ---- pass B: candidates, every key scoring >= tau
-  // slots hold (score bits, key) as they are found (slot j of every lane in
-  // one 512-byte row, so that the lanes' writes spread over the banks);
-  // ordered keys are formed when they are sorted
-  uint2* cand = reinterpret_cast<uint2*>(wl) + lane;
+  // Slot j of a lane holds a score bits at word 128 j + lane and its key at
+  // word 128 j + 64 + lane (so that the lanes' writes spread over the banks
+  // and a pair is one two-address write).  Every score is written to the
+  // lane's next free slot and the pointer moves on only past one >= tau, so
+  // no lane branches; a lane whose count reaches the last slot keeps
+  // counting and overwrites it (and the wave then takes the fallback below).
+  uint32_t* const cw = reinterpret_cast<uint32_t*>(wl) + lane;
+  uint32_t* wp = cw;
   int cnt = 0;
-  sc.for_tiles_deep(hbase, kbeg, kend, qi, g, [&](int t0, f32x4_t* acc) {
+  sc.template for_tiles_deep<kBDepth>(hbase, kbeg, kend, qi, g, [&](int t0, f32x4_t* acc) {
     mask_tile(t0, acc);
-    const int kb = t0 + 4 * g;
+    const uint32_t kb = (uint32_t)(t0 + 4 * g);
+    if (__ballot(cnt > kBSlots - 16) == 0) {  // room for the whole tile in every lane
 #pragma unroll
-    for (int sub = 0; sub < 4; ++sub)
+      for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
-      for (int v = 0; v < 4; ++v)
-        if (acc[sub][v] >= tau) {
-          cand[min(cnt, kBSlots - 1) * kWave] = uint2{__float_as_uint(acc[sub][v]), (uint32_t)(kb + 16 * sub + v)};
-          ++cnt;
+        for (int v = 0; v < 4; ++v) {
+          wp[0] = __float_as_uint(acc[sub][v]);
+          wp[kWave] = kb + (uint32_t)(16 * sub + v);
+          wp += acc[sub][v] >= tau ? 2 * kWave : 0;
         }
+      cnt = (int)(wp - cw) / (2 * kWave);
+    } else {
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          uint32_t* sp = cw + 2 * kWave * min(cnt, kBSlots - 1);
+          sp[0] = __float_as_uint(acc[sub][v]);
+          sp[kWave] = kb + (uint32_t)(16 * sub + v);
+          cnt += acc[sub][v] >= tau ? 1 : 0;
+        }
+      wp = cw + 2 * kWave * min(cnt, kBSlots - 1);
+    }
   });
 
   // the row's candidates: at least 64 unless every key of the row is one
   int row_cnt = cnt + (int)xor_shfl_u32((uint32_t)cnt, 16);
   row_cnt += (int)xor_shfl_u32((uint32_t)row_cnt, 32);
   const bool short_row = tau > -FLT_MAX && row_cnt < kList;
-  if (__ballot(cnt > kBSlots || short_row) == 0) {
+  if (__ballot(cnt >= kBSlots || short_row) == 0) {
     // ---- sort the candidates, keep the best 64
     wave_lds_sync();
     auto slot = [&](int j) {
-      const uint2 c = cand[min(j, kBSlots - 1) * kWave];
-      return j < min(cnt, kBSlots) ? KO::make(__uint_as_float(c.x), (int)c.y) : KO::pad();
+      const uint32_t* c = cw + 2 * kWave * min(j, kBSlots - 1);
+      return j < min(cnt, kBSlots) ? KO::make(__uint_as_float(c[0]), (int)c[kWave]) : KO::pad();
     };
     K x[16];
 #pragma unroll
@@ -1261,9 +1441,40 @@ __global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
       sort64_x16<KO>(y, g);
       merge64_x16<KO>(x, y, g);
     }
+    // x holds the best 64 by s' = z . c, sorted.  Adding b keeps the scores
+    // non-increasing; two that round to the same value must still stand in
+    // index order, so the rare row where they do not is sorted again.
+    bool disorder = false;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      x[i] = KO::make(KO::score(x[i]) + my_b, KO::index(x[i]));
+      if (i > 0) disorder |= KO::gt(x[i], x[i - 1]);
+    }
+    {  // entry 16 (g + 1) of the row, held by the lane 16 above
+      const uint32_t hi = (uint32_t)__shfl_down((int)(uint32_t)(x[0] >> 32), 16, kWave);
+      const uint32_t lo = (uint32_t)__shfl_down((int)(uint32_t)x[0], 16, kWave);
+      disorder |= g < 3 && KO::gt(((uint64_t)hi << 32) | lo, x[15]);
+    }
+    if (__ballot(disorder) != 0) sort64_x16<KO>(x, g);
     if (row_ok) {
       const size_t rw = bh * Q + my_row;
-      if (n_chunks == 1) {
+      // a lane's 16 entries are 64 contiguous bytes of its row
+      const bool vec = k == kMaxK && ((reinterpret_cast<uintptr_t>(top_idx) |
+                                       reinterpret_cast<uintptr_t>(top_score)) & 15) == 0;
+      if (n_chunks == 1 && vec) {
+        int4* ip = reinterpret_cast<int4*>(top_idx + rw * kMaxK + 16 * g);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          ip[u] = int4{out_index<KO>(x[4 * u]), out_index<KO>(x[4 * u + 1]),
+                       out_index<KO>(x[4 * u + 2]), out_index<KO>(x[4 * u + 3])};
+        if (top_score) {
+          float4* sp = reinterpret_cast<float4*>(top_score + rw * kMaxK + 16 * g);
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            sp[u] = float4{KO::score(x[4 * u]), KO::score(x[4 * u + 1]), KO::score(x[4 * u + 2]),
+                           KO::score(x[4 * u + 3])};
+        }
+      } else if (n_chunks == 1) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int e = 16 * g + i;
@@ -1280,7 +1491,9 @@ __global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
     return;
   }
 
-  // ---- fallback: online selection over the chunk, in two halves of 8 rows
+  // ---- fallback: online selection over the chunk, in two halves of 8 rows,
+  // scores formed whole (accumulators starting at b)
+  sc.init = my_b;
   wave_lds_sync();
   float* stage = reinterpret_cast<float*>(wl);  // [16][64], key column swizzled
   K* lists = reinterpret_cast<K*>(wl + kMR * kTile * 4);
@@ -3192,10 +3405,17 @@ void launch_score(const uint8_t* index, int B, int H_q, int H_kv, int index_head
   dim3 grid((unsigned)(p.row_blocks * ((p.n_chunks + cpg - 1) / cpg)), B * index_heads);
   dim3 block(kWave * p.waves);
   const int nt = (int)saki::n_tiles(N_cap);
-  if (p.mfma)
+  if (p.mfma) {
+    uint8_t* zq = ws + p.z_off;
+    float* zb = reinterpret_cast<float*>(ws + p.b_off);
+    const int parts = (Q + kQsRows - 1) / kQsRows;
+    const long long qs_groups = (long long)parts * B * H_q;
+    hipLaunchKernelGGL((query_sketch_kernel<RK, ST>), dim3((unsigned)(((qs_groups + kXcds - 1) / kXcds) * kXcds)),
+                       dim3(kQsWaves * kWave), 0, s, q, Bq, mu, Q, H_q, H_kv, B * H_q, parts, zq, zb);
     hipLaunchKernelGGL((score_batch_kernel<RK, ST>), xcd_grid(p, B * H_q), dim3(kBWaves * kWave), 0,
-                       s, index, nt, N_valid, Q, q_pos, q, Bq, mu, H_q, H_kv, gq, B * H_q,
+                       s, index, nt, N_valid, Q, q_pos, zq, zb, H_q, gq, B * H_q,
                        p.row_blocks, p.chunk, p.n_chunks, k, top_idx, top_score, part);
+  }
   else if (p.rows == 4)
     hipLaunchKernelGGL((score_stream_kernel<RK, ST, 4>), grid, block, 0, s, index, nt, N_valid,
                        Q, q_pos, q, Bq, mu, H_q, H_kv, gq, p.row_blocks, p.chunk, p.n_chunks,
@@ -3325,7 +3545,7 @@ int score_topk_impl(const void* index, int sketch_dtype, int B, int H_q, int H_k
     return SAKI_ERR_UNSUPPORTED;
   if (Q == 0) return SAKI_OK;
   if (!index || !q || !B_q || !mu || !top_idx) return SAKI_ERR_ARG;
-  const saki::Plan p = saki::score_plan(B, H_q, index_heads, Q, N_valid);
+  const saki::Plan p = saki::score_plan(B, H_q, index_heads, Q, N_valid, r, sketch_dtype);
   if (ws_bytes < p.ws_bytes) return SAKI_ERR_WORKSPACE;
   if (!ws) {  // the static scratch array, resolved only once the sizes fit it
     const int sst = scratch_address(&ws);

@@ -322,6 +322,15 @@ def test_scan_workspace_holds_lists_gates_and_flags():
     # enough rows that every row block scans its keys in one chunk: no partial
     # lists, gates or flags (the minimum workspace)
     assert S.saki_score_topk_workspace_bytes(1, 16, 2048, 16_384, 32, 64, "bf16") == 256
+    # rows shorter than 16,384 keys, 16 or more queries: the query sketches of
+    # every row (r bf16 values, r floats for float32 codes, and b) come first
+    rows = 32 * 4032
+    for sk, zb in (("bf16", 2), ("fp8", 2), ("f32", 4)):
+        ws = S.saki_score_topk_workspace_bytes(1, 32, 4032, 4096, 32, 64, sk)
+        assert rows * (32 * zb + 4) <= ws <= rows * (32 * zb + 4) + 512
+    # and past one 4,096-key chunk the partial lists besides
+    ws = S.saki_score_topk_workspace_bytes(2, 8, 64, 10_000, 64, 64, "bf16")
+    assert ws >= 2 * 8 * 64 * (3 * 64 * 8 + 64 * 2 + 4)
 
 
 def test_argument_validation_without_launch(lib):
