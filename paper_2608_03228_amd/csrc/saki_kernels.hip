@@ -1130,6 +1130,91 @@ __device__ __forceinline__ void merge64_x16(typename KO::K (&x)[16], const typen
   }
 }
 
+// ---- 32-bit keys, 64 per row held 16 per lane as in sort64_x16
+
+__device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
+__device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
+// a takes the larger key, b the smaller
+__device__ __forceinline__ void cx_u32(uint32_t& a, uint32_t& b) {
+  const uint32_t hi = umax32(a, b);
+  b = umin32(a, b);
+  a = hi;
+}
+// Compare-exchange of entry X of lane groups g and g ^ (M / 16), and the same
+// for entry Y; the lower lane group keeps the larger key.  The first permlane
+// swap hands every lane one such pair (of X in half of the lane groups, of Y
+// in the others), and the second sends the larger and the smaller back.
+template <int M>
+__device__ __forceinline__ void cx_rows_u32(uint32_t& X, uint32_t& Y) {
+  if constexpr (M == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(X, Y, false, false);
+    const auto t = __builtin_amdgcn_permlane16_swap(umax32(r[0], r[1]), umin32(r[0], r[1]), false, false);
+    X = t[0];
+    Y = t[1];
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(X, Y, false, false);
+    const auto t = __builtin_amdgcn_permlane32_swap(umax32(r[0], r[1]), umin32(r[0], r[1]), false, false);
+    X = t[0];
+    Y = t[1];
+  }
+}
+// Stages m = 8, 4, 2, 1 of a descending bitonic merge inside each lane.
+__device__ __forceinline__ void lane_merge_desc_u32(uint32_t (&x)[16]) {
+#pragma unroll
+  for (int m = 8; m > 0; m >>= 1)
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (!(i & m)) cx_u32(x[i], x[i | m]);
+}
+// Bitonic sort of one row's 64 keys into descending order of e = 16 g + i.
+// Blocks whose direction depends on the lane group (levels 16 and 32) are
+// sorted as complemented keys, so every stage there is descending.
+__device__ __forceinline__ void sort64_u32(uint32_t (&x)[16], int g) {
+#pragma unroll
+  for (int k = 2; k <= 8; k <<= 1)
+#pragma unroll
+    for (int m = k >> 1; m > 0; m >>= 1)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        if (i & m) continue;
+        if ((i & k) == 0)
+          cx_u32(x[i], x[i | m]);
+        else
+          cx_u32(x[i | m], x[i]);
+      }
+  const uint32_t c1 = (g & 1) ? ~0u : 0u, c2 = (g & 2) ? ~0u : 0u;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) x[i] ^= c1;
+  lane_merge_desc_u32(x);  // level 16
+#pragma unroll
+  for (int i = 0; i < 16; ++i) x[i] ^= c1 ^ c2;
+#pragma unroll
+  for (int i = 0; i < 16; i += 2) cx_rows_u32<16>(x[i], x[i + 1]);  // level 32
+  lane_merge_desc_u32(x);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) x[i] ^= c2;
+#pragma unroll
+  for (int i = 0; i < 16; i += 2) cx_rows_u32<32>(x[i], x[i + 1]);  // level 64
+#pragma unroll
+  for (int i = 0; i < 16; i += 2) cx_rows_u32<16>(x[i], x[i + 1]);
+  lane_merge_desc_u32(x);
+}
+// x <- the best 64 of x (descending) and y (ascending); dmax <- the largest
+// key left out so far.  The elementwise maxima form a bitonic sequence.
+__device__ __forceinline__ void merge64_u32(uint32_t (&x)[16], const uint32_t (&y)[16],
+                                            uint32_t& dmax) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    dmax = umax32(dmax, umin32(x[i], y[i]));
+    x[i] = umax32(x[i], y[i]);
+  }
+#pragma unroll
+  for (int i = 0; i < 16; i += 2) cx_rows_u32<32>(x[i], x[i + 1]);
+#pragma unroll
+  for (int i = 0; i < 16; i += 2) cx_rows_u32<16>(x[i], x[i + 1]);
+  lane_merge_desc_u32(x);
+}
+
 // grid: 1-D, 8 * ceil(groups * n_chunks * n_bh / 8) work-groups of kBWaves
 // waves; work-group (bh, chunk, group) takes the 16-row blocks 4 * group ..
 // 4 * group + 3 of (sequence, head) bh, the longest causal rows first.
@@ -1424,32 +1509,98 @@ __global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
   if (__ballot(cnt >= kBSlots || short_row) == 0) {
     // ---- sort the candidates, keep the best 64
     wave_lds_sync();
-    auto slot = [&](int j) {
-      const uint32_t* c = cw + 2 * kWave * min(j, kBSlots - 1);
-      return j < min(cnt, kBSlots) ? KO::make(__uint_as_float(c[0]), (int)c[kWave]) : KO::pad();
+    const uint32_t* const wbase = cw - lane;  // word 0 of the wave's slots
+    // 32-bit keys: the top 24 bits of the ordered score s', then the
+    // candidate's id 4 slot + g (0 past the lane's count)
+    auto key32 = [&](int j) -> uint32_t {
+      const uint32_t sb = cw[2 * kWave * min(j, kBSlots - 1)];
+      const uint32_t o = sb ^ ((uint32_t)((int32_t)sb >> 31) | 0x80000000u);
+      return j < cnt ? (o & 0xffffff00u) | (uint32_t)(4 * j + g) : 0u;
     };
-    K x[16];
+    uint32_t x32[16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) x[i] = slot(i);
-    sort64_x16<KO>(x, g);
-    // the slots past the first 16 of each lane, 16 at a time
+    for (int i = 0; i < 16; ++i) x32[i] = key32(i);
+    sort64_u32(x32, g);
+    uint32_t dmax = 0u;  // the best key left out
+    // the slots past the first 16 of each lane, 16 at a time, sorted
+    // ascending (as complemented keys) and merged
 #pragma unroll 1
     for (int set = 1; 16 * set < kBSlots && __ballot(cnt > 16 * set) != 0; ++set) {
-      K y[16];
+      uint32_t y[16];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) y[i] = slot(16 * set + i);
-      sort64_x16<KO>(y, g);
-      merge64_x16<KO>(x, y, g);
+      for (int i = 0; i < 16; ++i) y[i] = ~key32(16 * set + i);
+      sort64_u32(y, g);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) y[i] = ~y[i];
+      merge64_u32(x32, y, dmax);
     }
-    // x holds the best 64 by s' = z . c, sorted.  Adding b keeps the scores
-    // non-increasing; two that round to the same value must still stand in
-    // index order, so the rare row where they do not is sorted again.
+    // the kept set is certain unless the 64th kept key and the best one left
+    // out share their top 24 bits
+    dmax = umax32(dmax, xor_shfl_u32(dmax, 16));
+    dmax = umax32(dmax, xor_shfl_u32(dmax, 32));
+    // entry 63 of the row (x32[15] of lane group 3) in all four lanes; every
+    // lane takes part in both swaps
+    const uint32_t s32 = xor_shfl_u32(x32[15], 32);
+    const uint32_t t32 = (g & 2) ? x32[15] : s32;
+    const uint32_t s16 = xor_shfl_u32(t32, 16);
+    const uint32_t k64 = (g & 1) ? t32 : s16;
+    const bool unsure = dmax != 0u && (dmax >> 8) == (k64 >> 8);
+    K x[16];
+    if (__ballot(unsure) == 0) {
+      // the kept entries as exact keys of (s' + b, index), in key order up to
+      // runs of equal top 24 bits; two odd-even transposition steps put runs
+      // of two in order (what is left is found below)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const uint32_t id = x32[i] & 0xffu;
+        const uint32_t* c = wbase + 2 * kWave * (id >> 2) + 16 * (id & 3) + qi;
+        x[i] = x32[i] == 0u ? KO::pad() : KO::make(__uint_as_float(c[0]) + my_b, (int)c[kWave]);
+      }
+      auto cx64 = [](K& a, K& b2) {
+        const bool sw = KO::gt(b2, a);
+        const K t = a;
+        a = KO::sel(sw, b2, a);
+        b2 = KO::sel(sw, t, b2);
+      };
+#pragma unroll
+      for (int i = 0; i < 16; i += 2) cx64(x[i], x[i + 1]);
+#pragma unroll
+      for (int i = 1; i < 15; i += 2) cx64(x[i], x[i + 1]);
+      {  // entries 16 g + 15 and 16 (g + 1), held by lanes 16 apart
+        const K nxt = ((uint64_t)(uint32_t)__shfl_down((int)(uint32_t)(x[0] >> 32), 16, kWave) << 32) |
+                      (uint32_t)__shfl_down((int)(uint32_t)x[0], 16, kWave);
+        const K prv = ((uint64_t)(uint32_t)__shfl_up((int)(uint32_t)(x[15] >> 32), 16, kWave) << 32) |
+                      (uint32_t)__shfl_up((int)(uint32_t)x[15], 16, kWave);
+        if (g < 3 && KO::gt(nxt, x[15])) x[15] = nxt;
+        if (g > 0 && KO::gt(x[0], prv)) x[0] = prv;
+      }
+    } else {
+      // exact 64-bit keys of (s', index) over all slots
+      auto slot = [&](int j) {
+        const uint32_t* c = cw + 2 * kWave * min(j, kBSlots - 1);
+        return j < min(cnt, kBSlots) ? KO::make(__uint_as_float(c[0]), (int)c[kWave]) : KO::pad();
+      };
+#pragma unroll
+      for (int i = 0; i < 16; ++i) x[i] = slot(i);
+      sort64_x16<KO>(x, g);
+#pragma unroll 1
+      for (int set = 1; 16 * set < kBSlots && __ballot(cnt > 16 * set) != 0; ++set) {
+        K y[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) y[i] = slot(16 * set + i);
+        sort64_x16<KO>(y, g);
+        merge64_x16<KO>(x, y, g);
+      }
+      // x holds the best 64 by s', sorted; b is added (the scores stay
+      // non-increasing, and ties that arise are put in order below)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) x[i] = KO::make(KO::score(x[i]) + my_b, KO::index(x[i]));
+    }
+    // two entries whose scores are equal must stand in index order: the rare
+    // row where some do not is sorted again
     bool disorder = false;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      x[i] = KO::make(KO::score(x[i]) + my_b, KO::index(x[i]));
-      if (i > 0) disorder |= KO::gt(x[i], x[i - 1]);
-    }
+    for (int i = 1; i < 16; ++i) disorder |= KO::gt(x[i], x[i - 1]);
     {  // entry 16 (g + 1) of the row, held by the lane 16 above
       const uint32_t hi = (uint32_t)__shfl_down((int)(uint32_t)(x[0] >> 32), 16, kWave);
       const uint32_t lo = (uint32_t)__shfl_down((int)(uint32_t)x[0], 16, kWave);
