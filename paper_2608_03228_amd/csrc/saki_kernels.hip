@@ -1404,15 +1404,25 @@ __global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
       *reinterpret_cast<uint4*>(hist + ((16 * g + 4 * u) ^ sw)) = uint4{0u, 0u, 0u, 0u};
     wave_lds_sync();
     const float inv_w = (float)(kBBins - 1) / (hi - lo);  // bins 0..62 over [lo, hi), 63 above
+    const float off = -lo * inv_w;
     if (!done) {
+      // an entry (in the top 16 bits of o) counts in bin (its value - lo) * inv_w,
+      // cut to 63, unless that is below 0; an empty entry reads as NaN and
+      // does not count
+      auto count = [&](uint32_t o) {
+        const uint32_t bits = o ^ (~(uint32_t)((int32_t)o >> 31) | 0x80000000u);
+        const float x = fmaf(__uint_as_float(bits), inv_w, off);
+        const int b = min((int)x, kBBins - 1);
+        if (x >= 0.f) atomicAdd(&hist[b ^ sw], 1u);
+      };
+#pragma unroll 2
       for (int e0 = 8 * g; e0 < n_ent; e0 += 32) {  // this lane's quarter of the row's entries
         const uint4 w = *reinterpret_cast<const uint4*>(ent + ((e0 / 2) ^ sw));
         const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const uint32_t v = (ww[u / 2] >> (16 * (u % 2))) & 0xffffu;
-          const float x = (unord16(v) - lo) * inv_w;
-          if (v != 0u && x >= 0.f) atomicAdd(&hist[(int)fminf(x, (float)(kBBins - 1)) ^ sw], 1u);
+        for (int u = 0; u < 4; ++u) {
+          count(ww[u] << 16);
+          count(ww[u] & 0xffff0000u);
         }
       }
     }
