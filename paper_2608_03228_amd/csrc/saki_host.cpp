@@ -2,9 +2,9 @@
 // the weight-SVD baseline factors, status strings and size helpers.
 //
 // Calibration is O(d^3) per head and runs once per model; it uses its own
-// symmetric eigensolver (Householder tridiagonalisation followed by the
-// implicit QL iteration with Wilkinson-type shifts, as in Golub & Van Loan,
-// "Matrix Computations", Sec. 8.3) so that the library depends on no LAPACK.
+// symmetric eigensolver (Householder tridiagonalisation followed by implicit
+// symmetric QR steps with the Wilkinson shift, Golub & Van Loan, "Matrix
+// Computations", Sec. 8.3) so that the library depends on no LAPACK.
 //
 // Two mathematically identical routes compute the factors:
 //  * Cholesky route, used when the eigenvalue floor provably does not bind on
@@ -571,8 +571,8 @@ void apply_q(int n, const double* hv, const double* beta, double* X, int c) {
   }
 }
 
-// zt <- Q^T = H_{n-3} ... H_0 (row-major n x n), the starting point of the QL
-// eigenvector accumulation.
+// zt <- Q^T = H_{n-3} ... H_0 (row-major n x n), the starting point of the
+// eigenvector accumulation of the QR steps.
 void form_qt(int n, const double* hv, const double* beta, double* zt) {
   std::fill(zt, zt + (size_t)n * n, 0.0);
   for (int i = 0; i < n; ++i) zt[(size_t)i * n + i] = 1.0;
@@ -588,69 +588,82 @@ void form_qt(int n, const double* hv, const double* beta, double* zt) {
   }
 }
 
-// Implicit QL on the tridiagonal (diag, off).  zt, when not null, holds the
-// transpose of the accumulated orthogonal matrix (row i = current column i),
-// so that the rotations update two contiguous rows; without it only the
-// eigenvalues are computed.  Returns false without convergence.
-bool tridiag_ql(int n, double* diag, double* off, double* zt) {
-  const double eps = std::numeric_limits<double>::epsilon();
-  // Deflation test: relative to the neighbouring diagonal entries, or
-  // absolute at eps * ||T|| (an off-diagonal that small moves any eigenvalue
-  // by at most eps * ||T||); the absolute test ends the iteration on blocks
-  // of (near-)zero eigenvalues, where a purely relative test never does.
-  double tnorm = 0.0;
-  for (int i = 0; i < n; ++i) tnorm = std::max(tnorm, std::fabs(diag[i]) + std::fabs(off[i]));
-  const double abs_tol = eps * tnorm;
-  for (int l = 0; l < n; ++l) {
-    int iter = 0;
-    for (;;) {
-      int m = l;
-      for (; m + 1 < n; ++m) {
-        const double scale = std::fabs(diag[m]) + std::fabs(diag[m + 1]);
-        if (std::fabs(off[m]) <= std::max(eps * scale, abs_tol)) break;
+// One implicit symmetric QR step with the Wilkinson shift on the unreduced
+// block [l, m] of the tridiagonal (a: diagonal, b[i]: the entry coupling i and
+// i + 1), after Golub & Van Loan, "Matrix Computations", Algorithm 8.3.2.  The
+// shift mu is the eigenvalue of the block's trailing 2 x 2 nearer a[m]; the
+// first rotation acts on (a[l] - mu, b[l]) and each later one, on rows and
+// columns (k, k + 1), removes the bulge the previous one left at (k + 1, k - 1).
+// With rows (k, k+1) mixed as (c, s; -s, c) and the columns alike, the 2 x 2
+// block (p, r; r, q) becomes
+//   p' = c^2 p + 2cs r + s^2 q,  q' = s^2 p - 2cs r + c^2 q,
+//   r' = cs (q - p) + (c^2 - s^2) r,
+// and the next coupling b[k+1] splits into c b[k+1] and the new bulge s b[k+1].
+// zt (rows = columns of the accumulated orthogonal matrix) takes the same
+// rotations when not null.
+void qr_step(int n, int l, int m, double* a, double* b, double* zt) {
+  const double d = 0.5 * (a[m - 1] - a[m]);
+  const double e = b[m - 1];
+  const double den = d + std::copysign(hypot2(d, e), d);
+  const double mu = den != 0.0 ? a[m] - e * e / den : a[m];
+  double x = a[l] - mu, z = b[l];
+  for (int k = l; k < m; ++k) {
+    const double rad = hypot2(x, z);
+    const double c = rad > 0.0 ? x / rad : 1.0, s = rad > 0.0 ? z / rad : 0.0;
+    if (k > l) b[k - 1] = rad;
+    const double p = a[k], q = a[k + 1], r = b[k];
+    const double cc = c * c, ss = s * s, cs = c * s;
+    a[k] = cc * p + 2.0 * cs * r + ss * q;
+    a[k + 1] = ss * p - 2.0 * cs * r + cc * q;
+    b[k] = cs * (q - p) + (cc - ss) * r;
+    if (k + 1 < m) {
+      z = s * b[k + 1];
+      b[k + 1] *= c;
+      x = b[k];
+    }
+    if (zt) {
+      double* zk = zt + (size_t)k * n;
+      double* zk1 = zt + (size_t)(k + 1) * n;
+      for (int i = 0; i < n; ++i) {
+        const double u = zk[i], v = zk1[i];
+        zk[i] = c * u + s * v;
+        zk1[i] = c * v - s * u;
       }
-      if (m == l) break;
-      if (++iter > 80) return false;
-      // shift from the leading 2x2 block of the unreduced part
-      double g = (diag[l + 1] - diag[l]) / (2.0 * off[l]);
-      double rad = hypot2(g, 1.0);
-      g = diag[m] - diag[l] + off[l] / (g + std::copysign(rad, g));
-      double s = 1.0, c = 1.0, p = 0.0;
-      bool split = false;
-      for (int i = m - 1; i >= l; --i) {
-        const double f = s * off[i];
-        const double b = c * off[i];
-        rad = hypot2(f, g);
-        off[i + 1] = rad;
-        if (rad == 0.0) {  // an off-diagonal underflowed: deflate and restart
-          diag[i + 1] -= p;
-          off[m] = 0.0;
-          split = true;
-          break;
-        }
-        s = f / rad;
-        c = g / rad;
-        g = diag[i + 1] - p;
-        rad = (diag[i] - g) * s + 2.0 * c * b;
-        p = s * rad;
-        diag[i + 1] = g + p;
-        g = c * rad - b;
-        if (zt) {
-          double* zi = zt + (size_t)i * n;
-          double* zj = zt + (size_t)(i + 1) * n;
-          for (int k = 0; k < n; ++k) {
-            const double zik = zi[k], zjk = zj[k];
-            zj[k] = s * zik + c * zjk;
-            zi[k] = c * zik - s * zjk;
-          }
-        }
-      }
-      if (split) continue;
-      diag[l] -= p;
-      off[l] = g;
-      off[m] = 0.0;
     }
   }
+}
+
+// Eigenvalues (left in a) and, with zt, eigenvectors of the symmetric
+// tridiagonal (a, b) by implicit QR steps (Golub & Van Loan, Algorithm 8.3.3):
+// couplings that have become negligible are set to zero, and a step is
+// applied to the unreduced block that ends at the lowest row not yet split
+// off.  A coupling is negligible relative to its two diagonal entries, or
+// absolutely at eps * ||T|| (which moves any eigenvalue by at most that
+// much; the absolute test ends the iteration on blocks of (near-)zero
+// eigenvalues, where a purely relative one never does).  Returns false
+// without convergence.
+bool tridiag_qr(int n, double* a, double* b, double* zt) {
+  const double eps = std::numeric_limits<double>::epsilon();
+  double tnorm = 0.0;
+  for (int i = 0; i < n; ++i)
+    tnorm = std::max(tnorm, std::fabs(a[i]) + (i + 1 < n ? std::fabs(b[i]) : 0.0));
+  const double abs_tol = eps * tnorm;
+  auto negligible = [&](int i) {  // b[i], between rows i and i + 1
+    return std::fabs(b[i]) <= std::max(eps * (std::fabs(a[i]) + std::fabs(a[i + 1])), abs_tol);
+  };
+  long long steps = 0;
+  for (int m = n - 1; m > 0;) {
+    if (negligible(m - 1)) {
+      b[m - 1] = 0.0;
+      --m;
+      continue;
+    }
+    int l = m - 1;
+    while (l > 0 && !negligible(l - 1)) --l;
+    if (++steps > 80LL * n) return false;
+    qr_step(n, l, m, a, b, zt);
+  }
+  if (n > 0) b[n - 1] = 0.0;
   return true;
 }
 
@@ -668,7 +681,7 @@ bool sym_eig_rows(int n, const double* A, double* w, double* vt) {
   std::vector<double> diag(n), off(n), beta(n);
   householder_tridiag(n, a.data(), diag.data(), off.data(), q.data(), beta.data());
   form_qt(n, q.data(), beta.data(), zt.data());
-  if (!tridiag_ql(n, diag.data(), off.data(), zt.data())) return false;
+  if (!tridiag_qr(n, diag.data(), off.data(), zt.data())) return false;
   std::vector<int> order(n);
   for (int i = 0; i < n; ++i) order[i] = i;
   std::stable_sort(order.begin(), order.end(),
@@ -859,7 +872,7 @@ bool tridiag_of(int n, const double* A, double* diag, double* off, double* hv, d
 // The r largest eigenpairs of the symmetric matrix whose tridiagonal form
 // (diag, off) and reflectors (hv, beta) tridiag_of produced: w receives the
 // r largest eigenvalues in descending order (all n with all_values), row m
-// of `vecs` (r x n) the unit eigenvector of w[m].  Eigenvalues by QL without
+// of `vecs` (r x n) the unit eigenvector of w[m].  Eigenvalues by QR steps without
 // vectors (all_values) or by multisection on Sturm counts (only the r
 // largest), then inverse iteration on the tridiagonal for the r vectors
 // (Golub & Van Loan, Sec. 8.2.2 and 8.4), four shifts at a time,
@@ -872,7 +885,7 @@ bool top_eigpairs(int n, const double* diag, const double* off, const double* hv
   if (all_values) {
     std::vector<double> eo(off, off + n);
     std::copy(diag, diag + n, ev.begin());
-    if (!tridiag_ql(n, ev.data(), eo.data(), nullptr)) return false;
+    if (!tridiag_qr(n, ev.data(), eo.data(), nullptr)) return false;
     std::sort(ev.begin(), ev.end(), [](double x, double y) { return x > y; });
   } else {  // only the r largest, by multisection
     std::vector<double> off2(n, 0.0);

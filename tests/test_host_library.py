@@ -75,6 +75,23 @@ def test_sym_eig_structured_matrices(n):
         np.testing.assert_allclose(V.T @ V, np.eye(n), atol=1e-13 * n)
 
 
+def test_sym_eig_close_pairs_and_split_tridiagonals():
+    """Wilkinson's W21+ (its largest eigenvalues come in pairs that agree to
+    about 1e-14) and a tridiagonal whose couplings are partly below the
+    deflation threshold: eigenvalues against LAPACK, residuals, orthogonality."""
+    n = 21
+    W = np.diag(np.abs(np.arange(n) - 10.0)) + np.diag(np.ones(n - 1), 1) + np.diag(np.ones(n - 1), -1)
+    T = np.diag(np.linspace(-3.0, 5.0, 30)) + np.diag(np.where(np.arange(29) % 3 == 0, 1e-300, 0.5), 1)
+    T = np.triu(T) + np.triu(T, 1).T
+    for M in (W, T):
+        w, V = S.saki_sym_eig(M)
+        ref = np.linalg.eigvalsh(M)
+        scale = np.abs(ref).max()
+        assert np.max(np.abs(w - ref)) <= 1e-13 * len(M) * scale
+        assert np.max(np.abs(M @ V - V * w)) <= 1e-13 * len(M) * scale
+        np.testing.assert_allclose(V.T @ V, np.eye(len(M)), atol=1e-13 * len(M))
+
+
 def _m(B_q, B_k):
     return B_q.astype(np.float64) @ B_k.astype(np.float64).T
 
