@@ -44,6 +44,10 @@ def _score_both(inp, r, sketch, N_valid, q_pos=None):
     # 16 queries per head over long rows: the one-pass scan with chunk gates
     # and redo flags
     (dict(N=40_003, Q=16, H_q=2, H_kv=1), dict(N=17_000, Q=16, H_q=2, H_kv=1)),
+    # 16 or more queries per head over fewer than 16,384 keys: the two-pass
+    # scorer, whose query sketches (and, past 4,096 keys, partial lists) live
+    # in the scratch array
+    (dict(N=5_000, Q=64, H_q=8, H_kv=2), dict(N=3_000, Q=32, H_q=4, H_kv=1)),
 ])
 def test_noalloc_equals_workspace_entry_point(first, second):
     for shape, sketch in ((first, "bf16"), (second, "f32")):
