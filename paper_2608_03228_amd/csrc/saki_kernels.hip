@@ -22,6 +22,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <tuple>
@@ -47,6 +48,16 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
+  bf16x8_t r;
+  __builtin_memcpy(&r, &v, sizeof(r));
+  return r;
+}
+__device__ __forceinline__ i16x4_t as_i16x4(uint2 v) {
+  i16x4_t r;
+  __builtin_memcpy(&r, &v, sizeof(r));
+  return r;
+}
 
 constexpr int kStreamWaves = 4;  // waves per workgroup, streaming kernels
 constexpr int kMfmaWaves = 2;    // waves per workgroup, MFMA kernels
@@ -208,31 +219,62 @@ __device__ __forceinline__ int row_hits(int ej, const int* __restrict__ approx, 
 
 // ---------------------------------------------------------------- build index
 
-// Key codes c_j = B_k^T (k_j - mu) on the float32 MFMA (16x16x4).  A
-// work-group takes up to 1,024 keys of one KV head (16-key groups, 8 per
-// wave) and computes their codes for every query head of the group,
-// so each key is read once (a short range, a decode append, takes one query
-// head per work-group instead, so that the heads' factors load in parallel).
-// For a group of 16 keys and a block of 16 code dimensions the MFMA forms
-// D[m][key] = sum_c B_k[c][m] (k - mu)[key][c] in 32 steps of 4 dimensions;
-// the dimensions are taken in the order in which each lane's float4 loads
-// hold them (lane (key qi, group kg) loads dims 16 s + 4 kg .. + 3 of its key,
-// which are step 4 s + j's dimension 16 s + 4 kg + j), so the keys go from
-// registers straight into the B operand.  B_k of up to
-// kBuildLdsFloats / (128 (r + 4)) heads
-// at a time sits in LDS with rows of r + 4 floats (the four dimension groups of
-// a step start 0 and 16 banks apart).  Lane (qi, kg) ends with dims
-// m0 + 4 kg .. + 3 of key qi: one 16-byte float32 piece, half a bf16 piece or
-// a quarter of an fp8 piece.  Centring is float32 (k - mu) before the
-// product, as the paper writes it.
-constexpr int kBuildKeys = 1024;        // keys per work-group
-constexpr int kBuildSplitKeys = 256;    // ranges up to this many keys: one query head per work-group
-constexpr int kBuildLdsFloats = 18432;  // 72 KiB: B_k of up to 4 heads at r = 32
+// Key codes c_j = B_k^T (k_j - mu) on the bf16 MFMA (16x16x32).  Each float32
+// operand is split into three bf16 terms: x = x1 + x2 + x3 with x1 = bf16(x),
+// x2 = bf16(x - x1), x3 = bf16(x - x1 - x2) (each term takes the next 8
+// significant bits, so the three carry a float32's 24), and likewise
+// w = w1 + w2 + w3 for B_k.  The six products x_a w_b with a + b <= 4 are
+// formed, x1 w1 into one float32 accumulator and the five smaller ones into a
+// second; what is left out (x2 w3, x3 w2, x3 w3 and the splits' remainders)
+// is below 4 * 2^-24 |x| |w| per element, the size of float32 rounding, at
+// 6 bf16 products where float32 operands would take 16 times the MFMA time of
+// one.  A work-group takes a slice of the keys of one KV head (16-key groups,
+// taken by its 8 waves in turn) and computes their codes for every query head of the group, so
+// each key is read once (a short range, a decode append, takes one query head
+// per work-group instead, so that the heads' factors load in parallel).  For
+// a group of 16 keys and a block of 16 code dimensions the MFMA forms
+// D[m][key] = sum_c B_k[c][m] (k - mu)[key][c] in 4 steps of 32 dimensions:
+// lane (key qi, group g) loads dims 32 kk + 8 g .. + 7 of its key (the B
+// operand) and of B_k's column m = 16 mc + qi (the A operand).  The three
+// terms of B_k of up to build_heads_lds<r>() heads at a time sit in LDS,
+// transposed (one row of 128 dims per code dimension, rows of 136 bf16 so
+// that the 16 rows one read touches start 4 banks apart).  Lane (qi, g) ends
+// with dims 16 mc + 4 g .. + 3 of key qi: one 16-byte float32 piece, half a
+// bf16 piece or a quarter of an fp8 piece.  Centring is float32 (k - mu)
+// before the product, as the paper writes it.
+constexpr int kBuildKeys = 1024;         // keys per work-group, at least
+constexpr int kBuildSplitKeys = 256;     // ranges up to this many keys: one query head per work-group
+constexpr int kBuildRounds = 1;          // work-groups per slot the device holds
+constexpr int kBuildRow = 136;           // bf16 per LDS row of B_k (128 dims + 8)
+constexpr int kBuildLdsBytes = 104448;   // B_k of up to 4 heads at r = 32
 template <int RK>
-constexpr int build_heads_lds() { return kBuildLdsFloats / (saki::kHeadDim * (RK + 4)); }
+constexpr int build_heads_lds() { return kBuildLdsBytes / (3 * RK * kBuildRow * 2); }
 
-// grid (ceil(keys / kBuildKeys), H_kv or H_q (per_head), B), block 64 *
-// kBuildWaves; keys [k0, n_end) with k0 = n_begin rounded down to 16.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two floats rounded to bf16 (nearest even, v_cvt_pk_bf16_f32), packed low
+// first.
+__device__ __forceinline__ uint32_t bf16x2_bits(float a, float b) {
+  const bf16x2_t v = __builtin_convertvector(f32x2_t{a, b}, bf16x2_t);
+  uint32_t u;
+  __builtin_memcpy(&u, &v, sizeof(u));
+  return u;
+}
+
+// Splits a pair of floats into three packed bf16 pairs t[0] + t[1] + t[2].
+__device__ __forceinline__ void split3_bf16x2(float a, float b, uint32_t t[3]) {
+#pragma unroll
+  for (int p = 0; p < 3; ++p) {
+    t[p] = bf16x2_bits(a, b);
+    a -= __uint_as_float(t[p] << 16);
+    b -= __uint_as_float(t[p] & 0xffff0000u);
+  }
+}
+
+// grid (slices, H_kv or H_q (per_head), B), block 64 * kBuildWaves; the keys
+// [n_begin rounded down to 16, n_end) are cut into gridDim.x contiguous
+// slices, one per work-group, so that B_k is staged in LDS once per slice.
 constexpr int kBuildWaves = 8;
 template <int RK, bool KBF, int ST>
 __global__ __launch_bounds__(kBuildWaves * kWave) void build_index_kernel(
@@ -241,41 +283,72 @@ __global__ __launch_bounds__(kBuildWaves * kWave) void build_index_kernel(
     uint8_t* __restrict__ index, int n_begin, int n_end, int per_head) {
   constexpr int D = saki::kHeadDim;
   constexpr int ES = code_bytes<ST>();
-  constexpr int RS = RK + 4;  // LDS row stride of B_k (floats)
   constexpr int HB = build_heads_lds<RK>();
   static_assert(HB >= 1, "one head of B_k fits");
   constexpr size_t TB = (size_t)kTile * RK * ES;  // bytes of one 64-key tile
   constexpr int NM = RK / 16;
-  __shared__ float bks[HB * D * RS];
+  constexpr int SG = 2;                // 16-key groups per wave step
+  constexpr int MB = NM < 2 ? NM : 2;  // 16-dim code blocks per pass over a step's keys
+  constexpr int PS = RK * kBuildRow;  // bf16 per term of one head
+  __shared__ __align__(16) uint16_t bks[HB * 3 * PS];
   const int G = H_q / H_kv;
-  const int g = per_head ? (int)blockIdx.y / G : (int)blockIdx.y, b = blockIdx.z;
-  const int h_first = per_head ? (int)blockIdx.y : g * G;  // query heads [h_first, h_end)
+  const int gkv = per_head ? (int)blockIdx.y / G : (int)blockIdx.y, b = blockIdx.z;
+  const int h_first = per_head ? (int)blockIdx.y : gkv * G;  // query heads [h_first, h_end)
   const int h_end = per_head ? h_first + 1 : h_first + G;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-  const int qi = lane % 16, kg = lane / 16;
-  const int k0 = (n_begin / 16) * 16 + blockIdx.x * kBuildKeys;
-  const size_t key_base = ((size_t)b * H_kv + g) * N_cap;
-  float4 m4[8];  // mu at this lane's dims 16 s + 4 kg .. + 3
+  const int qi = lane % 16, g = lane / 16;
+  // this work-group's keys [k0, k1): slices of the range from n_begin rounded
+  // down to 16, a multiple of 16 keys each
+  const int kb = (n_begin / 16) * 16;
+  const int slice = ((n_end - kb + (int)gridDim.x - 1) / (int)gridDim.x + 15) / 16 * 16;
+  const int k0 = kb + (int)blockIdx.x * slice;
+  if (k0 >= n_end) return;  // the whole work-group
+  const int k1 = min(n_end, k0 + slice);
+  const size_t key_base = ((size_t)b * H_kv + gkv) * N_cap;
+  __shared__ __align__(16) float mus[D];  // mu of the KV head (read after the first barrier below)
+  if (tid < D / 4)
+    reinterpret_cast<float4*>(mus)[tid] = reinterpret_cast<const float4*>(mu + (size_t)gkv * D)[tid];
+  // raw key dims 32 kk + 8 g .. + 7 of key n (16 bytes of bf16 or 32 of float32 per kk)
+  struct RawKey {
+    uint4 v[KBF ? 4 : 8];
+  };
+  auto load_raw = [&](int n, bool ok, RawKey& r) {
 #pragma unroll
-  for (int s = 0; s < 8; ++s)
-    m4[s] = *reinterpret_cast<const float4*>(mu + (size_t)g * D + 16 * s + 4 * kg);
-  // (k - mu) of key n at dims 16 s + 4 kg + j, step t = 4 s + j (zero outside the range)
-  auto load_keys = [&](int n, bool ok, float* kf) {
-#pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      const float4 kv = ok ? load_key4<KBF>(keys, (key_base + n) * D + 16 * s + 4 * kg)
-                           : make_float4(0.f, 0.f, 0.f, 0.f);
-      kf[4 * s] = ok ? kv.x - m4[s].x : 0.f;
-      kf[4 * s + 1] = ok ? kv.y - m4[s].y : 0.f;
-      kf[4 * s + 2] = ok ? kv.z - m4[s].z : 0.f;
-      kf[4 * s + 3] = ok ? kv.w - m4[s].w : 0.f;
+    for (int i = 0; i < (KBF ? 4 : 8); ++i) {
+      const size_t off = (key_base + n) * D + (KBF ? 32 * i + 8 * g : 32 * (i / 2) + 8 * g + 4 * (i % 2));
+      r.v[i] = ok ? (KBF ? *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(keys) + off)
+                         : *reinterpret_cast<const uint4*>(reinterpret_cast<const float*>(keys) + off))
+                  : uint4{0u, 0u, 0u, 0u};
     }
   };
-  auto store = [&](int n, int h, const f32x4_t* acc) {
+  // (k - mu) split into three bf16 terms: xp[p][kk] holds dims 32 kk + 8 g .. + 7
+  auto split_key = [&](const RawKey& r, bool ok, uint4 xp[3][4]) {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      float f[8];
+      if constexpr (KBF) {
+        unpack_piece<true>(r.v[kk], f);
+      } else {
+        unpack_piece<false>(r.v[2 * kk], f);
+        unpack_piece<false>(r.v[2 * kk + 1], f + 4);
+      }
+      float m[8];
+      *reinterpret_cast<float4*>(m) = *reinterpret_cast<const float4*>(&mus[32 * kk + 8 * g]);
+      *reinterpret_cast<float4*>(m + 4) = *reinterpret_cast<const float4*>(&mus[32 * kk + 8 * g + 4]);
+      uint32_t t[4][3];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        split3_bf16x2(ok ? f[2 * e] - m[2 * e] : 0.f, ok ? f[2 * e + 1] - m[2 * e + 1] : 0.f, t[e]);
+#pragma unroll
+      for (int p = 0; p < 3; ++p) xp[p][kk] = uint4{t[0][p], t[1][p], t[2][p], t[3][p]};
+    }
+  };
+  // code dims 16 (mc0 + mc) + 4 g .. + 3 of key n, mc < MB
+  auto store = [&](int n, int h, int mc0, const f32x4_t* acc) {
     uint8_t* tb = index + (((size_t)b * H_q + h) * n_tiles + n / kTile) * TB;
 #pragma unroll
-    for (int mc = 0; mc < NM; ++mc) {
-      const int m = 16 * mc + 4 * kg;  // first code dim of this lane
+    for (int mc = 0; mc < MB; ++mc) {
+      const int m = 16 * (mc0 + mc) + 4 * g;  // first code dim of this lane
       uint8_t* dst = tb + (size_t)(m * ES / 16) * kTile * 16 + (size_t)(n % kTile) * 16 + (m * ES) % 16;
       const f32x4_t v = acc[mc];
       if constexpr (ST == kStFp8) {
@@ -290,36 +363,93 @@ __global__ __launch_bounds__(kBuildWaves * kWave) void build_index_kernel(
       }
     }
   };
+  // a wave takes SG groups of 16 keys per step, so that each B_k operand read
+  // from LDS serves SG products
+  const int n_steps = (k1 - k0 + 16 * SG - 1) / (16 * SG);
+  auto key_at = [&](int st, int sg) { return k0 + 16 * (SG * st + sg) + qi; };
+  auto key_ok = [&](int n) { return n >= n_begin && n < k1; };
+  constexpr int NT = kBuildWaves * kWave;
+  constexpr int FB = 4;  // B_k pairs per thread whose loads are issued together
   for (int h0 = h_first; h0 < h_end; h0 += HB) {
     const int nh = min(HB, h_end - h0);
     __syncthreads();  // the previous heads' reads are done
-    for (int e = tid * 4; e < nh * D * RK; e += kBuildWaves * kWave * 4) {
-      const float4 v = *reinterpret_cast<const float4*>(Bk + (size_t)h0 * D * RK + e);
-      const int hh = e / (D * RK), c = (e / RK) % D, m = e % RK;
-      *reinterpret_cast<float4*>(&bks[(hh * D + c) * RS + m]) = v;
+    // B_k[h][c][m] (row-major D x RK) -> term p at bks[((hh * 3 + p) * RK + m) * kBuildRow + c],
+    // dims c = 2 c2, 2 c2 + 1 per pair
+    for (int e0 = tid; e0 < nh * (D / 2) * RK; e0 += FB * NT) {
+      float2 w[FB];
+#pragma unroll
+      for (int i = 0; i < FB; ++i) {
+        const int e = e0 + i * NT;
+        const int m = e % RK, c2 = (e / RK) % (D / 2), hh = e / (RK * (D / 2));
+        const float* src = Bk + ((size_t)(h0 + hh) * D + 2 * c2) * RK + m;
+        w[i] = e < nh * (D / 2) * RK ? make_float2(src[0], src[RK]) : make_float2(0.f, 0.f);
+      }
+#pragma unroll
+      for (int i = 0; i < FB; ++i) {
+        const int e = e0 + i * NT;
+        const int m = e % RK, c2 = (e / RK) % (D / 2), hh = e / (RK * (D / 2));
+        uint32_t t[3];
+        split3_bf16x2(w[i].x, w[i].y, t);
+        if (e < nh * (D / 2) * RK)
+#pragma unroll
+          for (int p = 0; p < 3; ++p)
+            *reinterpret_cast<uint32_t*>(&bks[((hh * 3 + p) * RK + m) * kBuildRow + 2 * c2]) = t[p];
+      }
     }
     __syncthreads();
-    for (int grp = wave; grp < kBuildKeys / 16; grp += kBuildWaves) {
-      const int n0 = k0 + 16 * grp;
-      if (n0 >= n_end) break;  // wave-uniform
-      const int n = n0 + qi;
-      const bool ok = n >= n_begin && n < n_end;
-      float kf[32];
-      load_keys(n, ok, kf);
-      for (int hh = 0; hh < nh; ++hh) {
-        const float* bh = &bks[hh * D * RS];
-        f32x4_t acc[NM];
+    RawKey cur[SG];
+    if (wave < n_steps)
 #pragma unroll
-        for (int mc = 0; mc < NM; ++mc) acc[mc] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int sg = 0; sg < SG; ++sg) load_raw(key_at(wave, sg), key_ok(key_at(wave, sg)), cur[sg]);
+    for (int st = wave; st < n_steps; st += kBuildWaves) {
+      uint4 xp[SG][3][4];
 #pragma unroll
-        for (int st = 0; st < 32; ++st) {
-          const int c = 16 * (st / 4) + 4 * kg + st % 4;
+      for (int sg = 0; sg < SG; ++sg) split_key(cur[sg], key_ok(key_at(st, sg)), xp[sg]);
+      if (st + kBuildWaves < n_steps)  // the wave's next step, loaded under this one's products
 #pragma unroll
-          for (int mc = 0; mc < NM; ++mc)
-            acc[mc] = __builtin_amdgcn_mfma_f32_16x16x4f32(bh[c * RS + 16 * mc + qi], kf[st], acc[mc],
-                                                           0, 0, 0);
+        for (int sg = 0; sg < SG; ++sg)
+          load_raw(key_at(st + kBuildWaves, sg), key_ok(key_at(st + kBuildWaves, sg)), cur[sg]);
+#pragma unroll 1
+      for (int hm = 0; hm < nh * (NM / MB); ++hm) {  // head hh, code dims from 16 mc0
+        const int hh = hm / (NM / MB), mc0 = (hm % (NM / MB)) * MB;
+        f32x4_t hi[SG][MB], lo[SG][MB];
+#pragma unroll
+        for (int sg = 0; sg < SG; ++sg)
+#pragma unroll
+          for (int mc = 0; mc < MB; ++mc) {
+            hi[sg][mc] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            lo[sg][mc] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+          }
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          // the operands of one 32-dim step at a time (register room)
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int mc = 0; mc < MB; ++mc) {
+            const uint16_t* wr = &bks[(hh * 3 * RK + 16 * (mc0 + mc) + qi) * kBuildRow + 32 * kk + 8 * g];
+            const bf16x8_t w1 = as_bf16x8(*reinterpret_cast<const uint4*>(wr));
+            const bf16x8_t w2 = as_bf16x8(*reinterpret_cast<const uint4*>(wr + PS));
+            const bf16x8_t w3 = as_bf16x8(*reinterpret_cast<const uint4*>(wr + 2 * PS));
+#pragma unroll
+            for (int sg = 0; sg < SG; ++sg) {
+              const bf16x8_t x1 = as_bf16x8(xp[sg][0][kk]), x2 = as_bf16x8(xp[sg][1][kk]),
+                             x3 = as_bf16x8(xp[sg][2][kk]);
+              hi[sg][mc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, x1, hi[sg][mc], 0, 0, 0);
+              lo[sg][mc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w3, x1, lo[sg][mc], 0, 0, 0);
+              lo[sg][mc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w2, x2, lo[sg][mc], 0, 0, 0);
+              lo[sg][mc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, x3, lo[sg][mc], 0, 0, 0);
+              lo[sg][mc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w2, x1, lo[sg][mc], 0, 0, 0);
+              lo[sg][mc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1, x2, lo[sg][mc], 0, 0, 0);
+            }
+          }
         }
-        if (ok) store(n, h0 + hh, acc);
+#pragma unroll
+        for (int sg = 0; sg < SG; ++sg) {
+#pragma unroll
+          for (int mc = 0; mc < MB; ++mc) hi[sg][mc] += lo[sg][mc];
+          const int n = key_at(st, sg);
+          if (key_ok(n)) store(n, h0 + hh, mc0, hi[sg]);
+        }
       }
     }
   }
@@ -615,17 +745,6 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
 // batched kernel (score_batch_kernel), the one-pass kernel for long rows
 // (score_scan_kernel) and the exact-recall kernels.
 
-
-__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
-  bf16x8_t r;
-  __builtin_memcpy(&r, &v, sizeof(r));
-  return r;
-}
-__device__ __forceinline__ i16x4_t as_i16x4(uint2 v) {
-  i16x4_t r;
-  __builtin_memcpy(&r, &v, sizeof(r));
-  return r;
-}
 // Pack 8 floats that already hold bf16 values into a bf16x8 operand.
 __device__ __forceinline__ uint4 pack_bf16x8(const float* f) {
   uint4 u;
@@ -3451,18 +3570,6 @@ dim3 xcd_grid(const saki::Plan& p, int n_bh) {
   return dim3((unsigned)(((total + kXcds - 1) / kXcds) * kXcds));
 }
 
-template <int RK, bool KBF, int ST>
-void launch_build(const void* keys, const float* Bk, const float* mu, int B, int H_q,
-                  int H_kv, int N_cap, uint8_t* index, int n_begin, int n_end,
-                  hipStream_t s) {
-  const int k0 = (n_begin / 16) * 16;
-  const int groups = (n_end - k0 + kBuildKeys - 1) / kBuildKeys;
-  const int per_head = n_end - n_begin <= kBuildSplitKeys ? 1 : 0;
-  dim3 grid(groups, per_head ? H_q : H_kv, B);
-  hipLaunchKernelGGL((build_index_kernel<RK, KBF, ST>), grid, dim3(kBuildWaves * kWave), 0, s, keys, Bk, mu, H_q,
-                     H_kv, N_cap, (int)saki::n_tiles(N_cap), index, n_begin, n_end, per_head);
-}
-
 // Work-groups of `kernel` (block `threads`) resident on the whole current
 // device at once, or 0 if the runtime cannot tell.  Cached per (kernel,
 // block size, device).
@@ -3487,6 +3594,25 @@ int resident_groups(K kernel, int threads) {
   std::lock_guard<std::mutex> lock(mu);
   cache[key] = cus * per_cu;
   return cus * per_cu;
+}
+
+template <int RK, bool KBF, int ST>
+void launch_build(const void* keys, const float* Bk, const float* mu, int B, int H_q,
+                  int H_kv, int N_cap, uint8_t* index, int n_begin, int n_end,
+                  hipStream_t s) {
+  const int k0 = (n_begin / 16) * 16;
+  const int per_head = n_end - n_begin <= kBuildSplitKeys ? 1 : 0;
+  const long long units = (long long)(per_head ? H_q : H_kv) * B;
+  // slices of at least kBuildKeys keys, about as many work-groups as the
+  // device holds at once
+  int slices = (n_end - k0 + kBuildKeys - 1) / kBuildKeys;
+  if (!per_head) {
+    const int slots = resident_groups(build_index_kernel<RK, KBF, ST>, kBuildWaves * kWave);
+    if (slots > 0) slices = (int)std::max(1LL, std::min((long long)slices, kBuildRounds * slots / units));
+  }
+  dim3 grid(slices, per_head ? H_q : H_kv, B);
+  hipLaunchKernelGGL((build_index_kernel<RK, KBF, ST>), grid, dim3(kBuildWaves * kWave), 0, s, keys, Bk, mu, H_q,
+                     H_kv, N_cap, (int)saki::n_tiles(N_cap), index, n_begin, n_end, per_head);
 }
 
 // A split-N streaming launch that fills the GPU exactly once: the plan's

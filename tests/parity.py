@@ -43,6 +43,15 @@ FP8_SUBNORMAL_ABS = 2.0 ** -10 * (1 + 2.0 ** -8)
 # (2.8e-7 on the LLaMA-shaped layer's codes and sketches) times 3.5; the GPU's
 # exported float32 codes are checked against the same bound.
 AMBIG_REL = 1e-6
+# Rigorous bound on the GPU's float32 evaluation of one score from bf16 (or
+# fp8 widened to bf16) codes and query sketches: the r <= 32 products per MFMA
+# are exact and are summed with the mean term in float32, so
+# |fl(s) - s| <= gamma_33 (sum_e |z_e c_e| + |b|) <= gamma_33 T_ij with
+# gamma_33 = 33 u / (1 - 33 u), u = 2^-24 (1.97e-6).  A row whose GPU set
+# differs from the oracle's must be a swap within this bound (plus the one-ulp
+# allowance of codes and sketch elements near a rounding midpoint), five times
+# narrower than the per-score tolerance.
+TIGHT_EMUL = 2e-6
 
 
 def _bf16_ambiguity(exact, abs_sum):
@@ -67,14 +76,15 @@ def _fp8_ambiguity(exact, abs_sum):
     return amb, ulp
 
 
-def oracle_head(B_q, B_k, mu, q, keys, mode: str):
+def oracle_head(B_q, B_k, mu, q, keys, mode: str, tight: bool = False):
     """Oracle scores and per-score tolerances of one head.
 
     mode: "f32" (exact codes, tol 1e-5), "bf16_exact" (exact codes, tol 2e-2),
     "bf16_emul" (bf16-rounded codes and z, tol 1e-5 plus ambiguity),
     "fp8_exact" (exact codes, tol 7e-2 plus the subnormal term), "fp8_emul"
     (fp8 codes, bf16 z, tol 1e-5 plus ambiguity).
-    Returns (s [Q, N], eps [Q, N])."""
+    Returns (s [Q, N], eps [Q, N]), and with `tight` (emulating modes only)
+    also the swap bound TIGHT_EMUL * T plus ambiguity."""
     q = np.asarray(q, np.float64)
     keys = np.asarray(keys, np.float64)
     T = O.norm_scale(B_q, B_k, mu, q, keys)
@@ -93,12 +103,18 @@ def oracle_head(B_q, B_k, mu, q, keys, mode: str):
     amb_c, ulp_c = code_amb(c_ex, np.abs(keys - mu) @ np.abs(B_k))
     amb_z, ulp_z = _bf16_ambiguity(z_ex, np.abs(q) @ np.abs(B_q))
     extra = np.abs(z) @ (amb_c * ulp_c).T + (amb_z * ulp_z) @ np.abs(c).T
+    if tight:
+        return s, TOL_F32 * T + extra, TIGHT_EMUL * T + extra
     return s, TOL_F32 * T + extra
 
 
-def check_rows(gpu_idx, gpu_score, s, eps, limits, k):
+def check_rows(gpu_idx, gpu_score, s, eps, limits, k, tight=None, log=None):
     """Validate GPU top-k rows against oracle scores.  Raises AssertionError
-    with the first offending row; returns (rows, exempt rows, differing rows)."""
+    with the first offending row; returns (rows, exempt rows, differing rows).
+    With `tight` (per-score bounds, e.g. oracle_head's third result) a
+    differing row's swap must be explainable within them instead of eps;
+    `log` (a list) receives (row, gap, bound) of each differing row, gap being
+    the oracle's best dropped score minus its worst kept one."""
     n_exempt = n_diff = 0
     for i in range(s.shape[0]):
         lim = int(limits[i])
@@ -132,7 +148,11 @@ def check_rows(gpu_idx, gpu_score, s, eps, limits, k):
         assert exempt, f"row {i}: sets differ on a non-exempt row"
         out = np.array(sorted(sL - sG))
         inn = np.array(sorted(sG - sL))
-        lo_out = np.max(s[i, out] - eps[i, out])
-        hi_in = np.min(s[i, inn] + eps[i, inn])
+        bnd = eps if tight is None else tight
+        lo_out = np.max(s[i, out] - bnd[i, out])
+        hi_in = np.min(s[i, inn] + bnd[i, inn])
         assert lo_out <= hi_in, f"row {i}: unexplainable swap {out} <-> {inn}"
+        if log is not None:
+            a, b = out[np.argmax(s[i, out])], inn[np.argmin(s[i, inn])]
+            log.append((i, s[i, a] - s[i, b], bnd[i, a] + bnd[i, b]))
     return s.shape[0], n_exempt, n_diff

@@ -49,7 +49,7 @@ def oracle_factors(inp, h, r):
 
 
 def check_head(inp, out, b, h, r, mode, rows=None, k=64, N_valid=None, factors=None,
-               keys_override=None):
+               keys_override=None, tight=False, log=None):
     spec = inp["spec"]
     G = spec.H_q // spec.H_kv
     Bq, Bk, mu = factors if factors is not None else oracle_factors(inp, h, r)
@@ -57,10 +57,12 @@ def check_head(inp, out, b, h, r, mode, rows=None, k=64, N_valid=None, factors=N
     N = keys.shape[0] if N_valid is None else N_valid
     rows = np.arange(spec.Q) if rows is None else np.asarray(rows)
     q = inp["queries"][b, h][rows]
-    s, eps = oracle_head(Bq, Bk, mu, q, keys[:N], mode)
+    res = oracle_head(Bq, Bk, mu, q, keys[:N], mode, tight=tight)
+    s, eps, tb = res if tight else (*res, None)
     pos = inp["q_pos"][rows] if inp["q_pos"] is not None else None
     lim = O.candidate_limits(len(rows), N, pos)
-    return check_rows(out["idx"][b, h][rows], out["score"][b, h][rows], s, eps, lim, k)
+    return check_rows(out["idx"][b, h][rows], out["score"][b, h][rows], s, eps, lim, k,
+                      tight=tb, log=log)
 
 
 def test_single_head_f32_full():
