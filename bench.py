@@ -92,10 +92,11 @@ def kernel_source_digest():
 
 
 def measured_traffic(kernel, workload, instance):
-    """HBM bytes per launch of `kernel` on `workload` from the committed
-    rocprofv3 FETCH_SIZE / WRITE_SIZE summary (scaled by a plain copy of
-    known size), or None when no row matches the current kernel source and
-    the template instance the run launches."""
+    """HBM bytes per step of `kernel`'s launches on `workload` (the one-pass
+    scan launches twice per step) from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE summary (scaled by a plain copy of known size), or None when
+    no row matches the current kernel source and the template instance the
+    run launches."""
     try:
         lines = open(TRAFFIC_FILE).read().splitlines()
     except OSError:
