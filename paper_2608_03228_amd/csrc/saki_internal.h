@@ -14,7 +14,7 @@ constexpr int kChunkBytes = 16;
 constexpr int kScanWaves = 1;          // waves per work-group of the one-pass MFMA scoring kernel
 constexpr int kScanMinKeys = 16384;    // rows at least this long take it
 constexpr int kBatchMaxChunk = 4096;   // keys per chunk of the two-pass MFMA scoring kernel
-constexpr int kBatchWaves = 4;         // its waves per work-group (16 rows each)
+constexpr int kBatchWaves = 1;         // its waves per work-group (16 rows each)
 
 inline bool rank_supported(int r) { return r == 16 || r == 32 || r == 64 || r == 128; }
 // bytes per code element: float32 (0), bf16 (1), fp8 E4M3 (2)

@@ -1127,10 +1127,11 @@ __global__ __launch_bounds__(kQsWaves * kWave) void query_sketch_kernel(
 
 // ---------------------------------------------------------------- sketch scoring, MFMA, block-maximum gate
 
-// score_batch_kernel: four independent waves per work-group, each with a
-// block of 16 query rows and that block's keys of one chunk (at most 4,096
-// keys), and the exact top-64 per row in two passes over the codes (the MFMA
-// recomputes the scores in the second).  Rows are ranked by s' = z . c: b is
+// score_batch_kernel: one wave per work-group (its LDS is released the moment
+// it ends, where a wave of a larger work-group would hold its slot until the
+// slowest of its siblings ends), each with a block of 16 query rows and that
+// block's keys of one chunk (at most 4,096 keys), and the exact top-64 per row
+// in two passes over the codes (the MFMA recomputes the scores in the second).  Rows are ranked by s' = z . c: b is
 // the same for all keys of a row and is added to the 64 kept scores.
 //   A. each lane records the maxima of its keys in blocks of 8, 4, 2 or 1
 //      keys, the size set by the wave's longest row (at least 2,048, 1,024,
@@ -1335,8 +1336,9 @@ __device__ __forceinline__ void merge64_u32(uint32_t (&x)[16], const uint32_t (&
 }
 
 // grid: 1-D, 8 * ceil(groups * n_chunks * n_bh / 8) work-groups of kBWaves
-// waves; work-group (bh, chunk, group) takes the 16-row blocks 4 * group ..
-// 4 * group + 3 of (sequence, head) bh, the longest causal rows first.
+// waves; work-group (bh, chunk, group) takes the 16-row blocks kBWaves * group
+// .. kBWaves * group + kBWaves - 1 of (sequence, head) bh, the longest causal
+// rows first.
 template <int RK, int ST>
 __global__ __launch_bounds__(kBWaves * kWave) void score_batch_kernel(
     const uint8_t* __restrict__ index, int n_tiles, int N_valid, int Q,
