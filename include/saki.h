@@ -183,9 +183,12 @@ size_t saki_index_bytes(int B, int H_q, int N_cap, int r, int sketch_dtype);
 /*
  * saki_build_index (GPU) -- key codes c_j = B_k^(h)T (k_j - mu_g(h)) (Eq. 4)
  * for every query head h, keys j in [n_begin, n_begin + n_count).  Codes are
- * computed in float32 and stored as sketch_dtype (bf16: round to nearest
- * even; fp8: round to the nearest E4M3 value, ties to the even code,
- * magnitudes above 448 saturating to 448).  Codes outside the range are left
+ * computed to float32 accuracy: k - mu in float32, every product formed from
+ * three bf16 terms of each operand (what is left out is below
+ * 4 * 2^-24 |k_e - mu_e| |B_k[e][m]|) and accumulated in float32.  They are
+ * stored as sketch_dtype (bf16: round to nearest even; fp8: round to the
+ * nearest E4M3 value, ties to the even code, magnitudes above 448 saturating
+ * to 448).  Codes outside the range are left
  * untouched, so (0, N) builds the whole index and (n, 1) appends one decoded
  * token.
  *
