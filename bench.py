@@ -14,7 +14,8 @@ step is one pass of the whole path over that batch:
                  (enqueued in the next step ahead of its build: the host
                  factorisation outlasts a step's GPU work, and the GPU's wait
                  for it then precedes the evaluation, not the build and score;
-                 the last batch's recall runs inside the timed region)
+                 every timed step runs one recall, the first of them the last
+                 warm-up batch's, and the last batch's runs after timing)
 
 Inputs (keys, queries, positions, calibration tokens) are resident in HBM
 before timing starts.  `value` is the metric's unit of work, (query, allowed
@@ -366,15 +367,18 @@ def run_batched(inp, r, sk, k, steps, warmup, method="opt"):
 
     for _ in range(warmup):
         step(timed_stages=False)
-    if pending[0]:
-        recall(False)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
+        # each timed step runs one recall (of the batch before it: the first
+        # one evaluates the last warm-up batch), one build and one score
         step()  # stage events on the launch stream, inside the timed region
-    recall(True)  # the last batch's evaluation, inside the timed region
     torch.cuda.synchronize()
     dt = (time.perf_counter() - t0) / steps
+    # the last batch's evaluation, after the timed region (its time is used
+    # only when no timed step ran a recall: no warm-up and one step)
+    recall(not ev_recall)
+    torch.cuda.synchronize()
     names = ["build", "score_topk", "recall"]
     stage_ms = {n: float(np.mean([es[i].elapsed_time(es[i + 1]) for es in ev]))
                 for i, n in enumerate(names[:2])}
