@@ -6,8 +6,9 @@ keys, causal query rows at positions 64..4095, rank-32 bf16 sketches.  One
 step is one pass of the whole path over that batch:
 
   1. calibrate   float64 moments of the 512 calibration tokens on the GPU (side
-                 stream, for the next batch), copied back; host float64
-                 factorisation into B_q, B_k, mu; factors uploaded
+                 stream, for the next batch, after the score stage enqueued
+                 before it), copied back; host float64 factorisation into
+                 B_q, B_k, mu; factors uploaded
   2. build       key codes for every query head
   3. score_topk  query sketches, sketch scores and the top-64 per (query, head)
   4. recall      exact float64 q.k top-64 and hits against the sketch top-64
@@ -299,9 +300,15 @@ def run_batched(inp, r, sk, k, steps, warmup, method="opt"):
               for _ in range(2)]
     m_done = [None, None]
     side.wait_stream(torch.cuda.current_stream())  # calibration tokens uploaded
+    score_done = [None]  # the last score stage enqueued on the launch stream
 
     def enqueue_moments(sl):
         with torch.cuda.stream(side):
+            # after the score stage enqueued last: the moments then run while
+            # the GPU waits for the host factorisation, never beside a build
+            # or score
+            if score_done[0] is not None:
+                side.wait_event(score_done[0])
             S.saki_calibration_moments(q_cal, k_cal, m_dev[sl]["Sq"], m_dev[sl]["Sk"],
                                        m_dev[sl]["mu"], stream=side)
             for n in m_shape:
@@ -363,6 +370,8 @@ def run_batched(inp, r, sk, k, steps, warmup, method="opt"):
         if timed_stages:
             e[2].record()
             ev.append(e)
+        score_done[0] = torch.cuda.Event()
+        score_done[0].record()
         pending[0] = True
 
     for _ in range(warmup):
